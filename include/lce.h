@@ -1,0 +1,128 @@
+/*
+ * lce.h - C ABI of the MI355X (gfx950) bitpacked binary 2-D convolution.
+ *
+ * The operator is LceBConv2d of Larq Compute Engine (arXiv 2011.09398,
+ * Section 3.2, "Operator implementations"), preceded by the sign
+ * binarization and bitpacking of LceQuantize (same section):
+ *
+ *   1. bitpack:   bit = 1 (standing for -1.0) iff x < 0, else 0 (+1.0);
+ *                 channel c goes to 32-bit word c/32, bit c%32; the channel
+ *                 count is padded up to a multiple of 32 with 0 bits.
+ *   2. im2col over the bitpacked NHWC tensor, padded locations read as
+ *      0 bits, i.e. +1.0 ("one-padding").
+ *   3. XOR + POPCOUNT GEMM against bitpacked +-1 filters:
+ *          dot = K - 2 * sum_k popcount(a_k XOR w_k),  K = KH*KW*C_in.
+ *   4. fused output transform on the integer accumulator:
+ *          c = min(max(dot, clamp_min), clamp_max)   (fused activation)
+ *          float32 output:   y = fmaf((float)c, multiplier[co], bias[co])
+ *          bitpacked output: bit = 1 iff c < thresholds[co] (exact compare)
+ *
+ * Conventions shared by every entry point:
+ *   - All tensor pointers are DEVICE pointers owned by the caller.  The
+ *     library never allocates, frees or synchronizes; all work is enqueued
+ *     asynchronously on `stream` (NULL = the default stream).
+ *   - Activations are NHWC, filters OHWI (the TensorFlow Lite orders), and a
+ *     bitpacked tensor stores ceil(C/32) int32 words per pixel (or filter
+ *     tap) with its packed-channel axis innermost.  Bits beyond the real
+ *     channel count MUST be zero in every bitpacked input; lce_bitpack and
+ *     lce_bconv2d's bitpacked output always write them as zero.
+ *   - Outputs must not alias inputs.
+ *   - Arguments are validated on the host before anything is launched; on
+ *     any error nothing is written or launched, the status is returned, and
+ *     lce_last_error() describes it.  Asynchronous device faults surface at
+ *     the caller's next synchronization.  No C++ exception crosses the ABI.
+ */
+#ifndef LCE_H_
+#define LCE_H_
+
+#include <stdint.h>
+#include <hip/hip_runtime_api.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum {
+    LCE_OK = 0,
+    LCE_EINVAL = 1,        /* null pointer, bad size or enum, empty output   */
+    LCE_EUNSUPPORTED = 2,  /* well-formed request this build does not run    */
+    LCE_EALIGN = 3,        /* pointer not aligned to its element type        */
+    LCE_EHIP = 4           /* the HIP runtime reported an error at launch    */
+} lce_status;
+
+/* Spatial padding, TensorFlow semantics: SAME gives ceil(H/stride) outputs
+ * with floor(total/2) padding before and the rest after; VALID none. */
+typedef enum { LCE_PADDING_VALID = 0, LCE_PADDING_SAME = 1 } lce_padding;
+
+/* Value read at padded locations.  ONE (0 bits, +1.0) is the one-padding of
+ * Section 3.2.  ZERO (TensorFlow's default, which needs a correction step)
+ * is rejected with LCE_EUNSUPPORTED. */
+typedef enum { LCE_PAD_ONE = 0, LCE_PAD_ZERO = 1 } lce_pad_value;
+
+/* Output of lce_bconv2d:
+ *   FLOAT32   float  [N][OH][OW][C_out]
+ *   BITPACKED int32  [N][OH][OW][ceil(C_out/32)]
+ *   INT32     int32  [N][OH][OW][C_out], the clamped accumulator c itself */
+typedef enum { LCE_OUT_FLOAT32 = 0, LCE_OUT_BITPACKED = 1, LCE_OUT_INT32 = 2 } lce_out_type;
+
+/* One binary convolution.  Every field is a plain int32 (enums by value). */
+typedef struct {
+    int32_t n, h, w, c_in;          /* input activations, NHWC, >= 1          */
+    int32_t c_out, kh, kw;          /* filters, OHWI, >= 1                    */
+    int32_t stride_h, stride_w;     /* >= 1                                   */
+    int32_t padding;                /* lce_padding                            */
+    int32_t pad_value;              /* lce_pad_value                          */
+    int32_t clamp_min, clamp_max;   /* fused activation bounds on the integer
+                                       accumulator; clamp_min <= clamp_max.
+                                       INT32_MIN/INT32_MAX = no activation    */
+    int32_t out_type;               /* lce_out_type                           */
+} lce_bconv2d_desc;
+
+/* Number of 32-bit words holding `channels` packed channels: ceil(c/32).
+ * Returns -1 when channels < 0. */
+int32_t lce_packed_words(int32_t channels);
+
+/* Output height/width of `desc` (TensorFlow SAME/VALID).  Validates the
+ * descriptor exactly as lce_bconv2d does, except for pointers.
+ * Errors: LCE_EINVAL (null desc/oh/ow, bad field, no output). */
+lce_status lce_bconv2d_out_shape(const lce_bconv2d_desc *desc, int32_t *oh, int32_t *ow);
+
+/* LceQuantize (Section 3.2): sign-binarize and bitpack a row-major float
+ * array x[rows][channels] into out[rows][ceil(channels/32)].
+ * Bit c%32 of word c/32 is 1 iff x[r][c] < 0.0f (so -0.0 and NaN give 0,
+ * i.e. +1.0); the bits past `channels` are written as 0.
+ * For activations rows = N*H*W; for OHWI filters (the 1-bit weight storage
+ * of Section 3.1) rows = C_out*KH*KW with channels = C_in.
+ * rows == 0 is a no-op.  x must be 4-byte aligned (16-byte alignment and a
+ * channel count that is a multiple of 32 take the fastest path), out 4-byte.
+ * Errors: LCE_EINVAL (null pointer, rows < 0, channels < 1),
+ *         LCE_EALIGN, LCE_EHIP. */
+lce_status lce_bitpack(const float *x, int32_t *out, int64_t rows, int32_t channels,
+                       hipStream_t stream);
+
+/* LceBConv2d (Section 3.2): bitpacked binary convolution with the fused
+ * output transform.
+ *   x_packed   int32 [N][H][W][ceil(C_in/32)]          (device)
+ *   w_packed   int32 [C_out][KH][KW][ceil(C_in/32)]    (device)
+ *   multiplier float [C_out] or NULL (= 1.0)   used by FLOAT32 output only
+ *   bias       float [C_out] or NULL (= 0.0)   used by FLOAT32 output only
+ *   thresholds float [C_out], required by BITPACKED output only
+ *   out        see lce_out_type; shape from lce_bconv2d_out_shape
+ * Dilation and groups are not part of the operator (always 1).
+ * All pointers must be 4-byte aligned.
+ * Errors: LCE_EINVAL (null desc or required pointer, bad field, no output,
+ *         c_out > 2^20, a tensor of 2^31 or more words/elements),
+ *         LCE_EUNSUPPORTED (pad_value ZERO), LCE_EALIGN, LCE_EHIP. */
+lce_status lce_bconv2d(const lce_bconv2d_desc *desc,
+                       const int32_t *x_packed, const int32_t *w_packed,
+                       const float *multiplier, const float *bias,
+                       const float *thresholds, void *out, hipStream_t stream);
+
+/* Message describing the last error on the calling thread ("" if none). */
+const char *lce_last_error(void);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* LCE_H_ */

@@ -1,0 +1,210 @@
+"""MI355X (gfx950) bitpacked binary convolution: Python binding of include/lce.h.
+
+Argument marshalling only: every step of the operator runs in the HIP
+kernels of liblce.so.  torch supplies device memory and the current stream.
+If the library is not built this module raises; there is no CPU fallback.
+
+    bitpack(x)                        LceQuantize: float [..., C] -> int32 [..., ceil(C/32)]
+    bconv2d(x_packed, w_packed, c_in) LceBConv2d with the fused output transform
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+from typing import Optional, Sequence, Tuple, Union
+
+from . import build as _build
+
+LCE_OK, LCE_EINVAL, LCE_EUNSUPPORTED, LCE_EALIGN, LCE_EHIP = 0, 1, 2, 3, 4
+STATUS_NAMES = {0: "LCE_OK", 1: "LCE_EINVAL", 2: "LCE_EUNSUPPORTED", 3: "LCE_EALIGN",
+                4: "LCE_EHIP"}
+PADDING = {"valid": 0, "same": 1}
+PAD_VALUE = {"one": 0, "zero": 1}
+OUT_TYPE = {"float": 0, "bitpacked": 1, "int32": 2}
+INT32_MIN = -(2 ** 31)
+INT32_MAX = 2 ** 31 - 1
+
+# Every symbol include/lce.h declares.
+EXPORTS = ("lce_packed_words", "lce_bconv2d_out_shape", "lce_bitpack", "lce_bconv2d",
+           "lce_last_error")
+
+
+class Desc(ctypes.Structure):
+    """lce_bconv2d_desc: fourteen int32 fields, in header order."""
+    _fields_ = [(name, ctypes.c_int32) for name in (
+        "n", "h", "w", "c_in", "c_out", "kh", "kw", "stride_h", "stride_w",
+        "padding", "pad_value", "clamp_min", "clamp_max", "out_type")]
+
+
+class LceError(RuntimeError):
+    def __init__(self, status: int, message: str):
+        super().__init__(f"{STATUS_NAMES.get(status, status)}: {message}")
+        self.status = status
+
+
+_lib = None
+
+
+def lib() -> ctypes.CDLL:
+    """The loaded liblce.so (raises if it has not been built)."""
+    global _lib
+    if _lib is None:
+        if not os.path.exists(_build.LIB):
+            raise ImportError(f"{_build.LIB} is not built; run paper_2011_09398_amd.build.build()")
+        L = ctypes.CDLL(_build.LIB)
+        vp, i32, i64 = ctypes.c_void_p, ctypes.c_int32, ctypes.c_int64
+        L.lce_packed_words.argtypes = [i32]
+        L.lce_packed_words.restype = i32
+        L.lce_bconv2d_out_shape.argtypes = [ctypes.POINTER(Desc), ctypes.POINTER(i32),
+                                            ctypes.POINTER(i32)]
+        L.lce_bconv2d_out_shape.restype = ctypes.c_int
+        L.lce_bitpack.argtypes = [vp, vp, i64, i32, vp]
+        L.lce_bitpack.restype = ctypes.c_int
+        L.lce_bconv2d.argtypes = [ctypes.POINTER(Desc), vp, vp, vp, vp, vp, vp, vp]
+        L.lce_bconv2d.restype = ctypes.c_int
+        L.lce_last_error.argtypes = []
+        L.lce_last_error.restype = ctypes.c_char_p
+        _lib = L
+    return _lib
+
+
+def last_error() -> str:
+    return lib().lce_last_error().decode()
+
+
+def _check(status: int) -> None:
+    if status != LCE_OK:
+        raise LceError(status, last_error())
+
+
+def packed_words(channels: int) -> int:
+    return int(lib().lce_packed_words(int(channels)))
+
+
+def make_desc(n, h, w, c_in, c_out, kh, kw, stride=1, padding="same", pad_value="one",
+              clamp: Optional[Tuple[int, int]] = None, out_type="float") -> Desc:
+    sh, sw = (stride, stride) if isinstance(stride, int) else tuple(stride)
+    lo, hi = (INT32_MIN, INT32_MAX) if clamp is None else clamp
+    return Desc(n, h, w, c_in, c_out, kh, kw, sh, sw,
+                PADDING[padding] if isinstance(padding, str) else padding,
+                PAD_VALUE[pad_value] if isinstance(pad_value, str) else pad_value,
+                lo, hi, OUT_TYPE[out_type] if isinstance(out_type, str) else out_type)
+
+
+def out_shape(desc: Desc) -> Tuple[int, int]:
+    oh, ow = ctypes.c_int32(), ctypes.c_int32()
+    _check(lib().lce_bconv2d_out_shape(ctypes.byref(desc), ctypes.byref(oh), ctypes.byref(ow)))
+    return oh.value, ow.value
+
+
+def _stream_handle(t) -> int:
+    import torch
+    return torch.cuda.current_stream(t.device).cuda_stream
+
+
+def _require(t, dtype, name):
+    import torch
+    if not isinstance(t, torch.Tensor):
+        raise TypeError(f"{name} must be a torch.Tensor")
+    if t.device.type != "cuda":
+        raise ValueError(f"{name} must be a device tensor, got {t.device}")
+    if t.dtype != dtype:
+        raise TypeError(f"{name} must be {dtype}, got {t.dtype}")
+    if not t.is_contiguous():
+        raise ValueError(f"{name} must be contiguous")
+
+
+def bitpack(x, out=None):
+    """LceQuantize on a float32 device tensor [..., C] -> int32 [..., ceil(C/32)]."""
+    import torch
+    _require(x, torch.float32, "x")
+    c = x.shape[-1]
+    cw = packed_words(c)
+    rows = x.numel() // c if c else 0
+    if out is None:
+        out = torch.empty(tuple(x.shape[:-1]) + (cw,), dtype=torch.int32, device=x.device)
+    else:
+        _require(out, torch.int32, "out")
+        if out.numel() != rows * cw:
+            raise ValueError("out has the wrong size")
+    _check(lib().lce_bitpack(x.data_ptr(), out.data_ptr(), rows, c, _stream_handle(x)))
+    return out
+
+
+def bconv2d(x_packed, w_packed, c_in: int, *, stride: Union[int, Sequence[int]] = 1,
+            padding: str = "same", pad_value: str = "one",
+            clamp: Optional[Tuple[int, int]] = None, out_type: str = "float",
+            multiplier=None, bias=None, thresholds=None, out=None):
+    """LceBConv2d: x_packed int32 [N,H,W,Cw], w_packed int32 [Cout,KH,KW,Cw].
+
+    out_type "float" -> float32 [N,OH,OW,Cout]; "bitpacked" -> int32
+    [N,OH,OW,ceil(Cout/32)]; "int32" -> the clamped accumulator [N,OH,OW,Cout].
+    """
+    import torch
+    _require(x_packed, torch.int32, "x_packed")
+    _require(w_packed, torch.int32, "w_packed")
+    n, h, w, cw = x_packed.shape
+    cout, kh, kw, cw2 = w_packed.shape
+    if cw != packed_words(c_in) or cw2 != cw:
+        raise ValueError(f"packed channel words {cw}/{cw2} do not match c_in={c_in}")
+    desc = make_desc(n, h, w, c_in, cout, kh, kw, stride, padding, pad_value, clamp, out_type)
+    oh, ow = out_shape(desc)
+    ptrs = []
+    for t, name in ((multiplier, "multiplier"), (bias, "bias"), (thresholds, "thresholds")):
+        if t is None:
+            ptrs.append(None)
+        else:
+            _require(t, torch.float32, name)
+            if t.numel() != cout:
+                raise ValueError(f"{name} must have {cout} elements")
+            ptrs.append(t.data_ptr())
+    oc = packed_words(cout) if out_type == "bitpacked" else cout
+    if out is not None:
+        _require(out, torch.float32 if out_type == "float" else torch.int32, "out")
+        if out.numel() != n * oh * ow * oc:
+            raise ValueError(f"out must hold {n}x{oh}x{ow}x{oc} elements")
+    else:
+        if out_type == "float":
+            out = torch.empty((n, oh, ow, cout), dtype=torch.float32, device=x_packed.device)
+        elif out_type == "bitpacked":
+            out = torch.empty((n, oh, ow, packed_words(cout)), dtype=torch.int32,
+                              device=x_packed.device)
+        else:
+            out = torch.empty((n, oh, ow, cout), dtype=torch.int32, device=x_packed.device)
+    _check(lib().lce_bconv2d(ctypes.byref(desc), x_packed.data_ptr(), w_packed.data_ptr(),
+                             ptrs[0], ptrs[1], ptrs[2], out.data_ptr(),
+                             _stream_handle(x_packed)))
+    return out
+
+
+class PreparedBConv2d:
+    """A bconv2d call with its descriptor and pointers marshalled once.
+
+    Calling it enqueues the convolution on the given stream handle (default:
+    torch's current stream), with no per-call validation in Python; the C ABI
+    still validates.  The tensors must outlive the object.
+    """
+
+    def __init__(self, x_packed, w_packed, c_in, out, *, stride=1, padding="same",
+                 clamp=None, out_type="float", multiplier=None, bias=None, thresholds=None):
+        import torch
+        # one eager call validates shapes/dtypes and fills `out`
+        bconv2d(x_packed, w_packed, c_in, stride=stride, padding=padding, clamp=clamp,
+                out_type=out_type, multiplier=multiplier, bias=bias, thresholds=thresholds,
+                out=out)
+        n, h, w, _ = x_packed.shape
+        cout, kh, kw, _ = w_packed.shape
+        self.desc = make_desc(n, h, w, c_in, cout, kh, kw, stride, padding, "one", clamp,
+                              out_type)
+        self._desc_ref = ctypes.byref(self.desc)
+        ptr = lambda t: None if t is None else t.data_ptr()
+        self.args = (x_packed.data_ptr(), w_packed.data_ptr(), ptr(multiplier), ptr(bias),
+                     ptr(thresholds), out.data_ptr())
+        self.keep = (x_packed, w_packed, multiplier, bias, thresholds, out)
+        self.stream = torch.cuda.current_stream(x_packed.device).cuda_stream
+        self._fn = lib().lce_bconv2d
+
+    def __call__(self, stream=None):
+        st = self._fn(self._desc_ref, *self.args, self.stream if stream is None else stream)
+        if st != LCE_OK:
+            raise LceError(st, last_error())

@@ -1,0 +1,250 @@
+// C ABI of the MI355X bitpacked binary convolution (declared in include/lce.h):
+// host-side validation, geometry and kernel dispatch.  No allocation, no
+// synchronization: every launch goes on the caller's stream.
+#include <hip/hip_runtime.h>
+
+#include <climits>
+#include <cstdarg>
+#include <cstdint>
+#include <cstdio>
+#include <string>
+
+#include "lce.h"
+#include "bitpack.hpp"
+#include "bconv.hpp"
+
+namespace {
+
+thread_local std::string g_last_error;
+
+lce_status fail(lce_status st, const char *fmt, ...) {
+    char buf[512];
+    va_list ap;
+    va_start(ap, fmt);
+    vsnprintf(buf, sizeof buf, fmt, ap);
+    va_end(ap);
+    g_last_error = buf;
+    return st;
+}
+
+lce_status ok() {
+    g_last_error.clear();
+    return LCE_OK;
+}
+
+lce_status check_launch(const char *what) {
+    hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return fail(LCE_EHIP, "%s: %s", what, hipGetErrorString(e));
+    return ok();
+}
+
+bool aligned(const void *p, uintptr_t a) { return (reinterpret_cast<uintptr_t>(p) % a) == 0; }
+
+int packed_words(int channels) { return (channels + 31) / 32; }
+
+// TensorFlow SAME/VALID output size and leading pad of one dimension.
+bool out_dim(int in, int k, int s, int padding, int *out, int *pad_before) {
+    if (padding == LCE_PADDING_SAME) {
+        const int o = in / s + (in % s != 0);
+        long total = (long)(o - 1) * s + k - in;
+        if (total < 0) total = 0;
+        *out = o;
+        *pad_before = (int)(total / 2);
+        return true;
+    }
+    if (in < k) return false;
+    *out = (in - k) / s + 1;
+    *pad_before = 0;
+    return true;
+}
+
+struct Geometry {
+    int oh, ow, pt, pl;
+};
+
+lce_status validate_desc(const lce_bconv2d_desc *d, Geometry *g) {
+    if (!d) return fail(LCE_EINVAL, "desc is NULL");
+    if (d->n < 1 || d->h < 1 || d->w < 1 || d->c_in < 1)
+        return fail(LCE_EINVAL, "input dims must be >= 1 (n=%d h=%d w=%d c_in=%d)", d->n, d->h,
+                    d->w, d->c_in);
+    if (d->c_out < 1 || d->kh < 1 || d->kw < 1)
+        return fail(LCE_EINVAL, "filter dims must be >= 1 (c_out=%d kh=%d kw=%d)", d->c_out,
+                    d->kh, d->kw);
+    if (d->stride_h < 1 || d->stride_w < 1)
+        return fail(LCE_EINVAL, "strides must be >= 1 (%d, %d)", d->stride_h, d->stride_w);
+    if (d->padding != LCE_PADDING_VALID && d->padding != LCE_PADDING_SAME)
+        return fail(LCE_EINVAL, "unknown padding %d", d->padding);
+    if (d->pad_value != LCE_PAD_ONE && d->pad_value != LCE_PAD_ZERO)
+        return fail(LCE_EINVAL, "unknown pad_value %d", d->pad_value);
+    if (d->out_type != LCE_OUT_FLOAT32 && d->out_type != LCE_OUT_BITPACKED &&
+        d->out_type != LCE_OUT_INT32)
+        return fail(LCE_EINVAL, "unknown out_type %d", d->out_type);
+    if (d->clamp_min > d->clamp_max)
+        return fail(LCE_EINVAL, "clamp_min %d > clamp_max %d", d->clamp_min, d->clamp_max);
+    if (!out_dim(d->h, d->kh, d->stride_h, d->padding, &g->oh, &g->pt) ||
+        !out_dim(d->w, d->kw, d->stride_w, d->padding, &g->ow, &g->pl))
+        return fail(LCE_EINVAL, "VALID convolution with a %dx%d filter has no output on %dx%d",
+                    d->kh, d->kw, d->h, d->w);
+    const int64_t cw = packed_words(d->c_in);
+    const int64_t m = (int64_t)d->n * g->oh * g->ow;
+    const int64_t x_words = (int64_t)d->n * d->h * d->w * cw;
+    const int64_t w_words = (int64_t)d->c_out * d->kh * d->kw * cw;
+    const int64_t out_elems = m * (d->out_type == LCE_OUT_BITPACKED ? packed_words(d->c_out)
+                                                                    : d->c_out);
+    const int64_t k = (int64_t)d->kh * d->kw * d->c_in;
+    const int64_t lim = INT32_MAX;
+    if (m > lim - lce::kPix || x_words > lim || w_words > lim || out_elems > lim || k > lim / 2)
+        return fail(LCE_EINVAL,
+                    "tensor too large (pixels %lld, input words %lld, filter words %lld, "
+                    "output elements %lld, K %lld; each must stay below 2^31)",
+                    (long long)m, (long long)x_words, (long long)w_words, (long long)out_elems,
+                    (long long)k);
+    if (d->c_out > (1 << 20)) return fail(LCE_EINVAL, "c_out %d exceeds 2^20", d->c_out);
+    if (d->pad_value == LCE_PAD_ZERO)
+        return fail(LCE_EUNSUPPORTED, "zero-padding is not supported (one-padding only)");
+    return ok();
+}
+
+using lce::BconvParams;
+
+template <int CW, int KH, int KW, int OUT>
+void launch_static(const BconvParams &p, dim3 grid, hipStream_t s, int vec) {
+    constexpr int RN = 8, KC = 8;
+    if (vec == 4 && CW % 4 == 0)
+        hipLaunchKernelGGL((lce::bconv2d_static_kernel<CW, KH, KW, RN, KC, (CW % 4 == 0 ? 4 : 1), OUT>),
+                           grid, dim3(lce::kThreads), 0, s, p);
+    else if (vec >= 2 && CW % 2 == 0)
+        hipLaunchKernelGGL((lce::bconv2d_static_kernel<CW, KH, KW, RN, KC, (CW % 2 == 0 ? 2 : 1), OUT>),
+                           grid, dim3(lce::kThreads), 0, s, p);
+    else
+        hipLaunchKernelGGL((lce::bconv2d_static_kernel<CW, KH, KW, RN, KC, 1, OUT>), grid,
+                           dim3(lce::kThreads), 0, s, p);
+}
+
+template <int OUT>
+void launch_generic(const BconvParams &p, dim3 grid, hipStream_t s) {
+    constexpr int RN = 8, KC = 8;
+    const size_t lds = (size_t)lce::kPix * p.rs * sizeof(uint32_t);
+    hipLaunchKernelGGL((lce::bconv2d_generic_kernel<RN, KC, OUT>), grid, dim3(lce::kThreads), lds,
+                       s, p);
+}
+
+// True when a shape-specialized kernel was launched.
+template <int OUT>
+bool dispatch_static(const BconvParams &p, dim3 grid, hipStream_t s, int vec) {
+    if (p.kh == 3 && p.kw == 3) {
+        switch (p.cw) {
+            case 1: launch_static<1, 3, 3, OUT>(p, grid, s, vec); return true;
+            case 2: launch_static<2, 3, 3, OUT>(p, grid, s, vec); return true;
+            case 4: launch_static<4, 3, 3, OUT>(p, grid, s, vec); return true;
+            case 8: launch_static<8, 3, 3, OUT>(p, grid, s, vec); return true;
+            case 16: launch_static<16, 3, 3, OUT>(p, grid, s, vec); return true;
+            default: return false;
+        }
+    }
+    return false;
+}
+
+template <int OUT>
+void dispatch(const BconvParams &p, dim3 grid, hipStream_t s, int vec) {
+    if (!dispatch_static<OUT>(p, grid, s, vec)) launch_generic<OUT>(p, grid, s);
+}
+
+}  // namespace
+
+extern "C" {
+
+int32_t lce_packed_words(int32_t channels) {
+    if (channels < 0) return -1;
+    return packed_words(channels);
+}
+
+lce_status lce_bconv2d_out_shape(const lce_bconv2d_desc *desc, int32_t *oh, int32_t *ow) {
+    if (!oh || !ow) return fail(LCE_EINVAL, "oh/ow output pointer is NULL");
+    Geometry g;
+    lce_status st = validate_desc(desc, &g);
+    if (st != LCE_OK && st != LCE_EUNSUPPORTED) return st;
+    *oh = g.oh;
+    *ow = g.ow;
+    return ok();
+}
+
+lce_status lce_bitpack(const float *x, int32_t *out, int64_t rows, int32_t channels,
+                       hipStream_t stream) {
+    if (!x || !out) return fail(LCE_EINVAL, "x/out is NULL");
+    if (rows < 0) return fail(LCE_EINVAL, "rows %lld < 0", (long long)rows);
+    if (channels < 1) return fail(LCE_EINVAL, "channels %d < 1", channels);
+    if (!aligned(x, 4) || !aligned(out, 4)) return fail(LCE_EALIGN, "x/out not 4-byte aligned");
+    if (rows > (INT64_MAX / 64) / channels) return fail(LCE_EINVAL, "tensor too large");
+    if (rows == 0) return ok();
+    const int cw = packed_words(channels);
+    const int64_t nwords = rows * cw;
+    if (channels % 32 == 0 && aligned(x, 16)) {
+        const int64_t chunks = (nwords + 7) / 8;
+        const int64_t per_block = (lce::kBitpackThreads / 64) * lce::kBitpackUnroll;
+        int64_t blocks = (chunks + per_block - 1) / per_block;
+        if (blocks > 256 * 16) blocks = 256 * 16;
+        hipLaunchKernelGGL(lce::bitpack32_kernel, dim3((unsigned)blocks),
+                           dim3(lce::kBitpackThreads), 0, stream,
+                           reinterpret_cast<const float4 *>(x), reinterpret_cast<uint32_t *>(out),
+                           nwords);
+    } else {
+        int64_t blocks = (nwords + lce::kBitpackThreads - 1) / lce::kBitpackThreads;
+        if (blocks > 256 * 32) blocks = 256 * 32;
+        hipLaunchKernelGGL(lce::bitpack_generic_kernel, dim3((unsigned)blocks),
+                           dim3(lce::kBitpackThreads), 0, stream, x,
+                           reinterpret_cast<uint32_t *>(out), rows, (int)channels, cw);
+    }
+    return check_launch("lce_bitpack launch");
+}
+
+lce_status lce_bconv2d(const lce_bconv2d_desc *desc, const int32_t *x_packed,
+                       const int32_t *w_packed, const float *multiplier, const float *bias,
+                       const float *thresholds, void *out, hipStream_t stream) {
+    Geometry g;
+    lce_status st = validate_desc(desc, &g);
+    if (st != LCE_OK) return st;
+    const lce_bconv2d_desc &d = *desc;
+    if (!x_packed || !w_packed || !out) return fail(LCE_EINVAL, "x_packed/w_packed/out is NULL");
+    if (d.out_type == LCE_OUT_BITPACKED && !thresholds)
+        return fail(LCE_EINVAL, "bitpacked output needs thresholds");
+    if (!aligned(x_packed, 4) || !aligned(w_packed, 4) || !aligned(out, 4) ||
+        (multiplier && !aligned(multiplier, 4)) || (bias && !aligned(bias, 4)) ||
+        (thresholds && !aligned(thresholds, 4)))
+        return fail(LCE_EALIGN, "tensor pointers must be 4-byte aligned");
+
+    BconvParams p{};
+    p.x = reinterpret_cast<const uint32_t *>(x_packed);
+    p.w = reinterpret_cast<const uint32_t *>(w_packed);
+    p.mult = d.out_type == LCE_OUT_FLOAT32 ? multiplier : nullptr;
+    p.bias = d.out_type == LCE_OUT_FLOAT32 ? bias : nullptr;
+    p.thr = thresholds;
+    p.out = out;
+    p.n = d.n; p.h = d.h; p.wd = d.w; p.cw = packed_words(d.c_in);
+    p.oh = g.oh; p.ow = g.ow; p.cout = d.c_out; p.cwo = packed_words(d.c_out);
+    p.kh = d.kh; p.kw = d.kw; p.sh = d.stride_h; p.sw = d.stride_w; p.pt = g.pt; p.pl = g.pl;
+    p.kwords = d.kh * d.kw * p.cw;
+    p.k = d.kh * d.kw * d.c_in;
+    p.lo = d.clamp_min; p.hi = d.clamp_max;
+    p.m = d.n * g.oh * g.ow;
+    p.ohw = g.oh * g.ow;
+    p.slab = p.kwords < lce::kSlabWords ? p.kwords : lce::kSlabWords;
+    p.rs = lce::row_stride(p.slab);
+
+    const int rn = 8;
+    const int filters = d.out_type == LCE_OUT_BITPACKED ? p.cwo * 32 : p.cout;
+    const int per_block = rn * lce::kWaves;
+    dim3 grid((unsigned)((p.m + lce::kPix - 1) / lce::kPix),
+              (unsigned)((filters + per_block - 1) / per_block));
+    const int vec = aligned(x_packed, 16) ? 4 : aligned(x_packed, 8) ? 2 : 1;
+    switch (d.out_type) {
+        case LCE_OUT_FLOAT32: dispatch<lce::OUT_FLOAT>(p, grid, stream, vec); break;
+        case LCE_OUT_BITPACKED: dispatch<lce::OUT_BITS>(p, grid, stream, vec); break;
+        default: dispatch<lce::OUT_INT>(p, grid, stream, vec); break;
+    }
+    return check_launch("lce_bconv2d launch");
+}
+
+const char *lce_last_error(void) { return g_last_error.c_str(); }
+
+}  // extern "C"

@@ -1,0 +1,146 @@
+"""Host side of the C ABI, on the CPU: exports, geometry, validation errors.
+
+Every call here fails validation (or needs no device work), so nothing is
+ever launched; fake non-null pointers are plain integers.
+"""
+import ctypes
+import os
+import re
+import subprocess
+from itertools import product
+
+import pytest
+
+import oracle
+import paper_2011_09398_amd as lce
+from paper_2011_09398_amd import build as lce_build
+from tests.conftest import ROOT
+
+HEADER = os.path.join(ROOT, "include", "lce.h")
+P = 0x10000          # a fake, suitably aligned device pointer (never dereferenced)
+
+
+@pytest.fixture(scope="module", autouse=True)
+def built():
+    if lce_build.is_stale():
+        lce_build.build()
+
+
+def declared_functions():
+    text = open(HEADER).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"\b(lce_[a-z0-9_]+)\s*\(", text)))
+
+
+def test_header_declares_the_binding_exports():
+    assert declared_functions() == sorted(lce.EXPORTS)
+
+
+def test_library_exports_every_declared_symbol():
+    L = lce.lib()
+    for name in declared_functions():
+        assert hasattr(L, name), name
+    out = subprocess.run(["nm", "-D", "--defined-only", lce_build.LIB], capture_output=True,
+                         text=True, check=True).stdout
+    exported = set(re.findall(r"\bT (lce_\w+)", out))
+    assert set(declared_functions()) <= exported
+
+
+def test_desc_layout_matches_header():
+    # 14 int32 fields, no padding
+    assert ctypes.sizeof(lce.Desc) == 14 * 4
+
+
+def test_packed_words():
+    assert [lce.packed_words(c) for c in (0, 1, 31, 32, 33, 64, 65, 512)] == \
+        [0, 1, 1, 1, 2, 2, 3, 16]
+    assert lce.packed_words(-1) == -1
+
+
+def desc(**kw):
+    base = dict(n=1, h=8, w=8, c_in=64, c_out=64, kh=3, kw=3, stride=1, padding="same",
+                pad_value="one", clamp=None, out_type="float")
+    base.update(kw)
+    return lce.make_desc(**base)
+
+
+def test_out_shape_matches_oracle_geometry():
+    for h, k, s, pad in product((1, 2, 5, 7, 8, 28, 56), (1, 2, 3, 5), (1, 2, 3), ("same", "valid")):
+        if pad == "valid" and h < k:
+            continue
+        d = desc(h=h, w=h + 1 if h + 1 >= k else h, kh=k, kw=k, stride=s, padding=pad)
+        oh, ow = lce.out_shape(d)
+        assert oh == oracle.out_size(h, k, s, pad)[0]
+        assert ow == oracle.out_size(d.w, k, s, pad)[0]
+
+
+def test_out_shape_config_examples():
+    assert lce.out_shape(desc(h=56, w=56, stride=2)) == (28, 28)
+    assert lce.out_shape(desc(h=7, w=7)) == (7, 7)
+    assert lce.out_shape(desc(h=8, w=8, padding="valid")) == (6, 6)
+    # geometry does not depend on the pad value
+    assert lce.out_shape(desc(pad_value="zero")) == (8, 8)
+
+
+@pytest.mark.parametrize("field,value", [
+    ("n", 0), ("h", 0), ("w", -1), ("c_in", 0), ("c_out", 0), ("kh", 0), ("kw", 0),
+    ("stride_h", 0), ("stride_w", -2), ("padding", 7), ("pad_value", 3), ("out_type", 9),
+])
+def test_out_shape_rejects_bad_field(field, value):
+    d = desc()
+    setattr(d, field, value)
+    with pytest.raises(lce.LceError) as e:
+        lce.out_shape(d)
+    assert e.value.status == lce.LCE_EINVAL
+    assert lce.last_error()
+
+
+def call_bconv(d, x=P, w=P, m=None, b=None, t=P, out=P):
+    return lce.lib().lce_bconv2d(ctypes.byref(d), x, w, m, b, t, out, None)
+
+
+def test_bconv2d_validation_errors():
+    L = lce.lib()
+    assert L.lce_bconv2d(None, P, P, None, None, P, P, None) == lce.LCE_EINVAL
+    assert "desc" in lce.last_error()
+    assert call_bconv(desc(clamp=(5, 4))) == lce.LCE_EINVAL
+    assert "clamp" in lce.last_error()
+    assert call_bconv(desc(h=2, w=2, padding="valid")) == lce.LCE_EINVAL
+    assert call_bconv(desc(), x=None) == lce.LCE_EINVAL
+    assert call_bconv(desc(), w=None) == lce.LCE_EINVAL
+    assert call_bconv(desc(), out=None) == lce.LCE_EINVAL
+    assert call_bconv(desc(out_type="bitpacked"), t=None) == lce.LCE_EINVAL
+    assert "threshold" in lce.last_error()
+    assert call_bconv(desc(pad_value="zero")) == lce.LCE_EUNSUPPORTED
+    assert call_bconv(desc(), x=P + 2) == lce.LCE_EALIGN
+    assert call_bconv(desc(), out=P + 1) == lce.LCE_EALIGN
+    assert call_bconv(desc(), m=P + 3) == lce.LCE_EALIGN
+    # too large: 2^31 output pixels
+    assert call_bconv(desc(n=2 ** 14, h=2 ** 9, w=2 ** 9, c_in=32, c_out=32)) == lce.LCE_EINVAL
+    assert call_bconv(desc(c_out=(1 << 20) + 1, c_in=32, h=1, w=1)) == lce.LCE_EINVAL
+
+
+def test_bitpack_validation_errors():
+    L = lce.lib()
+    assert L.lce_bitpack(None, P, 4, 32, None) == lce.LCE_EINVAL
+    assert L.lce_bitpack(P, None, 4, 32, None) == lce.LCE_EINVAL
+    assert L.lce_bitpack(P, P, -1, 32, None) == lce.LCE_EINVAL
+    assert L.lce_bitpack(P, P, 4, 0, None) == lce.LCE_EINVAL
+    assert L.lce_bitpack(P + 2, P, 4, 32, None) == lce.LCE_EALIGN
+    assert L.lce_bitpack(P, P + 1, 4, 32, None) == lce.LCE_EALIGN
+    assert L.lce_bitpack(P, P, 2 ** 62, 64, None) == lce.LCE_EINVAL
+    # zero rows is a valid no-op: nothing is launched
+    assert L.lce_bitpack(P, P, 0, 32, None) == lce.LCE_OK
+    assert lce.last_error() == ""
+
+
+def test_error_message_is_thread_local():
+    import threading
+    L = lce.lib()
+    assert L.lce_bitpack(None, P, 4, 32, None) == lce.LCE_EINVAL
+    seen = []
+    th = threading.Thread(target=lambda: seen.append(lce.last_error()))
+    th.start()
+    th.join()
+    assert seen == [""]
+    assert lce.last_error() != ""

@@ -38,6 +38,11 @@ class Layer:
     clamp: Optional[Tuple[int, int]] = None
     input_kind: str = "float"
     chained_from: Optional[int] = None
+    stride_w: Optional[int] = None   # None = same as `stride` (the height stride)
+
+    @property
+    def strides(self) -> Tuple[int, int]:
+        return (self.stride, self.stride if self.stride_w is None else self.stride_w)
 
     @property
     def cw(self) -> int:
@@ -53,10 +58,10 @@ class Layer:
         return self.kh * self.kw * self.c_in
 
     def out_hw(self) -> Tuple[int, int]:
+        sh, sw = self.strides
         if self.padding == "same":
-            return (-(-self.h // self.stride), -(-self.w // self.stride))
-        return ((self.h - self.kh) // self.stride + 1,
-                (self.w - self.kw) // self.stride + 1)
+            return (-(-self.h // sh), -(-self.w // sw))
+        return ((self.h - self.kh) // sh + 1, (self.w - self.kw) // sw + 1)
 
     @property
     def m(self) -> int:
