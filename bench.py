@@ -1,17 +1,26 @@
 """Benchmark of the bitpacked binary convolution on one MI355X.
 
-A step is one pass over the batch-64 QuickNet-shaped layers (bitpacked
-input, bitpacked output): 56x56x64->128 stride 2, whose output feeds
-28x28x128->128, then 14x14x256->256 and 7x7x512->512.  The JSON line also
-carries the batch-1 layers (float input through lce_bitpack, timed as its
-own line) as per-layer microseconds, the roofline of the dominant kernel,
-and the CPU oracle timed on a bounded sample of the same step.
+Default workload (one step): the four batch-64 QuickNet-shaped binary 3x3
+convolutions with bitpacked input and output: 56x56x64->128 stride 2, whose
+output feeds 28x28x128->128, then 14x14x256->256 and 7x7x512->512.
+
+Measured on the launch stream with HIP events:
+  * the timed region: K steps back to back (events at its two ends, plus
+    wall clock around it, synchronized on both sides) -> value, ms_per_step;
+  * per launch: each layer launched R times back to back between two events
+    -> average launch duration, the figure the roofline uses;
+  * batch-1 layers (float input: lce_bitpack timed as its own line) the same
+    way, but from a captured HIP graph of the R launches, since eager launch
+    cost exceeds their run time;
+  * a probe of the achievable xor+popcount VALU rate, next to the spec peak.
+Then the CPU oracle, as it stands, on a bounded sample of the same step.
 
     python bench.py [--steps K] [--warmup W] [--no-cpu] [--workload b64|stack16]
 """
 from __future__ import annotations
 
 import argparse
+import ctypes
 import json
 import os
 import platform
@@ -37,11 +46,16 @@ HBM_PEAK_GBS = 8000.0
 def parse():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
-    ap.add_argument("--steps", type=int, default=200)
-    ap.add_argument("--warmup", type=int, default=20)
+    ap.add_argument("--steps", type=int, default=500)
+    ap.add_argument("--warmup", type=int, default=50)
+    ap.add_argument("--reps", type=int, default=100, help="launches per per-kernel timing")
     ap.add_argument("--workload", choices=("b64", "stack16"), default="b64")
     ap.add_argument("--no-cpu", action="store_true", help="skip the CPU oracle baseline")
     ap.add_argument("--no-batch1", action="store_true", help="skip the batch-1 lines")
+    ap.add_argument("--no-probe", action="store_true", help="skip the VALU rate probe")
+    ap.add_argument("--profile-pass", action="store_true",
+                    help="short run for counter collection: a 512 MiB copy (the byte-counter "
+                         "calibration) then a few steps")
     ap.add_argument("--cpu-seconds", type=float, default=10.0,
                     help="target wall time of the CPU baseline sample")
     return ap.parse_args()
@@ -49,12 +63,12 @@ def parse():
 
 def ensure_built():
     from paper_2011_09398_amd import build as lb
-    if not os.path.exists(lb.LIB):
+    if not (os.path.exists(lb.LIB) and os.path.exists(lb.PROBE_LIB)):
         lb.build()
 
 
 class Step:
-    """Device buffers and prepared calls for one config's layers."""
+    """Device buffers and prepared calls for one configuration's layers."""
 
     def __init__(self, cfg_idx: int):
         import numpy as np
@@ -65,17 +79,17 @@ class Step:
         self.layers = config(cfg_idx)
         self.inputs = [make_layer_inputs(l, 0, cfg_idx, i) for i, l in enumerate(self.layers)]
         dev = lambda a: torch.from_numpy(np.ascontiguousarray(a)).cuda()
-        self.calls, self.outs, self.keep = [], [], []
-        self.x_float = None
-        self.pack_call = None
+        self.calls, self.packs, self.outs, self.keep = [], [], [], []
         for i, (layer, inp) in enumerate(zip(self.layers, self.inputs)):
             w_packed = lce.bitpack(dev(inp.w_float))          # 1-bit weight storage
+            pack = None
             if layer.chained_from is not None:
                 x_packed = self.outs[layer.chained_from]
             elif inp.x_float is not None:
                 xf = dev(inp.x_float)
-                x_packed = lce.bitpack(xf)
-                self.x_float = (xf, x_packed)
+                x_packed = torch.empty(xf.shape[:-1] + (layer.cw,), dtype=torch.int32,
+                                       device="cuda")
+                pack = lce.PreparedBitpack(xf, x_packed)
             else:
                 x_packed = dev(inp.x_words.view(np.int32))
             oh, ow = layer.out_hw()
@@ -90,56 +104,73 @@ class Step:
             self.calls.append(lce.PreparedBConv2d(
                 x_packed, w_packed, layer.c_in, out, stride=layer.strides,
                 padding=layer.padding, clamp=layer.clamp, out_type=layer.out, **kw))
+            self.packs.append(pack)
             self.outs.append(out)
             self.keep.append((w_packed, x_packed, kw))
 
-    def bitpack(self):
-        import paper_2011_09398_amd as lce
-        xf, xp = self.x_float
-        lce.bitpack(xf, out=xp)
-
-
-def time_step(step: Step, steps: int, warmup: int, with_bitpack: bool):
-    """Time `steps` passes; per-launch HIP event durations on the launch stream."""
-    import torch
-    ncalls = len(step.calls) + (1 if with_bitpack else 0)
-
-    def run(evs=None):
-        k = 0
-        if evs is not None:
-            evs[0].record()
-        if with_bitpack:
-            step.bitpack()
-            if evs is not None:
-                evs[1].record()
-            k = 1
-        for i, call in enumerate(step.calls):
+    def run(self):
+        """One pass of the hot path: bitpack any float input, then every conv."""
+        for pack, call in zip(self.packs, self.calls):
+            if pack is not None:
+                pack()
             call()
-            if evs is not None:
-                evs[k + i + 1].record()
 
+
+def time_steps(step: Step, steps: int, warmup: int):
+    import torch
     for _ in range(warmup):
-        run()
+        step.run()
     torch.cuda.synchronize()
-    events = [[torch.cuda.Event(enable_timing=True) for _ in range(ncalls + 1)]
-              for _ in range(steps)]
-    torch.cuda.synchronize()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
     t0 = time.perf_counter()
-    for s in range(steps):
-        run(events[s])
+    e0.record()
+    for _ in range(steps):
+        step.run()
+    e1.record()
     torch.cuda.synchronize()
     wall = time.perf_counter() - t0
-    per_call_ms = [sum(events[s][i].elapsed_time(events[s][i + 1]) for s in range(steps)) / steps
-                   for i in range(ncalls)]
-    return wall, per_call_ms
+    return wall, e0.elapsed_time(e1) * 1e-3
 
 
-def layer_record(layer, ms):
+def time_repeated(fn, reps: int, graph: bool) -> float:
+    """Average duration (ms) of `fn` launched `reps` times back to back."""
+    import torch
+    for _ in range(5):
+        fn()
+    torch.cuda.synchronize()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    if graph:
+        g = torch.cuda.CUDAGraph()
+        s = torch.cuda.Stream()
+        s.wait_stream(torch.cuda.current_stream())
+        with torch.cuda.stream(s):
+            with torch.cuda.graph(g, stream=s):
+                for _ in range(reps):
+                    fn()
+        torch.cuda.current_stream().wait_stream(s)
+        g.replay()
+        torch.cuda.synchronize()
+        e0.record()
+        g.replay()
+        e1.record()
+    else:
+        e0.record()
+        for _ in range(reps):
+            fn()
+        e1.record()
+    torch.cuda.synchronize()
+    return e0.elapsed_time(e1) / reps
+
+
+def layer_record(layer, ms, probe_tops=None):
     ops = layer.binary_ops
     tops = ops / (ms * 1e-3) / 1e12
-    return {"layer": layer.name, "batch": layer.n, "us": round(ms * 1e3, 3),
-            "binary_gops": round(tops * 1e3, 1),
-            "valu_frac": round(tops / PEAK_BINARY_TOPS, 4), "binary_ops": ops}
+    r = {"layer": layer.name, "batch": layer.n, "us": round(ms * 1e3, 3),
+         "binary_gops": round(tops * 1e3, 1), "valu_frac": round(tops / PEAK_BINARY_TOPS, 4),
+         "binary_ops": ops}
+    if probe_tops:
+        r["probe_frac"] = round(tops / probe_tops, 4)
+    return r
 
 
 def bitpack_record(layer, ms):
@@ -151,9 +182,27 @@ def bitpack_record(layer, ms):
             "hbm_frac": round(gbs / HBM_PEAK_GBS, 4)}
 
 
+def valu_probe():
+    """Achievable xor+popcount rate in binary TOP/s (a pair covers 32 MACs = 64 ops)."""
+    import torch
+    from paper_2011_09398_amd import build as lb
+    L = ctypes.CDLL(lb.PROBE_LIB)
+    L.lce_probe_xor_popcount.argtypes = [ctypes.c_void_p, ctypes.c_void_p, ctypes.c_int,
+                                         ctypes.c_int, ctypes.c_void_p]
+    L.lce_probe_pairs.restype = ctypes.c_longlong
+    L.lce_probe_pairs.argtypes = [ctypes.c_int, ctypes.c_int]
+    blocks, iters = CUS * 8, 2000
+    seed = torch.randint(0, 2 ** 31 - 1, (128,), dtype=torch.int32, device="cuda")
+    out = torch.empty(blocks * 256, dtype=torch.int32, device="cuda")
+    st = torch.cuda.current_stream().cuda_stream
+    fn = lambda: L.lce_probe_xor_popcount(seed.data_ptr(), out.data_ptr(), blocks, iters, st)
+    ms = time_repeated(fn, 5, graph=False)
+    pairs = L.lce_probe_pairs(blocks, iters)   # one v_xor_b32 + one v_bcnt_u32_b32 each
+    return pairs * 2 * BINARY_OPS_PER_LANE_OP / (ms * 1e-3) / 1e12
+
+
 def cpu_baseline(cfg_idx: int, target_s: float):
     """The oracle, as it stands, on a bounded sample of the same step."""
-    import numpy as np
     import oracle
     from workloads import config, make_layer_inputs
 
@@ -192,6 +241,10 @@ def cpu_baseline(cfg_idx: int, target_s: float):
             "cpu": platform.processor() or platform.machine()}
 
 
+def log(msg):
+    print(f"[bench] {msg}", file=sys.stderr, flush=True)
+
+
 def main():
     args = parse()
     if args.gpus != 1:
@@ -204,62 +257,62 @@ def main():
         sys.exit(1)
     ensure_built()
     import paper_2011_09398_amd as lce
+    from workloads import CONFIG_NAMES
     lce.lib()
 
     cfg_idx = 4 if args.workload == "b64" else 5
     step = Step(cfg_idx)
-    with_bp = step.x_float is not None and cfg_idx == 5
-    print(f"[bench] timing config {cfg_idx}: {args.warmup} warmup + {args.steps} steps",
-          file=sys.stderr, flush=True)
-    wall, per_call = time_step(step, args.steps, args.warmup, with_bp)
+    if args.profile_pass:
+        src = torch.ones(128 * 2 ** 20, dtype=torch.float32, device="cuda")   # 512 MiB
+        dst = torch.empty_like(src)
+        for _ in range(3):
+            dst.copy_(src)
+        for _ in range(3):
+            step.run()
+        torch.cuda.synchronize()
+        log("profile pass done: 3 copies of 512 MiB, 3 steps")
+        return
+    log(f"timing config {cfg_idx}: {args.warmup} warmup + {args.steps} steps")
+    wall, ev_s = time_steps(step, args.steps, args.warmup)
     ms_per_step = wall * 1e3 / args.steps
     total_ops = sum(l.binary_ops for l in step.layers)
     value = total_ops / (ms_per_step * 1e-3) / 1e9
 
-    layer_ms = per_call[1:] if with_bp else per_call
-    layers = [layer_record(l, ms) for l, ms in zip(step.layers, layer_ms)]
-    if with_bp:
-        layers.insert(0, bitpack_record(step.layers[0], per_call[0]))
+    probe = None
+    if not args.no_probe:
+        log("VALU xor+popcount probe")
+        probe = valu_probe()
+
+    log(f"per-launch timing, {args.reps} launches each")
+    layers = []
+    for pack, call, layer in zip(step.packs, step.calls, step.layers):
+        if pack is not None:
+            layers.append(bitpack_record(layer, time_repeated(pack, args.reps, graph=False)))
+        layers.append(layer_record(layer, time_repeated(call, args.reps, graph=False), probe))
     conv = [r for r in layers if "binary_ops" in r]
     dom = max(conv, key=lambda r: r["us"])
     roofline = {"bound": "alu", "achieved": round(dom["binary_gops"] / 1e3, 2),
                 "peak": round(PEAK_BINARY_TOPS, 1), "unit": "TOP/s",
                 "frac": dom["valu_frac"], "traffic": None,
                 "kernel": f"bconv2d {dom['layer']} (batch {dom['batch']})",
-                "per_launch_binary_ops": dom["binary_ops"], "avg_launch_us": dom["us"]}
+                "per_launch_binary_ops": dom["binary_ops"], "avg_launch_us": dom["us"],
+                "probe_peak": None if probe is None else round(probe, 1),
+                "probe_frac": dom.get("probe_frac")}
 
     batch1 = None
     if not args.no_batch1:
-        print("[bench] timing batch-1 layers", file=sys.stderr, flush=True)
+        log("batch-1 layers (graph-captured repeats)")
         s1 = Step(3)
-        recs = []
-        import paper_2011_09398_amd as lce  # noqa: F811
-        for i, call in enumerate(s1.calls):
-            layer, inp = s1.layers[i], s1.inputs[i]
-            # bitpack of this layer's float input, then the conv, each timed alone
-            xf = torch.from_numpy(inp.x_float).cuda()
-            xp = call.keep[0]
-            for name, fn in (("bitpack", lambda: lce.bitpack(xf, out=xp)), ("conv", call)):
-                for _ in range(20):
-                    fn()
-                e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-                reps = 200
-                e0.record()
-                for _ in range(reps):
-                    fn()
-                e1.record()
-                torch.cuda.synchronize()
-                ms = e0.elapsed_time(e1) / reps
-                recs.append(bitpack_record(layer, ms) if name == "bitpack"
-                            else layer_record(layer, ms))
-        batch1 = recs
+        batch1 = []
+        for pack, call, layer in zip(s1.packs, s1.calls, s1.layers):
+            batch1.append(bitpack_record(layer, time_repeated(pack, args.reps, graph=True)))
+            batch1.append(layer_record(layer, time_repeated(call, args.reps, graph=True), probe))
 
     cpu = None
     if not args.no_cpu:
-        print("[bench] timing the CPU oracle sample", file=sys.stderr, flush=True)
+        log("CPU oracle sample")
         cpu = cpu_baseline(cfg_idx, args.cpu_seconds)
 
-    from workloads import CONFIG_NAMES
     line = {
         "metric": METRIC, "value": round(value, 1), "unit": "GOPS", "n_gpus": 1,
         "steps": args.steps, "warmup": args.warmup, "ms_per_step": round(ms_per_step, 5),
@@ -270,6 +323,7 @@ def main():
                    "batch": step.layers[0].n,
                    "layers": [l.name for l in step.layers],
                    "binary_ops_per_step": total_ops},
+        "event_ms_per_step": round(ev_s * 1e3 / args.steps, 5),
         "roofline": roofline, "cpu_baseline": cpu, "layers": layers, "batch1": batch1,
         "device": torch.cuda.get_device_name(0),
     }

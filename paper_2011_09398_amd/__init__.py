@@ -177,17 +177,21 @@ def bconv2d(x_packed, w_packed, c_in: int, *, stride: Union[int, Sequence[int]] 
     return out
 
 
+def _current_stream():
+    import torch
+    return torch.cuda.current_stream().cuda_stream
+
+
 class PreparedBConv2d:
     """A bconv2d call with its descriptor and pointers marshalled once.
 
-    Calling it enqueues the convolution on the given stream handle (default:
-    torch's current stream), with no per-call validation in Python; the C ABI
-    still validates.  The tensors must outlive the object.
+    Calling it enqueues the convolution on `stream` (default: torch's current
+    stream at call time, so it can be captured in a graph) with no Python-side
+    validation; the C ABI still validates.  The tensors must outlive it.
     """
 
     def __init__(self, x_packed, w_packed, c_in, out, *, stride=1, padding="same",
                  clamp=None, out_type="float", multiplier=None, bias=None, thresholds=None):
-        import torch
         # one eager call validates shapes/dtypes and fills `out`
         bconv2d(x_packed, w_packed, c_in, stride=stride, padding=padding, clamp=clamp,
                 out_type=out_type, multiplier=multiplier, bias=bias, thresholds=thresholds,
@@ -201,10 +205,25 @@ class PreparedBConv2d:
         self.args = (x_packed.data_ptr(), w_packed.data_ptr(), ptr(multiplier), ptr(bias),
                      ptr(thresholds), out.data_ptr())
         self.keep = (x_packed, w_packed, multiplier, bias, thresholds, out)
-        self.stream = torch.cuda.current_stream(x_packed.device).cuda_stream
         self._fn = lib().lce_bconv2d
 
     def __call__(self, stream=None):
-        st = self._fn(self._desc_ref, *self.args, self.stream if stream is None else stream)
+        st = self._fn(self._desc_ref, *self.args, _current_stream() if stream is None else stream)
+        if st != LCE_OK:
+            raise LceError(st, last_error())
+
+
+class PreparedBitpack:
+    """A bitpack call marshalled once (see PreparedBConv2d)."""
+
+    def __init__(self, x, out):
+        bitpack(x, out=out)
+        c = x.shape[-1]
+        self.args = (x.data_ptr(), out.data_ptr(), x.numel() // c, c)
+        self.keep = (x, out)
+        self._fn = lib().lce_bitpack
+
+    def __call__(self, stream=None):
+        st = self._fn(*self.args, _current_stream() if stream is None else stream)
         if st != LCE_OK:
             raise LceError(st, last_error())

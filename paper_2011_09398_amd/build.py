@@ -11,6 +11,9 @@ CSRC = os.path.join(PKG, "csrc")
 INCLUDE = os.path.join(ROOT, "include")
 LIB = os.path.join(PKG, "liblce.so")
 SOURCES = [os.path.join(CSRC, "lce.hip")]
+# Measurement-only probe of the xor/popcount VALU rate (not part of the C ABI).
+PROBE_LIB = os.path.join(PKG, "libprobe.so")
+PROBE_SOURCES = [os.path.join(CSRC, "valu_probe.hip")]
 HEADERS = [os.path.join(CSRC, f) for f in ("bitpack.hpp", "bconv.hpp")] + \
           [os.path.join(INCLUDE, "lce.h")]
 
@@ -24,21 +27,26 @@ FLAGS = [
 ]
 
 
-def build(verbose: bool = False, extra=()) -> str:
-    tmp = LIB + f".tmp{os.getpid()}"
-    cmd = [HIPCC, *FLAGS, *extra, "-I", INCLUDE, "-I", CSRC, "-o", tmp, *SOURCES]
+def _compile(sources, lib, verbose, extra=()):
+    tmp = lib + f".tmp{os.getpid()}"
+    cmd = [HIPCC, *FLAGS, *extra, "-I", INCLUDE, "-I", CSRC, "-o", tmp, *sources]
     if verbose:
         print(" ".join(cmd), flush=True)
     subprocess.run(cmd, check=True)
-    os.replace(tmp, LIB)
+    os.replace(tmp, lib)
+
+
+def build(verbose: bool = False, extra=()) -> str:
+    _compile(SOURCES, LIB, verbose, extra)
+    _compile(PROBE_SOURCES, PROBE_LIB, verbose, extra)
     return LIB
 
 
 def is_stale() -> bool:
-    if not os.path.exists(LIB):
+    if not os.path.exists(LIB) or not os.path.exists(PROBE_LIB):
         return True
-    t = os.path.getmtime(LIB)
-    return any(os.path.getmtime(f) > t for f in SOURCES + HEADERS)
+    t = min(os.path.getmtime(LIB), os.path.getmtime(PROBE_LIB))
+    return any(os.path.getmtime(f) > t for f in SOURCES + HEADERS + PROBE_SOURCES)
 
 
 if __name__ == "__main__":

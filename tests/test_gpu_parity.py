@@ -245,3 +245,32 @@ def test_repeated_launches_are_deterministic():
     a = sync_np(gpu_layer(layer, inp, x_packed=xp, w_packed=wp))
     for _ in range(3):
         assert np.array_equal(sync_np(gpu_layer(layer, inp, x_packed=xp, w_packed=wp)), a)
+
+
+def test_graph_replay_matches_eager():
+    """A captured graph of the batch-1 step (bitpack + conv per layer) replays
+    to the eager result every time, with eager work and syncs in between."""
+    import torch
+    import bench
+    step = bench.Step(3)
+    step.run()
+    torch.cuda.synchronize()
+    ref = [o.clone() for o in step.outs]
+    g = torch.cuda.CUDAGraph()
+    s = torch.cuda.Stream()
+    s.wait_stream(torch.cuda.current_stream())
+    with torch.cuda.stream(s):
+        with torch.cuda.graph(g, stream=s):
+            step.run()
+    torch.cuda.current_stream().wait_stream(s)
+    torch.cuda.synchronize()
+    for _ in range(4):
+        for o in step.outs:
+            o.fill_(POISON_I32)
+        torch.cuda.synchronize()
+        g.replay()
+        torch.cuda.synchronize()
+        for o, r in zip(step.outs, ref):
+            assert torch.equal(o, r)
+        step.run()                     # eager work between replays
+        torch.cuda.synchronize()
