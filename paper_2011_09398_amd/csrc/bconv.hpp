@@ -2,20 +2,36 @@
 // as one fused kernel: implicit im2col -> XOR/POPCOUNT GEMM -> output transform.
 //
 // Work decomposition (gfx950, wave64):
-//   * a workgroup is 4 waves and owns 64 consecutive output pixels
-//     m = (n, oy, ox); lane l of every wave computes pixel m0 + l;
-//   * each wave owns RN consecutive filters (wave-uniform), so the packed
-//     filter words are uniform across the wave and live in scalar registers
-//     (s_load), feeding v_xor_b32 as its scalar operand;
-//   * the 64 pixels' im2col rows (KH*KW*Cw words each) are staged in LDS,
-//     padded taps written as 0 words (= +1.0, one-padding), so the hot loop
-//     is only LDS reads plus v_xor_b32 / v_bcnt_u32_b32 (popcount+accumulate);
+//   * a workgroup (4 waves) owns 64 consecutive output pixels m = (n, oy, ox)
+//     and a contiguous range of filters; lane l of every wave computes
+//     pixel m0 + l;
+//   * the 64 pixels' im2col rows (KH*KW*Cw words each) are staged once in LDS,
+//     padded taps written as 0 words (= +1.0, one-padding);
+//   * a wave works on blocks of RN = 8 consecutive filters.  Their packed
+//     words are uniform across the wave, so they live in scalar registers
+//     (s_load) and feed v_xor_b32 as its scalar operand; the hot loop is only
+//     LDS reads plus v_xor_b32 / v_bcnt_u32_b32 (popcount + accumulate);
+//   * the 4 waves split the workgroup's work either over filter blocks
+//     (each wave then walks `nb` blocks, reusing the staged rows) or over
+//     the K range (`ks` = 2 or 4 waves per block, partial sums reduced
+//     through LDS) when there are too few pixel x filter blocks to fill the
+//     chip's 1024 SIMDs evenly;
 //   * the accumulator stays in VGPRs and the output transform is applied
-//     before anything is written (clamp, then fma or threshold compare).
+//     before anything is written.
 //
 // The filter words of a wave are read in the same k order as the im2col row
 // (OHWI filters: k = (ky*KW + kx)*Cw + cw), so the GEMM's k loop is one
 // contiguous walk over both.
+//
+// Output transform, with acc = sum popcount(a XOR w) and dot = K - 2*acc:
+//   int32:     c = clamp(dot, lo, hi)
+//   float32:   fmaf((float)c, multiplier, bias)
+//   bitpacked: bit = c < threshold, evaluated exactly.  For an integer c,
+//              c < t  <=>  c < ceil(t); with the clamp this is constant when
+//              ceil(t) <= lo (never) or ceil(t) > hi (always), and otherwise
+//              dot < ceil(t)  <=>  acc >= floor((K - ceil(t)) / 2) + 1.
+//              Each workgroup turns its thresholds into that bound once
+//              (thr_to_acc_bound), so a bit costs one unsigned compare.
 #pragma once
 
 #include <hip/hip_runtime.h>
@@ -25,10 +41,31 @@ namespace lce {
 
 enum OutKind : int { OUT_FLOAT = 0, OUT_BITS = 1, OUT_INT = 2 };
 
-constexpr int kPix = 64;      // output pixels per workgroup (one per lane)
-constexpr int kWaves = 4;     // waves per workgroup
+constexpr int kPix = 64;          // output pixels per workgroup (one per lane)
+constexpr int kWaves = 4;         // waves per workgroup
 constexpr int kThreads = kPix * kWaves;
-constexpr int kSlabWords = 160;   // max im2col words staged per row at once
+constexpr int kRN = 8;            // filters per block (one output byte when bitpacked)
+constexpr int kKC = 8;            // k words per scalar-load chunk
+constexpr int kMaxNB = 4;         // filter blocks per wave
+constexpr int kMaxFiltersWG = kWaves * kMaxNB * kRN;   // 128
+constexpr int kSlabWords = 160;   // generic kernel: im2col words staged per pass
+
+// Unsigned division n / d for n < 2^31 by multiply-high (Granlund-Montgomery
+// round-up variant): q = (mulhi(n, magic) + n) >> shift.
+struct FastDiv {
+    uint32_t d, magic, shift;
+};
+
+__host__ inline FastDiv make_fastdiv(uint32_t d) {
+    uint32_t l = 0;
+    while ((1ull << l) < d) ++l;                       // l = ceil(log2 d)
+    const uint64_t magic = ((1ull << 32) * ((1ull << l) - d)) / d + 1;
+    return FastDiv{d, (uint32_t)magic, l};
+}
+
+__device__ __forceinline__ uint32_t fast_div(uint32_t n, const FastDiv &f) {
+    return (__umulhi(n, f.magic) + n) >> f.shift;
+}
 
 struct BconvParams {
     const uint32_t *x;      // [N][H][W][Cw]
@@ -44,7 +81,13 @@ struct BconvParams {
     int32_t k;              // KH*KW*C_in, the number of +-1 products
     int32_t lo, hi;         // fused activation bounds
     int32_t m;              // N*OH*OW
-    int32_t ohw;            // OH*OW
+    FastDiv div_ohw;        // m -> image
+    FastDiv div_ow;         // pixel within image -> row
+    int32_t nb;             // filter blocks per wave (ks == 1)
+    int32_t ks;             // waves sharing one block's K range (1, 2 or 4)
+    int32_t fwg;            // filters per workgroup = (4 / ks) * nb * RN
+    int32_t ksplit;         // K words per split (multiple of 4), ks > 1
+    int32_t out_vec4;       // out is 16-byte aligned (float output may use float4 stores)
     int32_t slab;           // generic kernel: words staged per pass
     int32_t rs;             // generic kernel: LDS row stride (words)
 };
@@ -54,6 +97,21 @@ struct BconvParams {
 // neighbouring lanes start in different bank groups.
 __host__ __device__ constexpr int row_stride(int words) {
     return ((words + 3) / 4) % 2 == 1 ? (words + 3) / 4 * 4 : (words + 3) / 4 * 4 + 4;
+}
+
+// Read-only tensors (packed filters) are read through the constant address
+// space: the kernel never writes them, so a wave-uniform read there is always
+// a scalar load (s_load), even after the epilogue has stored output.
+typedef const __attribute__((address_space(4))) uint32_t *const_u32_ptr;
+
+typedef const __attribute__((address_space(4))) float *const_f32_ptr;
+
+__device__ __forceinline__ const_u32_ptr as_const(const uint32_t *p) {
+    return (const_u32_ptr)p;
+}
+
+__device__ __forceinline__ const_f32_ptr as_const(const float *p) {
+    return (const_f32_ptr)p;
 }
 
 template <int N>
@@ -66,7 +124,7 @@ __device__ __forceinline__ void lds_read(uint32_t (&a)[N], const uint32_t *p) {
     }
 }
 
-// acc += popcount(a XOR w) as one v_bcnt_u32_b32 (popcount plus accumulate).
+// acc += popcount(x) as one v_bcnt_u32_b32 (popcount plus accumulate).
 // The empty asm pins the running sum to a register after every step, so the
 // compiler cannot re-associate a chunk's popcounts into an add tree (which
 // costs an extra v_add3 per two words).
@@ -76,13 +134,14 @@ __device__ __forceinline__ void bcnt_acc(uint32_t &acc, uint32_t x) {
 }
 
 // acc[f] += sum_k popcount(a_k XOR w[f][k]) over `nwords` words starting at
-// word 0 of `arow` (LDS) and of each filter row `wrow + f*kwords` (global,
-// wave-uniform).  FULL: all RN filters exist; otherwise filters past `nvalid`
-// re-read the last valid row (results unused) so no load leaves the tensor.
+// word 0 of `arow` (LDS, 16-byte aligned) and of each filter row
+// `wrow + f*kwords` (global, wave-uniform).  FULL: all RN filters exist;
+// otherwise filters past `nvalid` re-read the last valid row (results
+// unused) so no load leaves the tensor.
 template <int RN, int KC, bool FULL>
 __device__ __forceinline__ void xor_popcount(uint32_t (&acc)[RN], const uint32_t *arow,
-                                             const uint32_t *__restrict__ wrow, int kwords,
-                                             int nwords, int nvalid) {
+                                             const_u32_ptr wrow, int kwords, int nwords,
+                                             int nvalid) {
     int k = 0;
     for (; k + KC <= nwords; k += KC) {
         uint32_t a[KC];
@@ -95,6 +154,19 @@ __device__ __forceinline__ void xor_popcount(uint32_t (&acc)[RN], const uint32_t
                 bcnt_acc(acc[f], a[j] ^ wrow[(size_t)fo * kwords + k + j]);
             }
         }
+    }
+    if (k + 4 <= nwords) {
+        uint32_t a[4];
+        lds_read<4>(a, arow + k);
+#pragma unroll
+        for (int j = 0; j < 4; ++j) {
+#pragma unroll
+            for (int f = 0; f < RN; ++f) {
+                const int fo = FULL ? f : min(f, nvalid - 1);
+                bcnt_acc(acc[f], a[j] ^ wrow[(size_t)fo * kwords + k + j]);
+            }
+        }
+        k += 4;
     }
     for (; k < nwords; ++k) {
         const uint32_t a0 = arow[k];
@@ -120,85 +192,185 @@ template <> struct VecOf<1> {
     __device__ static uint32_t zero() { return 0u; }
 };
 
+// The bound b such that the output bit of a filter is (acc >= b); see the
+// header comment.  0 = always 1, 0xFFFFFFFF = always 0 (acc < 2^31).
+__device__ inline uint32_t thr_to_acc_bound(float thr, int k, int lo, int hi) {
+    const double t = (double)thr;
+    if (t != t) return 0xFFFFFFFFu;                          // NaN: c < NaN is false
+    const double tc = ceil(t);
+    if (tc <= (double)lo) return 0xFFFFFFFFu;               // c >= lo >= ceil(t)
+    if (tc > (double)hi) return 0u;                          // c <= hi < ceil(t)
+    const int64_t T = (int64_t)tc;                           // lo < T <= hi: int32 range
+    const int64_t diff = (int64_t)k - T;
+    const int64_t b = (diff >= 0 ? diff / 2 : -((-diff + 1) / 2)) + 1;   // floor(diff/2)+1
+    if (b <= 0) return 0u;
+    if (b >= 0xFFFFFFFFll) return 0xFFFFFFFFu;
+    return (uint32_t)b;
+}
+
+// Workgroup prologue for bitpacked output: bounds of filters
+// [co_wg, co_wg + n) into `bound` (LDS).  Filters past cout get "never".
+__device__ __forceinline__ void load_bounds(const BconvParams &p, int co_wg, int n,
+                                            uint32_t *bound) {
+    for (int t = threadIdx.x; t < n; t += kThreads) {
+        const int co = co_wg + t;
+        bound[t] = co < p.cout ? thr_to_acc_bound(p.thr[co], p.k, p.lo, p.hi) : 0xFFFFFFFFu;
+    }
+}
+
 // Output transform of one lane's RN accumulators (Section 3.2: the fused
 // activation and the per-channel multiplier/bias, or the threshold compare,
-// applied to the accumulator before it is written).
+// applied to the accumulator before it is written).  `bound` is this block's
+// slice of the workgroup's threshold bounds (bitpacked output only).
 template <int RN, int OUT>
 __device__ __forceinline__ void epilogue(const BconvParams &p, const uint32_t (&acc)[RN],
-                                         int m, int co0) {
-    const int nvalid = min(RN, p.cout - co0);   // may be <= 0 for pad-bit waves
+                                         int m, int co0, const uint32_t *bound) {
+    const int nvalid = min(RN, p.cout - co0);   // may be <= 0 for pad-bit blocks
     if constexpr (OUT == OUT_BITS) {
+        uint32_t b[RN];
+        lds_read<RN>(b, bound);                  // broadcast read, same for all lanes
         uint32_t bits = 0;
 #pragma unroll
-        for (int f = 0; f < RN; ++f) {
-            if (f < nvalid) {
-                const int dot = p.k - 2 * (int)acc[f];
-                const int c = min(max(dot, p.lo), p.hi);
-                if ((double)c < (double)p.thr[co0 + f]) bits |= 1u << f;
-            }
-        }
+        for (int f = 0; f < RN; ++f) bits |= (uint32_t)(acc[f] >= b[f]) << f;
         uint8_t *o = reinterpret_cast<uint8_t *>(p.out) + (size_t)m * p.cwo * 4 + co0 / 8;
-        if constexpr (RN == 8) {
-            *o = (uint8_t)bits;
-        } else if constexpr (RN == 16) {
-            *reinterpret_cast<uint16_t *>(o) = (uint16_t)bits;
-        } else {
-            static_assert(RN == 32, "bitpacked output needs 8, 16 or 32 filters per wave");
-            *reinterpret_cast<uint32_t *>(o) = bits;
-        }
+        static_assert(RN == 8, "one output byte per filter block");
+        *o = (uint8_t)bits;
     } else if constexpr (OUT == OUT_FLOAT) {
         float *o = reinterpret_cast<float *>(p.out) + (size_t)m * p.cout + co0;
+        if (nvalid == RN && p.mult && p.bias && (p.cout % 4) == 0 && p.out_vec4) {
+            float y[RN];
 #pragma unroll
-        for (int f = 0; f < RN; ++f) {
-            if (f < nvalid) {
-                const int dot = p.k - 2 * (int)acc[f];
-                const int c = min(max(dot, p.lo), p.hi);
-                const float mu = p.mult ? p.mult[co0 + f] : 1.0f;
-                const float bi = p.bias ? p.bias[co0 + f] : 0.0f;
-                o[f] = __builtin_fmaf((float)c, mu, bi);
+            for (int f = 0; f < RN; ++f) {
+                const int c = min(max(p.k - 2 * (int)acc[f], p.lo), p.hi);
+                y[f] = __builtin_fmaf((float)c, as_const(p.mult)[co0 + f],
+                                      as_const(p.bias)[co0 + f]);
+            }
+#pragma unroll
+            for (int f = 0; f < RN; f += 4)
+                *reinterpret_cast<float4 *>(o + f) = make_float4(y[f], y[f + 1], y[f + 2], y[f + 3]);
+        } else {
+#pragma unroll
+            for (int f = 0; f < RN; ++f) {
+                if (f < nvalid) {
+                    const int c = min(max(p.k - 2 * (int)acc[f], p.lo), p.hi);
+                    const float mu = p.mult ? as_const(p.mult)[co0 + f] : 1.0f;
+                    const float bi = p.bias ? as_const(p.bias)[co0 + f] : 0.0f;
+                    o[f] = __builtin_fmaf((float)c, mu, bi);
+                }
             }
         }
     } else {
         int32_t *o = reinterpret_cast<int32_t *>(p.out) + (size_t)m * p.cout + co0;
 #pragma unroll
-        for (int f = 0; f < RN; ++f) {
-            if (f < nvalid) {
-                const int dot = p.k - 2 * (int)acc[f];
-                o[f] = min(max(dot, p.lo), p.hi);
-            }
+        for (int f = 0; f < RN; ++f)
+            if (f < nvalid) o[f] = min(max(p.k - 2 * (int)acc[f], p.lo), p.hi);
+    }
+}
+
+// Decompose pixel m into (image, oy, ox) and return the image's base word
+// offset plus the window origin.
+__device__ __forceinline__ void pixel_origin(const BconvParams &p, int m, uint32_t &img_off,
+                                             int &iy0, int &ix0, int cw) {
+    const uint32_t img = fast_div((uint32_t)m, p.div_ohw);
+    const uint32_t r = (uint32_t)m - img * p.div_ohw.d;
+    const uint32_t oy = fast_div(r, p.div_ow);
+    const uint32_t ox = r - oy * (uint32_t)p.ow;
+    img_off = img * (uint32_t)(p.h * p.wd * cw);
+    iy0 = (int)oy * p.sh - p.pt;
+    ix0 = (int)ox * p.sw - p.pl;
+}
+
+// Accumulate one filter block over [k_lo, k_hi) of the staged rows.
+// co0, k_lo and k_hi are wave-uniform; readfirstlane states it, so the filter
+// words are always fetched with scalar loads whatever control flow
+// surrounds the call.
+template <int RN, int KC>
+__device__ __forceinline__ void block_gemm(uint32_t (&acc)[RN], const uint32_t *arow,
+                                           const uint32_t *w, int kwords, int co0, int cout,
+                                           int k_lo, int k_hi) {
+#pragma unroll
+    for (int f = 0; f < RN; ++f) acc[f] = 0;
+    co0 = __builtin_amdgcn_readfirstlane(co0);
+    k_lo = __builtin_amdgcn_readfirstlane(k_lo);
+    k_hi = __builtin_amdgcn_readfirstlane(k_hi);
+    if (co0 >= cout) return;
+    const const_u32_ptr wrow = as_const(w) + (size_t)co0 * kwords + k_lo;
+    if (co0 + RN <= cout)
+        xor_popcount<RN, KC, true>(acc, arow + k_lo, wrow, kwords, k_hi - k_lo, RN);
+    else
+        xor_popcount<RN, KC, false>(acc, arow + k_lo, wrow, kwords, k_hi - k_lo, cout - co0);
+}
+
+// The per-workgroup schedule after staging: `nb` blocks per wave (ks == 1),
+// or ks waves per block with an LDS reduction of the partial sums.
+template <int RN, int KC, int OUT>
+__device__ __forceinline__ void compute_and_store(const BconvParams &p, const uint32_t *arow,
+                                                  int kwords, int wave, int lane, int m,
+                                                  int co_wg, const uint32_t *bound,
+                                                  uint32_t *red) {
+    const bool px_ok = m < p.m;
+    const int limit = OUT == OUT_BITS ? p.cwo * 32 : p.cout;
+    if (p.ks == 1) {
+        for (int b = 0; b < p.nb; ++b) {
+            const int fl = (wave * p.nb + b) * RN;
+            const int co0 = co_wg + fl;
+            if (co0 >= limit) break;
+            uint32_t acc[RN];
+            block_gemm<RN, KC>(acc, arow, p.w, kwords, co0, p.cout, 0, kwords);
+            if (px_ok) epilogue<RN, OUT>(p, acc, m, co0, bound + fl);
         }
+        return;
+    }
+    // ks waves per block: wave = group * ks + part
+    const int part = wave % p.ks;
+    const int group = wave / p.ks;
+    const int fl = group * RN;
+    const int co0 = co_wg + fl;
+    const int k_lo = min(part * p.ksplit, kwords);
+    const int k_hi = min(k_lo + p.ksplit, kwords);
+    uint32_t acc[RN];
+    block_gemm<RN, KC>(acc, arow, p.w, kwords, co0, p.cout, k_lo, k_hi);
+    __syncthreads();   // `red` aliases the staged rows: every wave is done reading them
+    if (part != 0) {
+#pragma unroll
+        for (int f = 0; f < RN; ++f) red[(wave * RN + f) * kPix + lane] = acc[f];
+    }
+    __syncthreads();
+    if (part == 0 && co0 < limit) {
+        for (int q = 1; q < p.ks; ++q)
+#pragma unroll
+            for (int f = 0; f < RN; ++f) acc[f] += red[((wave + q) * RN + f) * kPix + lane];
+        if (px_ok) epilogue<RN, OUT>(p, acc, m, co0, bound + fl);
     }
 }
 
 // Shape-specialized kernel: Cw, KH, KW known at compile time, so the whole
 // im2col row fits one LDS slab and the filter-row offsets are immediates.
 // VEC = words per global load when staging (needs x aligned to 4*VEC bytes).
-template <int CW, int KH, int KW, int RN, int KC, int VEC, int OUT>
+template <int CW, int KH, int KW, int VEC, int OUT>
 __global__ __launch_bounds__(kThreads) void bconv2d_static_kernel(BconvParams p) {
     constexpr int kTaps = KH * KW;
     constexpr int kWords = kTaps * CW;
     constexpr int kRS = row_stride(kWords);
-    __shared__ __attribute__((aligned(16))) uint32_t lds[kPix * kRS];
+    constexpr int kRed = kWaves * kRN * kPix;   // K-split partial sums, after the rows
+    __shared__ __attribute__((aligned(16))) uint32_t lds[kPix * kRS > kRed ? kPix * kRS : kRed];
+    __shared__ __attribute__((aligned(16))) uint32_t bound[kMaxFiltersWG];
 
     const int lane = threadIdx.x & 63;
     const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
     const int m = blockIdx.x * kPix + lane;
     const bool px_ok = m < p.m;
+    const int co_wg = blockIdx.y * p.fwg;
 
     // ---- stage the im2col rows: wave w copies taps w, w+4, ... of every pixel.
     // All global loads are issued before any LDS store; a padded tap loads
     // from the image's first pixel (always in bounds) and is replaced by 0.
+    // The threshold bounds are computed while those loads are in flight.
     {
-        int img = 0, oy = 0, ox = 0;
-        if (px_ok) {
-            img = m / p.ohw;
-            const int r = m - img * p.ohw;
-            oy = r / p.ow;
-            ox = r - oy * p.ow;
-        }
-        const int iy0 = oy * p.sh - p.pt;
-        const int ix0 = ox * p.sw - p.pl;
-        const uint32_t *ximg = p.x + (size_t)img * p.h * p.wd * CW;
+        uint32_t img_off = 0;
+        int iy0 = 0, ix0 = 0;
+        if (px_ok) pixel_origin(p, m, img_off, iy0, ix0, CW);
+        const uint32_t *ximg = p.x + img_off;
         constexpr int kIters = (kTaps + kWaves - 1) / kWaves;
         constexpr int kVecs = CW / VEC;
         using Vec = typename VecOf<VEC>::type;
@@ -210,11 +382,12 @@ __global__ __launch_bounds__(kThreads) void bconv2d_static_kernel(BconvParams p)
             const int ky = t / KW, kx = t - (t / KW) * KW;
             const int iy = iy0 + ky, ix = ix0 + kx;
             in[i] = px_ok && (unsigned)iy < (unsigned)p.h && (unsigned)ix < (unsigned)p.wd;
-            const size_t off = in[i] ? ((size_t)iy * p.wd + ix) * CW : 0;
+            const uint32_t off = in[i] ? ((uint32_t)iy * (uint32_t)p.wd + (uint32_t)ix) * CW : 0u;
             const Vec *src = reinterpret_cast<const Vec *>(ximg + off);
 #pragma unroll
             for (int c = 0; c < kVecs; ++c) v[i][c] = src[c];
         }
+        if constexpr (OUT == OUT_BITS) load_bounds(p, co_wg, p.fwg, bound);
         uint32_t *row = lds + lane * kRS;
 #pragma unroll
         for (int i = 0; i < kIters; ++i) {
@@ -227,46 +400,31 @@ __global__ __launch_bounds__(kThreads) void bconv2d_static_kernel(BconvParams p)
         }
     }
     __syncthreads();
-
-    const int co0 = (blockIdx.y * kWaves + wave) * RN;
-    uint32_t acc[RN];
-#pragma unroll
-    for (int f = 0; f < RN; ++f) acc[f] = 0;
-    if (co0 < p.cout) {
-        const uint32_t *arow = lds + lane * kRS;
-        const uint32_t *wrow = p.w + (size_t)co0 * kWords;
-        if (co0 + RN <= p.cout)
-            xor_popcount<RN, KC, true>(acc, arow, wrow, kWords, kWords, RN);
-        else
-            xor_popcount<RN, KC, false>(acc, arow, wrow, kWords, kWords, p.cout - co0);
-    }
-    if (!px_ok) return;
-    if (OUT == OUT_BITS ? co0 >= p.cwo * 32 : co0 >= p.cout) return;
-    epilogue<RN, OUT>(p, acc, m, co0);
+    compute_and_store<kRN, kKC, OUT>(p, lds + lane * kRS, kWords, wave, lane, m, co_wg, bound,
+                                     lds);
 }
 
-// Generic kernel: any Cw/KH/KW.  The im2col row is staged in slabs of
-// p.slab words (k range [k0, k0+slab)), one word per copy.
-template <int RN, int KC, int OUT>
+// Generic kernel: any Cw/KH/KW, one filter block per wave.  The im2col row
+// is staged in slabs of p.slab words (k range [k0, k0+slab)), one word per
+// copy.
+template <int OUT>
 __global__ __launch_bounds__(kThreads) void bconv2d_generic_kernel(BconvParams p) {
+    constexpr int RN = kRN;
     extern __shared__ __attribute__((aligned(16))) uint32_t lds_dyn[];
+    __shared__ __attribute__((aligned(16))) uint32_t bound[kWaves * kRN];
     const int lane = threadIdx.x & 63;
     const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
     const int m = blockIdx.x * kPix + lane;
     const bool px_ok = m < p.m;
-    int img = 0, oy = 0, ox = 0;
-    if (px_ok) {
-        img = m / p.ohw;
-        const int r = m - img * p.ohw;
-        oy = r / p.ow;
-        ox = r - oy * p.ow;
-    }
-    const int iy0 = oy * p.sh - p.pt;
-    const int ix0 = ox * p.sw - p.pl;
-    const uint32_t *ximg = p.x + (size_t)img * p.h * p.wd * p.cw;
+    const int co_wg = blockIdx.y * kWaves * RN;
+    if constexpr (OUT == OUT_BITS) load_bounds(p, co_wg, kWaves * RN, bound);
+    uint32_t img_off = 0;
+    int iy0 = 0, ix0 = 0;
+    if (px_ok) pixel_origin(p, m, img_off, iy0, ix0, p.cw);
+    const uint32_t *ximg = p.x + img_off;
     uint32_t *row = lds_dyn + lane * p.rs;
 
-    const int co0 = (blockIdx.y * kWaves + wave) * RN;
+    const int co0 = co_wg + wave * RN;
     uint32_t acc[RN];
 #pragma unroll
     for (int f = 0; f < RN; ++f) acc[f] = 0;
@@ -281,21 +439,21 @@ __global__ __launch_bounds__(kThreads) void bconv2d_generic_kernel(BconvParams p
             const int ky = tap / p.kw, kx = tap - (tap / p.kw) * p.kw;
             const int iy = iy0 + ky, ix = ix0 + kx;
             const bool in = px_ok && (unsigned)iy < (unsigned)p.h && (unsigned)ix < (unsigned)p.wd;
-            const size_t off = in ? ((size_t)iy * p.wd + ix) * p.cw + c : 0;
+            const uint32_t off = in ? ((uint32_t)iy * (uint32_t)p.wd + (uint32_t)ix) * p.cw + c : 0u;
             row[kk] = in ? ximg[off] : 0u;
         }
         __syncthreads();
         if (co0 < p.cout) {
-            const uint32_t *wrow = p.w + (size_t)co0 * p.kwords + k0;
+            const const_u32_ptr wrow = as_const(p.w) + (size_t)co0 * p.kwords + k0;
             if (co0 + RN <= p.cout)
-                xor_popcount<RN, KC, true>(acc, row, wrow, p.kwords, nw, RN);
+                xor_popcount<RN, kKC, true>(acc, row, wrow, p.kwords, nw, RN);
             else
-                xor_popcount<RN, KC, false>(acc, row, wrow, p.kwords, nw, p.cout - co0);
+                xor_popcount<RN, kKC, false>(acc, row, wrow, p.kwords, nw, p.cout - co0);
         }
     }
     if (!px_ok) return;
     if (OUT == OUT_BITS ? co0 >= p.cwo * 32 : co0 >= p.cout) return;
-    epilogue<RN, OUT>(p, acc, m, co0);
+    epilogue<RN, OUT>(p, acc, m, co0, bound + wave * RN);
 }
 
 }  // namespace lce

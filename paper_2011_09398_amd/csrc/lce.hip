@@ -5,6 +5,7 @@
 
 #include <climits>
 #include <cstdarg>
+#include <cstdlib>
 #include <cstdint>
 #include <cstdio>
 #include <string>
@@ -109,45 +110,72 @@ using lce::BconvParams;
 
 template <int CW, int KH, int KW, int OUT>
 void launch_static(const BconvParams &p, dim3 grid, hipStream_t s, int vec) {
-    constexpr int RN = 8, KC = 8;
     if (vec == 4 && CW % 4 == 0)
-        hipLaunchKernelGGL((lce::bconv2d_static_kernel<CW, KH, KW, RN, KC, (CW % 4 == 0 ? 4 : 1), OUT>),
+        hipLaunchKernelGGL((lce::bconv2d_static_kernel<CW, KH, KW, (CW % 4 == 0 ? 4 : 1), OUT>),
                            grid, dim3(lce::kThreads), 0, s, p);
     else if (vec >= 2 && CW % 2 == 0)
-        hipLaunchKernelGGL((lce::bconv2d_static_kernel<CW, KH, KW, RN, KC, (CW % 2 == 0 ? 2 : 1), OUT>),
+        hipLaunchKernelGGL((lce::bconv2d_static_kernel<CW, KH, KW, (CW % 2 == 0 ? 2 : 1), OUT>),
                            grid, dim3(lce::kThreads), 0, s, p);
     else
-        hipLaunchKernelGGL((lce::bconv2d_static_kernel<CW, KH, KW, RN, KC, 1, OUT>), grid,
+        hipLaunchKernelGGL((lce::bconv2d_static_kernel<CW, KH, KW, 1, OUT>), grid,
                            dim3(lce::kThreads), 0, s, p);
 }
 
 template <int OUT>
 void launch_generic(const BconvParams &p, dim3 grid, hipStream_t s) {
-    constexpr int RN = 8, KC = 8;
     const size_t lds = (size_t)lce::kPix * p.rs * sizeof(uint32_t);
-    hipLaunchKernelGGL((lce::bconv2d_generic_kernel<RN, KC, OUT>), grid, dim3(lce::kThreads), lds,
-                       s, p);
+    hipLaunchKernelGGL((lce::bconv2d_generic_kernel<OUT>), grid, dim3(lce::kThreads), lds, s, p);
 }
 
-// True when a shape-specialized kernel was launched.
-template <int OUT>
-bool dispatch_static(const BconvParams &p, dim3 grid, hipStream_t s, int vec) {
-    if (p.kh == 3 && p.kw == 3) {
-        switch (p.cw) {
-            case 1: launch_static<1, 3, 3, OUT>(p, grid, s, vec); return true;
-            case 2: launch_static<2, 3, 3, OUT>(p, grid, s, vec); return true;
-            case 4: launch_static<4, 3, 3, OUT>(p, grid, s, vec); return true;
-            case 8: launch_static<8, 3, 3, OUT>(p, grid, s, vec); return true;
-            case 16: launch_static<16, 3, 3, OUT>(p, grid, s, vec); return true;
-            default: return false;
-        }
-    }
-    return false;
+bool has_static(int cw, int kh, int kw) {
+    return kh == 3 && kw == 3 && (cw == 1 || cw == 2 || cw == 4 || cw == 8 || cw == 16);
 }
 
 template <int OUT>
 void dispatch(const BconvParams &p, dim3 grid, hipStream_t s, int vec) {
-    if (!dispatch_static<OUT>(p, grid, s, vec)) launch_generic<OUT>(p, grid, s);
+    if (p.kh == 3 && p.kw == 3) {
+        switch (p.cw) {
+            case 1: launch_static<1, 3, 3, OUT>(p, grid, s, vec); return;
+            case 2: launch_static<2, 3, 3, OUT>(p, grid, s, vec); return;
+            case 4: launch_static<4, 3, 3, OUT>(p, grid, s, vec); return;
+            case 8: launch_static<8, 3, 3, OUT>(p, grid, s, vec); return;
+            case 16: launch_static<16, 3, 3, OUT>(p, grid, s, vec); return;
+            default: break;
+        }
+    }
+    launch_generic<OUT>(p, grid, s);
+}
+
+int env_int(const char *name, int fallback) {
+    const char *v = getenv(name);
+    return v && *v ? atoi(v) : fallback;
+}
+
+// Work schedule of the shape-specialized kernel.  A unit is 64 pixels x 8
+// filters x the whole K range, one wave's work at nb = ks = 1.  Measured on
+// MI355X, one unit per wave is best whenever there are >= 4 units per SIMD;
+// with fewer, splitting K over 2 (or, below one unit per SIMD, 4) waves
+// spreads the work over more SIMDs.  Several filter blocks per wave (nb > 1)
+// never paid off on the measured shapes but stays selectable.
+// LCE_BCONV_NB / LCE_BCONV_KS override the choice (tuning only).
+void choose_schedule(BconvParams &p, int filters) {
+    const long pix_blocks = (p.m + lce::kPix - 1) / lce::kPix;
+    const long units = pix_blocks * ((filters + lce::kRN - 1) / lce::kRN);
+    int nb = 1, ks = 1;
+    if (units < 1024 && p.kwords >= 32)
+        ks = 4;
+    else if (units < 4096 && p.kwords >= 16)
+        ks = 2;
+    ks = env_int("LCE_BCONV_KS", ks);
+    nb = env_int("LCE_BCONV_NB", nb);
+    if (ks != 1 && ks != 2 && ks != 4) ks = 1;
+    if (ks > 1) nb = 1;
+    if (nb < 1) nb = 1;
+    if (nb > lce::kMaxNB) nb = lce::kMaxNB;
+    p.ks = ks;
+    p.nb = nb;
+    p.fwg = (lce::kWaves / ks) * nb * lce::kRN;
+    p.ksplit = ((p.kwords + ks - 1) / ks + 3) / 4 * 4;
 }
 
 }  // namespace
@@ -227,15 +255,20 @@ lce_status lce_bconv2d(const lce_bconv2d_desc *desc, const int32_t *x_packed,
     p.k = d.kh * d.kw * d.c_in;
     p.lo = d.clamp_min; p.hi = d.clamp_max;
     p.m = d.n * g.oh * g.ow;
-    p.ohw = g.oh * g.ow;
+    p.out_vec4 = aligned(out, 16) ? 1 : 0;
+    p.div_ohw = lce::make_fastdiv((uint32_t)(g.oh * g.ow));
+    p.div_ow = lce::make_fastdiv((uint32_t)g.ow);
     p.slab = p.kwords < lce::kSlabWords ? p.kwords : lce::kSlabWords;
     p.rs = lce::row_stride(p.slab);
 
-    const int rn = 8;
     const int filters = d.out_type == LCE_OUT_BITPACKED ? p.cwo * 32 : p.cout;
-    const int per_block = rn * lce::kWaves;
+    if (has_static(p.cw, p.kh, p.kw)) {
+        choose_schedule(p, filters);
+    } else {
+        p.nb = 1; p.ks = 1; p.fwg = lce::kWaves * lce::kRN; p.ksplit = p.kwords;
+    }
     dim3 grid((unsigned)((p.m + lce::kPix - 1) / lce::kPix),
-              (unsigned)((filters + per_block - 1) / per_block));
+              (unsigned)((filters + p.fwg - 1) / p.fwg));
     const int vec = aligned(x_packed, 16) ? 4 : aligned(x_packed, 8) ? 2 : 1;
     switch (d.out_type) {
         case LCE_OUT_FLOAT32: dispatch<lce::OUT_FLOAT>(p, grid, stream, vec); break;

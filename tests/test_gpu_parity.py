@@ -274,3 +274,41 @@ def test_graph_replay_matches_eager():
             assert torch.equal(o, r)
         step.run()                     # eager work between replays
         torch.cuda.synchronize()
+
+
+SCHEDULES = [(1, 1), (2, 1), (3, 1), (4, 1), (1, 2), (1, 4)]
+
+
+@pytest.mark.parametrize("nb,ks", SCHEDULES)
+@pytest.mark.parametrize("shape", [
+    # (n, h, w, c_in, c_out, stride, out)
+    (2, 9, 7, 64, 40, 1, "bitpacked"),
+    (3, 8, 8, 128, 72, 2, "float"),
+    (1, 7, 7, 512, 96, 1, "int32"),
+    (2, 5, 6, 256, 130, 1, "bitpacked"),
+    (1, 6, 6, 32, 100, 1, "float"),
+])
+def test_every_schedule_matches_oracle(monkeypatch, nb, ks, shape):
+    """Every work split of the shape-specialized kernel (filter blocks per
+    wave, K split across waves) gives the oracle's result."""
+    n, h, w, c_in, c_out, s, out = shape
+    monkeypatch.setenv("LCE_BCONV_NB", str(nb))
+    monkeypatch.setenv("LCE_BCONV_KS", str(ks))
+    layer = Layer(f"sched{nb}{ks}", n, h, w, c_in, c_out, stride=s, out=out,
+                  clamp=(-50, 60) if out != "bitpacked" else None, input_kind="bits")
+    run_case(layer, make_layer_inputs(layer, nb * 10 + ks, 60, c_out))
+
+
+def test_config4_every_schedule_sampled(monkeypatch):
+    sample = [0, 63]
+    for i, layer in enumerate(config(4)):
+        if layer.chained_from is not None:
+            continue
+        inp = make_layer_inputs(layer, 0, 4, i)
+        xp, wp = gpu_input(inp), gpu_pack_weights(inp)
+        ref = oracle_layer(layer, inp, oracle_signs(inp, sample))
+        for nb, ks in SCHEDULES:
+            monkeypatch.setenv("LCE_BCONV_NB", str(nb))
+            monkeypatch.setenv("LCE_BCONV_KS", str(ks))
+            got = sync_np(gpu_layer(layer, inp, x_packed=xp, w_packed=wp))
+            assert_match(layer, got[sample], ref, f"{layer.name} nb={nb} ks={ks}")
