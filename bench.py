@@ -241,6 +241,22 @@ def cpu_baseline(cfg_idx: int, target_s: float):
             "cpu": platform.processor() or platform.machine()}
 
 
+def measured_traffic(layer_name):
+    """HBM bytes per launch from the committed counter summary, or None when
+    the kernel sources have changed since those counters were taken."""
+    import hashlib
+    path = os.path.join(ROOT, "profiles", "bconv2d_qn-b64_traffic.json")
+    if not os.path.exists(path):
+        return None
+    rec = json.load(open(path))
+    h = hashlib.sha256()
+    for f in rec["kernel_sources"]:
+        h.update(open(os.path.join(ROOT, f), "rb").read())
+    if h.hexdigest() != rec["kernel_sources_sha256"]:
+        return None
+    return rec["per_launch_bytes"].get(layer_name)
+
+
 def log(msg):
     print(f"[bench] {msg}", file=sys.stderr, flush=True)
 
@@ -293,7 +309,8 @@ def main():
     dom = max(conv, key=lambda r: r["us"])
     roofline = {"bound": "alu", "achieved": round(dom["binary_gops"] / 1e3, 2),
                 "peak": round(PEAK_BINARY_TOPS, 1), "unit": "TOP/s",
-                "frac": dom["valu_frac"], "traffic": None,
+                "frac": dom["valu_frac"],
+                "traffic": measured_traffic(dom["layer"]) if cfg_idx == 4 else None,
                 "kernel": f"bconv2d {dom['layer']} (batch {dom['batch']})",
                 "per_launch_binary_ops": dom["binary_ops"], "avg_launch_us": dom["us"],
                 "probe_peak": None if probe is None else round(probe, 1),
