@@ -151,21 +151,55 @@ int env_int(const char *name, int fallback) {
     return v && *v ? atoi(v) : fallback;
 }
 
+// SIMDs of the current device (4 per compute unit), cached per device.
+int device_simds() {
+    static int cache[64];
+    int dev = 0;
+    if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= 64) return 1024;
+    if (cache[dev] == 0) {
+        int cus = 0;
+        if (hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess ||
+            cus <= 0)
+            cus = 256;
+        cache[dev] = 4 * cus;
+    }
+    return cache[dev];
+}
+
 // Work schedule of the shape-specialized kernel.  A unit is 64 pixels x 8
-// filters x the whole K range, one wave's work at nb = ks = 1.  Measured on
-// MI355X, one unit per wave is best whenever there are >= 4 units per SIMD;
-// with fewer, splitting K over 2 (or, below one unit per SIMD, 4) waves
-// spreads the work over more SIMDs.  Several filter blocks per wave (nb > 1)
-// never paid off on the measured shapes but stays selectable.
-// LCE_BCONV_NB / LCE_BCONV_KS override the choice (tuning only).
+// filters x the whole K range.  Each schedule (nb filter blocks per wave, or
+// K split over ks waves) is priced as the VALU instructions on the busiest
+// SIMD: ceil(waves / SIMDs) x instructions per wave, where a wave issues
+// 16 * Kw * nb / ks xor/popcount instructions plus ~105 + Kw/2 for staging
+// and set-up, ~35 per extra block and ~20 for a K-split reduction (counts
+// from the measured instruction mix).  Schedules with fewer than 2 waves per
+// SIMD are only used when nothing else is possible: a lone wave cannot hide
+// its own memory latency.  LCE_BCONV_NB / LCE_BCONV_KS override the choice
+// (tuning only).
 void choose_schedule(BconvParams &p, int filters) {
     const long pix_blocks = (p.m + lce::kPix - 1) / lce::kPix;
     const long units = pix_blocks * ((filters + lce::kRN - 1) / lce::kRN);
+    const long simds = device_simds();
+    static const int kOptions[][2] = {{1, 1}, {2, 1}, {4, 1}, {1, 2}, {1, 4}};
+    // key: occupied schedules first; among them the lowest cost, otherwise
+    // the most waves.
     int nb = 1, ks = 1;
-    if (units < 1024 && p.kwords >= 32)
-        ks = 4;
-    else if (units < 4096 && p.kwords >= 16)
-        ks = 2;
+    bool have = false, best_occupied = false;
+    double best_key = 0;
+    for (const auto &o : kOptions) {
+        const int onb = o[0], oks = o[1];
+        if (oks > 1 && p.kwords < 4 * oks) continue;
+        const long waves = (units * oks + onb - 1) / onb;
+        const long rounds = (waves + simds - 1) / simds;
+        const double per_wave = 16.0 * p.kwords * onb / oks + 105.0 + 0.5 * p.kwords +
+                                35.0 * (onb - 1) + (oks > 1 ? 20.0 : 0.0);
+        const bool occupied = waves >= 2 * simds;
+        const double key = occupied ? (double)rounds * per_wave : -(double)waves;
+        if (!have || (occupied && !best_occupied) ||
+            (occupied == best_occupied && key < best_key)) {
+            have = true; best_occupied = occupied; best_key = key; nb = onb; ks = oks;
+        }
+    }
     ks = env_int("LCE_BCONV_KS", ks);
     nb = env_int("LCE_BCONV_NB", nb);
     if (ks != 1 && ks != 2 && ks != 4) ks = 1;
