@@ -47,6 +47,14 @@ def lib():
         L.oracle_conv_dot.argtypes = [_i8p, _int, _int, _int, _int, _i8p, _int, _int, _int,
                                       _int, _int, _int, _i32p]
         L.oracle_conv_dot.restype = _int
+        L.oracle_conv_dot_padded.argtypes = [_i8p, _int, _int, _int, _int, _i8p, _int, _int,
+                                             _int, _int, _int, _int, _int, _i32p]
+        L.oracle_conv_dot_padded.restype = _int
+        L.oracle_bmaxpool.argtypes = [_i8p, _int, _int, _int, _int, _int, _int, _int, _int,
+                                      _int, _i8p]
+        L.oracle_bmaxpool.restype = _int
+        L.oracle_sign_of_affine.argtypes = [_i32p, _i64, ctypes.c_float, ctypes.c_float,
+                                            np.ctypeslib.ndpointer(np.uint8, flags="C_CONTIGUOUS")]
         L.oracle_clamp.argtypes = [_i32p, _i64, ctypes.c_int32, ctypes.c_int32, _i32p]
         L.oracle_out_float.argtypes = [_i32p, _i64, _int, ctypes.c_void_p, ctypes.c_void_p, _f64p]
         L.oracle_out_bits.argtypes = [_i32p, _i64, _int, _f32p, _u32p]
@@ -97,8 +105,11 @@ def unpack(words: np.ndarray, channels: int) -> np.ndarray:
     return s
 
 
-def conv_dot(a: np.ndarray, w: np.ndarray, stride=1, padding: str = "same") -> np.ndarray:
-    """+-1 cross-correlation with one-padding: int8 NHWC x int8 OHWI -> int32 NHWC."""
+def conv_dot(a: np.ndarray, w: np.ndarray, stride=1, padding: str = "same",
+             pad_value: int = 1) -> np.ndarray:
+    """+-1 cross-correlation: int8 NHWC x int8 OHWI -> int32 NHWC.
+
+    pad_value 1 = one-padding (padded bits read as +1), 0 = zero-padding."""
     a = np.ascontiguousarray(a, dtype=np.int8)
     w = np.ascontiguousarray(w, dtype=np.int8)
     n, h, wd, c = a.shape
@@ -108,8 +119,9 @@ def conv_dot(a: np.ndarray, w: np.ndarray, stride=1, padding: str = "same") -> n
     oh, _ = out_size(h, kh, sh, padding)
     ow, _ = out_size(wd, kw, sw, padding)
     dot = np.empty((n, oh, ow, cout), np.int32)
-    rc = lib().oracle_conv_dot(a.reshape(-1), n, h, wd, c, w.reshape(-1), cout, kh, kw,
-                               sh, sw, 1 if padding == "same" else 0, dot.reshape(-1))
+    rc = lib().oracle_conv_dot_padded(a.reshape(-1), n, h, wd, c, w.reshape(-1), cout, kh, kw,
+                                      sh, sw, 1 if padding == "same" else 0, int(pad_value),
+                                      dot.reshape(-1))
     if rc != 0:
         raise ValueError("shape has no output")
     return dot
@@ -149,16 +161,41 @@ INT32_MIN = -(2 ** 31)
 INT32_MAX = 2 ** 31 - 1
 
 
+def bmaxpool(a: np.ndarray, kh: int, kw: int, stride=1, padding: str = "valid") -> np.ndarray:
+    """Max pooling of +-1 int8 NHWC values (padded locations ignored)."""
+    a = np.ascontiguousarray(a, dtype=np.int8)
+    n, h, wd, c = a.shape
+    sh, sw = (stride, stride) if np.isscalar(stride) else stride
+    oh, _ = out_size(h, kh, sh, padding)
+    ow, _ = out_size(wd, kw, sw, padding)
+    out = np.empty((n, oh, ow, c), np.int8)
+    if lib().oracle_bmaxpool(a.reshape(-1), n, h, wd, c, kh, kw, sh, sw,
+                             1 if padding == "same" else 0, out.reshape(-1)) != 0:
+        raise ValueError("shape has no output")
+    return out
+
+
+def sign_of_affine(c: np.ndarray, mult: float, bias: float) -> np.ndarray:
+    """1 where fmaf(float(c), mult, bias) < 0, else 0 (exact sign)."""
+    c = np.ascontiguousarray(c, dtype=np.int32)
+    bits = np.empty(c.shape, np.uint8)
+    lib().oracle_sign_of_affine(c.reshape(-1), c.size, float(np.float32(mult)),
+                                float(np.float32(bias)), bits.reshape(-1))
+    return bits
+
+
 def bconv2d(a: np.ndarray, w: np.ndarray, *, stride=1, padding="same",
             clamp_range=(INT32_MIN, INT32_MAX), out="float",
-            mult=None, bias=None, thr=None) -> np.ndarray:
+            mult=None, bias=None, thr=None, pad_value=1, flip=None) -> np.ndarray:
     """The whole operator on +-1 activations a (int8 NHWC) and +-1 filters w.
 
     out="int32"     -> clamped accumulator, int32 NHWC
     out="float"     -> fp64 NHWC values of clamp(dot) * mult + bias
-    out="bitpacked" -> uint32 NHWC words (bit 1 iff clamp(dot) < thr)
+    out="bitpacked" -> uint32 NHWC words (bit 1 iff clamp(dot) < thr, XOR flip[co]
+                       when a per-channel 0/1 `flip` is given)
+    pad_value        -> 1 one-padding, 0 zero-padding
     """
-    dot = conv_dot(a, w, stride, padding)
+    dot = conv_dot(a, w, stride, padding, pad_value)
     lo, hi = clamp_range
     c = clamp(dot, lo, hi)
     if out == "int32":
@@ -166,5 +203,12 @@ def bconv2d(a: np.ndarray, w: np.ndarray, *, stride=1, padding="same",
     if out == "float":
         return out_float(c, mult, bias)
     if out == "bitpacked":
-        return out_bits(c, thr)
+        words = out_bits(c, thr)
+        if flip is not None:
+            flip = np.asarray(flip, dtype=np.uint8)
+            cout = c.shape[-1]
+            signs = unpack(words, cout)
+            signs = np.where(flip.astype(bool), -signs, signs).astype(np.int8)
+            words = pack(signs)
+        return words
     raise ValueError(out)

@@ -116,9 +116,24 @@ void oracle_unpack(const uint32_t *words, int64_t rows, int channels, int8_t *s)
  *   dot : int32, NHWC [n][oh][ow][cout]
  * Returns 0, or -1 for a shape with no output.
  */
+int oracle_conv_dot_padded(const int8_t *a, int n, int h, int w, int c,
+                           const int8_t *wt, int cout, int kh, int kw,
+                           int sh, int sw, int same, int pad, int32_t *dot);
+
 int oracle_conv_dot(const int8_t *a, int n, int h, int w, int c,
                     const int8_t *wt, int cout, int kh, int kw,
                     int sh, int sw, int same, int32_t *dot) {
+    return oracle_conv_dot_padded(a, n, h, w, c, wt, cout, kh, kw, sh, sw, same, 1, dot);
+}
+
+/*
+ * The same cross-correlation with an explicit value at padded locations:
+ * pad = 1 is the one-padding above; pad = 0 is TensorFlow's zero-padding,
+ * which LCE also supports at the cost of a correction step (Section 3.2).
+ */
+int oracle_conv_dot_padded(const int8_t *a, int n, int h, int w, int c,
+                           const int8_t *wt, int cout, int kh, int kw,
+                           int sh, int sw, int same, int pad, int32_t *dot) {
     int oh, ow, pt, pl;
     if (oracle_out_size(h, kh, sh, same, &oh, &pt) != 0) return -1;
     if (oracle_out_size(w, kw, sw, same, &ow, &pl) != 0) return -1;
@@ -139,7 +154,7 @@ int oracle_conv_dot(const int8_t *a, int n, int h, int w, int c,
                         const int8_t *arow =
                             inside ? a + (((int64_t)b * h + iy) * w + ix) * c : NULL;
                         for (int ci = 0; ci < c; ++ci) {
-                            int32_t av = inside ? arow[ci] : 1;
+                            int32_t av = inside ? arow[ci] : pad;
                             acc += av * (int32_t)wrow[ci];
                         }
                     }
@@ -191,5 +206,50 @@ void oracle_out_bits(const int32_t *c, int64_t m, int cout, const float *thr, ui
             if ((double)c[i * cout + co] < (double)thr[co])
                 words[i * cw + co / 32] |= (uint32_t)1 << (co % 32);
         }
+    }
+}
+
+/*
+ * Binarized max pooling (LceBMaxPool2d, Section 3.2): the maximum of +-1
+ * values over each window, i.e. +1 if any value in the window is +1.
+ * Locations outside the image do not take part (TensorFlow max pooling).
+ *   a   : int8 +-1, NHWC [n][h][w][c]
+ *   out : int8 +-1, NHWC [n][oh][ow][c]
+ * Returns 0, or -1 for a shape with no output.
+ */
+int oracle_bmaxpool(const int8_t *a, int n, int h, int w, int c, int kh, int kw,
+                    int sh, int sw, int same, int8_t *out) {
+    int oh, ow, pt, pl;
+    if (oracle_out_size(h, kh, sh, same, &oh, &pt) != 0) return -1;
+    if (oracle_out_size(w, kw, sw, same, &ow, &pl) != 0) return -1;
+    for (int b = 0; b < n; ++b)
+        for (int oy = 0; oy < oh; ++oy)
+            for (int ox = 0; ox < ow; ++ox)
+                for (int ci = 0; ci < c; ++ci) {
+                    int best = -2;   /* below both values: no valid location seen yet */
+                    for (int ky = 0; ky < kh; ++ky)
+                        for (int kx = 0; kx < kw; ++kx) {
+                            int iy = oy * sh - pt + ky, ix = ox * sw - pl + kx;
+                            if (iy < 0 || iy >= h || ix < 0 || ix >= w) continue;
+                            int v = a[(((int64_t)b * h + iy) * w + ix) * c + ci];
+                            if (v > best) best = v;
+                        }
+                    out[(((int64_t)b * oh + oy) * ow + ox) * c + ci] = (int8_t)best;
+                }
+    return 0;
+}
+
+/*
+ * The next layer's binarization of a float-output transform (Section 3.1):
+ * bit(c) = 1 iff fmaf((float)c, mult, bias) < 0.  For integer c and float
+ * mult, bias, the exact value c*mult + bias is a multiple of 2^-149, so it is
+ * never rounded to -0.0 and its sign decides; c*mult is exact in fp64 for
+ * |c| < 2^24 and fp64 rounding of the sum keeps a nonzero sign.
+ */
+void oracle_sign_of_affine(const int32_t *c, int64_t count, float mult, float bias,
+                           uint8_t *bits) {
+    for (int64_t i = 0; i < count; ++i) {
+        double x = (double)c[i] * (double)mult + (double)bias;
+        bits[i] = (uint8_t)(x < 0.0);
     }
 }

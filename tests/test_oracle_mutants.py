@@ -19,7 +19,14 @@ MUTANTS = {
     "bit_order_msb_first": ("word |= (uint32_t)1 << b;", "word |= (uint32_t)1 << (31 - b);"),
     "unpack_polarity": ("s[r * channels + c] = bit ? (int8_t)-1 : (int8_t)1;",
                         "s[r * channels + c] = bit ? (int8_t)1 : (int8_t)-1;"),
-    "zero_padding": ("int32_t av = inside ? arow[ci] : 1;", "int32_t av = inside ? arow[ci] : 0;"),
+    "zero_padding": ("int32_t av = inside ? arow[ci] : pad;", "int32_t av = inside ? arow[ci] : 0;"),
+    "pad_value_ignored": ("int32_t av = inside ? arow[ci] : pad;", "int32_t av = inside ? arow[ci] : 1;"),
+    "maxpool_takes_min": ("if (v > best) best = v;", "if (best == -2 || v < best) best = v;"),
+    "maxpool_counts_padding": ("if (iy < 0 || iy >= h || ix < 0 || ix >= w) continue;",
+                               "if (iy < 0 || iy >= h || ix < 0 || ix >= w) { best = 1; continue; }"),
+    "affine_sign_le": ("bits[i] = (uint8_t)(x < 0.0);", "bits[i] = (uint8_t)(x <= 0.0);"),
+    "affine_in_float": ("double x = (double)c[i] * (double)mult + (double)bias;",
+                        "double x = (double)((float)c[i] * mult + bias);"),
     "same_pad_leading_heavy": ("*pad_before = total / 2;", "*pad_before = (total + 1) / 2;"),
     "ix_uses_ky": ("int ix = ox * sw - pl + kx;", "int ix = ox * sw - pl + ky;"),
     "iy_plus_pad": ("int iy = oy * sh - pt + ky;", "int iy = oy * sh + pt + ky;"),

@@ -371,3 +371,111 @@ def test_bconv2d_composite_against_torch():
     y = oracle.bconv2d(a, w, out="float", mult=m, bias=b, clamp_range=(-100, 50))
     ref = np.clip(brute_torch(a, w, 1, 1, "same"), -100, 50) * m.astype(np.float64) + b
     np.testing.assert_allclose(y, ref, rtol=1e-15, atol=1e-12)
+
+
+# ---------------------------------------------------------------- zero padding (Section 3.2)
+
+def brute_torch_zero(a, w, sh, sw, padding):
+    """torch's float64 cross-correlation on explicitly zero-padded input."""
+    import torch
+    import torch.nn.functional as F
+    n, h, wd, c = a.shape
+    cout, kh, kw, _ = w.shape
+    x = torch.from_numpy(a.astype(np.float64)).permute(0, 3, 1, 2)
+    if padding == "same":
+        oh, ow = -(-h // sh), -(-wd // sw)
+        ph = max((oh - 1) * sh + kh - h, 0)
+        pw = max((ow - 1) * sw + kw - wd, 0)
+        x = F.pad(x, (pw // 2, pw - pw // 2, ph // 2, ph - ph // 2), value=0.0)
+    wt = torch.from_numpy(w.astype(np.float64)).permute(0, 3, 1, 2)
+    return F.conv2d(x, wt, stride=(sh, sw)).permute(0, 2, 3, 1).numpy()
+
+
+@pytest.mark.parametrize("shape", TINY)
+def test_zero_padding_against_torch(shape):
+    n, h, wd, c, cout, kh, kw, sh, sw, padding = shape
+    a = rand_signs((n, h, wd, c))
+    w = rand_signs((cout, kh, kw, c))
+    dot = oracle.conv_dot(a, w, (sh, sw), padding, pad_value=0)
+    assert np.array_equal(dot, brute_torch_zero(a, w, sh, sw, padding).astype(np.int64))
+
+
+def test_zero_padding_hand_example():
+    g = golden("e2_one_padding.json")
+    a = np.full(g["input_shape"], g["input_value"], np.int8)
+    w = np.full(g["filter_shape"], g["filter_value"], np.int8)
+    dot = oracle.conv_dot(a, w, g["stride"], g["padding"], pad_value=0)
+    assert (dot == g["dot_if_zero_padded"]).all()
+
+
+@pytest.mark.parametrize("h,w_,k,s", [(5, 6, 3, 1), (7, 7, 3, 2), (6, 5, 5, 1), (1, 1, 3, 1)])
+def test_zero_padding_is_one_padding_minus_padded_tap_sums(h, w_, k, s):
+    # The correction step: a padded tap contributes its filter tap's sum of
+    # weights under one-padding and nothing under zero-padding.
+    a = rand_signs((2, h, w_, 40))
+    w = rand_signs((3, k, k, 40))
+    one = oracle.conv_dot(a, w, s, "same", pad_value=1)
+    zero = oracle.conv_dot(a, w, s, "same", pad_value=0)
+    oh, pt = oracle.out_size(h, k, s, "same")
+    ow, pl = oracle.out_size(w_, k, s, "same")
+    tapsum = w.astype(np.int64).sum(axis=3)                      # [cout, k, k]
+    for oy, ox in product(range(oh), range(ow)):
+        corr = np.zeros(3, np.int64)
+        for ky, kx in product(range(k), range(k)):
+            iy, ix = oy * s - pt + ky, ox * s - pl + kx
+            if not (0 <= iy < h and 0 <= ix < w_):
+                corr += tapsum[:, ky, kx]
+        assert np.array_equal(zero[:, oy, ox], one[:, oy, ox] - corr)
+
+
+# ---------------------------------------------------------------- binarized max pooling (Section 3.2)
+
+@pytest.mark.parametrize("h,w_,k,s,padding", [(6, 6, 2, 2, "valid"), (7, 5, 3, 2, "same"),
+                                              (5, 5, 3, 1, "same"), (4, 7, 3, 3, "valid"),
+                                              (1, 1, 3, 2, "same")])
+def test_bmaxpool_commutes_with_sign(h, w_, k, s, padding):
+    # max(sign(X)) = sign(max(X)): binarizing before max pooling gives the
+    # same bits as binarizing after it (torch's float max pooling).
+    import torch
+    import torch.nn.functional as F
+    rng = np.random.default_rng(h * 100 + k)
+    x = rng.standard_normal((2, h, w_, 37)).astype(np.float32)
+    got = oracle.bmaxpool(oracle.binarize(x), k, k, s, padding)
+    t = torch.from_numpy(x).permute(0, 3, 1, 2)
+    if padding == "same":
+        oh, ow = -(-h // s), -(-w_ // s)
+        ph = max((oh - 1) * s + k - h, 0)
+        pw = max((ow - 1) * s + k - w_, 0)
+        t = F.pad(t, (pw // 2, pw - pw // 2, ph // 2, ph - ph // 2), value=float("-inf"))
+    ref = F.max_pool2d(t, k, s).permute(0, 2, 3, 1).numpy()
+    assert np.array_equal(got, oracle.binarize(ref))
+
+
+def test_bmaxpool_is_and_of_bits():
+    # In bitpacked form the pooled bit is the AND of the window's bits
+    # (a 1 bit, -1.0, survives only if every value is -1).
+    a = rand_signs((1, 4, 4, 64))
+    got = oracle.pack(oracle.bmaxpool(a, 2, 2, 2, "valid"))
+    words = oracle.pack(a)
+    ref = words[:, 0::2, 0::2] & words[:, 1::2, 0::2] & words[:, 0::2, 1::2] & words[:, 1::2, 1::2]
+    assert np.array_equal(got, ref)
+
+
+# ---------------------------------------------------------------- sign of the float transform (Section 3.1)
+
+def test_sign_of_affine_exact():
+    rng = np.random.default_rng(11)
+    c = np.arange(-600, 601, dtype=np.int32)
+    cases = [(1.0, 0.0), (1.0, -0.5), (-0.75, 3.0), (0.0, -1.0), (0.0, 1.0), (-0.0, 0.0),
+             (3.0, -6.0), (0.1, 0.3),
+             # near-cancelling: exact c*m + b is a hair below 0 where a float
+             # evaluation rounds it to 0 (e.g. c = 3: -7.45e-9)
+             (0.1, -0.3), (0.7, -2.1), (1.1, -3.3), (-0.3, 0.9)] + [
+             (float(np.float32(m)), float(np.float32(b)))
+                                         for m, b in rng.normal(0, 1, (20, 2))]
+    for m, b in cases:
+        m32, b32 = np.float32(m), np.float32(b)
+        bits = oracle.sign_of_affine(c, m32, b32)
+        ref = [1 if Fraction(int(ci)) * Fraction(float(m32)) + Fraction(float(b32)) < 0 else 0
+               for ci in c]
+        assert bits.tolist() == ref, (m, b)
