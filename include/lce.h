@@ -9,13 +9,15 @@
  *                 channel c goes to 32-bit word c/32, bit c%32; the channel
  *                 count is padded up to a multiple of 32 with 0 bits.
  *   2. im2col over the bitpacked NHWC tensor, padded locations read as
- *      0 bits, i.e. +1.0 ("one-padding").
+ *      0 bits, i.e. +1.0 ("one-padding"), or, on request, as 0.0
+ *      (TensorFlow's zero padding, through a correction step).
  *   3. XOR + POPCOUNT GEMM against bitpacked +-1 filters:
  *          dot = K - 2 * sum_k popcount(a_k XOR w_k),  K = KH*KW*C_in.
  *   4. fused output transform on the integer accumulator:
  *          c = min(max(dot, clamp_min), clamp_max)   (fused activation)
  *          float32 output:   y = fmaf((float)c, multiplier[co], bias[co])
- *          bitpacked output: bit = 1 iff c < thresholds[co] (exact compare)
+ *          bitpacked output: bit = 1 iff c < thresholds[co] (exact compare),
+ *                            optionally inverted per channel
  *
  * Conventions shared by every entry point:
  *   - All tensor pointers are DEVICE pointers owned by the caller.  The
@@ -55,8 +57,10 @@ typedef enum {
 typedef enum { LCE_PADDING_VALID = 0, LCE_PADDING_SAME = 1 } lce_padding;
 
 /* Value read at padded locations.  ONE (0 bits, +1.0) is the one-padding of
- * Section 3.2.  ZERO (TensorFlow's default, which needs a correction step)
- * is rejected with LCE_EUNSUPPORTED. */
+ * Section 3.2, the fast path.  ZERO is TensorFlow's zero padding, which the
+ * same section supports through a correction step: the padded taps are
+ * computed as +1.0 and their filter sums are taken out again, using the
+ * table of lce_bconv2d_pad_correction. */
 typedef enum { LCE_PAD_ONE = 0, LCE_PAD_ZERO = 1 } lce_pad_value;
 
 /* Output of lce_bconv2d:
@@ -107,16 +111,63 @@ lce_status lce_bitpack(const float *x, int32_t *out, int64_t rows, int32_t chann
  *   multiplier float [C_out] or NULL (= 1.0)   used by FLOAT32 output only
  *   bias       float [C_out] or NULL (= 0.0)   used by FLOAT32 output only
  *   thresholds float [C_out], required by BITPACKED output only
+ *   flip       int32 [ceil(C_out/32)] or NULL, used by BITPACKED output
+ *              only: output bits of the channels whose bit is set here are
+ *              inverted (bit = NOT(c < thresholds[co])), the direction that
+ *              lce_fold_thresholds derives from a negative multiplier.  Bits
+ *              past C_out are ignored.
+ *   pad_correction int32 table from lce_bconv2d_pad_correction for these
+ *              filters; required when pad_value is ZERO and some window
+ *              reaches outside the image (SAME with a nonzero total padding),
+ *              ignored (may be NULL) otherwise
  *   out        see lce_out_type; shape from lce_bconv2d_out_shape
  * Dilation and groups are not part of the operator (always 1).
  * All pointers must be 4-byte aligned.
  * Errors: LCE_EINVAL (null desc or required pointer, bad field, no output,
- *         c_out > 2^20, a tensor of 2^31 or more words/elements),
- *         LCE_EUNSUPPORTED (pad_value ZERO), LCE_EALIGN, LCE_EHIP. */
+ *         c_out > 2^20, a tensor of 2^31 or more words/elements; with zero
+ *         padding also K >= 2^29), LCE_EALIGN, LCE_EHIP. */
 lce_status lce_bconv2d(const lce_bconv2d_desc *desc,
                        const int32_t *x_packed, const int32_t *w_packed,
                        const float *multiplier, const float *bias,
-                       const float *thresholds, void *out, hipStream_t stream);
+                       const float *thresholds, const int32_t *flip,
+                       const int32_t *pad_correction, void *out, hipStream_t stream);
+
+/* Number of int32 elements of the zero-padding correction table of `desc`:
+ * (KH+1)*(KW+1)*C_out.  Validates the descriptor as lce_bconv2d does.
+ * Errors: LCE_EINVAL (null desc/elements, bad field). */
+lce_status lce_bconv2d_pad_correction_size(const lce_bconv2d_desc *desc, int64_t *elements);
+
+/* The correction step of zero padding (Section 3.2), prepared once per
+ * filter tensor: with S(co, ky, kx) the sum of the +-1 weights of one tap,
+ *   pad_correction[(y*(KW+1) + x)*C_out + co] = sum over ky < y, kx < x of
+ *                                               S(co, ky, kx),
+ * the summed-area table from which lce_bconv2d takes the sum of any window's
+ * padded taps.  w_packed as for lce_bconv2d (device, 4-byte aligned);
+ * pad_correction: device int32 array of lce_bconv2d_pad_correction_size
+ * elements, written asynchronously on `stream`.
+ * Errors: LCE_EINVAL (null pointer, bad field, table of 2^31 or more
+ *         elements), LCE_EALIGN, LCE_EHIP. */
+lce_status lce_bconv2d_pad_correction(const lce_bconv2d_desc *desc, const int32_t *w_packed,
+                                      int32_t *pad_correction, hipStream_t stream);
+
+/* Converter-side threshold derivation (Sections 3.1 and 3.2: a binary
+ * convolution whose float output only feeds the next layer's binarization
+ * can write bits instead, compared against thresholds computed ahead of
+ * time).  For each channel it returns thresholds[co] and flip bit co such
+ * that, for every clamped accumulator c a convolution with K = k and
+ * [clamp_min, clamp_max] can produce,
+ *     (c < thresholds[co]) XOR flip[co]  ==  fmaf((float)c, m[co], b[co]) < 0,
+ * i.e. lce_bconv2d's bitpacked output with (thresholds, flip) equals
+ * lce_bitpack of its float output with (multiplier, bias).  A negative
+ * multiplier sets the flip bit; a zero one gives a constant (+-infinity).
+ * HOST pointers: multiplier, bias float [c_out] or NULL (= 1.0 / 0.0);
+ * thresholds float [c_out] and flip int32 [ceil(c_out/32)] written (pad
+ * bits 0).  Synchronous, no GPU work.
+ * Errors: LCE_EINVAL (null output, c_out < 1, k outside [1, 2^24],
+ *         clamp_min > clamp_max, a non-finite multiplier or bias). */
+lce_status lce_fold_thresholds(const float *multiplier, const float *bias, int32_t c_out,
+                               int32_t k, int32_t clamp_min, int32_t clamp_max,
+                               float *thresholds, int32_t *flip);
 
 /* Message describing the last error on the calling thread ("" if none). */
 const char *lce_last_error(void);

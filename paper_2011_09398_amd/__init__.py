@@ -6,6 +6,8 @@ If the library is not built this module raises; there is no CPU fallback.
 
     bitpack(x)                        LceQuantize: float [..., C] -> int32 [..., ceil(C/32)]
     bconv2d(x_packed, w_packed, c_in) LceBConv2d with the fused output transform
+    pad_correction(w_packed, c_in)    zero-padding correction table of a filter tensor
+    fold_thresholds(m, b, k, clamp)   float transform + binarization -> thresholds, flip
 """
 from __future__ import annotations
 
@@ -26,7 +28,8 @@ INT32_MAX = 2 ** 31 - 1
 
 # Every symbol include/lce.h declares.
 EXPORTS = ("lce_packed_words", "lce_bconv2d_out_shape", "lce_bitpack", "lce_bconv2d",
-           "lce_last_error")
+           "lce_bconv2d_pad_correction_size", "lce_bconv2d_pad_correction",
+           "lce_fold_thresholds", "lce_last_error")
 
 
 class Desc(ctypes.Structure):
@@ -60,8 +63,15 @@ def lib() -> ctypes.CDLL:
         L.lce_bconv2d_out_shape.restype = ctypes.c_int
         L.lce_bitpack.argtypes = [vp, vp, i64, i32, vp]
         L.lce_bitpack.restype = ctypes.c_int
-        L.lce_bconv2d.argtypes = [ctypes.POINTER(Desc), vp, vp, vp, vp, vp, vp, vp]
+        L.lce_bconv2d.argtypes = [ctypes.POINTER(Desc), vp, vp, vp, vp, vp, vp, vp, vp, vp]
         L.lce_bconv2d.restype = ctypes.c_int
+        L.lce_bconv2d_pad_correction_size.argtypes = [ctypes.POINTER(Desc),
+                                                       ctypes.POINTER(i64)]
+        L.lce_bconv2d_pad_correction_size.restype = ctypes.c_int
+        L.lce_bconv2d_pad_correction.argtypes = [ctypes.POINTER(Desc), vp, vp, vp]
+        L.lce_bconv2d_pad_correction.restype = ctypes.c_int
+        L.lce_fold_thresholds.argtypes = [vp, vp, i32, i32, i32, i32, vp, vp]
+        L.lce_fold_thresholds.restype = ctypes.c_int
         L.lce_last_error.argtypes = []
         L.lce_last_error.restype = ctypes.c_char_p
         _lib = L
@@ -131,14 +141,74 @@ def bitpack(x, out=None):
     return out
 
 
+def _filter_desc(w_packed, c_in, padding="same", pad_value="zero", stride=1) -> Desc:
+    """A descriptor for filter-only calls (the input dims do not matter)."""
+    cout, kh, kw, _ = w_packed.shape
+    return make_desc(1, kh, kw, c_in, cout, kh, kw, stride, padding, pad_value, None, "int32")
+
+
+def pad_correction_size(desc: Desc) -> int:
+    n = ctypes.c_int64()
+    _check(lib().lce_bconv2d_pad_correction_size(ctypes.byref(desc), ctypes.byref(n)))
+    return n.value
+
+
+def pad_correction(w_packed, c_in: int, out=None):
+    """Zero-padding correction table of w_packed: int32 [(KH+1)*(KW+1), Cout]."""
+    import torch
+    _require(w_packed, torch.int32, "w_packed")
+    cout, kh, kw, cw = w_packed.shape
+    if cw != packed_words(c_in):
+        raise ValueError(f"packed channel words {cw} do not match c_in={c_in}")
+    desc = _filter_desc(w_packed, c_in)
+    size = pad_correction_size(desc)
+    if out is None:
+        out = torch.empty(((kh + 1) * (kw + 1), cout), dtype=torch.int32, device=w_packed.device)
+    else:
+        _require(out, torch.int32, "out")
+        if out.numel() != size:
+            raise ValueError(f"out must hold {size} elements")
+    _check(lib().lce_bconv2d_pad_correction(ctypes.byref(desc), w_packed.data_ptr(),
+                                            out.data_ptr(), _stream_handle(w_packed)))
+    return out
+
+
+def fold_thresholds(multiplier, bias, c_out: int, k: int,
+                    clamp: Optional[Tuple[int, int]] = None):
+    """Host-side fold of (multiplier, bias) into (thresholds float32 [c_out],
+    flip int32 [ceil(c_out/32)]), both numpy arrays.  multiplier/bias: array-likes
+    of c_out floats, or None for 1 / 0."""
+    import numpy as np
+    lo, hi = (INT32_MIN, INT32_MAX) if clamp is None else clamp
+    arrs = []
+    for a, name in ((multiplier, "multiplier"), (bias, "bias")):
+        if a is None:
+            arrs.append(None)
+        else:
+            a = np.ascontiguousarray(a, dtype=np.float32)
+            if a.size != c_out:
+                raise ValueError(f"{name} must have {c_out} elements")
+            arrs.append(a)
+    thr = np.empty(c_out, dtype=np.float32)
+    flip = np.empty(max(packed_words(c_out), 0), dtype=np.int32)
+    ptr = lambda a: None if a is None else a.ctypes.data
+    _check(lib().lce_fold_thresholds(ptr(arrs[0]), ptr(arrs[1]), int(c_out), int(k), int(lo),
+                                     int(hi), thr.ctypes.data, flip.ctypes.data))
+    return thr, flip
+
+
 def bconv2d(x_packed, w_packed, c_in: int, *, stride: Union[int, Sequence[int]] = 1,
             padding: str = "same", pad_value: str = "one",
             clamp: Optional[Tuple[int, int]] = None, out_type: str = "float",
-            multiplier=None, bias=None, thresholds=None, out=None):
+            multiplier=None, bias=None, thresholds=None, flip=None, pad_correction=None,
+            out=None):
     """LceBConv2d: x_packed int32 [N,H,W,Cw], w_packed int32 [Cout,KH,KW,Cw].
 
     out_type "float" -> float32 [N,OH,OW,Cout]; "bitpacked" -> int32
     [N,OH,OW,ceil(Cout/32)]; "int32" -> the clamped accumulator [N,OH,OW,Cout].
+    flip: int32 [ceil(Cout/32)] direction bits (bitpacked output).
+    pad_correction: the table of pad_correction(w_packed, c_in), needed by
+    pad_value "zero" when the geometry pads.
     """
     import torch
     _require(x_packed, torch.int32, "x_packed")
@@ -150,13 +220,18 @@ def bconv2d(x_packed, w_packed, c_in: int, *, stride: Union[int, Sequence[int]] 
     desc = make_desc(n, h, w, c_in, cout, kh, kw, stride, padding, pad_value, clamp, out_type)
     oh, ow = out_shape(desc)
     ptrs = []
-    for t, name in ((multiplier, "multiplier"), (bias, "bias"), (thresholds, "thresholds")):
+    for t, name, dtype, numel in ((multiplier, "multiplier", torch.float32, cout),
+                                  (bias, "bias", torch.float32, cout),
+                                  (thresholds, "thresholds", torch.float32, cout),
+                                  (flip, "flip", torch.int32, packed_words(cout)),
+                                  (pad_correction, "pad_correction", torch.int32,
+                                   (kh + 1) * (kw + 1) * cout)):
         if t is None:
             ptrs.append(None)
         else:
-            _require(t, torch.float32, name)
-            if t.numel() != cout:
-                raise ValueError(f"{name} must have {cout} elements")
+            _require(t, dtype, name)
+            if t.numel() != numel:
+                raise ValueError(f"{name} must have {numel} elements")
             ptrs.append(t.data_ptr())
     oc = packed_words(cout) if out_type == "bitpacked" else cout
     if out is not None:
@@ -172,8 +247,7 @@ def bconv2d(x_packed, w_packed, c_in: int, *, stride: Union[int, Sequence[int]] 
         else:
             out = torch.empty((n, oh, ow, cout), dtype=torch.int32, device=x_packed.device)
     _check(lib().lce_bconv2d(ctypes.byref(desc), x_packed.data_ptr(), w_packed.data_ptr(),
-                             ptrs[0], ptrs[1], ptrs[2], out.data_ptr(),
-                             _stream_handle(x_packed)))
+                             *ptrs, out.data_ptr(), _stream_handle(x_packed)))
     return out
 
 
@@ -191,20 +265,21 @@ class PreparedBConv2d:
     """
 
     def __init__(self, x_packed, w_packed, c_in, out, *, stride=1, padding="same",
-                 clamp=None, out_type="float", multiplier=None, bias=None, thresholds=None):
+                 pad_value="one", clamp=None, out_type="float", multiplier=None, bias=None,
+                 thresholds=None, flip=None, pad_correction=None):
         # one eager call validates shapes/dtypes and fills `out`
-        bconv2d(x_packed, w_packed, c_in, stride=stride, padding=padding, clamp=clamp,
-                out_type=out_type, multiplier=multiplier, bias=bias, thresholds=thresholds,
-                out=out)
+        bconv2d(x_packed, w_packed, c_in, stride=stride, padding=padding, pad_value=pad_value,
+                clamp=clamp, out_type=out_type, multiplier=multiplier, bias=bias,
+                thresholds=thresholds, flip=flip, pad_correction=pad_correction, out=out)
         n, h, w, _ = x_packed.shape
         cout, kh, kw, _ = w_packed.shape
-        self.desc = make_desc(n, h, w, c_in, cout, kh, kw, stride, padding, "one", clamp,
+        self.desc = make_desc(n, h, w, c_in, cout, kh, kw, stride, padding, pad_value, clamp,
                               out_type)
         self._desc_ref = ctypes.byref(self.desc)
         ptr = lambda t: None if t is None else t.data_ptr()
         self.args = (x_packed.data_ptr(), w_packed.data_ptr(), ptr(multiplier), ptr(bias),
-                     ptr(thresholds), out.data_ptr())
-        self.keep = (x_packed, w_packed, multiplier, bias, thresholds, out)
+                     ptr(thresholds), ptr(flip), ptr(pad_correction), out.data_ptr())
+        self.keep = (x_packed, w_packed, multiplier, bias, thresholds, flip, pad_correction, out)
         self._fn = lib().lce_bconv2d
 
     def __call__(self, stream=None):

@@ -32,10 +32,24 @@
 //              dot < ceil(t)  <=>  acc >= floor((K - ceil(t)) / 2) + 1.
 //              Each workgroup turns its thresholds into that bound once
 //              (thr_to_acc_bound), so a bit costs one unsigned compare.
+//              An optional per-channel flip mask then inverts chosen bits
+//              (the direction of a threshold folded from a negative
+//              multiplier).
+//
+// Zero padding (TensorFlow's padding value, Section 3.2 notes it needs a
+// correction): padded taps are still staged as 0 words, so the XOR/POPCOUNT
+// sum is the one-padded one, and the taps outside the image are taken out
+// afterwards.  With S(co, ky, kx) = sum_ci W(co, ky, kx, ci) and the window's
+// in-image taps forming the rectangle [y0, y1) x [x0, x1),
+//     dot_zero = dot_one - sum_{padded taps} S = (K - Total) - 2*acc + In,
+// Total = sum of S over all taps and In = sum of S over the rectangle.  In
+// comes from a summed-area table of S per filter (four reads per filter),
+// computed once per filter tensor by pad_table_kernel.
 #pragma once
 
 #include <hip/hip_runtime.h>
 #include <stdint.h>
+#include <climits>
 
 namespace lce {
 
@@ -49,6 +63,8 @@ constexpr int kKC = 8;            // k words per scalar-load chunk
 constexpr int kMaxNB = 4;         // filter blocks per wave
 constexpr int kMaxFiltersWG = kWaves * kMaxNB * kRN;   // 128
 constexpr int kSlabWords = 160;   // generic kernel: im2col words staged per pass
+constexpr int kNever = INT32_MAX;   // zero-padding bound that no accumulator reaches
+constexpr int kAlways = INT32_MIN;  // zero-padding bound that every accumulator reaches
 
 // Unsigned division n / d for n < 2^31 by multiply-high (Granlund-Montgomery
 // round-up variant): q = (mulhi(n, magic) + n) >> shift.
@@ -90,6 +106,8 @@ struct BconvParams {
     int32_t out_vec4;       // out is 16-byte aligned (float output may use float4 stores)
     int32_t slab;           // generic kernel: words staged per pass
     int32_t rs;             // generic kernel: LDS row stride (words)
+    const uint32_t *flip;   // [Cwo] or null: output bits to invert (bitpacked output)
+    const int32_t *padc;    // zero padding: summed-area table [(KH+1)*(KW+1)][Cout]
 };
 
 // LDS row stride for a row of `words` words: a multiple of 4 (16-byte rows
@@ -208,62 +226,171 @@ __device__ inline uint32_t thr_to_acc_bound(float thr, int k, int lo, int hi) {
     return (uint32_t)b;
 }
 
-// Workgroup prologue for bitpacked output: bounds of filters
-// [co_wg, co_wg + n) into `bound` (LDS).  Filters past cout get "never".
+// Zero padding, bitpacked output: with dot_zero = kt - 2*acc + In (kt = K -
+// Total) and T = ceil(thr) inside (lo, hi], the bit is
+//     dot_zero < T  <=>  2*acc - In >= kt - T + 1,
+// and a constant outside.  The left side lies in [-K, 3K] (K < 2^29), so
+// saturating the bound to kNever / kAlways keeps the compare exact.
+__device__ inline int32_t thr_to_padz_bound(float thr, int kt, int lo, int hi) {
+    const double t = (double)thr;
+    if (t != t) return kNever;
+    const double tc = ceil(t);
+    if (tc <= (double)lo) return kNever;
+    if (tc > (double)hi) return kAlways;
+    const int64_t b = (int64_t)kt - (int64_t)tc + 1;
+    if (b >= (int64_t)kNever) return kNever;
+    if (b <= (int64_t)kAlways) return kAlways;
+    return (int32_t)b;
+}
+
+// Workgroup prologue: the per-filter value the epilogue needs, for filters
+// [co_wg, co_wg + n), into `bound` (LDS):
+//   one padding, bitpacked output:   the accumulator bound (thr_to_acc_bound);
+//   zero padding, bitpacked output:  the bound on 2*acc - In (thr_to_padz_bound);
+//   zero padding, other outputs:     kt = K - Total.
+// Filters past cout get "never" (bitpacked) or 0.
+template <int OUT, bool PADZ>
 __device__ __forceinline__ void load_bounds(const BconvParams &p, int co_wg, int n,
                                             uint32_t *bound) {
-    for (int t = threadIdx.x; t < n; t += kThreads) {
-        const int co = co_wg + t;
-        bound[t] = co < p.cout ? thr_to_acc_bound(p.thr[co], p.k, p.lo, p.hi) : 0xFFFFFFFFu;
+    if constexpr (PADZ || OUT == OUT_BITS) {
+        const size_t total_row = (size_t)((p.kh + 1) * (p.kw + 1) - 1) * p.cout;
+        for (int t = threadIdx.x; t < n; t += kThreads) {
+            const int co = co_wg + t;
+            uint32_t v;
+            if constexpr (!PADZ) {
+                v = co < p.cout ? thr_to_acc_bound(p.thr[co], p.k, p.lo, p.hi) : 0xFFFFFFFFu;
+            } else if (co < p.cout) {
+                const int kt = p.k - p.padc[total_row + co];
+                v = OUT == OUT_BITS ? (uint32_t)thr_to_padz_bound(p.thr[co], kt, p.lo, p.hi)
+                                    : (uint32_t)kt;
+            } else {
+                v = OUT == OUT_BITS ? (uint32_t)kNever : 0u;
+            }
+            bound[t] = v;
+        }
+    }
+}
+
+// Zero padding: word offsets of the four summed-area-table corners of one
+// lane's window, whose in-image taps are rows [y0, y1) x columns [x0, x1)
+// (table rows `stride` words apart).
+struct PadWin {
+    int o11, o01, o10, o00;
+};
+
+__device__ __forceinline__ PadWin pad_window(const BconvParams &p, int iy0, int ix0, int stride) {
+    const int y0 = max(0, -iy0), y1 = max(y0, min(p.kh, p.h - iy0));
+    const int x0 = max(0, -ix0), x1 = max(x0, min(p.kw, p.wd - ix0));
+    const int row = p.kw + 1;
+    return PadWin{(y1 * row + x1) * stride, (y0 * row + x1) * stride, (y1 * row + x0) * stride,
+                  (y0 * row + x0) * stride};
+}
+
+// In = sum of S over one lane's in-image taps, for the RN filters whose table
+// column starts at `sat`.  LDS_TABLE: the workgroup's slice staged in LDS with
+// every column present (0 past cout), read as 16-byte vectors.  Otherwise
+// the table in global memory, where filters past `nvalid` re-read the last
+// valid column.
+template <int RN, bool LDS_TABLE>
+__device__ __forceinline__ void inside_sum(int32_t (&in)[RN], const int32_t *sat,
+                                           const PadWin &w, int nvalid) {
+    if constexpr (LDS_TABLE) {
+        const uint32_t *t = reinterpret_cast<const uint32_t *>(sat);
+        uint32_t a[RN], b[RN], c[RN], d[RN];
+        lds_read<RN>(a, t + w.o11);
+        lds_read<RN>(b, t + w.o01);
+        lds_read<RN>(c, t + w.o10);
+        lds_read<RN>(d, t + w.o00);
+#pragma unroll
+        for (int f = 0; f < RN; ++f) in[f] = (int)a[f] - (int)b[f] - (int)c[f] + (int)d[f];
+    } else {
+#pragma unroll
+        for (int f = 0; f < RN; ++f) {
+            const int fo = min(f, nvalid - 1);
+            in[f] = sat[w.o11 + fo] - sat[w.o01 + fo] - sat[w.o10 + fo] + sat[w.o00 + fo];
+        }
     }
 }
 
 // Output transform of one lane's RN accumulators (Section 3.2: the fused
 // activation and the per-channel multiplier/bias, or the threshold compare,
 // applied to the accumulator before it is written).  `bound` is this block's
-// slice of the workgroup's threshold bounds (bitpacked output only).
-template <int RN, int OUT>
+// slice of the workgroup's per-filter values (load_bounds); `sat` and `pw`
+// locate the zero-padding correction (PADZ only).
+template <int RN, int OUT, bool PADZ, bool LDS_TABLE>
 __device__ __forceinline__ void epilogue(const BconvParams &p, const uint32_t (&acc)[RN],
-                                         int m, int co0, const uint32_t *bound) {
+                                         int m, int co0, const uint32_t *bound,
+                                         const int32_t *sat, const PadWin &pw) {
     const int nvalid = min(RN, p.cout - co0);   // may be <= 0 for pad-bit blocks
+    int32_t in[RN];
+    if constexpr (PADZ) {
+        if (nvalid > 0) {
+            inside_sum<RN, LDS_TABLE>(in, sat, pw, nvalid);
+        } else {
+#pragma unroll
+            for (int f = 0; f < RN; ++f) in[f] = 0;
+        }
+    }
     if constexpr (OUT == OUT_BITS) {
         uint32_t b[RN];
         lds_read<RN>(b, bound);                  // broadcast read, same for all lanes
         uint32_t bits = 0;
 #pragma unroll
-        for (int f = 0; f < RN; ++f) bits |= (uint32_t)(acc[f] >= b[f]) << f;
+        for (int f = 0; f < RN; ++f) {
+            if constexpr (PADZ)
+                bits |= (uint32_t)(2 * (int)acc[f] - in[f] >= (int)b[f]) << f;
+            else
+                bits |= (uint32_t)(acc[f] >= b[f]) << f;
+        }
+        if (p.flip) {
+            const uint32_t word = as_const(p.flip)[co0 >> 5];
+            uint32_t fb = (word >> (co0 & 31)) & 0xFFu;
+            if (nvalid < RN) fb &= nvalid > 0 ? (1u << nvalid) - 1u : 0u;
+            bits ^= fb;
+        }
         uint8_t *o = reinterpret_cast<uint8_t *>(p.out) + (size_t)m * p.cwo * 4 + co0 / 8;
         static_assert(RN == 8, "one output byte per filter block");
         *o = (uint8_t)bits;
-    } else if constexpr (OUT == OUT_FLOAT) {
-        float *o = reinterpret_cast<float *>(p.out) + (size_t)m * p.cout + co0;
-        if (nvalid == RN && p.mult && p.bias && (p.cout % 4) == 0 && p.out_vec4) {
-            float y[RN];
+    } else {
+        int32_t c[RN];
+        if constexpr (PADZ) {
+            uint32_t kt[RN];
+            lds_read<RN>(kt, bound);
 #pragma unroll
-            for (int f = 0; f < RN; ++f) {
-                const int c = min(max(p.k - 2 * (int)acc[f], p.lo), p.hi);
-                y[f] = __builtin_fmaf((float)c, as_const(p.mult)[co0 + f],
-                                      as_const(p.bias)[co0 + f]);
-            }
-#pragma unroll
-            for (int f = 0; f < RN; f += 4)
-                *reinterpret_cast<float4 *>(o + f) = make_float4(y[f], y[f + 1], y[f + 2], y[f + 3]);
+            for (int f = 0; f < RN; ++f)
+                c[f] = min(max((int)kt[f] - 2 * (int)acc[f] + in[f], p.lo), p.hi);
         } else {
 #pragma unroll
-            for (int f = 0; f < RN; ++f) {
-                if (f < nvalid) {
-                    const int c = min(max(p.k - 2 * (int)acc[f], p.lo), p.hi);
-                    const float mu = p.mult ? as_const(p.mult)[co0 + f] : 1.0f;
-                    const float bi = p.bias ? as_const(p.bias)[co0 + f] : 0.0f;
-                    o[f] = __builtin_fmaf((float)c, mu, bi);
+            for (int f = 0; f < RN; ++f) c[f] = min(max(p.k - 2 * (int)acc[f], p.lo), p.hi);
+        }
+        if constexpr (OUT == OUT_FLOAT) {
+            float *o = reinterpret_cast<float *>(p.out) + (size_t)m * p.cout + co0;
+            if (nvalid == RN && p.mult && p.bias && (p.cout % 4) == 0 && p.out_vec4) {
+                float y[RN];
+#pragma unroll
+                for (int f = 0; f < RN; ++f)
+                    y[f] = __builtin_fmaf((float)c[f], as_const(p.mult)[co0 + f],
+                                          as_const(p.bias)[co0 + f]);
+#pragma unroll
+                for (int f = 0; f < RN; f += 4)
+                    *reinterpret_cast<float4 *>(o + f) =
+                        make_float4(y[f], y[f + 1], y[f + 2], y[f + 3]);
+            } else {
+#pragma unroll
+                for (int f = 0; f < RN; ++f) {
+                    if (f < nvalid) {
+                        const float mu = p.mult ? as_const(p.mult)[co0 + f] : 1.0f;
+                        const float bi = p.bias ? as_const(p.bias)[co0 + f] : 0.0f;
+                        o[f] = __builtin_fmaf((float)c[f], mu, bi);
+                    }
                 }
             }
-        }
-    } else {
-        int32_t *o = reinterpret_cast<int32_t *>(p.out) + (size_t)m * p.cout + co0;
+        } else {
+            int32_t *o = reinterpret_cast<int32_t *>(p.out) + (size_t)m * p.cout + co0;
 #pragma unroll
-        for (int f = 0; f < RN; ++f)
-            if (f < nvalid) o[f] = min(max(p.k - 2 * (int)acc[f], p.lo), p.hi);
+            for (int f = 0; f < RN; ++f)
+                if (f < nvalid) o[f] = c[f];
+        }
     }
 }
 
@@ -303,10 +430,13 @@ __device__ __forceinline__ void block_gemm(uint32_t (&acc)[RN], const uint32_t *
 
 // The per-workgroup schedule after staging: `nb` blocks per wave (ks == 1),
 // or ks waves per block with an LDS reduction of the partial sums.
-template <int RN, int KC, int OUT>
+// Block fl (first filter co_wg + fl) finds its epilogue values at bound + fl
+// and its correction-table column at sat + fl.
+template <int RN, int KC, int OUT, bool PADZ, bool LDS_TABLE>
 __device__ __forceinline__ void compute_and_store(const BconvParams &p, const uint32_t *arow,
                                                   int kwords, int wave, int lane, int m,
                                                   int co_wg, const uint32_t *bound,
+                                                  const int32_t *sat, const PadWin &pw,
                                                   uint32_t *red) {
     const bool px_ok = m < p.m;
     const int limit = OUT == OUT_BITS ? p.cwo * 32 : p.cout;
@@ -317,7 +447,7 @@ __device__ __forceinline__ void compute_and_store(const BconvParams &p, const ui
             if (co0 >= limit) break;
             uint32_t acc[RN];
             block_gemm<RN, KC>(acc, arow, p.w, kwords, co0, p.cout, 0, kwords);
-            if (px_ok) epilogue<RN, OUT>(p, acc, m, co0, bound + fl);
+            if (px_ok) epilogue<RN, OUT, PADZ, LDS_TABLE>(p, acc, m, co0, bound + fl, sat + fl, pw);
         }
         return;
     }
@@ -340,36 +470,42 @@ __device__ __forceinline__ void compute_and_store(const BconvParams &p, const ui
         for (int q = 1; q < p.ks; ++q)
 #pragma unroll
             for (int f = 0; f < RN; ++f) acc[f] += red[((wave + q) * RN + f) * kPix + lane];
-        if (px_ok) epilogue<RN, OUT>(p, acc, m, co0, bound + fl);
+        if (px_ok) epilogue<RN, OUT, PADZ, LDS_TABLE>(p, acc, m, co0, bound + fl, sat + fl, pw);
     }
 }
 
 // Shape-specialized kernel: Cw, KH, KW known at compile time, so the whole
 // im2col row fits one LDS slab and the filter-row offsets are immediates.
 // VEC = words per global load when staging (needs x aligned to 4*VEC bytes).
-template <int CW, int KH, int KW, int VEC, int OUT>
+// PADZ: zero padding with padded taps; the workgroup's columns of the
+// correction table are staged in LDS next to the rows.
+template <int CW, int KH, int KW, int VEC, int OUT, bool PADZ>
 __global__ __launch_bounds__(kThreads) void bconv2d_static_kernel(BconvParams p) {
     constexpr int kTaps = KH * KW;
     constexpr int kWords = kTaps * CW;
     constexpr int kRS = row_stride(kWords);
     constexpr int kRed = kWaves * kRN * kPix;   // K-split partial sums, after the rows
+    constexpr int kCorners = (KH + 1) * (KW + 1);
+    constexpr int kSat = PADZ ? kCorners * kMaxFiltersWG : 4;
     __shared__ __attribute__((aligned(16))) uint32_t lds[kPix * kRS > kRed ? kPix * kRS : kRed];
     __shared__ __attribute__((aligned(16))) uint32_t bound[kMaxFiltersWG];
+    __shared__ __attribute__((aligned(16))) int32_t sat[kSat];
 
     const int lane = threadIdx.x & 63;
     const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
     const int m = blockIdx.x * kPix + lane;
     const bool px_ok = m < p.m;
     const int co_wg = blockIdx.y * p.fwg;
+    uint32_t img_off = 0;
+    int iy0 = 0, ix0 = 0;
+    if (px_ok) pixel_origin(p, m, img_off, iy0, ix0, CW);
 
     // ---- stage the im2col rows: wave w copies taps w, w+4, ... of every pixel.
     // All global loads are issued before any LDS store; a padded tap loads
     // from the image's first pixel (always in bounds) and is replaced by 0.
-    // The threshold bounds are computed while those loads are in flight.
+    // The per-filter epilogue values (and, for zero padding, the correction
+    // table) are fetched while those loads are in flight.
     {
-        uint32_t img_off = 0;
-        int iy0 = 0, ix0 = 0;
-        if (px_ok) pixel_origin(p, m, img_off, iy0, ix0, CW);
         const uint32_t *ximg = p.x + img_off;
         constexpr int kIters = (kTaps + kWaves - 1) / kWaves;
         constexpr int kVecs = CW / VEC;
@@ -387,7 +523,19 @@ __global__ __launch_bounds__(kThreads) void bconv2d_static_kernel(BconvParams p)
 #pragma unroll
             for (int c = 0; c < kVecs; ++c) v[i][c] = src[c];
         }
-        if constexpr (OUT == OUT_BITS) load_bounds(p, co_wg, p.fwg, bound);
+        load_bounds<OUT, PADZ>(p, co_wg, p.fwg, bound);
+        constexpr int kSatIters = PADZ ? (kSat + kThreads - 1) / kThreads : 1;
+        int32_t sv[kSatIters];
+        if constexpr (PADZ) {
+#pragma unroll
+            for (int i = 0; i < kSatIters; ++i) {
+                const int idx = (int)threadIdx.x + i * kThreads;
+                const int c = idx / kMaxFiltersWG, fl = idx % kMaxFiltersWG;
+                const int co = co_wg + fl;
+                sv[i] = (idx < kSat && fl < p.fwg && co < p.cout)
+                            ? p.padc[(size_t)c * p.cout + co] : 0;
+            }
+        }
         uint32_t *row = lds + lane * kRS;
 #pragma unroll
         for (int i = 0; i < kIters; ++i) {
@@ -398,16 +546,25 @@ __global__ __launch_bounds__(kThreads) void bconv2d_static_kernel(BconvParams p)
                 for (int c = 0; c < kVecs; ++c) dst[c] = in[i] ? v[i][c] : VecOf<VEC>::zero();
             }
         }
+        if constexpr (PADZ) {
+#pragma unroll
+            for (int i = 0; i < kSatIters; ++i) {
+                const int idx = (int)threadIdx.x + i * kThreads;
+                if (idx < kSat) sat[idx] = sv[i];
+            }
+        }
     }
     __syncthreads();
-    compute_and_store<kRN, kKC, OUT>(p, lds + lane * kRS, kWords, wave, lane, m, co_wg, bound,
-                                     lds);
+    PadWin pw{0, 0, 0, 0};
+    if constexpr (PADZ) pw = pad_window(p, iy0, ix0, kMaxFiltersWG);
+    compute_and_store<kRN, kKC, OUT, PADZ, true>(p, lds + lane * kRS, kWords, wave, lane, m,
+                                                 co_wg, bound, sat, pw, lds);
 }
 
 // Generic kernel: any Cw/KH/KW, one filter block per wave.  The im2col row
 // is staged in slabs of p.slab words (k range [k0, k0+slab)), one word per
-// copy.
-template <int OUT>
+// copy.  PADZ reads the correction table from global memory.
+template <int OUT, bool PADZ>
 __global__ __launch_bounds__(kThreads) void bconv2d_generic_kernel(BconvParams p) {
     constexpr int RN = kRN;
     extern __shared__ __attribute__((aligned(16))) uint32_t lds_dyn[];
@@ -417,7 +574,7 @@ __global__ __launch_bounds__(kThreads) void bconv2d_generic_kernel(BconvParams p
     const int m = blockIdx.x * kPix + lane;
     const bool px_ok = m < p.m;
     const int co_wg = blockIdx.y * kWaves * RN;
-    if constexpr (OUT == OUT_BITS) load_bounds(p, co_wg, kWaves * RN, bound);
+    load_bounds<OUT, PADZ>(p, co_wg, kWaves * RN, bound);
     uint32_t img_off = 0;
     int iy0 = 0, ix0 = 0;
     if (px_ok) pixel_origin(p, m, img_off, iy0, ix0, p.cw);
@@ -453,7 +610,35 @@ __global__ __launch_bounds__(kThreads) void bconv2d_generic_kernel(BconvParams p
     }
     if (!px_ok) return;
     if (OUT == OUT_BITS ? co0 >= p.cwo * 32 : co0 >= p.cout) return;
-    epilogue<RN, OUT>(p, acc, m, co0, bound + wave * RN);
+    PadWin pw{0, 0, 0, 0};
+    if constexpr (PADZ) pw = pad_window(p, iy0, ix0, p.cout);
+    epilogue<RN, OUT, PADZ, false>(p, acc, m, co0, bound + wave * RN, p.padc + co0, pw);
+}
+
+// Summed-area table of the per-tap filter sums used by zero padding:
+//   table[(y*(KW+1) + x)*Cout + co] = sum over ky < y, kx < x of S(co, ky, kx),
+//   S(co, ky, kx) = C_in - 2*popcount(W[co][ky][kx][:])  (the sum of the tap's
+//   +-1 weights; pad bits are 0 and count nothing).
+// One thread per filter; a filter tensor needs it once.
+__global__ __launch_bounds__(256) void pad_table_kernel(const uint32_t *__restrict__ w,
+                                                        int32_t *__restrict__ table, int cout,
+                                                        int kh, int kw, int cw, int cin) {
+    const int co = blockIdx.x * blockDim.x + threadIdx.x;
+    if (co >= cout) return;
+    const size_t row = (size_t)kw + 1;
+    for (size_t x = 0; x < row; ++x) table[x * cout + co] = 0;
+    for (int y = 1; y <= kh; ++y) {
+        table[(size_t)y * row * cout + co] = 0;
+        int run = 0;
+        for (int x = 1; x <= kw; ++x) {
+            const uint32_t *wt = w + (((size_t)co * kh + (y - 1)) * kw + (x - 1)) * cw;
+            int pc = 0;
+            for (int j = 0; j < cw; ++j) pc += __builtin_popcount(wt[j]);
+            run += cin - 2 * pc;
+            table[((size_t)y * row + x) * cout + co] =
+                table[((size_t)(y - 1) * row + x) * cout + co] + run;
+        }
+    }
 }
 
 }  // namespace lce

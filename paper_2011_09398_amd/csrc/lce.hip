@@ -3,11 +3,14 @@
 // synchronization: every launch goes on the caller's stream.
 #include <hip/hip_runtime.h>
 
+#include <algorithm>
 #include <climits>
+#include <cmath>
 #include <cstdarg>
 #include <cstdlib>
 #include <cstdint>
 #include <cstdio>
+#include <cstring>
 #include <string>
 
 #include "lce.h"
@@ -43,25 +46,35 @@ bool aligned(const void *p, uintptr_t a) { return (reinterpret_cast<uintptr_t>(p
 
 int packed_words(int channels) { return (channels + 31) / 32; }
 
-// TensorFlow SAME/VALID output size and leading pad of one dimension.
-bool out_dim(int in, int k, int s, int padding, int *out, int *pad_before) {
+// TensorFlow SAME/VALID output size, leading pad and total pad of one
+// dimension.
+bool out_dim(int in, int k, int s, int padding, int *out, int *pad_before, long *pad_total) {
     if (padding == LCE_PADDING_SAME) {
         const int o = in / s + (in % s != 0);
         long total = (long)(o - 1) * s + k - in;
         if (total < 0) total = 0;
         *out = o;
         *pad_before = (int)(total / 2);
+        *pad_total = total;
         return true;
     }
     if (in < k) return false;
     *out = (in - k) / s + 1;
     *pad_before = 0;
+    *pad_total = 0;
     return true;
 }
 
 struct Geometry {
     int oh, ow, pt, pl;
+    bool pads;   // some window reaches outside the image
 };
+
+// Zero padding changes the result only where some window reaches outside
+// the image; there it needs the correction table.
+bool zero_padded(const lce_bconv2d_desc &d, const Geometry &g) {
+    return d.pad_value == LCE_PAD_ZERO && g.pads;
+}
 
 lce_status validate_desc(const lce_bconv2d_desc *d, Geometry *g) {
     if (!d) return fail(LCE_EINVAL, "desc is NULL");
@@ -82,10 +95,12 @@ lce_status validate_desc(const lce_bconv2d_desc *d, Geometry *g) {
         return fail(LCE_EINVAL, "unknown out_type %d", d->out_type);
     if (d->clamp_min > d->clamp_max)
         return fail(LCE_EINVAL, "clamp_min %d > clamp_max %d", d->clamp_min, d->clamp_max);
-    if (!out_dim(d->h, d->kh, d->stride_h, d->padding, &g->oh, &g->pt) ||
-        !out_dim(d->w, d->kw, d->stride_w, d->padding, &g->ow, &g->pl))
+    long th = 0, tw = 0;
+    if (!out_dim(d->h, d->kh, d->stride_h, d->padding, &g->oh, &g->pt, &th) ||
+        !out_dim(d->w, d->kw, d->stride_w, d->padding, &g->ow, &g->pl, &tw))
         return fail(LCE_EINVAL, "VALID convolution with a %dx%d filter has no output on %dx%d",
                     d->kh, d->kw, d->h, d->w);
+    g->pads = th > 0 || tw > 0;
     const int64_t cw = packed_words(d->c_in);
     const int64_t m = (int64_t)d->n * g->oh * g->ow;
     const int64_t x_words = (int64_t)d->n * d->h * d->w * cw;
@@ -101,49 +116,63 @@ lce_status validate_desc(const lce_bconv2d_desc *d, Geometry *g) {
                     (long long)m, (long long)x_words, (long long)w_words, (long long)out_elems,
                     (long long)k);
     if (d->c_out > (1 << 20)) return fail(LCE_EINVAL, "c_out %d exceeds 2^20", d->c_out);
-    if (d->pad_value == LCE_PAD_ZERO)
-        return fail(LCE_EUNSUPPORTED, "zero-padding is not supported (one-padding only)");
+    const int64_t table = (int64_t)(d->kh + 1) * (d->kw + 1) * d->c_out;
+    if (zero_padded(*d, *g) && (k >= (1 << 29) || table > lim))
+        return fail(LCE_EINVAL,
+                    "zero padding needs K < 2^29 and a correction table below 2^31 elements "
+                    "(K %lld, table %lld)", (long long)k, (long long)table);
     return ok();
 }
 
 using lce::BconvParams;
 
-template <int CW, int KH, int KW, int OUT>
+template <int CW, int KH, int KW, int OUT, bool PADZ>
 void launch_static(const BconvParams &p, dim3 grid, hipStream_t s, int vec) {
     if (vec == 4 && CW % 4 == 0)
-        hipLaunchKernelGGL((lce::bconv2d_static_kernel<CW, KH, KW, (CW % 4 == 0 ? 4 : 1), OUT>),
-                           grid, dim3(lce::kThreads), 0, s, p);
+        hipLaunchKernelGGL(
+            (lce::bconv2d_static_kernel<CW, KH, KW, (CW % 4 == 0 ? 4 : 1), OUT, PADZ>), grid,
+            dim3(lce::kThreads), 0, s, p);
     else if (vec >= 2 && CW % 2 == 0)
-        hipLaunchKernelGGL((lce::bconv2d_static_kernel<CW, KH, KW, (CW % 2 == 0 ? 2 : 1), OUT>),
-                           grid, dim3(lce::kThreads), 0, s, p);
+        hipLaunchKernelGGL(
+            (lce::bconv2d_static_kernel<CW, KH, KW, (CW % 2 == 0 ? 2 : 1), OUT, PADZ>), grid,
+            dim3(lce::kThreads), 0, s, p);
     else
-        hipLaunchKernelGGL((lce::bconv2d_static_kernel<CW, KH, KW, 1, OUT>), grid,
+        hipLaunchKernelGGL((lce::bconv2d_static_kernel<CW, KH, KW, 1, OUT, PADZ>), grid,
                            dim3(lce::kThreads), 0, s, p);
 }
 
-template <int OUT>
+template <int OUT, bool PADZ>
 void launch_generic(const BconvParams &p, dim3 grid, hipStream_t s) {
     const size_t lds = (size_t)lce::kPix * p.rs * sizeof(uint32_t);
-    hipLaunchKernelGGL((lce::bconv2d_generic_kernel<OUT>), grid, dim3(lce::kThreads), lds, s, p);
+    hipLaunchKernelGGL((lce::bconv2d_generic_kernel<OUT, PADZ>), grid, dim3(lce::kThreads), lds,
+                       s, p);
 }
 
 bool has_static(int cw, int kh, int kw) {
     return kh == 3 && kw == 3 && (cw == 1 || cw == 2 || cw == 4 || cw == 8 || cw == 16);
 }
 
-template <int OUT>
+template <int OUT, bool PADZ>
 void dispatch(const BconvParams &p, dim3 grid, hipStream_t s, int vec) {
     if (p.kh == 3 && p.kw == 3) {
         switch (p.cw) {
-            case 1: launch_static<1, 3, 3, OUT>(p, grid, s, vec); return;
-            case 2: launch_static<2, 3, 3, OUT>(p, grid, s, vec); return;
-            case 4: launch_static<4, 3, 3, OUT>(p, grid, s, vec); return;
-            case 8: launch_static<8, 3, 3, OUT>(p, grid, s, vec); return;
-            case 16: launch_static<16, 3, 3, OUT>(p, grid, s, vec); return;
+            case 1: launch_static<1, 3, 3, OUT, PADZ>(p, grid, s, vec); return;
+            case 2: launch_static<2, 3, 3, OUT, PADZ>(p, grid, s, vec); return;
+            case 4: launch_static<4, 3, 3, OUT, PADZ>(p, grid, s, vec); return;
+            case 8: launch_static<8, 3, 3, OUT, PADZ>(p, grid, s, vec); return;
+            case 16: launch_static<16, 3, 3, OUT, PADZ>(p, grid, s, vec); return;
             default: break;
         }
     }
-    launch_generic<OUT>(p, grid, s);
+    launch_generic<OUT, PADZ>(p, grid, s);
+}
+
+template <int OUT>
+void dispatch(const BconvParams &p, dim3 grid, hipStream_t s, int vec, bool padz) {
+    if (padz)
+        dispatch<OUT, true>(p, grid, s, vec);
+    else
+        dispatch<OUT, false>(p, grid, s, vec);
 }
 
 int env_int(const char *name, int fallback) {
@@ -262,17 +291,23 @@ lce_status lce_bitpack(const float *x, int32_t *out, int64_t rows, int32_t chann
 
 lce_status lce_bconv2d(const lce_bconv2d_desc *desc, const int32_t *x_packed,
                        const int32_t *w_packed, const float *multiplier, const float *bias,
-                       const float *thresholds, void *out, hipStream_t stream) {
+                       const float *thresholds, const int32_t *flip,
+                       const int32_t *pad_correction, void *out, hipStream_t stream) {
     Geometry g;
     lce_status st = validate_desc(desc, &g);
     if (st != LCE_OK) return st;
     const lce_bconv2d_desc &d = *desc;
+    const bool padz = zero_padded(d, g);
     if (!x_packed || !w_packed || !out) return fail(LCE_EINVAL, "x_packed/w_packed/out is NULL");
     if (d.out_type == LCE_OUT_BITPACKED && !thresholds)
         return fail(LCE_EINVAL, "bitpacked output needs thresholds");
+    if (padz && !pad_correction)
+        return fail(LCE_EINVAL,
+                    "zero padding on a padded geometry needs the pad_correction table");
     if (!aligned(x_packed, 4) || !aligned(w_packed, 4) || !aligned(out, 4) ||
         (multiplier && !aligned(multiplier, 4)) || (bias && !aligned(bias, 4)) ||
-        (thresholds && !aligned(thresholds, 4)))
+        (thresholds && !aligned(thresholds, 4)) || (flip && !aligned(flip, 4)) ||
+        (pad_correction && !aligned(pad_correction, 4)))
         return fail(LCE_EALIGN, "tensor pointers must be 4-byte aligned");
 
     BconvParams p{};
@@ -281,6 +316,8 @@ lce_status lce_bconv2d(const lce_bconv2d_desc *desc, const int32_t *x_packed,
     p.mult = d.out_type == LCE_OUT_FLOAT32 ? multiplier : nullptr;
     p.bias = d.out_type == LCE_OUT_FLOAT32 ? bias : nullptr;
     p.thr = thresholds;
+    p.flip = d.out_type == LCE_OUT_BITPACKED ? reinterpret_cast<const uint32_t *>(flip) : nullptr;
+    p.padc = padz ? pad_correction : nullptr;
     p.out = out;
     p.n = d.n; p.h = d.h; p.wd = d.w; p.cw = packed_words(d.c_in);
     p.oh = g.oh; p.ow = g.ow; p.cout = d.c_out; p.cwo = packed_words(d.c_out);
@@ -305,11 +342,98 @@ lce_status lce_bconv2d(const lce_bconv2d_desc *desc, const int32_t *x_packed,
               (unsigned)((filters + p.fwg - 1) / p.fwg));
     const int vec = aligned(x_packed, 16) ? 4 : aligned(x_packed, 8) ? 2 : 1;
     switch (d.out_type) {
-        case LCE_OUT_FLOAT32: dispatch<lce::OUT_FLOAT>(p, grid, stream, vec); break;
-        case LCE_OUT_BITPACKED: dispatch<lce::OUT_BITS>(p, grid, stream, vec); break;
-        default: dispatch<lce::OUT_INT>(p, grid, stream, vec); break;
+        case LCE_OUT_FLOAT32: dispatch<lce::OUT_FLOAT>(p, grid, stream, vec, padz); break;
+        case LCE_OUT_BITPACKED: dispatch<lce::OUT_BITS>(p, grid, stream, vec, padz); break;
+        default: dispatch<lce::OUT_INT>(p, grid, stream, vec, padz); break;
     }
     return check_launch("lce_bconv2d launch");
+}
+
+lce_status lce_bconv2d_pad_correction_size(const lce_bconv2d_desc *desc, int64_t *elements) {
+    if (!elements) return fail(LCE_EINVAL, "elements output pointer is NULL");
+    Geometry g;
+    lce_status st = validate_desc(desc, &g);
+    if (st != LCE_OK) return st;
+    *elements = (int64_t)(desc->kh + 1) * (desc->kw + 1) * desc->c_out;
+    return ok();
+}
+
+lce_status lce_bconv2d_pad_correction(const lce_bconv2d_desc *desc, const int32_t *w_packed,
+                                      int32_t *pad_correction, hipStream_t stream) {
+    Geometry g;
+    lce_status st = validate_desc(desc, &g);
+    if (st != LCE_OK) return st;
+    const lce_bconv2d_desc &d = *desc;
+    if (!w_packed || !pad_correction) return fail(LCE_EINVAL, "w_packed/pad_correction is NULL");
+    if (!aligned(w_packed, 4) || !aligned(pad_correction, 4))
+        return fail(LCE_EALIGN, "tensor pointers must be 4-byte aligned");
+    const int64_t table = (int64_t)(d.kh + 1) * (d.kw + 1) * d.c_out;
+    if (table > INT32_MAX)
+        return fail(LCE_EINVAL, "correction table of %lld elements exceeds 2^31",
+                    (long long)table);
+    const unsigned blocks = (unsigned)((d.c_out + 255) / 256);
+    hipLaunchKernelGGL(lce::pad_table_kernel, dim3(blocks), dim3(256), 0, stream,
+                       reinterpret_cast<const uint32_t *>(w_packed), pad_correction, d.c_out,
+                       d.kh, d.kw, packed_words(d.c_in), d.c_in);
+    return check_launch("lce_bconv2d_pad_correction launch");
+}
+
+// Converter-side fold of a float output transform followed by the next
+// layer's binarization into a threshold and a direction per channel.  For an
+// integer c, fmaf((float)c, m, b) < 0 exactly when c*m + b < 0 (c*m + b is a
+// multiple of 2^-149, so it neither rounds to zero nor changes sign), and
+// that is evaluated exactly in fp64 for |c| <= 2^24.  It is monotone in c:
+// m > 0 gives "c < T" and m < 0 gives "not (c < T)" for the T found by
+// bisection over the reachable clamped range; m == 0 gives the constant
+// b < 0.
+lce_status lce_fold_thresholds(const float *multiplier, const float *bias, int32_t c_out,
+                               int32_t k, int32_t clamp_min, int32_t clamp_max,
+                               float *thresholds, int32_t *flip) {
+    if (!thresholds || !flip) return fail(LCE_EINVAL, "thresholds/flip is NULL");
+    if (c_out < 1) return fail(LCE_EINVAL, "c_out %d < 1", c_out);
+    if (k < 1 || k > (1 << 24)) return fail(LCE_EINVAL, "k %d outside [1, 2^24]", k);
+    if (clamp_min > clamp_max)
+        return fail(LCE_EINVAL, "clamp_min %d > clamp_max %d", clamp_min, clamp_max);
+    for (int co = 0; co < c_out; ++co) {
+        const float m = multiplier ? multiplier[co] : 1.0f;
+        const float b = bias ? bias[co] : 0.0f;
+        if (!std::isfinite(m) || !std::isfinite(b))
+            return fail(LCE_EINVAL, "channel %d: multiplier %g / bias %g not finite", co,
+                        (double)m, (double)b);
+    }
+    // reachable clamped accumulators: c = min(max(dot, lo), hi), |dot| <= k
+    const int64_t cmin = std::min<int64_t>(std::max<int64_t>(-(int64_t)k, clamp_min), clamp_max);
+    const int64_t cmax = std::min<int64_t>(std::max<int64_t>((int64_t)k, clamp_min), clamp_max);
+    const float kInf = INFINITY;
+    std::memset(flip, 0, sizeof(int32_t) * (size_t)packed_words(c_out));
+    for (int co = 0; co < c_out; ++co) {
+        const double m = multiplier ? (double)multiplier[co] : 1.0;
+        const double b = bias ? (double)bias[co] : 0.0;
+        auto neg = [&](int64_t c) { return (double)c * m + b < 0.0; };
+        float thr;
+        bool inv = false;
+        if (m == 0.0) {
+            thr = b < 0.0 ? kInf : -kInf;
+        } else {
+            // `lo_c` keeps the sign of cmin's side, `hi_c` the other one
+            const bool at_min = neg(cmin), at_max = neg(cmax);
+            if (at_min == at_max) {
+                thr = at_min ? kInf : -kInf;
+            } else {
+                int64_t lo_c = cmin, hi_c = cmax;
+                while (hi_c - lo_c > 1) {
+                    const int64_t mid = lo_c + (hi_c - lo_c) / 2;
+                    (neg(mid) == at_min ? lo_c : hi_c) = mid;
+                }
+                // hi_c is the first c whose sign differs from cmin's
+                thr = (float)hi_c;
+                inv = m < 0.0;   // negative for c >= hi_c: the inverse of c < hi_c
+            }
+        }
+        thresholds[co] = thr;
+        if (inv) flip[co / 32] |= (int32_t)(1u << (co % 32));
+    }
+    return ok();
 }
 
 const char *lce_last_error(void) { return g_last_error.c_str(); }

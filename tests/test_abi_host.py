@@ -95,13 +95,13 @@ def test_out_shape_rejects_bad_field(field, value):
     assert lce.last_error()
 
 
-def call_bconv(d, x=P, w=P, m=None, b=None, t=P, out=P):
-    return lce.lib().lce_bconv2d(ctypes.byref(d), x, w, m, b, t, out, None)
+def call_bconv(d, x=P, w=P, m=None, b=None, t=P, flip=None, corr=None, out=P):
+    return lce.lib().lce_bconv2d(ctypes.byref(d), x, w, m, b, t, flip, corr, out, None)
 
 
 def test_bconv2d_validation_errors():
     L = lce.lib()
-    assert L.lce_bconv2d(None, P, P, None, None, P, P, None) == lce.LCE_EINVAL
+    assert L.lce_bconv2d(None, P, P, None, None, P, None, None, P, None) == lce.LCE_EINVAL
     assert "desc" in lce.last_error()
     assert call_bconv(desc(clamp=(5, 4))) == lce.LCE_EINVAL
     assert "clamp" in lce.last_error()
@@ -111,7 +111,14 @@ def test_bconv2d_validation_errors():
     assert call_bconv(desc(), out=None) == lce.LCE_EINVAL
     assert call_bconv(desc(out_type="bitpacked"), t=None) == lce.LCE_EINVAL
     assert "threshold" in lce.last_error()
-    assert call_bconv(desc(pad_value="zero")) == lce.LCE_EUNSUPPORTED
+    # zero padding on a padded geometry needs the correction table
+    assert call_bconv(desc(pad_value="zero")) == lce.LCE_EINVAL
+    assert "pad_correction" in lce.last_error()
+    assert call_bconv(desc(pad_value="zero"), corr=P + 2) == lce.LCE_EALIGN
+    assert call_bconv(desc(out_type="bitpacked"), flip=P + 1) == lce.LCE_EALIGN
+    # zero padding K limit (2^29): 3x3 x 2^26 input channels
+    assert call_bconv(desc(pad_value="zero", c_in=2 ** 26, c_out=1, h=1, w=1),
+                      corr=P) == lce.LCE_EINVAL
     assert call_bconv(desc(), x=P + 2) == lce.LCE_EALIGN
     assert call_bconv(desc(), out=P + 1) == lce.LCE_EALIGN
     assert call_bconv(desc(), m=P + 3) == lce.LCE_EALIGN
@@ -144,3 +151,39 @@ def test_error_message_is_thread_local():
     th.join()
     assert seen == [""]
     assert lce.last_error() != ""
+
+
+def test_pad_correction_validation_errors():
+    L = lce.lib()
+    n = ctypes.c_int64(-1)
+    assert L.lce_bconv2d_pad_correction_size(ctypes.byref(desc(kh=3, kw=5, c_out=7)),
+                                             ctypes.byref(n)) == lce.LCE_OK
+    assert n.value == 4 * 6 * 7
+    assert L.lce_bconv2d_pad_correction_size(None, ctypes.byref(n)) == lce.LCE_EINVAL
+    assert L.lce_bconv2d_pad_correction_size(ctypes.byref(desc()), None) == lce.LCE_EINVAL
+    assert L.lce_bconv2d_pad_correction(ctypes.byref(desc()), None, P, None) == lce.LCE_EINVAL
+    assert L.lce_bconv2d_pad_correction(ctypes.byref(desc()), P, None, None) == lce.LCE_EINVAL
+    assert L.lce_bconv2d_pad_correction(ctypes.byref(desc()), P + 2, P, None) == lce.LCE_EALIGN
+    assert L.lce_bconv2d_pad_correction(ctypes.byref(desc(c_out=0)), P, P, None) == lce.LCE_EINVAL
+
+
+def test_fold_validation_errors():
+    import numpy as np
+    L = lce.lib()
+    thr = np.zeros(4, np.float32)
+    flip = np.zeros(1, np.int32)
+    T, F = thr.ctypes.data, flip.ctypes.data
+    m = np.ones(4, np.float32)
+    assert L.lce_fold_thresholds(None, None, 4, 9, -9, 9, None, F) == lce.LCE_EINVAL
+    assert L.lce_fold_thresholds(None, None, 4, 9, -9, 9, T, None) == lce.LCE_EINVAL
+    assert L.lce_fold_thresholds(None, None, 0, 9, -9, 9, T, F) == lce.LCE_EINVAL
+    assert L.lce_fold_thresholds(None, None, 4, 0, -9, 9, T, F) == lce.LCE_EINVAL
+    assert L.lce_fold_thresholds(None, None, 4, 2 ** 24 + 1, -9, 9, T, F) == lce.LCE_EINVAL
+    assert L.lce_fold_thresholds(None, None, 4, 9, 9, -9, T, F) == lce.LCE_EINVAL
+    for bad in (np.inf, -np.inf, np.nan):
+        mm = m.copy()
+        mm[2] = bad
+        assert L.lce_fold_thresholds(mm.ctypes.data, None, 4, 9, -9, 9, T, F) == lce.LCE_EINVAL
+        assert "channel 2" in lce.last_error()
+        assert L.lce_fold_thresholds(None, mm.ctypes.data, 4, 9, -9, 9, T, F) == lce.LCE_EINVAL
+    assert L.lce_fold_thresholds(m.ctypes.data, None, 4, 9, -9, 9, T, F) == lce.LCE_OK
