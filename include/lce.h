@@ -133,16 +133,20 @@ lce_status lce_bconv2d(const lce_bconv2d_desc *desc,
                        const int32_t *pad_correction, void *out, hipStream_t stream);
 
 /* Number of int32 elements of the zero-padding correction table of `desc`:
- * (KH+1)*(KW+1)*C_out.  Validates the descriptor as lce_bconv2d does.
+ * (KH+1) * KW*(KW+1)/2 * C_out.  Validates the descriptor as lce_bconv2d
+ * does.
  * Errors: LCE_EINVAL (null desc/elements, bad field). */
 lce_status lce_bconv2d_pad_correction_size(const lce_bconv2d_desc *desc, int64_t *elements);
 
 /* The correction step of zero padding (Section 3.2), prepared once per
- * filter tensor: with S(co, ky, kx) the sum of the +-1 weights of one tap,
- *   pad_correction[(y*(KW+1) + x)*C_out + co] = sum over ky < y, kx < x of
- *                                               S(co, ky, kx),
- * the summed-area table from which lce_bconv2d takes the sum of any window's
- * padded taps.  w_packed as for lce_bconv2d (device, 4-byte aligned);
+ * filter tensor.  With S(co, ky, kx) the sum of the +-1 weights of one tap
+ * and I = [x0, x1) one of the NI = KW*(KW+1)/2 non-empty column intervals
+ * (numbered by x0, then x1: I = x0*(2*KW - x0 + 1)/2 + x1 - x0 - 1),
+ *   pad_correction[(y*NI + I)*C_out + co] = sum over ky < y, kx in I of
+ *                                           S(co, ky, kx),   y in [0, KH].
+ * The in-image taps of any window form rows [y0, y1) x an interval I, so
+ * lce_bconv2d takes their sum as the difference of two entries and removes
+ * the padded taps' share.  w_packed as for lce_bconv2d (device, 4-byte aligned);
  * pad_correction: device int32 array of lce_bconv2d_pad_correction_size
  * elements, written asynchronously on `stream`.
  * Errors: LCE_EINVAL (null pointer, bad field, table of 2^31 or more

@@ -154,7 +154,7 @@ def pad_correction_size(desc: Desc) -> int:
 
 
 def pad_correction(w_packed, c_in: int, out=None):
-    """Zero-padding correction table of w_packed: int32 [(KH+1)*(KW+1), Cout]."""
+    """Zero-padding correction table of w_packed: int32 [(KH+1)*KW*(KW+1)/2, Cout]."""
     import torch
     _require(w_packed, torch.int32, "w_packed")
     cout, kh, kw, cw = w_packed.shape
@@ -163,7 +163,8 @@ def pad_correction(w_packed, c_in: int, out=None):
     desc = _filter_desc(w_packed, c_in)
     size = pad_correction_size(desc)
     if out is None:
-        out = torch.empty(((kh + 1) * (kw + 1), cout), dtype=torch.int32, device=w_packed.device)
+        out = torch.empty(((kh + 1) * (kw * (kw + 1) // 2), cout), dtype=torch.int32,
+                          device=w_packed.device)
     else:
         _require(out, torch.int32, "out")
         if out.numel() != size:
@@ -225,7 +226,7 @@ def bconv2d(x_packed, w_packed, c_in: int, *, stride: Union[int, Sequence[int]] 
                                   (thresholds, "thresholds", torch.float32, cout),
                                   (flip, "flip", torch.int32, packed_words(cout)),
                                   (pad_correction, "pad_correction", torch.int32,
-                                   (kh + 1) * (kw + 1) * cout)):
+                                   (kh + 1) * (kw * (kw + 1) // 2) * cout)):
         if t is None:
             ptrs.append(None)
         else:

@@ -42,14 +42,18 @@
 // afterwards.  With S(co, ky, kx) = sum_ci W(co, ky, kx, ci) and the window's
 // in-image taps forming the rectangle [y0, y1) x [x0, x1),
 //     dot_zero = dot_one - sum_{padded taps} S = (K - Total) - 2*acc + In,
-// Total = sum of S over all taps and In = sum of S over the rectangle.  In
-// comes from a summed-area table of S per filter (four reads per filter),
-// computed once per filter tensor by pad_table_kernel.
+// Total = sum of S over all taps and In = sum of S over the rectangle.  The
+// columns [x0, x1) form one of the KW(KW+1)/2 non-empty intervals I, so with
+// the per-filter table of row prefixes over column intervals
+//     T[y][I] = sum over ky < y, kx in I of S(co, ky, kx),
+// In = T[y1][I] - T[y0][I]: two reads per filter.  pad_table_kernel computes
+// T once per filter tensor.
 #pragma once
 
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 #include <climits>
+#include <type_traits>
 
 namespace lce {
 
@@ -107,7 +111,8 @@ struct BconvParams {
     int32_t slab;           // generic kernel: words staged per pass
     int32_t rs;             // generic kernel: LDS row stride (words)
     const uint32_t *flip;   // [Cwo] or null: output bits to invert (bitpacked output)
-    const int32_t *padc;    // zero padding: summed-area table [(KH+1)*(KW+1)][Cout]
+    const int32_t *padc;    // zero padding: table T [(KH+1)*KW*(KW+1)/2][Cout]
+    FastDiv div_fwg;        // static kernel, zero padding: flat table index -> row
 };
 
 // LDS row stride for a row of `words` words: a multiple of 4 (16-byte rows
@@ -115,6 +120,16 @@ struct BconvParams {
 // neighbouring lanes start in different bank groups.
 __host__ __device__ constexpr int row_stride(int words) {
     return ((words + 3) / 4) % 2 == 1 ? (words + 3) / 4 * 4 : (words + 3) / 4 * 4 + 4;
+}
+
+// Number of non-empty column intervals [x0, x1) of a KW-wide window, and the
+// index of one of them (intervals ordered by x0, then x1).
+__host__ __device__ inline int interval_count(int kw) { return kw * (kw + 1) / 2; }
+
+__host__ __device__ inline int interval_index(int x0, int x1, int kw) {
+    // intervals starting before x0: sum_{j < x0} (kw - j) = x0 * (2kw - x0 + 1) / 2
+    // (unsigned: below 2^32 whenever the table fits 2^31 elements)
+    return (int)((uint32_t)x0 * (uint32_t)(2 * kw - x0 + 1) / 2u) + (x1 - x0 - 1);
 }
 
 // Read-only tensors (packed filters) are read through the constant address
@@ -253,7 +268,9 @@ template <int OUT, bool PADZ>
 __device__ __forceinline__ void load_bounds(const BconvParams &p, int co_wg, int n,
                                             uint32_t *bound) {
     if constexpr (PADZ || OUT == OUT_BITS) {
-        const size_t total_row = (size_t)((p.kh + 1) * (p.kw + 1) - 1) * p.cout;
+        // Total = T[KH][interval [0, KW)]
+        const size_t total_row =
+            (size_t)(p.kh * interval_count(p.kw) + interval_index(0, p.kw, p.kw)) * p.cout;
         for (int t = threadIdx.x; t < n; t += kThreads) {
             const int co = co_wg + t;
             uint32_t v;
@@ -271,43 +288,55 @@ __device__ __forceinline__ void load_bounds(const BconvParams &p, int co_wg, int
     }
 }
 
-// Zero padding: word offsets of the four summed-area-table corners of one
-// lane's window, whose in-image taps are rows [y0, y1) x columns [x0, x1)
-// (table rows `stride` words apart).
+// Zero padding: word offsets of the two table entries of one lane's window,
+// whose in-image taps are rows [y0, y1) x columns [x0, x1) (table rows
+// `stride` words apart): o1 = row (y1, I), o0 = row (y0, I).  Every window of
+// a padded (SAME) geometry overlaps the image, so x1 > x0.  PadWin keeps
+// them as they are (table in global memory); PadWin16 packs both into one
+// register (LDS table, offsets below 2^16), since the window stays live
+// through the whole GEMM.
 struct PadWin {
-    int o11, o01, o10, o00;
+    int o1, o0;
+    __device__ void get(int &a, int &b) const { a = o1; b = o0; }
+};
+
+struct PadWin16 {
+    uint32_t v;
+    __device__ PadWin16() : v(0) {}
+    __device__ explicit PadWin16(const PadWin &w) : v((uint32_t)w.o1 | (uint32_t)w.o0 << 16) {}
+    __device__ void get(int &a, int &b) const { a = (int)(v & 0xFFFFu); b = (int)(v >> 16); }
 };
 
 __device__ __forceinline__ PadWin pad_window(const BconvParams &p, int iy0, int ix0, int stride) {
     const int y0 = max(0, -iy0), y1 = max(y0, min(p.kh, p.h - iy0));
-    const int x0 = max(0, -ix0), x1 = max(x0, min(p.kw, p.wd - ix0));
-    const int row = p.kw + 1;
-    return PadWin{(y1 * row + x1) * stride, (y0 * row + x1) * stride, (y1 * row + x0) * stride,
-                  (y0 * row + x0) * stride};
+    const int x0 = max(0, -ix0), x1 = max(x0 + 1, min(p.kw, p.wd - ix0));
+    const int ni = interval_count(p.kw);
+    const int iv = interval_index(x0, x1, p.kw);
+    return PadWin{(y1 * ni + iv) * stride, (y0 * ni + iv) * stride};
 }
 
 // In = sum of S over one lane's in-image taps, for the RN filters whose table
-// column starts at `sat`.  LDS_TABLE: the workgroup's slice staged in LDS with
-// every column present (0 past cout), read as 16-byte vectors.  Otherwise
-// the table in global memory, where filters past `nvalid` re-read the last
-// valid column.
-template <int RN, bool LDS_TABLE>
-__device__ __forceinline__ void inside_sum(int32_t (&in)[RN], const int32_t *sat,
-                                           const PadWin &w, int nvalid) {
-    if constexpr (LDS_TABLE) {
+// column starts at `sat`.  PadWin16 (static kernel): the workgroup's columns
+// staged in LDS, every column of the block readable, read as 16-byte
+// vectors.  PadWin (generic kernel): the table in global memory, where
+// filters past `nvalid` re-read the last valid column.
+template <int RN, class Win>
+__device__ __forceinline__ void inside_sum(int32_t (&in)[RN], const int32_t *sat, const Win &w,
+                                           int nvalid) {
+    int o1, o0;
+    w.get(o1, o0);
+    if constexpr (std::is_same<Win, PadWin16>::value) {
         const uint32_t *t = reinterpret_cast<const uint32_t *>(sat);
-        uint32_t a[RN], b[RN], c[RN], d[RN];
-        lds_read<RN>(a, t + w.o11);
-        lds_read<RN>(b, t + w.o01);
-        lds_read<RN>(c, t + w.o10);
-        lds_read<RN>(d, t + w.o00);
+        uint32_t a[RN], b[RN];
+        lds_read<RN>(a, t + o1);
+        lds_read<RN>(b, t + o0);
 #pragma unroll
-        for (int f = 0; f < RN; ++f) in[f] = (int)a[f] - (int)b[f] - (int)c[f] + (int)d[f];
+        for (int f = 0; f < RN; ++f) in[f] = (int)(a[f] - b[f]);
     } else {
 #pragma unroll
         for (int f = 0; f < RN; ++f) {
             const int fo = min(f, nvalid - 1);
-            in[f] = sat[w.o11 + fo] - sat[w.o01 + fo] - sat[w.o10 + fo] + sat[w.o00 + fo];
+            in[f] = sat[o1 + fo] - sat[o0 + fo];
         }
     }
 }
@@ -317,15 +346,15 @@ __device__ __forceinline__ void inside_sum(int32_t (&in)[RN], const int32_t *sat
 // applied to the accumulator before it is written).  `bound` is this block's
 // slice of the workgroup's per-filter values (load_bounds); `sat` and `pw`
 // locate the zero-padding correction (PADZ only).
-template <int RN, int OUT, bool PADZ, bool LDS_TABLE>
+template <int RN, int OUT, bool PADZ, class Win>
 __device__ __forceinline__ void epilogue(const BconvParams &p, const uint32_t (&acc)[RN],
                                          int m, int co0, const uint32_t *bound,
-                                         const int32_t *sat, const PadWin &pw) {
+                                         const int32_t *sat, const Win &pw) {
     const int nvalid = min(RN, p.cout - co0);   // may be <= 0 for pad-bit blocks
     int32_t in[RN];
     if constexpr (PADZ) {
         if (nvalid > 0) {
-            inside_sum<RN, LDS_TABLE>(in, sat, pw, nvalid);
+            inside_sum<RN>(in, sat, pw, nvalid);
         } else {
 #pragma unroll
             for (int f = 0; f < RN; ++f) in[f] = 0;
@@ -432,11 +461,11 @@ __device__ __forceinline__ void block_gemm(uint32_t (&acc)[RN], const uint32_t *
 // or ks waves per block with an LDS reduction of the partial sums.
 // Block fl (first filter co_wg + fl) finds its epilogue values at bound + fl
 // and its correction-table column at sat + fl.
-template <int RN, int KC, int OUT, bool PADZ, bool LDS_TABLE>
+template <int RN, int KC, int OUT, bool PADZ, class Win>
 __device__ __forceinline__ void compute_and_store(const BconvParams &p, const uint32_t *arow,
                                                   int kwords, int wave, int lane, int m,
                                                   int co_wg, const uint32_t *bound,
-                                                  const int32_t *sat, const PadWin &pw,
+                                                  const int32_t *sat, const Win &pw,
                                                   uint32_t *red) {
     const bool px_ok = m < p.m;
     const int limit = OUT == OUT_BITS ? p.cwo * 32 : p.cout;
@@ -447,7 +476,7 @@ __device__ __forceinline__ void compute_and_store(const BconvParams &p, const ui
             if (co0 >= limit) break;
             uint32_t acc[RN];
             block_gemm<RN, KC>(acc, arow, p.w, kwords, co0, p.cout, 0, kwords);
-            if (px_ok) epilogue<RN, OUT, PADZ, LDS_TABLE>(p, acc, m, co0, bound + fl, sat + fl, pw);
+            if (px_ok) epilogue<RN, OUT, PADZ>(p, acc, m, co0, bound + fl, sat + fl, pw);
         }
         return;
     }
@@ -470,26 +499,59 @@ __device__ __forceinline__ void compute_and_store(const BconvParams &p, const ui
         for (int q = 1; q < p.ks; ++q)
 #pragma unroll
             for (int f = 0; f < RN; ++f) acc[f] += red[((wave + q) * RN + f) * kPix + lane];
-        if (px_ok) epilogue<RN, OUT, PADZ, LDS_TABLE>(p, acc, m, co0, bound + fl, sat + fl, pw);
+        if (px_ok) epilogue<RN, OUT, PADZ>(p, acc, m, co0, bound + fl, sat + fl, pw);
     }
 }
+
+typedef __attribute__((address_space(1))) void global_void;
+typedef __attribute__((address_space(3))) void lds_void;
+
+// Zero padding: copy the workgroup's columns of the correction table into
+// LDS, densely (`sat`: ROWS rows of p.fwg words), by LDS DMA
+// (global_load_lds): one instruction moves 64 consecutive words of the flat
+// index c*fwg + fl, lane l's word landing at word l of the destination, so
+// no register holds them and the copies are in flight together with the
+// staging loads.  Columns past cout re-read a valid column (never used), and
+// the last instruction's lanes past the table write the LDS slack that
+// table_lds_words() adds.
+template <int ROWS>
+__device__ __forceinline__ void stage_table(const BconvParams &p, int co_wg, int wave, int lane,
+                                            int32_t *sat) {
+    const int words = ROWS * p.fwg;
+    for (int u = wave; u * 64 < words; u += kWaves) {
+        const int idx = min(u * 64 + lane, words - 1);
+        const int c = (int)fast_div((uint32_t)idx, p.div_fwg);
+        const int co = min(co_wg + (idx - c * p.fwg), p.cout - 1);
+        const int32_t *src = p.padc + (size_t)c * p.cout + co;
+        __builtin_amdgcn_global_load_lds((global_void *)src, (lds_void *)(sat + u * 64), 4, 0, 0);
+    }
+}
+
+// LDS words the static kernel's table needs: `rows` rows of fwg words,
+// rounded up to whole 64-word DMA instructions.
+__host__ inline int table_lds_words(int rows, int fwg) { return (rows * fwg + 63) / 64 * 64; }
+
+// The LDS DMA of stage_table completes with the wave's vector-memory counter;
+// waiting for it to reach 0 before the barrier makes the table visible to
+// every wave of the workgroup.  (s_waitcnt vmcnt(0): expcnt and lgkmcnt
+// fields at their maxima, i.e. not waited on.)
+__device__ __forceinline__ void wait_table() { __builtin_amdgcn_s_waitcnt(0x0F70); }
 
 // Shape-specialized kernel: Cw, KH, KW known at compile time, so the whole
 // im2col row fits one LDS slab and the filter-row offsets are immediates.
 // VEC = words per global load when staging (needs x aligned to 4*VEC bytes).
 // PADZ: zero padding with padded taps; the workgroup's columns of the
-// correction table are staged in LDS next to the rows.
+// correction table are staged in dynamic LDS next to the rows.
 template <int CW, int KH, int KW, int VEC, int OUT, bool PADZ>
 __global__ __launch_bounds__(kThreads) void bconv2d_static_kernel(BconvParams p) {
     constexpr int kTaps = KH * KW;
     constexpr int kWords = kTaps * CW;
     constexpr int kRS = row_stride(kWords);
     constexpr int kRed = kWaves * kRN * kPix;   // K-split partial sums, after the rows
-    constexpr int kCorners = (KH + 1) * (KW + 1);
-    constexpr int kSat = PADZ ? kCorners * kMaxFiltersWG : 4;
+    constexpr int kTableRows = (KH + 1) * KW * (KW + 1) / 2;
     __shared__ __attribute__((aligned(16))) uint32_t lds[kPix * kRS > kRed ? kPix * kRS : kRed];
     __shared__ __attribute__((aligned(16))) uint32_t bound[kMaxFiltersWG];
-    __shared__ __attribute__((aligned(16))) int32_t sat[kSat];
+    extern __shared__ __attribute__((aligned(16))) int32_t sat[];   // PADZ: kTableRows rows
 
     const int lane = threadIdx.x & 63;
     const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
@@ -523,19 +585,8 @@ __global__ __launch_bounds__(kThreads) void bconv2d_static_kernel(BconvParams p)
 #pragma unroll
             for (int c = 0; c < kVecs; ++c) v[i][c] = src[c];
         }
+        if constexpr (PADZ) stage_table<kTableRows>(p, co_wg, wave, lane, sat);
         load_bounds<OUT, PADZ>(p, co_wg, p.fwg, bound);
-        constexpr int kSatIters = PADZ ? (kSat + kThreads - 1) / kThreads : 1;
-        int32_t sv[kSatIters];
-        if constexpr (PADZ) {
-#pragma unroll
-            for (int i = 0; i < kSatIters; ++i) {
-                const int idx = (int)threadIdx.x + i * kThreads;
-                const int c = idx / kMaxFiltersWG, fl = idx % kMaxFiltersWG;
-                const int co = co_wg + fl;
-                sv[i] = (idx < kSat && fl < p.fwg && co < p.cout)
-                            ? p.padc[(size_t)c * p.cout + co] : 0;
-            }
-        }
         uint32_t *row = lds + lane * kRS;
 #pragma unroll
         for (int i = 0; i < kIters; ++i) {
@@ -546,19 +597,13 @@ __global__ __launch_bounds__(kThreads) void bconv2d_static_kernel(BconvParams p)
                 for (int c = 0; c < kVecs; ++c) dst[c] = in[i] ? v[i][c] : VecOf<VEC>::zero();
             }
         }
-        if constexpr (PADZ) {
-#pragma unroll
-            for (int i = 0; i < kSatIters; ++i) {
-                const int idx = (int)threadIdx.x + i * kThreads;
-                if (idx < kSat) sat[idx] = sv[i];
-            }
-        }
     }
+    if constexpr (PADZ) wait_table();
     __syncthreads();
-    PadWin pw{0, 0, 0, 0};
-    if constexpr (PADZ) pw = pad_window(p, iy0, ix0, kMaxFiltersWG);
-    compute_and_store<kRN, kKC, OUT, PADZ, true>(p, lds + lane * kRS, kWords, wave, lane, m,
-                                                 co_wg, bound, sat, pw, lds);
+    PadWin16 pw;
+    if constexpr (PADZ) pw = PadWin16(pad_window(p, iy0, ix0, p.fwg));
+    compute_and_store<kRN, kKC, OUT, PADZ>(p, lds + lane * kRS, kWords, wave, lane, m, co_wg,
+                                           bound, sat, pw, lds);
 }
 
 // Generic kernel: any Cw/KH/KW, one filter block per wave.  The im2col row
@@ -610,33 +655,41 @@ __global__ __launch_bounds__(kThreads) void bconv2d_generic_kernel(BconvParams p
     }
     if (!px_ok) return;
     if (OUT == OUT_BITS ? co0 >= p.cwo * 32 : co0 >= p.cout) return;
-    PadWin pw{0, 0, 0, 0};
+    PadWin pw{0, 0};
     if constexpr (PADZ) pw = pad_window(p, iy0, ix0, p.cout);
-    epilogue<RN, OUT, PADZ, false>(p, acc, m, co0, bound + wave * RN, p.padc + co0, pw);
+    epilogue<RN, OUT, PADZ>(p, acc, m, co0, bound + wave * RN, p.padc + co0, pw);
 }
 
-// Summed-area table of the per-tap filter sums used by zero padding:
-//   table[(y*(KW+1) + x)*Cout + co] = sum over ky < y, kx < x of S(co, ky, kx),
+// The zero-padding table of one filter tensor:
+//   table[(y*NI + I)*Cout + co] = sum over ky < y, kx in I of S(co, ky, kx),
 //   S(co, ky, kx) = C_in - 2*popcount(W[co][ky][kx][:])  (the sum of the tap's
-//   +-1 weights; pad bits are 0 and count nothing).
+//   +-1 weights; pad bits are 0 and count nothing),
+// for y in [0, KH] and the NI = KW(KW+1)/2 column intervals I = [x0, x1).
 // One thread per filter; a filter tensor needs it once.
+__device__ inline int tap_sum(const uint32_t *w, int co, int ky, int kx, int kh, int kw, int cw,
+                              int cin) {
+    const uint32_t *wt = w + (((size_t)co * kh + ky) * kw + kx) * cw;
+    int pc = 0;
+    for (int j = 0; j < cw; ++j) pc += __builtin_popcount(wt[j]);
+    return cin - 2 * pc;
+}
+
 __global__ __launch_bounds__(256) void pad_table_kernel(const uint32_t *__restrict__ w,
                                                         int32_t *__restrict__ table, int cout,
                                                         int kh, int kw, int cw, int cin) {
     const int co = blockIdx.x * blockDim.x + threadIdx.x;
     if (co >= cout) return;
-    const size_t row = (size_t)kw + 1;
-    for (size_t x = 0; x < row; ++x) table[x * cout + co] = 0;
+    const size_t ni = (size_t)interval_count(kw);
+    for (size_t i = 0; i < ni; ++i) table[i * cout + co] = 0;        // y = 0
     for (int y = 1; y <= kh; ++y) {
-        table[(size_t)y * row * cout + co] = 0;
-        int run = 0;
-        for (int x = 1; x <= kw; ++x) {
-            const uint32_t *wt = w + (((size_t)co * kh + (y - 1)) * kw + (x - 1)) * cw;
-            int pc = 0;
-            for (int j = 0; j < cw; ++j) pc += __builtin_popcount(wt[j]);
-            run += cin - 2 * pc;
-            table[((size_t)y * row + x) * cout + co] =
-                table[((size_t)(y - 1) * row + x) * cout + co] + run;
+        for (int x0 = 0; x0 < kw; ++x0) {
+            int run = 0;
+            for (int x1 = x0 + 1; x1 <= kw; ++x1) {
+                run += tap_sum(w, co, y - 1, x1 - 1, kh, kw, cw, cin);
+                const size_t i = (size_t)interval_index(x0, x1, kw);
+                table[((size_t)y * ni + i) * cout + co] =
+                    table[((size_t)(y - 1) * ni + i) * cout + co] + run;
+            }
         }
     }
 }

@@ -70,6 +70,12 @@ struct Geometry {
     bool pads;   // some window reaches outside the image
 };
 
+// Elements of the zero-padding table: (KH+1) row prefixes x KW(KW+1)/2
+// column intervals x C_out.
+int64_t table_elements(const lce_bconv2d_desc &d) {
+    return (int64_t)(d.kh + 1) * ((int64_t)d.kw * (d.kw + 1) / 2) * d.c_out;
+}
+
 // Zero padding changes the result only where some window reaches outside
 // the image; there it needs the correction table.
 bool zero_padded(const lce_bconv2d_desc &d, const Geometry &g) {
@@ -116,7 +122,7 @@ lce_status validate_desc(const lce_bconv2d_desc *d, Geometry *g) {
                     (long long)m, (long long)x_words, (long long)w_words, (long long)out_elems,
                     (long long)k);
     if (d->c_out > (1 << 20)) return fail(LCE_EINVAL, "c_out %d exceeds 2^20", d->c_out);
-    const int64_t table = (int64_t)(d->kh + 1) * (d->kw + 1) * d->c_out;
+    const int64_t table = table_elements(*d);
     if (zero_padded(*d, *g) && (k >= (1 << 29) || table > lim))
         return fail(LCE_EINVAL,
                     "zero padding needs K < 2^29 and a correction table below 2^31 elements "
@@ -128,17 +134,22 @@ using lce::BconvParams;
 
 template <int CW, int KH, int KW, int OUT, bool PADZ>
 void launch_static(const BconvParams &p, dim3 grid, hipStream_t s, int vec) {
+    // zero padding: the correction table's rows in dynamic LDS
+    const size_t lds =
+        PADZ ? (size_t)lce::table_lds_words((KH + 1) * lce::interval_count(KW), p.fwg) *
+                   sizeof(int32_t)
+             : 0;
     if (vec == 4 && CW % 4 == 0)
         hipLaunchKernelGGL(
             (lce::bconv2d_static_kernel<CW, KH, KW, (CW % 4 == 0 ? 4 : 1), OUT, PADZ>), grid,
-            dim3(lce::kThreads), 0, s, p);
+            dim3(lce::kThreads), lds, s, p);
     else if (vec >= 2 && CW % 2 == 0)
         hipLaunchKernelGGL(
             (lce::bconv2d_static_kernel<CW, KH, KW, (CW % 2 == 0 ? 2 : 1), OUT, PADZ>), grid,
-            dim3(lce::kThreads), 0, s, p);
+            dim3(lce::kThreads), lds, s, p);
     else
         hipLaunchKernelGGL((lce::bconv2d_static_kernel<CW, KH, KW, 1, OUT, PADZ>), grid,
-                           dim3(lce::kThreads), 0, s, p);
+                           dim3(lce::kThreads), lds, s, p);
 }
 
 template <int OUT, bool PADZ>
@@ -338,6 +349,7 @@ lce_status lce_bconv2d(const lce_bconv2d_desc *desc, const int32_t *x_packed,
     } else {
         p.nb = 1; p.ks = 1; p.fwg = lce::kWaves * lce::kRN; p.ksplit = p.kwords;
     }
+    p.div_fwg = lce::make_fastdiv((uint32_t)p.fwg);
     dim3 grid((unsigned)((p.m + lce::kPix - 1) / lce::kPix),
               (unsigned)((filters + p.fwg - 1) / p.fwg));
     const int vec = aligned(x_packed, 16) ? 4 : aligned(x_packed, 8) ? 2 : 1;
@@ -354,7 +366,7 @@ lce_status lce_bconv2d_pad_correction_size(const lce_bconv2d_desc *desc, int64_t
     Geometry g;
     lce_status st = validate_desc(desc, &g);
     if (st != LCE_OK) return st;
-    *elements = (int64_t)(desc->kh + 1) * (desc->kw + 1) * desc->c_out;
+    *elements = table_elements(*desc);
     return ok();
 }
 
@@ -367,7 +379,7 @@ lce_status lce_bconv2d_pad_correction(const lce_bconv2d_desc *desc, const int32_
     if (!w_packed || !pad_correction) return fail(LCE_EINVAL, "w_packed/pad_correction is NULL");
     if (!aligned(w_packed, 4) || !aligned(pad_correction, 4))
         return fail(LCE_EALIGN, "tensor pointers must be 4-byte aligned");
-    const int64_t table = (int64_t)(d.kh + 1) * (d.kw + 1) * d.c_out;
+    const int64_t table = table_elements(d);
     if (table > INT32_MAX)
         return fail(LCE_EINVAL, "correction table of %lld elements exceeds 2^31",
                     (long long)table);

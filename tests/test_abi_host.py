@@ -158,7 +158,7 @@ def test_pad_correction_validation_errors():
     n = ctypes.c_int64(-1)
     assert L.lce_bconv2d_pad_correction_size(ctypes.byref(desc(kh=3, kw=5, c_out=7)),
                                              ctypes.byref(n)) == lce.LCE_OK
-    assert n.value == 4 * 6 * 7
+    assert n.value == 4 * 15 * 7        # (KH+1) x KW(KW+1)/2 intervals x C_out
     assert L.lce_bconv2d_pad_correction_size(None, ctypes.byref(n)) == lce.LCE_EINVAL
     assert L.lce_bconv2d_pad_correction_size(ctypes.byref(desc()), None) == lce.LCE_EINVAL
     assert L.lce_bconv2d_pad_correction(ctypes.byref(desc()), None, P, None) == lce.LCE_EINVAL

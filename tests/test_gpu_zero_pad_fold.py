@@ -67,18 +67,21 @@ def oracle_run(layer, inp, a_signs, pad_value=0):
 
 @pytest.mark.parametrize("c_in,c_out,kh,kw", [(64, 40, 3, 3), (33, 13, 5, 3), (512, 8, 1, 1),
                                                (7, 100, 3, 5), (96, 1, 7, 7)])
-def test_pad_correction_table_is_summed_area_of_filter_sums(c_in, c_out, kh, kw):
-    """table[y][x][co] = sum over ky < y, kx < x of the tap sums of the +-1
-    filter (computed here from the oracle-side signs, not from the GPU)."""
+def test_pad_correction_table_is_prefix_of_interval_sums(c_in, c_out, kh, kw):
+    """table[y][I][co] = sum over ky < y and kx in the column interval I of
+    the tap sums of the +-1 filter, intervals [x0, x1) numbered by x0 then
+    x1 (computed here from the oracle-side signs, not from the GPU)."""
     import paper_2011_09398_amd as lce
     layer = Layer("tab", 1, 4, 4, c_in, c_out, kh=kh, kw=kw, input_kind="bits")
     inp = make_layer_inputs(layer, 3, 70, c_out)
     got = sync_np(lce.pad_correction(gpu_pack_weights(inp), c_in))
     s = inp.w_sign.astype(np.int64).sum(axis=3)                       # [co, ky, kx]
-    sat = np.zeros((c_out, kh + 1, kw + 1), np.int64)
-    sat[:, 1:, 1:] = s.cumsum(axis=1).cumsum(axis=2)
-    want = sat.reshape(c_out, -1).T                                   # [(y, x), co]
-    assert np.array_equal(got.astype(np.int64), want)
+    intervals = [(x0, x1) for x0 in range(kw) for x1 in range(x0 + 1, kw + 1)]
+    want = np.zeros((kh + 1, len(intervals), c_out), np.int64)
+    for y in range(1, kh + 1):
+        for i, (x0, x1) in enumerate(intervals):
+            want[y, i] = s[:, :y, x0:x1].sum(axis=(1, 2))
+    assert np.array_equal(got.astype(np.int64), want.reshape(-1, c_out))
 
 
 # ---------------------------------------------------------------- zero-padding parity
