@@ -12,7 +12,12 @@ Measured on the launch stream with HIP events:
   * batch-1 layers (float input: lce_bitpack timed as its own line) the same
     way, but from a captured HIP graph of the R launches, since eager launch
     cost exceeds their run time;
-  * a probe of the achievable xor+popcount VALU rate, next to the spec peak.
+  * a probe of the achievable xor+popcount VALU rate, next to the spec peak;
+  * the same layers with zero padding (the correction-step variant);
+  * the memory-bound operators at sizes beyond the 256 MB last-level cache,
+    inputs (or outputs) rotated over buffers totalling more than 512 MB:
+    bitpack (LceQuantize), binary max pooling (LceBMaxPool2d) and
+    dequantize (LceDequantize), in GB/s of algorithmic bytes vs 8 TB/s.
 Then the CPU oracle, as it stands, on a bounded sample of the same step.
 
     python bench.py [--steps K] [--warmup W] [--no-cpu] [--workload b64|stack16]
@@ -53,6 +58,8 @@ def parse():
     ap.add_argument("--no-cpu", action="store_true", help="skip the CPU oracle baseline")
     ap.add_argument("--no-batch1", action="store_true", help="skip the batch-1 lines")
     ap.add_argument("--no-probe", action="store_true", help="skip the VALU rate probe")
+    ap.add_argument("--no-extra", action="store_true",
+                    help="skip the zero-padding and memory-bound operator lines")
     ap.add_argument("--profile-pass", action="store_true",
                     help="short run for counter collection: a 512 MiB copy (the byte-counter "
                          "calibration) then a few steps")
@@ -180,6 +187,93 @@ def bitpack_record(layer, ms):
     return {"layer": f"bitpack {layer.n}x{layer.h}x{layer.w}x{layer.c_in}", "batch": layer.n,
             "us": round(ms * 1e3, 3), "bytes": nbytes, "GB/s": round(gbs, 1),
             "hbm_frac": round(gbs / HBM_PEAK_GBS, 4)}
+
+
+def mem_record(name, nbytes, ms):
+    gbs = nbytes / (ms * 1e-3) / 1e9
+    return {"op": name, "us": round(ms * 1e3, 3), "bytes": nbytes, "GB/s": round(gbs, 1),
+            "hbm_frac": round(gbs / HBM_PEAK_GBS, 4)}
+
+
+def rotating(calls):
+    """One callable that launches calls[0], calls[1], ... in turn."""
+    state = {"i": 0}
+
+    def fn():
+        calls[state["i"]]()
+        state["i"] = (state["i"] + 1) % len(calls)
+    return fn
+
+
+def memory_bound_lines(reps: int):
+    """bitpack, binary max pooling and dequantize beyond the last-level cache."""
+    import numpy as np
+    import torch
+    import paper_2011_09398_amd as lce
+    from workloads.gen import random_words
+    rng = np.random.default_rng(0)
+    lines = []
+    # reference: a plain device copy of 512 MiB (read + write), the bandwidth
+    # a streaming kernel can reach in practice
+    src = torch.ones(128 * 2 ** 20, dtype=torch.float32, device="cuda")
+    dst = torch.empty_like(src)
+    lines.append(mem_record("copy 512 MiB (torch)", 2 * 4 * src.numel(),
+                            time_repeated(lambda: dst.copy_(src), 20, graph=False)))
+    del src, dst
+    # LceQuantize: 256x56x56x64 float (205 MB) -> 6.4 MB, 3 rotating inputs
+    n, h, c = 256, 56, 64
+    xs = [torch.randn((n, h, h, c), dtype=torch.float32, device="cuda") for _ in range(3)]
+    outs = [torch.empty((n, h, h, 2), dtype=torch.int32, device="cuda") for _ in range(3)]
+    calls = [lce.PreparedBitpack(x, o) for x, o in zip(xs, outs)]
+    nbytes = 4 * n * h * h * c + 4 * n * h * h * 2
+    lines.append(mem_record(f"bitpack {n}x{h}x{h}x{c}", nbytes,
+                            time_repeated(rotating(calls), reps, graph=False)))
+    del xs, outs, calls
+    # LceBMaxPool2d 3x3 stride 2 SAME: 8192x56x56x64 bits (205 MB) -> 28x28, 3 inputs
+    n, h, c = 8192, 56, 64
+    words = torch.from_numpy(random_words(rng, (n, h, h), c).view(np.int32)).cuda()
+    xs = [words] + [words.clone() for _ in range(2)]
+    desc = lce.make_pool_desc(n, h, h, c, 3, 2, "same")
+    oh, ow = lce.pool_out_shape(desc)
+    outs = [torch.empty((n, oh, ow, 2), dtype=torch.int32, device="cuda") for _ in range(3)]
+    L, st = lce.lib(), torch.cuda.current_stream().cuda_stream
+    ref = ctypes.byref(desc)
+    calls = [(lambda x=x, o=o: L.lce_bmaxpool2d(ref, x.data_ptr(), o.data_ptr(), st))
+             for x, o in zip(xs, outs)]
+    nbytes = 4 * words.numel() + 4 * outs[0].numel()
+    lines.append(mem_record(f"bmaxpool2d 3x3/2 {n}x{h}x{h}x{c}", nbytes,
+                            time_repeated(rotating(calls), reps, graph=False)))
+    del words, xs, outs, calls
+    # LceDequantize: 256x28x28x128 bits (3.2 MB) -> float (103 MB), 3 rotating outputs
+    n, h, c = 256, 28, 128
+    x = torch.from_numpy(random_words(rng, (n, h, h), c).view(np.int32)).cuda()
+    outs = [torch.empty((n, h, h, c), dtype=torch.float32, device="cuda") for _ in range(3)]
+    rows = n * h * h
+    calls = [(lambda o=o: L.lce_dequantize(x.data_ptr(), o.data_ptr(), rows, c, st))
+             for o in outs]
+    nbytes = 4 * x.numel() + 4 * outs[0].numel()
+    lines.append(mem_record(f"dequantize {n}x{h}x{h}x{c}", nbytes,
+                            time_repeated(rotating(calls), reps, graph=False)))
+    del x, outs, calls
+    torch.cuda.synchronize()
+    torch.cuda.empty_cache()
+    return lines
+
+
+def zero_padding_lines(step, reps: int, probe_tops=None):
+    """The step's layers with zero padding (correction table prepared once)."""
+    import paper_2011_09398_amd as lce
+    lines = []
+    for call, layer, (w_packed, x_packed, kw), out in zip(step.calls, step.layers, step.keep,
+                                                          step.outs):
+        corr = lce.pad_correction(w_packed, layer.c_in)
+        z = lce.PreparedBConv2d(x_packed, w_packed, layer.c_in, out, stride=layer.strides,
+                                padding=layer.padding, pad_value="zero", clamp=layer.clamp,
+                                out_type=layer.out, pad_correction=corr, **kw)
+        r = layer_record(layer, time_repeated(z, reps, graph=False), probe_tops)
+        r["padding"] = "zero"
+        lines.append(r)
+    return lines
 
 
 def valu_probe():
@@ -316,6 +410,13 @@ def main():
                 "probe_peak": None if probe is None else round(probe, 1),
                 "probe_frac": dom.get("probe_frac")}
 
+    zero_pad = mem_lines = None
+    if not args.no_extra:
+        log("zero-padding variant of the step's layers")
+        zero_pad = zero_padding_lines(step, args.reps, probe)
+        log("memory-bound operators beyond the last-level cache")
+        mem_lines = memory_bound_lines(args.reps)
+
     batch1 = None
     if not args.no_batch1:
         log("batch-1 layers (graph-captured repeats)")
@@ -342,6 +443,7 @@ def main():
                    "binary_ops_per_step": total_ops},
         "event_ms_per_step": round(ev_s * 1e3 / args.steps, 5),
         "roofline": roofline, "cpu_baseline": cpu, "layers": layers, "batch1": batch1,
+        "zero_padding": zero_pad, "memory_bound": mem_lines,
         "device": torch.cuda.get_device_name(0),
     }
     print(json.dumps(line), flush=True)

@@ -97,8 +97,9 @@ lce_status lce_bconv2d_out_shape(const lce_bconv2d_desc *desc, int32_t *oh, int3
  * i.e. +1.0); the bits past `channels` are written as 0.
  * For activations rows = N*H*W; for OHWI filters (the 1-bit weight storage
  * of Section 3.1) rows = C_out*KH*KW with channels = C_in.
- * rows == 0 is a no-op.  x must be 4-byte aligned (16-byte alignment and a
- * channel count that is a multiple of 32 take the fastest path), out 4-byte.
+ * rows == 0 is a no-op (pointers may then be NULL).  x must be 4-byte
+ * aligned (16-byte alignment and a channel count that is a multiple of 32
+ * take the fastest path), out 4-byte.
  * Errors: LCE_EINVAL (null pointer, rows < 0, channels < 1),
  *         LCE_EALIGN, LCE_EHIP. */
 lce_status lce_bitpack(const float *x, int32_t *out, int64_t rows, int32_t channels,
@@ -172,6 +173,44 @@ lce_status lce_bconv2d_pad_correction(const lce_bconv2d_desc *desc, const int32_
 lce_status lce_fold_thresholds(const float *multiplier, const float *bias, int32_t c_out,
                                int32_t k, int32_t clamp_min, int32_t clamp_max,
                                float *thresholds, int32_t *flip);
+
+/* LceBMaxPool2d (Section 3.2): max pooling of +-1 activations held as
+ * bits.  Since max(sign(x)) = sign(max(x)), a max pooling that feeds a
+ * binarized layer can run after the binarization, on the packed tensor,
+ * where the maximum of +-1 values is the bitwise AND of the window's words
+ * (bit 1 = -1.0 survives only if every value in the window is -1).
+ * Locations outside the image take no part (TensorFlow max pooling).  The
+ * window geometry follows lce_padding like the convolution's. */
+typedef struct {
+    int32_t n, h, w, channels;     /* input, NHWC bitpacked, >= 1             */
+    int32_t kh, kw;                /* window, >= 1                            */
+    int32_t stride_h, stride_w;    /* >= 1                                    */
+    int32_t padding;               /* lce_padding                             */
+} lce_bmaxpool2d_desc;
+
+/* Output height/width of `desc`.
+ * Errors: LCE_EINVAL (null pointer, bad field, no output). */
+lce_status lce_bmaxpool2d_out_shape(const lce_bmaxpool2d_desc *desc, int32_t *oh, int32_t *ow);
+
+/*   x_packed int32 [N][H][W][ceil(channels/32)]    (device)
+ *   out      int32 [N][OH][OW][ceil(channels/32)]  (device); pad bits 0
+ * Pointers 4-byte aligned (16-byte alignment and a word count that is a
+ * multiple of 4 take the widest loads).
+ * Errors: LCE_EINVAL (null pointer, bad field, no output, a tensor of 2^31
+ *         or more words), LCE_EALIGN, LCE_EHIP. */
+lce_status lce_bmaxpool2d(const lce_bmaxpool2d_desc *desc, const int32_t *x_packed,
+                          int32_t *out, hipStream_t stream);
+
+/* LceDequantize (Section 3.2): bitpacked x_packed[rows][ceil(channels/32)]
+ * back to float out[rows][channels]: -1.0f where the bit is 1, +1.0f where
+ * it is 0 (the inverse of lce_bitpack's sign binarization on +-1 data).
+ * rows == 0 is a no-op (pointers may then be NULL).  Pointers 4-byte
+ * aligned (a channel count that is a multiple of 32 with out 16-byte aligned
+ * takes the widest stores).
+ * Errors: LCE_EINVAL (null pointer, rows < 0, channels < 1), LCE_EALIGN,
+ *         LCE_EHIP. */
+lce_status lce_dequantize(const int32_t *x_packed, float *out, int64_t rows, int32_t channels,
+                          hipStream_t stream);
 
 /* Message describing the last error on the calling thread ("" if none). */
 const char *lce_last_error(void);

@@ -8,6 +8,8 @@ If the library is not built this module raises; there is no CPU fallback.
     bconv2d(x_packed, w_packed, c_in) LceBConv2d with the fused output transform
     pad_correction(w_packed, c_in)    zero-padding correction table of a filter tensor
     fold_thresholds(m, b, k, clamp)   float transform + binarization -> thresholds, flip
+    bmaxpool2d(x_packed, channels)    LceBMaxPool2d: AND over each window of packed words
+    dequantize(x_packed, channels)    LceDequantize: packed bits -> +-1.0 float32
 """
 from __future__ import annotations
 
@@ -29,7 +31,8 @@ INT32_MAX = 2 ** 31 - 1
 # Every symbol include/lce.h declares.
 EXPORTS = ("lce_packed_words", "lce_bconv2d_out_shape", "lce_bitpack", "lce_bconv2d",
            "lce_bconv2d_pad_correction_size", "lce_bconv2d_pad_correction",
-           "lce_fold_thresholds", "lce_last_error")
+           "lce_fold_thresholds", "lce_bmaxpool2d_out_shape", "lce_bmaxpool2d",
+           "lce_dequantize", "lce_last_error")
 
 
 class Desc(ctypes.Structure):
@@ -37,6 +40,12 @@ class Desc(ctypes.Structure):
     _fields_ = [(name, ctypes.c_int32) for name in (
         "n", "h", "w", "c_in", "c_out", "kh", "kw", "stride_h", "stride_w",
         "padding", "pad_value", "clamp_min", "clamp_max", "out_type")]
+
+
+class PoolDesc(ctypes.Structure):
+    """lce_bmaxpool2d_desc: nine int32 fields, in header order."""
+    _fields_ = [(name, ctypes.c_int32) for name in (
+        "n", "h", "w", "channels", "kh", "kw", "stride_h", "stride_w", "padding")]
 
 
 class LceError(RuntimeError):
@@ -72,6 +81,13 @@ def lib() -> ctypes.CDLL:
         L.lce_bconv2d_pad_correction.restype = ctypes.c_int
         L.lce_fold_thresholds.argtypes = [vp, vp, i32, i32, i32, i32, vp, vp]
         L.lce_fold_thresholds.restype = ctypes.c_int
+        L.lce_bmaxpool2d_out_shape.argtypes = [ctypes.POINTER(PoolDesc), ctypes.POINTER(i32),
+                                               ctypes.POINTER(i32)]
+        L.lce_bmaxpool2d_out_shape.restype = ctypes.c_int
+        L.lce_bmaxpool2d.argtypes = [ctypes.POINTER(PoolDesc), vp, vp, vp]
+        L.lce_bmaxpool2d.restype = ctypes.c_int
+        L.lce_dequantize.argtypes = [vp, vp, i64, i32, vp]
+        L.lce_dequantize.restype = ctypes.c_int
         L.lce_last_error.argtypes = []
         L.lce_last_error.restype = ctypes.c_char_p
         _lib = L
@@ -249,6 +265,64 @@ def bconv2d(x_packed, w_packed, c_in: int, *, stride: Union[int, Sequence[int]] 
             out = torch.empty((n, oh, ow, cout), dtype=torch.int32, device=x_packed.device)
     _check(lib().lce_bconv2d(ctypes.byref(desc), x_packed.data_ptr(), w_packed.data_ptr(),
                              *ptrs, out.data_ptr(), _stream_handle(x_packed)))
+    return out
+
+
+def make_pool_desc(n, h, w, channels, kernel=2, stride=None, padding="valid") -> PoolDesc:
+    kh, kw = (kernel, kernel) if isinstance(kernel, int) else tuple(kernel)
+    if stride is None:
+        stride = (kh, kw)
+    sh, sw = (stride, stride) if isinstance(stride, int) else tuple(stride)
+    return PoolDesc(n, h, w, channels, kh, kw, sh, sw,
+                    PADDING[padding] if isinstance(padding, str) else padding)
+
+
+def pool_out_shape(desc: PoolDesc) -> Tuple[int, int]:
+    oh, ow = ctypes.c_int32(), ctypes.c_int32()
+    _check(lib().lce_bmaxpool2d_out_shape(ctypes.byref(desc), ctypes.byref(oh),
+                                          ctypes.byref(ow)))
+    return oh.value, ow.value
+
+
+def bmaxpool2d(x_packed, channels: int, kernel=2, stride=None, padding: str = "valid",
+               out=None):
+    """LceBMaxPool2d on int32 [N,H,W,ceil(C/32)] -> int32 [N,OH,OW,ceil(C/32)]
+    (stride defaults to the window size, as in TensorFlow)."""
+    import torch
+    _require(x_packed, torch.int32, "x_packed")
+    n, h, w, cw = x_packed.shape
+    if cw != packed_words(channels):
+        raise ValueError(f"packed words {cw} do not match channels={channels}")
+    desc = make_pool_desc(n, h, w, channels, kernel, stride, padding)
+    oh, ow = pool_out_shape(desc)
+    if out is None:
+        out = torch.empty((n, oh, ow, cw), dtype=torch.int32, device=x_packed.device)
+    else:
+        _require(out, torch.int32, "out")
+        if out.numel() != n * oh * ow * cw:
+            raise ValueError(f"out must hold {n}x{oh}x{ow}x{cw} words")
+    _check(lib().lce_bmaxpool2d(ctypes.byref(desc), x_packed.data_ptr(), out.data_ptr(),
+                                _stream_handle(x_packed)))
+    return out
+
+
+def dequantize(x_packed, channels: int, out=None):
+    """LceDequantize: int32 [..., ceil(C/32)] -> float32 [..., C] of +-1.0."""
+    import torch
+    _require(x_packed, torch.int32, "x_packed")
+    cw = x_packed.shape[-1]
+    if cw != packed_words(channels):
+        raise ValueError(f"packed words {cw} do not match channels={channels}")
+    rows = x_packed.numel() // cw if cw else 0
+    if out is None:
+        out = torch.empty(tuple(x_packed.shape[:-1]) + (channels,), dtype=torch.float32,
+                          device=x_packed.device)
+    else:
+        _require(out, torch.float32, "out")
+        if out.numel() != rows * channels:
+            raise ValueError("out has the wrong size")
+    _check(lib().lce_dequantize(x_packed.data_ptr(), out.data_ptr(), rows, channels,
+                                _stream_handle(x_packed)))
     return out
 
 

@@ -16,6 +16,7 @@
 #include "lce.h"
 #include "bitpack.hpp"
 #include "bconv.hpp"
+#include "pool.hpp"
 
 namespace {
 
@@ -252,6 +253,44 @@ void choose_schedule(BconvParams &p, int filters) {
     p.ksplit = ((p.kwords + ks - 1) / ks + 3) / 4 * 4;
 }
 
+lce_status validate_pool(const lce_bmaxpool2d_desc *d, Geometry *g) {
+    if (!d) return fail(LCE_EINVAL, "desc is NULL");
+    if (d->n < 1 || d->h < 1 || d->w < 1 || d->channels < 1)
+        return fail(LCE_EINVAL, "input dims must be >= 1 (n=%d h=%d w=%d channels=%d)", d->n,
+                    d->h, d->w, d->channels);
+    if (d->kh < 1 || d->kw < 1 || d->stride_h < 1 || d->stride_w < 1)
+        return fail(LCE_EINVAL, "window %dx%d and strides (%d, %d) must be >= 1", d->kh, d->kw,
+                    d->stride_h, d->stride_w);
+    if (d->padding != LCE_PADDING_VALID && d->padding != LCE_PADDING_SAME)
+        return fail(LCE_EINVAL, "unknown padding %d", d->padding);
+    long th = 0, tw = 0;
+    if (!out_dim(d->h, d->kh, d->stride_h, d->padding, &g->oh, &g->pt, &th) ||
+        !out_dim(d->w, d->kw, d->stride_w, d->padding, &g->ow, &g->pl, &tw))
+        return fail(LCE_EINVAL, "VALID pooling with a %dx%d window has no output on %dx%d",
+                    d->kh, d->kw, d->h, d->w);
+    g->pads = th > 0 || tw > 0;
+    const int64_t cw = packed_words(d->channels);
+    const int64_t in_words = (int64_t)d->n * d->h * d->w * cw;
+    const int64_t out_words = (int64_t)d->n * g->oh * g->ow * cw;
+    if (in_words > INT32_MAX || out_words > INT32_MAX)
+        return fail(LCE_EINVAL, "tensor too large (input words %lld, output words %lld; each "
+                    "must stay below 2^31)", (long long)in_words, (long long)out_words);
+    return ok();
+}
+
+template <int VEC>
+void launch_pool(const lce::PoolParams &p, hipStream_t s) {
+    int64_t blocks = (p.units + lce::kPoolThreads - 1) / lce::kPoolThreads;
+    if (blocks > 256 * 16) blocks = 256 * 16;
+    const dim3 grid((unsigned)blocks), block(lce::kPoolThreads);
+    if (p.kh == 2 && p.kw == 2)
+        hipLaunchKernelGGL((lce::bmaxpool_kernel<VEC, 2, 2>), grid, block, 0, s, p);
+    else if (p.kh == 3 && p.kw == 3)
+        hipLaunchKernelGGL((lce::bmaxpool_kernel<VEC, 3, 3>), grid, block, 0, s, p);
+    else
+        hipLaunchKernelGGL((lce::bmaxpool_kernel<VEC, 0, 0>), grid, block, 0, s, p);
+}
+
 }  // namespace
 
 extern "C" {
@@ -273,12 +312,12 @@ lce_status lce_bconv2d_out_shape(const lce_bconv2d_desc *desc, int32_t *oh, int3
 
 lce_status lce_bitpack(const float *x, int32_t *out, int64_t rows, int32_t channels,
                        hipStream_t stream) {
-    if (!x || !out) return fail(LCE_EINVAL, "x/out is NULL");
     if (rows < 0) return fail(LCE_EINVAL, "rows %lld < 0", (long long)rows);
     if (channels < 1) return fail(LCE_EINVAL, "channels %d < 1", channels);
+    if (rows == 0) return ok();   // empty tensors may have null pointers
+    if (!x || !out) return fail(LCE_EINVAL, "x/out is NULL");
     if (!aligned(x, 4) || !aligned(out, 4)) return fail(LCE_EALIGN, "x/out not 4-byte aligned");
     if (rows > (INT64_MAX / 64) / channels) return fail(LCE_EINVAL, "tensor too large");
-    if (rows == 0) return ok();
     const int cw = packed_words(channels);
     const int64_t nwords = rows * cw;
     if (channels % 32 == 0 && aligned(x, 16)) {
@@ -446,6 +485,76 @@ lce_status lce_fold_thresholds(const float *multiplier, const float *bias, int32
         if (inv) flip[co / 32] |= (int32_t)(1u << (co % 32));
     }
     return ok();
+}
+
+lce_status lce_bmaxpool2d_out_shape(const lce_bmaxpool2d_desc *desc, int32_t *oh, int32_t *ow) {
+    if (!oh || !ow) return fail(LCE_EINVAL, "oh/ow output pointer is NULL");
+    Geometry g;
+    lce_status st = validate_pool(desc, &g);
+    if (st != LCE_OK) return st;
+    *oh = g.oh;
+    *ow = g.ow;
+    return ok();
+}
+
+lce_status lce_bmaxpool2d(const lce_bmaxpool2d_desc *desc, const int32_t *x_packed,
+                          int32_t *out, hipStream_t stream) {
+    Geometry g;
+    lce_status st = validate_pool(desc, &g);
+    if (st != LCE_OK) return st;
+    if (!x_packed || !out) return fail(LCE_EINVAL, "x_packed/out is NULL");
+    if (!aligned(x_packed, 4) || !aligned(out, 4))
+        return fail(LCE_EALIGN, "tensor pointers must be 4-byte aligned");
+    const lce_bmaxpool2d_desc &d = *desc;
+    lce::PoolParams p{};
+    p.x = reinterpret_cast<const uint32_t *>(x_packed);
+    p.out = reinterpret_cast<uint32_t *>(out);
+    p.h = d.h; p.w = d.w; p.cw = packed_words(d.channels);
+    p.oh = g.oh; p.ow = g.ow;
+    p.kh = d.kh; p.kw = d.kw; p.sh = d.stride_h; p.sw = d.stride_w; p.pt = g.pt; p.pl = g.pl;
+    const int vec = (p.cw % 4 == 0 && aligned(x_packed, 16) && aligned(out, 16)) ? 4
+                    : (p.cw % 2 == 0 && aligned(x_packed, 8) && aligned(out, 8)) ? 2 : 1;
+    const int64_t pixels = (int64_t)d.n * g.oh * g.ow;
+    p.units = pixels * (p.cw / vec);
+    p.div_cwv = lce::make_fastdiv((uint32_t)(p.cw / vec));
+    p.div_ow = lce::make_fastdiv((uint32_t)g.ow);
+    p.div_oh = lce::make_fastdiv((uint32_t)g.oh);
+    if (vec == 4)
+        launch_pool<4>(p, stream);
+    else if (vec == 2)
+        launch_pool<2>(p, stream);
+    else
+        launch_pool<1>(p, stream);
+    return check_launch("lce_bmaxpool2d launch");
+}
+
+lce_status lce_dequantize(const int32_t *x_packed, float *out, int64_t rows, int32_t channels,
+                          hipStream_t stream) {
+    if (rows < 0) return fail(LCE_EINVAL, "rows %lld < 0", (long long)rows);
+    if (channels < 1) return fail(LCE_EINVAL, "channels %d < 1", channels);
+    if (rows == 0) return ok();   // empty tensors may have null pointers
+    if (!x_packed || !out) return fail(LCE_EINVAL, "x_packed/out is NULL");
+    if (!aligned(x_packed, 4) || !aligned(out, 4))
+        return fail(LCE_EALIGN, "x_packed/out not 4-byte aligned");
+    if (rows > (INT64_MAX / 64) / channels) return fail(LCE_EINVAL, "tensor too large");
+    const int64_t count = rows * channels;
+    if (channels % 32 == 0 && aligned(out, 16)) {
+        const int64_t n4 = count / 4;
+        int64_t blocks = (n4 + lce::kPoolThreads - 1) / lce::kPoolThreads;
+        if (blocks > 256 * 16) blocks = 256 * 16;
+        hipLaunchKernelGGL(lce::dequantize32_kernel, dim3((unsigned)blocks),
+                           dim3(lce::kPoolThreads), 0, stream,
+                           reinterpret_cast<const uint32_t *>(x_packed),
+                           reinterpret_cast<float4 *>(out), n4);
+    } else {
+        int64_t blocks = (count + lce::kPoolThreads - 1) / lce::kPoolThreads;
+        if (blocks > 256 * 16) blocks = 256 * 16;
+        hipLaunchKernelGGL(lce::dequantize_generic_kernel, dim3((unsigned)blocks),
+                           dim3(lce::kPoolThreads), 0, stream,
+                           reinterpret_cast<const uint32_t *>(x_packed), out, count, channels,
+                           packed_words(channels));
+    }
+    return check_launch("lce_dequantize launch");
 }
 
 const char *lce_last_error(void) { return g_last_error.c_str(); }

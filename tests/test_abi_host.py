@@ -138,6 +138,7 @@ def test_bitpack_validation_errors():
     assert L.lce_bitpack(P, P, 2 ** 62, 64, None) == lce.LCE_EINVAL
     # zero rows is a valid no-op: nothing is launched
     assert L.lce_bitpack(P, P, 0, 32, None) == lce.LCE_OK
+    assert L.lce_bitpack(None, None, 0, 32, None) == lce.LCE_OK
     assert lce.last_error() == ""
 
 
@@ -187,3 +188,45 @@ def test_fold_validation_errors():
         assert "channel 2" in lce.last_error()
         assert L.lce_fold_thresholds(None, mm.ctypes.data, 4, 9, -9, 9, T, F) == lce.LCE_EINVAL
     assert L.lce_fold_thresholds(m.ctypes.data, None, 4, 9, -9, 9, T, F) == lce.LCE_OK
+
+
+def test_pool_desc_layout_and_out_shape():
+    assert ctypes.sizeof(lce.PoolDesc) == 9 * 4
+    for h, k, s, pad in product((1, 2, 5, 7, 28, 56), (1, 2, 3, 5), (1, 2, 3), ("same", "valid")):
+        if pad == "valid" and h < k:
+            continue
+        d = lce.make_pool_desc(2, h, h, 64, k, s, pad)
+        assert lce.pool_out_shape(d) == (oracle.out_size(h, k, s, pad)[0],) * 2
+
+
+def test_pool_validation_errors():
+    L = lce.lib()
+    oh, ow = ctypes.c_int32(), ctypes.c_int32()
+    good = lce.make_pool_desc(2, 8, 8, 64, 2)
+    assert L.lce_bmaxpool2d_out_shape(ctypes.byref(good), None, ctypes.byref(ow)) == \
+        lce.LCE_EINVAL
+    assert L.lce_bmaxpool2d(None, P, P, None) == lce.LCE_EINVAL
+    for field, value in (("n", 0), ("h", 0), ("channels", 0), ("kh", 0), ("stride_w", 0),
+                         ("padding", 5)):
+        d = lce.make_pool_desc(2, 8, 8, 64, 2)
+        setattr(d, field, value)
+        assert L.lce_bmaxpool2d(ctypes.byref(d), P, P, None) == lce.LCE_EINVAL, field
+    assert L.lce_bmaxpool2d(ctypes.byref(lce.make_pool_desc(1, 2, 2, 32, 3)), P, P, None) == \
+        lce.LCE_EINVAL                                  # VALID 3x3 on 2x2: no output
+    assert L.lce_bmaxpool2d(ctypes.byref(good), None, P, None) == lce.LCE_EINVAL
+    assert L.lce_bmaxpool2d(ctypes.byref(good), P, None, None) == lce.LCE_EINVAL
+    assert L.lce_bmaxpool2d(ctypes.byref(good), P + 2, P, None) == lce.LCE_EALIGN
+    big = lce.make_pool_desc(2 ** 12, 2 ** 10, 2 ** 10, 64, 1)   # 2^33 input words
+    assert L.lce_bmaxpool2d(ctypes.byref(big), P, P, None) == lce.LCE_EINVAL
+
+
+def test_dequantize_validation_errors():
+    L = lce.lib()
+    assert L.lce_dequantize(None, P, 4, 32, None) == lce.LCE_EINVAL
+    assert L.lce_dequantize(P, None, 4, 32, None) == lce.LCE_EINVAL
+    assert L.lce_dequantize(P, P, -1, 32, None) == lce.LCE_EINVAL
+    assert L.lce_dequantize(P, P, 4, 0, None) == lce.LCE_EINVAL
+    assert L.lce_dequantize(P + 1, P, 4, 32, None) == lce.LCE_EALIGN
+    assert L.lce_dequantize(P, P, 2 ** 62, 64, None) == lce.LCE_EINVAL
+    assert L.lce_dequantize(P, P, 0, 32, None) == lce.LCE_OK
+    assert L.lce_dequantize(None, None, 0, 32, None) == lce.LCE_OK     # empty: may be NULL
