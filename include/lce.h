@@ -174,6 +174,44 @@ lce_status lce_fold_thresholds(const float *multiplier, const float *bias, int32
                                int32_t k, int32_t clamp_min, int32_t clamp_max,
                                float *thresholds, int32_t *flip);
 
+/* ---- The same convolution on the matrix cores --------------------------
+ *
+ * LceBConv2d's dot (Section 3.2) is a dense contraction of +-1 values.  The
+ * paper's XOR + POPCOUNT (lce_bconv2d) is how a CPU multiplies them; gfx950's
+ * MFMA multiplies 4-bit floats, in which +1.0, -1.0 and 0.0 are exact, and
+ * accumulates in fp32, exact for |dot| < 2^24, at eight times the VALU's
+ * xor+popcount rate.  lce_bconv2d_mfma computes the identical result from the
+ * same bitpacked activations: each bit is widened to a 4-bit +-1.0 only inside
+ * the kernel.  The filters are widened once, ahead of time, into a caller-owned
+ * buffer (lce_bconv2d_mfma_weights).  Zero padding needs no correction table
+ * there: padded locations simply widen to 0.0. */
+
+/* Bytes of the widened filter buffer of `desc` (16 bytes per 32 weights:
+ * KH*KW x Cw' words x C_out' filters, Cw' = ceil(C_in/32) rounded up to an
+ * even word count or a multiple of 4, C_out' = C_out rounded up to 32).
+ * Errors: LCE_EINVAL (null pointer, bad field). */
+lce_status lce_bconv2d_mfma_weights_size(const lce_bconv2d_desc *desc, int64_t *bytes);
+
+/* Widen packed filters w_packed (as for lce_bconv2d, device, 4-byte aligned)
+ * into w_fp4 (device, 16-byte aligned, lce_bconv2d_mfma_weights_size bytes),
+ * asynchronously on `stream`.  Channels past C_in and filters past C_out
+ * widen to 0.0.  Run once per filter tensor.
+ * Errors: LCE_EINVAL, LCE_EALIGN, LCE_EHIP. */
+lce_status lce_bconv2d_mfma_weights(const lce_bconv2d_desc *desc, const int32_t *w_packed,
+                                    void *w_fp4, hipStream_t stream);
+
+/* LceBConv2d on the matrix cores: arguments, output and every rounding as
+ * lce_bconv2d (multiplier/bias for FLOAT32, thresholds and optional flip for
+ * BITPACKED), with the widened filters in place of w_packed and either
+ * pad_value (no correction table).
+ * Errors: as lce_bconv2d, plus LCE_EUNSUPPORTED when K = KH*KW*C_in >= 2^24
+ * or when the input region a workgroup stages exceeds the LDS of one
+ * workgroup (very wide images); w_fp4 must be 16-byte aligned. */
+lce_status lce_bconv2d_mfma(const lce_bconv2d_desc *desc, const int32_t *x_packed,
+                            const void *w_fp4, const float *multiplier, const float *bias,
+                            const float *thresholds, const int32_t *flip, void *out,
+                            hipStream_t stream);
+
 /* LceBMaxPool2d (Section 3.2): max pooling of +-1 activations held as
  * bits.  Since max(sign(x)) = sign(max(x)), a max pooling that feeds a
  * binarized layer can run after the binarization, on the packed tensor,

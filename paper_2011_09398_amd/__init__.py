@@ -8,6 +8,8 @@ If the library is not built this module raises; there is no CPU fallback.
     bconv2d(x_packed, w_packed, c_in) LceBConv2d with the fused output transform
     pad_correction(w_packed, c_in)    zero-padding correction table of a filter tensor
     fold_thresholds(m, b, k, clamp)   float transform + binarization -> thresholds, flip
+    mfma_weights(w_packed, c_in)      filters widened to 4-bit +-1.0 for the matrix-core path
+    bconv2d_mfma(x_packed, w_fp4, ..) LceBConv2d on the matrix cores (same result)
     bmaxpool2d(x_packed, channels)    LceBMaxPool2d: AND over each window of packed words
     dequantize(x_packed, channels)    LceDequantize: packed bits -> +-1.0 float32
 """
@@ -32,7 +34,8 @@ INT32_MAX = 2 ** 31 - 1
 EXPORTS = ("lce_packed_words", "lce_bconv2d_out_shape", "lce_bitpack", "lce_bconv2d",
            "lce_bconv2d_pad_correction_size", "lce_bconv2d_pad_correction",
            "lce_fold_thresholds", "lce_bmaxpool2d_out_shape", "lce_bmaxpool2d",
-           "lce_dequantize", "lce_last_error")
+           "lce_dequantize", "lce_bconv2d_mfma_weights_size", "lce_bconv2d_mfma_weights",
+           "lce_bconv2d_mfma", "lce_last_error")
 
 
 class Desc(ctypes.Structure):
@@ -88,6 +91,12 @@ def lib() -> ctypes.CDLL:
         L.lce_bmaxpool2d.restype = ctypes.c_int
         L.lce_dequantize.argtypes = [vp, vp, i64, i32, vp]
         L.lce_dequantize.restype = ctypes.c_int
+        L.lce_bconv2d_mfma_weights_size.argtypes = [ctypes.POINTER(Desc), ctypes.POINTER(i64)]
+        L.lce_bconv2d_mfma_weights_size.restype = ctypes.c_int
+        L.lce_bconv2d_mfma_weights.argtypes = [ctypes.POINTER(Desc), vp, vp, vp]
+        L.lce_bconv2d_mfma_weights.restype = ctypes.c_int
+        L.lce_bconv2d_mfma.argtypes = [ctypes.POINTER(Desc), vp, vp, vp, vp, vp, vp, vp, vp]
+        L.lce_bconv2d_mfma.restype = ctypes.c_int
         L.lce_last_error.argtypes = []
         L.lce_last_error.restype = ctypes.c_char_p
         _lib = L
@@ -324,6 +333,93 @@ def dequantize(x_packed, channels: int, out=None):
     _check(lib().lce_dequantize(x_packed.data_ptr(), out.data_ptr(), rows, channels,
                                 _stream_handle(x_packed)))
     return out
+
+
+def mfma_weights(w_packed, c_in: int, out=None):
+    """Widened filters for bconv2d_mfma: uint8 device buffer (16-byte aligned)."""
+    import torch
+    _require(w_packed, torch.int32, "w_packed")
+    cout, kh, kw, cw = w_packed.shape
+    if cw != packed_words(c_in):
+        raise ValueError(f"packed channel words {cw} do not match c_in={c_in}")
+    desc = _filter_desc(w_packed, c_in)
+    n = ctypes.c_int64()
+    _check(lib().lce_bconv2d_mfma_weights_size(ctypes.byref(desc), ctypes.byref(n)))
+    if out is None:
+        out = torch.empty(n.value, dtype=torch.uint8, device=w_packed.device)
+    elif out.numel() * out.element_size() < n.value:
+        raise ValueError(f"out must hold {n.value} bytes")
+    _check(lib().lce_bconv2d_mfma_weights(ctypes.byref(desc), w_packed.data_ptr(),
+                                          out.data_ptr(), _stream_handle(w_packed)))
+    return out
+
+
+def bconv2d_mfma(x_packed, w_fp4, c_in: int, c_out: int, kernel, *, stride=1,
+                 padding: str = "same", pad_value: str = "one",
+                 clamp: Optional[Tuple[int, int]] = None, out_type: str = "float",
+                 multiplier=None, bias=None, thresholds=None, flip=None, out=None):
+    """LceBConv2d on the matrix cores: x_packed int32 [N,H,W,Cw], w_fp4 from
+    mfma_weights(); kernel = (KH, KW) or an int.  Output as bconv2d."""
+    import torch
+    _require(x_packed, torch.int32, "x_packed")
+    if not isinstance(w_fp4, torch.Tensor) or w_fp4.device.type != "cuda":
+        raise TypeError("w_fp4 must be a device tensor")
+    n, h, w, cw = x_packed.shape
+    if cw != packed_words(c_in):
+        raise ValueError(f"packed channel words {cw} do not match c_in={c_in}")
+    kh, kw = (kernel, kernel) if isinstance(kernel, int) else tuple(kernel)
+    desc = make_desc(n, h, w, c_in, c_out, kh, kw, stride, padding, pad_value, clamp, out_type)
+    oh, ow = out_shape(desc)
+    ptrs = []
+    for t, name, dtype, numel in ((multiplier, "multiplier", torch.float32, c_out),
+                                  (bias, "bias", torch.float32, c_out),
+                                  (thresholds, "thresholds", torch.float32, c_out),
+                                  (flip, "flip", torch.int32, packed_words(c_out))):
+        if t is None:
+            ptrs.append(None)
+        else:
+            _require(t, dtype, name)
+            if t.numel() != numel:
+                raise ValueError(f"{name} must have {numel} elements")
+            ptrs.append(t.data_ptr())
+    oc = packed_words(c_out) if out_type == "bitpacked" else c_out
+    dt = torch.float32 if out_type == "float" else torch.int32
+    if out is None:
+        out = torch.empty((n, oh, ow, oc), dtype=dt, device=x_packed.device)
+    else:
+        _require(out, dt, "out")
+        if out.numel() != n * oh * ow * oc:
+            raise ValueError(f"out must hold {n}x{oh}x{ow}x{oc} elements")
+    _check(lib().lce_bconv2d_mfma(ctypes.byref(desc), x_packed.data_ptr(), w_fp4.data_ptr(),
+                                  *ptrs, out.data_ptr(), _stream_handle(x_packed)))
+    return out
+
+
+class PreparedBConv2dMfma:
+    """A bconv2d_mfma call marshalled once (see PreparedBConv2d)."""
+
+    def __init__(self, x_packed, w_fp4, c_in, c_out, kernel, out, *, stride=1, padding="same",
+                 pad_value="one", clamp=None, out_type="float", multiplier=None, bias=None,
+                 thresholds=None, flip=None):
+        bconv2d_mfma(x_packed, w_fp4, c_in, c_out, kernel, stride=stride, padding=padding,
+                     pad_value=pad_value, clamp=clamp, out_type=out_type,
+                     multiplier=multiplier, bias=bias, thresholds=thresholds, flip=flip,
+                     out=out)
+        n, h, w, _ = x_packed.shape
+        kh, kw = (kernel, kernel) if isinstance(kernel, int) else tuple(kernel)
+        self.desc = make_desc(n, h, w, c_in, c_out, kh, kw, stride, padding, pad_value, clamp,
+                              out_type)
+        self._desc_ref = ctypes.byref(self.desc)
+        ptr = lambda t: None if t is None else t.data_ptr()
+        self.args = (x_packed.data_ptr(), w_fp4.data_ptr(), ptr(multiplier), ptr(bias),
+                     ptr(thresholds), ptr(flip), out.data_ptr())
+        self.keep = (x_packed, w_fp4, multiplier, bias, thresholds, flip, out)
+        self._fn = lib().lce_bconv2d_mfma
+
+    def __call__(self, stream=None):
+        st = self._fn(self._desc_ref, *self.args, _current_stream() if stream is None else stream)
+        if st != LCE_OK:
+            raise LceError(st, last_error())
 
 
 def _current_stream():

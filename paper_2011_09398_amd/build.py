@@ -14,7 +14,8 @@ SOURCES = [os.path.join(CSRC, "lce.hip")]
 # Measurement-only probe of the xor/popcount VALU rate (not part of the C ABI).
 PROBE_LIB = os.path.join(PKG, "libprobe.so")
 PROBE_SOURCES = [os.path.join(CSRC, "valu_probe.hip")]
-HEADERS = [os.path.join(CSRC, f) for f in ("bitpack.hpp", "bconv.hpp", "pool.hpp")] + \
+HEADERS = [os.path.join(CSRC, f) for f in ("bitpack.hpp", "bconv.hpp", "pool.hpp",
+                                                 "bconv_mfma.hpp")] + \
           [os.path.join(INCLUDE, "lce.h")]
 
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")

@@ -1,0 +1,363 @@
+// Bitpacked binary 2-D convolution (LceBConv2d, arXiv 2011.09398 Section 3.2)
+// on the gfx950 matrix cores.
+//
+// The binary convolution is a dense contraction of +-1 values: dot =
+// sum_k a_k * w_k.  Section 3.2 evaluates it with XOR + POPCOUNT because the
+// paper's CPUs have no faster way to multiply +-1 values.  gfx950 has one:
+// its MFMA multiplies 4-bit floats (e2m1), in which +1.0 and -1.0 (and 0.0)
+// are exact, and accumulates in fp32, which is exact for every |dot| < 2^24.
+// The MFMA therefore returns the same integer dot, at a dense rate (10.1
+// PFLOP/s) eight times the VALU's xor+popcount rate.  The data stay
+// bitpacked in memory; each 1-bit value is widened to a 4-bit +-1.0 only in
+// LDS, right before the matrix cores read it.
+//
+// Instruction: v_mfma_scale_f32_32x32x64_f8f6f4 with both operands fp4 and
+// unit scales (E8M0 127 = 2^0).  Lane l holds row (or column) l % 32 and one
+// block of 32 consecutive k values, l / 32 choosing the block.  A dot product
+// does not depend on the order of k, so a lane's block is simply one packed
+// word (32 channels of one tap) widened to 16 bytes; the filter side is
+// widened the same way once per filter tensor (mfma_expand_weights_kernel).
+//
+// Work decomposition: a workgroup (4 waves) owns 128 consecutive output
+// pixels and 32*NBLK filters; wave w computes pixels [32w, 32w+32) of them
+// against all the workgroup's filters (NBLK 32x32 accumulator blocks).
+//   * A: the input region the 128 pixels read (rows of the batch stacked as
+//     padded images, all padded columns) is widened once per channel chunk
+//     of CC words into LDS; every tap of the im2col is then an address
+//     offset into it, so a word is widened once, not once per tap.
+//     Padding locations widen to +1.0 (one-padding, Section 3.2) or 0.0
+//     (zero padding): zero padding costs nothing on this path.
+//   * B: the widened filters of one tap and chunk, staged in LDS (two
+//     buffers, the next tap's copy in flight during the current tap).
+//   * Epilogue: the fp32 accumulator is the exact integer dot; the fused
+//     activation clamp and the float transform or threshold compare follow
+//     as on the XOR path.  Bitpacked output gathers each pixel's 32 filter
+//     bits with one ballot per accumulator row pair.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+#include "bconv.hpp"   // FastDiv, OutKind, thr_to_padz-style bounds
+
+namespace lce {
+
+constexpr int kMfmaPix = 128;      // output pixels per workgroup (32 per wave)
+
+// 16 bytes as a native vector (HIP's uint4 is a class, which keeps arrays of
+// it out of registers)
+typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
+constexpr int kMfmaThreads = 256;
+
+// e2m1 codes: +1.0 = 0x2, -1.0 = 0xA.  Byte for two bits (lo, hi):
+// code(lo) | code(hi) << 4, indexed by lo | hi << 1.
+constexpr uint32_t kFp4PlusMinusLut = 0xAAA22A22u;
+// Byte for two validity bits: 0xF for each valid half, 0x0 otherwise.
+constexpr uint32_t kFp4ValidLut = 0xFFF00F00u;
+
+struct MfmaParams {
+    const uint32_t *x;      // [N][H][W][Cw] bitpacked activations
+    const u32x4 *wexp;      // [KH*KW*CwE][CoutP] widened filters (16 bytes = 32 values)
+    const float *mult;      // [Cout] or null (float output)
+    const float *bias;      // [Cout] or null (float output)
+    const float *thr;       // [Cout] (bitpacked output)
+    const uint32_t *flip;   // [Cwo] or null (bitpacked output)
+    void *out;
+    int32_t n, h, w, cw, cwe;        // cwe: Cw rounded up to a multiple of CC
+    int32_t oh, ow, cout, coutp, cwo;
+    int32_t kh, kw, sh, sw, pt, pl;
+    int32_t ph, pw;                  // padded image: (OH-1)*sh + KH rows, (OW-1)*sw + KW cols
+    int32_t lo, hi, m;
+    int32_t tile_rows;               // stacked padded rows staged per workgroup
+    int32_t pad_zero;                // 1: padded locations are 0.0
+    FastDiv div_ohw, div_ow, div_ph, div_pw;
+};
+
+typedef int mfma_v8i __attribute__((ext_vector_type(8)));
+typedef float mfma_v16f __attribute__((ext_vector_type(16)));
+
+
+// One packed byte -> four bytes holding its 2-bit groups (bits 2i, 2i+1 of
+// x land in bits 0-1 of byte i).
+__device__ __forceinline__ uint32_t spread_pairs(uint32_t x) {
+    uint32_t t = ((x << 12) | x) & 0x000F000Fu;
+    return ((t << 6) | t) & 0x03030303u;
+}
+
+// Packed word -> 32 e2m1 codes (16 bytes), channel c in nibble c of the
+// result (little-endian): the lookup `lut` maps each 2-bit group to a byte
+// (kFp4PlusMinusLut for +-1.0, 0 for all 0.0).
+__device__ __forceinline__ u32x4 widen_word(uint32_t w, uint32_t lut) {
+    u32x4 o;
+    o.x = __builtin_amdgcn_perm(lut, lut, spread_pairs(w & 0xFFu));
+    o.y = __builtin_amdgcn_perm(lut, lut, spread_pairs((w >> 8) & 0xFFu));
+    o.z = __builtin_amdgcn_perm(lut, lut, spread_pairs((w >> 16) & 0xFFu));
+    o.w = __builtin_amdgcn_perm(lut, lut, spread_pairs(w >> 24));
+    return o;
+}
+
+__device__ __forceinline__ mfma_v16f mfma_fp4(u32x4 a, u32x4 b, mfma_v16f c) {
+    const mfma_v8i av = {(int)a.x, (int)a.y, (int)a.z, (int)a.w, 0, 0, 0, 0};
+    const mfma_v8i bv = {(int)b.x, (int)b.y, (int)b.z, (int)b.w, 0, 0, 0, 0};
+    // operand formats 4 = e2m1; scales 127 = 2^0
+    return __builtin_amdgcn_mfma_scale_f32_32x32x64_f8f6f4(av, bv, c, 4, 4, 0, 127, 0, 127);
+}
+
+// Threshold as a bound on the unclamped dot: bit = clamp(dot) < thr becomes
+// dot < T with T = ceil(thr) inside (lo, hi], kAlways-like INT32_MAX when
+// ceil(thr) > hi, never (INT32_MIN) when ceil(thr) <= lo or thr is NaN.
+__device__ inline int32_t thr_to_dot_bound(float thr, int lo, int hi) {
+    const double t = (double)thr;
+    if (t != t) return INT32_MIN;
+    const double tc = ceil(t);
+    if (tc <= (double)lo) return INT32_MIN;
+    if (tc > (double)hi) return INT32_MAX;
+    return (int32_t)tc;
+}
+
+// Stacked padded row of output pixel m's window origin, and its column.
+__device__ __forceinline__ void mfma_pixel(const MfmaParams &p, int m, int &row, int &col) {
+    const uint32_t img = fast_div((uint32_t)m, p.div_ohw);
+    const uint32_t r = (uint32_t)m - img * p.div_ohw.d;
+    const uint32_t oy = fast_div(r, p.div_ow);
+    const uint32_t ox = r - oy * (uint32_t)p.ow;
+    row = (int)img * p.ph + (int)oy * p.sh;
+    col = (int)ox * p.sw;
+}
+
+// 16 zero bytes in device memory: the DMA source of every padding word.
+__device__ __attribute__((aligned(16))) const uint32_t g_mfma_zero[4] = {0u, 0u, 0u, 0u};
+
+typedef __attribute__((address_space(1))) void mfma_global_void;
+typedef __attribute__((address_space(3))) void mfma_lds_void;
+
+// s_waitcnt vmcnt(N) alone (expcnt and lgkmcnt fields at their maxima).
+template <int N>
+__device__ __forceinline__ void wait_vmcnt() {
+    static_assert(N >= 0 && N < 64, "vmcnt range");
+    __builtin_amdgcn_s_waitcnt((N & 0xF) | ((N >> 4) << 14) | 0x70 | 0xF00);
+}
+
+constexpr int kMfmaDepth = 4;       // B stages in flight (registers) ahead of the one in use
+
+template <int CC, int OUT, int NBLK>
+__global__ __launch_bounds__(kMfmaThreads) void bconv2d_mfma_kernel(MfmaParams p) {
+    constexpr int BN = 32 * NBLK;
+    constexpr int kStage = CC * BN;                                   // u32x4 per B stage
+    constexpr int kBPer = (kStage + kMfmaThreads - 1) / kMfmaThreads; // u32x4 per thread
+    extern __shared__ __attribute__((aligned(16))) u32x4 smem[];
+    const int tid = threadIdx.x;
+    const int lane = tid & 63, half = lane >> 5, l32 = lane & 31;
+    const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+    const int m0 = blockIdx.x * kMfmaPix;
+    const int n_base = blockIdx.y * BN;
+    const int taps = p.kh * p.kw;
+    const int chunks = p.cwe / CC;
+    const int stages = chunks * taps;
+    const int TR = p.tile_rows, PW = p.pw, plane = TR * PW;
+    const int bits_words = plane * p.cw;                      // packed input region
+    u32x4 *bbuf = smem;                                       // [2][CC][BN]
+    u32x4 *atile = bbuf + 2 * kStage;                         // [CC][TR][PW] e2m1
+    uint32_t *abits = reinterpret_cast<uint32_t *>(atile + CC * plane);   // [TR][PW][Cw]
+
+    int row0, col0;
+    mfma_pixel(p, m0, row0, col0);
+    const int mp = min(m0 + wave * 32 + l32, p.m - 1);
+    int prow, pcol;
+    mfma_pixel(p, mp, prow, pcol);
+    const int a_base = (half * TR + (prow - row0)) * PW + pcol;
+
+    // ---- the packed input region, by LDS DMA: tile word e = (r*PW + c)*Cw + j;
+    // padding reads the zero buffer.  The last instruction's extra lanes land
+    // in the slack of the LDS allocation.
+    for (int u = wave; u * 64 < bits_words; u += 4) {
+        const int e = min(u * 64 + lane, bits_words - 1);
+        const int rc = e / p.cw, j = e - (e / p.cw) * p.cw;
+        const int r = (int)fast_div((uint32_t)rc, p.div_pw);
+        const int c = rc - r * PW;
+        const int R = row0 + r;
+        const int img = (int)fast_div((uint32_t)R, p.div_ph);
+        const int yy = R - img * p.ph - p.pt, xx = c - p.pl;
+        const bool inside = img < p.n && (unsigned)yy < (unsigned)p.h &&
+                            (unsigned)xx < (unsigned)p.w;
+        const uint32_t *src = inside ? p.x + (((size_t)img * p.h + yy) * p.w + xx) * p.cw + j
+                                     : g_mfma_zero;
+        __builtin_amdgcn_global_load_lds((mfma_global_void *)src,
+                                         (mfma_lds_void *)(abits + u * 64), 4, 0, 0);
+    }
+
+    // ---- B stage s = (chunk s / taps, tap s % taps): words [c0, c0+CC) of the
+    // tap, filters [n_base, n_base + BN), u32x4 e = j*BN + f of the stage.
+    // Loads are unconditional (past the last stage they re-read it, and a
+    // thread past the stage re-reads its last element), so each lands
+    // straight in its ring register and the compiler's wait for it can be
+    // deferred to the store that needs it.
+    auto load_b = [&](int s, u32x4 (&r)[kBPer]) __attribute__((always_inline)) {
+        s = min(s, stages - 1);
+        const int c0 = (s / taps) * CC, t = s - (s / taps) * taps;
+#pragma unroll
+        for (int i = 0; i < kBPer; ++i) {
+            const int e = min(tid + i * kMfmaThreads, kStage - 1);
+            const int j = e / BN, f = e - (e / BN) * BN;
+            const int co = min(n_base + f, p.coutp - 1);
+            r[i] = p.wexp[(size_t)(t * p.cwe + c0 + j) * p.coutp + co];
+        }
+    };
+    auto store_b = [&](int s, const u32x4 (&r)[kBPer]) __attribute__((always_inline)) {
+        u32x4 *slot = bbuf + (s & 1) * kStage;     // (past the last stage: unused data)
+#pragma unroll
+        for (int i = 0; i < kBPer; ++i) {
+            const int e = tid + i * kMfmaThreads;
+            if (e < kStage) slot[e] = r[i];
+        }
+    };
+
+    u32x4 breg[kMfmaDepth][kBPer];
+#pragma unroll
+    for (int d = 0; d < kMfmaDepth; ++d) load_b(d, breg[d]);
+    wait_vmcnt<0>();                 // this wave's input words (and the first B stages)
+    store_b(0, breg[0]);
+    __syncthreads();
+
+    mfma_v16f acc[NBLK];
+#pragma unroll
+    for (int i = 0; i < NBLK; ++i)
+#pragma unroll
+        for (int v = 0; v < 16; ++v) acc[i][v] = 0.0f;
+
+    const uint32_t pad_lut = p.pad_zero ? 0u : kFp4PlusMinusLut;
+    auto widen_chunk = [&](int c0) __attribute__((always_inline)) {
+        for (int e = tid; e < CC * plane; e += kMfmaThreads) {
+            const int j = e / plane;
+            const int rc = e - j * plane;
+            const int r = (int)fast_div((uint32_t)rc, p.div_pw);
+            const int c = rc - r * PW;
+            const int R = row0 + r;
+            const int img = (int)fast_div((uint32_t)R, p.div_ph);
+            const int yy = R - img * p.ph - p.pt, xx = c - p.pl;
+            const int word = c0 + j;
+            const bool inside = img < p.n && (unsigned)yy < (unsigned)p.h &&
+                                (unsigned)xx < (unsigned)p.w;
+            uint32_t bits = 0u, lut = pad_lut;
+            if (word < p.cw && inside) {
+                bits = abits[rc * p.cw + word];
+                lut = kFp4PlusMinusLut;
+            }
+            atile[e] = widen_word(bits, lut);
+        }
+    };
+
+    // One stage: (at a chunk's first tap) widen the chunk, then the MFMAs of
+    // stage s against LDS slot s & 1; stage s+1 goes to the other slot and
+    // stage s + kMfmaDepth starts loading into the registers s freed.  The
+    // loop runs a multiple of four stages with no branch around any of them
+    // (a branch would let the compiler sink each load down to its use): a
+    // stage past the last one reads in-bounds data and feeds the MFMA a zero
+    // A operand, which adds nothing.
+    auto stage = [&](int s, u32x4 (&mine)[kBPer], u32x4 (&next)[kBPer]) __attribute__((always_inline)) {
+        const int ch = s / taps, t = s - ch * taps;
+        const bool live = s < stages;
+        if (t == 0 && live) {
+            widen_chunk(ch * CC);
+            __syncthreads();
+        }
+        load_b(s + kMfmaDepth, mine);
+        const int ky = t / p.kw, kx = t - (t / p.kw) * p.kw;
+        const int a_tap = a_base + ky * PW + kx;
+        const u32x4 *bt = bbuf + (s & 1) * kStage;
+        const u32x4 zero = u32x4{0u, 0u, 0u, 0u};
+#pragma unroll
+        for (int q = 0; q < CC / 2; ++q) {
+            u32x4 a = atile[a_tap + 2 * q * plane];
+            if (!live) a = zero;
+            u32x4 b[NBLK];
+#pragma unroll
+            for (int i = 0; i < NBLK; ++i) b[i] = bt[(2 * q + half) * BN + 32 * i + l32];
+#pragma unroll
+            for (int i = 0; i < NBLK; ++i) acc[i] = mfma_fp4(a, b[i], acc[i]);
+        }
+        store_b(s + 1, next);
+        __syncthreads();
+    };
+    static_assert(kMfmaDepth == 4, "the stage loop below is unrolled by four");
+    for (int s = 0; s < stages; s += 4) {
+        stage(s, breg[0], breg[1]);
+        stage(s + 1, breg[1], breg[2]);
+        stage(s + 2, breg[2], breg[3]);
+        stage(s + 3, breg[3], breg[0]);
+    }
+    const int nblk = min(NBLK, (p.coutp - n_base) >> 5);
+
+    // ---- epilogue: accumulator value v of block i is pixel
+    // (v/4)*8 + half*4 + v%4 of the wave and filter n_base + 32i + l32.
+    const int mw = m0 + wave * 32;
+#pragma unroll
+    for (int i = 0; i < NBLK; ++i) {
+        if (i >= nblk) break;
+        const int co = n_base + 32 * i + l32;
+        const bool co_ok = co < p.cout;
+        if constexpr (OUT == OUT_BITS) {
+            const int32_t T = co_ok ? thr_to_dot_bound(p.thr[co], p.lo, p.hi) : INT32_MIN;
+            uint32_t fbit = 0;
+            if (p.flip && co_ok) fbit = (p.flip[co >> 5] >> (co & 31)) & 1u;
+            uint32_t word = 0;
+#pragma unroll
+            for (int v = 0; v < 16; ++v) {
+                const int dot = (int)acc[i][v];
+                const uint32_t bit = (uint32_t)(dot < T) ^ fbit;
+                const uint64_t mask = __ballot(bit);
+                const int r0 = (v >> 2) * 8 + (v & 3);          // pixel of lanes 0-31
+                if (lane == r0) word = (uint32_t)mask;
+                if (lane == r0 + 4) word = (uint32_t)(mask >> 32);
+            }
+            const int m = mw + lane;
+            if (lane < 32 && m < p.m)
+                reinterpret_cast<uint32_t *>(p.out)[(size_t)m * p.cwo + (co >> 5)] = word;
+        } else {
+            float mu = 1.0f, bi = 0.0f;
+            if constexpr (OUT == OUT_FLOAT) {
+                if (co_ok && p.mult) mu = p.mult[co];
+                if (co_ok && p.bias) bi = p.bias[co];
+            }
+#pragma unroll
+            for (int v = 0; v < 16; ++v) {
+                const int m = mw + (v >> 2) * 8 + half * 4 + (v & 3);
+                const int c = min(max((int)acc[i][v], p.lo), p.hi);
+                if (co_ok && m < p.m) {
+                    if constexpr (OUT == OUT_FLOAT)
+                        reinterpret_cast<float *>(p.out)[(size_t)m * p.cout + co] =
+                            __builtin_fmaf((float)c, mu, bi);
+                    else
+                        reinterpret_cast<int32_t *>(p.out)[(size_t)m * p.cout + co] = c;
+                }
+            }
+        }
+    }
+}
+
+// Filters widened once per filter tensor into the B layout:
+//   wexp[(t*CwE + j)*CoutP + co] = 32 e2m1 codes of word j of tap t of
+//   filter co; channels past C_in, words past Cw and filters past Cout are
+//   0.0 (they then add nothing to any dot).
+__global__ __launch_bounds__(256) void mfma_expand_weights_kernel(const uint32_t *__restrict__ w,
+                                                                  u32x4 *__restrict__ wexp,
+                                                                  int cout, int coutp, int taps,
+                                                                  int cw, int cwe, int cin) {
+    const int64_t total = (int64_t)taps * cwe * coutp;
+    for (int64_t idx = (int64_t)blockIdx.x * 256 + threadIdx.x; idx < total;
+         idx += (int64_t)gridDim.x * 256) {
+        const int64_t k = idx / coutp;
+        const int co = (int)(idx - k * coutp);
+        const int t = (int)(k / cwe), j = (int)(k - (int64_t)t * cwe);
+        u32x4 o = {0u, 0u, 0u, 0u};
+        if (co < cout && j < cw) {
+            const uint32_t bits = w[((size_t)co * taps + t) * cw + j];
+            const int nvalid = min(32, cin - 32 * j);
+            const uint32_t valid = nvalid >= 32 ? 0xFFFFFFFFu : (1u << nvalid) - 1u;
+            o = widen_word(bits, kFp4PlusMinusLut) & widen_word(valid, kFp4ValidLut);
+        }
+        wexp[idx] = o;
+    }
+}
+
+}  // namespace lce

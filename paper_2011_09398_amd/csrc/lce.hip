@@ -17,6 +17,7 @@
 #include "bitpack.hpp"
 #include "bconv.hpp"
 #include "pool.hpp"
+#include "bconv_mfma.hpp"
 
 namespace {
 
@@ -291,6 +292,69 @@ void launch_pool(const lce::PoolParams &p, hipStream_t s) {
         hipLaunchKernelGGL((lce::bmaxpool_kernel<VEC, 0, 0>), grid, block, 0, s, p);
 }
 
+// ---- matrix-core path
+
+// Channel words per LDS chunk (2 or 4; the K step of the MFMA is a word
+// pair) and the word count padded to it: the smaller padding wins, 4 on ties.
+void mfma_chunk(int cw, int *cc, int *cwe) {
+    const int e2 = (cw + 1) / 2 * 2, e4 = (cw + 3) / 4 * 4;
+    *cc = e2 < e4 ? 2 : 4;
+    *cwe = e2 < e4 ? e2 : e4;
+}
+
+int64_t mfma_weight_bytes(const lce_bconv2d_desc &d) {
+    int cc, cwe;
+    mfma_chunk(packed_words(d.c_in), &cc, &cwe);
+    const int64_t coutp = (int64_t)(d.c_out + 31) / 32 * 32;
+    return (int64_t)d.kh * d.kw * cwe * coutp * 16;
+}
+
+int device_max_lds() {
+    static int cache[64];
+    int dev = 0;
+    if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= 64) return 65536;
+    if (cache[dev] == 0) {
+        int v = 0;
+        if (hipDeviceGetAttribute(&v, hipDeviceAttributeMaxSharedMemoryPerBlock, dev) !=
+                hipSuccess || v <= 0)
+            v = 65536;
+        cache[dev] = v;
+    }
+    return cache[dev];
+}
+
+// Stacked padded rows a 128-pixel workgroup reads, maximized over the
+// workgroups (the span repeats with the image, so one period suffices).
+int mfma_tile_rows(const lce::MfmaParams &p) {
+    const int64_t per_img = (int64_t)p.oh * p.ow;
+    const int64_t blocks = ((int64_t)p.m + lce::kMfmaPix - 1) / lce::kMfmaPix;
+    int64_t g = per_img, b = lce::kMfmaPix;
+    while (b) { const int64_t t = g % b; g = b; b = t; }
+    const int64_t period = per_img / g;           // blocks until the pattern repeats
+    auto row_of = [&](int64_t m) {
+        const int64_t img = m / per_img, r = m % per_img;
+        return img * p.ph + (r / p.ow) * p.sh;
+    };
+    int64_t best = 0;
+    for (int64_t i = 0; i < std::min(blocks, period + 1); ++i) {
+        const int64_t first = i * lce::kMfmaPix;
+        const int64_t last = std::min(first + lce::kMfmaPix - 1, (int64_t)p.m - 1);
+        best = std::max(best, row_of(last) - row_of(first) + p.kh);
+    }
+    return (int)best;
+}
+
+template <int CC, int OUT>
+void launch_mfma(const lce::MfmaParams &p, int nblk, dim3 grid, size_t lds, hipStream_t s) {
+    const dim3 block(lce::kMfmaThreads);
+    if (nblk == 4)
+        hipLaunchKernelGGL((lce::bconv2d_mfma_kernel<CC, OUT, 4>), grid, block, lds, s, p);
+    else if (nblk == 2)
+        hipLaunchKernelGGL((lce::bconv2d_mfma_kernel<CC, OUT, 2>), grid, block, lds, s, p);
+    else
+        hipLaunchKernelGGL((lce::bconv2d_mfma_kernel<CC, OUT, 1>), grid, block, lds, s, p);
+}
+
 }  // namespace
 
 extern "C" {
@@ -555,6 +619,119 @@ lce_status lce_dequantize(const int32_t *x_packed, float *out, int64_t rows, int
                            packed_words(channels));
     }
     return check_launch("lce_dequantize launch");
+}
+
+lce_status lce_bconv2d_mfma_weights_size(const lce_bconv2d_desc *desc, int64_t *bytes) {
+    if (!bytes) return fail(LCE_EINVAL, "bytes output pointer is NULL");
+    Geometry g;
+    lce_status st = validate_desc(desc, &g);
+    if (st != LCE_OK) return st;
+    *bytes = mfma_weight_bytes(*desc);
+    return ok();
+}
+
+lce_status lce_bconv2d_mfma_weights(const lce_bconv2d_desc *desc, const int32_t *w_packed,
+                                    void *w_fp4, hipStream_t stream) {
+    Geometry g;
+    lce_status st = validate_desc(desc, &g);
+    if (st != LCE_OK) return st;
+    const lce_bconv2d_desc &d = *desc;
+    if (!w_packed || !w_fp4) return fail(LCE_EINVAL, "w_packed/w_fp4 is NULL");
+    if (!aligned(w_packed, 4) || !aligned(w_fp4, 16))
+        return fail(LCE_EALIGN, "w_packed must be 4-byte and w_fp4 16-byte aligned");
+    int cc, cwe;
+    const int cw = packed_words(d.c_in);
+    mfma_chunk(cw, &cc, &cwe);
+    const int coutp = (d.c_out + 31) / 32 * 32;
+    const int taps = d.kh * d.kw;
+    const int64_t total = (int64_t)taps * cwe * coutp;
+    int64_t blocks = (total + 255) / 256;
+    if (blocks > 256 * 16) blocks = 256 * 16;
+    hipLaunchKernelGGL(lce::mfma_expand_weights_kernel, dim3((unsigned)blocks), dim3(256), 0,
+                       stream, reinterpret_cast<const uint32_t *>(w_packed),
+                       reinterpret_cast<lce::u32x4 *>(w_fp4), d.c_out, coutp, taps, cw, cwe,
+                       d.c_in);
+    return check_launch("lce_bconv2d_mfma_weights launch");
+}
+
+lce_status lce_bconv2d_mfma(const lce_bconv2d_desc *desc, const int32_t *x_packed,
+                            const void *w_fp4, const float *multiplier, const float *bias,
+                            const float *thresholds, const int32_t *flip, void *out,
+                            hipStream_t stream) {
+    Geometry g;
+    lce_status st = validate_desc(desc, &g);
+    if (st != LCE_OK) return st;
+    const lce_bconv2d_desc &d = *desc;
+    if (!x_packed || !w_fp4 || !out) return fail(LCE_EINVAL, "x_packed/w_fp4/out is NULL");
+    if (d.out_type == LCE_OUT_BITPACKED && !thresholds)
+        return fail(LCE_EINVAL, "bitpacked output needs thresholds");
+    if (!aligned(x_packed, 4) || !aligned(w_fp4, 16) || !aligned(out, 4) ||
+        (multiplier && !aligned(multiplier, 4)) || (bias && !aligned(bias, 4)) ||
+        (thresholds && !aligned(thresholds, 4)) || (flip && !aligned(flip, 4)))
+        return fail(LCE_EALIGN, "tensor pointers must be 4-byte aligned (w_fp4 16-byte)");
+    if ((int64_t)d.n * g.oh * g.ow > INT32_MAX - lce::kMfmaPix)
+        return fail(LCE_EINVAL, "too many output pixels for the matrix-core path");
+    const int64_t k = (int64_t)d.kh * d.kw * d.c_in;
+    if (k >= (1 << 24))
+        return fail(LCE_EUNSUPPORTED,
+                    "K = %lld: the matrix-core path keeps dots exact in fp32 only below 2^24",
+                    (long long)k);
+
+    lce::MfmaParams p{};
+    p.x = reinterpret_cast<const uint32_t *>(x_packed);
+    p.wexp = reinterpret_cast<const lce::u32x4 *>(w_fp4);
+    p.mult = d.out_type == LCE_OUT_FLOAT32 ? multiplier : nullptr;
+    p.bias = d.out_type == LCE_OUT_FLOAT32 ? bias : nullptr;
+    p.thr = thresholds;
+    p.flip = d.out_type == LCE_OUT_BITPACKED ? reinterpret_cast<const uint32_t *>(flip) : nullptr;
+    p.out = out;
+    int cc, cwe;
+    p.n = d.n; p.h = d.h; p.w = d.w; p.cw = packed_words(d.c_in);
+    mfma_chunk(p.cw, &cc, &cwe);
+    p.cwe = cwe;
+    p.oh = g.oh; p.ow = g.ow; p.cout = d.c_out; p.coutp = (d.c_out + 31) / 32 * 32;
+    p.cwo = packed_words(d.c_out);
+    p.kh = d.kh; p.kw = d.kw; p.sh = d.stride_h; p.sw = d.stride_w; p.pt = g.pt; p.pl = g.pl;
+    p.ph = (g.oh - 1) * d.stride_h + d.kh;
+    p.pw = (g.ow - 1) * d.stride_w + d.kw;
+    p.lo = d.clamp_min; p.hi = d.clamp_max;
+    p.m = d.n * g.oh * g.ow;
+    p.pad_zero = d.pad_value == LCE_PAD_ZERO ? 1 : 0;
+    p.div_ohw = lce::make_fastdiv((uint32_t)(g.oh * g.ow));
+    p.div_ow = lce::make_fastdiv((uint32_t)g.ow);
+    p.div_ph = lce::make_fastdiv((uint32_t)p.ph);
+    p.div_pw = lce::make_fastdiv((uint32_t)p.pw);
+    p.tile_rows = mfma_tile_rows(p);
+
+    // filter blocks per workgroup: 4, unless that leaves CUs idle
+    const int64_t pix_groups = ((int64_t)p.m + lce::kMfmaPix - 1) / lce::kMfmaPix;
+    const int64_t cus = device_simds() / 4;
+    const int blocks32 = p.coutp / 32;
+    int nblk = blocks32 >= 4 ? 4 : blocks32 >= 2 ? 2 : 1;
+    while (nblk > 1 && pix_groups * ((blocks32 + nblk - 1) / nblk) < cus) nblk /= 2;
+    nblk = env_int("LCE_MFMA_NBLK", nblk);
+    if (nblk != 1 && nblk != 2 && nblk != 4) nblk = 4;
+    // LDS: two B stages, the widened A chunk, the packed input region (with
+    // the 64-word slack of its last DMA instruction)
+    const size_t region_words = (size_t)p.tile_rows * p.pw * p.cw;
+    const size_t lds = (2 * (size_t)cc * 32 * nblk + (size_t)cc * p.tile_rows * p.pw) * 16 +
+                       (region_words + 64) * 4;
+    if (lds > (size_t)device_max_lds())
+        return fail(LCE_EUNSUPPORTED,
+                    "matrix-core tile of %zu bytes exceeds the %d bytes of LDS per workgroup "
+                    "(padded width %d, %d rows)", lds, device_max_lds(), p.pw, p.tile_rows);
+    if ((int64_t)p.tile_rows * p.pw * cc > INT32_MAX / 2)
+        return fail(LCE_EUNSUPPORTED, "matrix-core tile too large");
+    const dim3 grid((unsigned)pix_groups, (unsigned)((blocks32 + nblk - 1) / nblk));
+    switch (d.out_type * 2 + (cc == 4)) {
+        case LCE_OUT_FLOAT32 * 2 + 0: launch_mfma<2, lce::OUT_FLOAT>(p, nblk, grid, lds, stream); break;
+        case LCE_OUT_FLOAT32 * 2 + 1: launch_mfma<4, lce::OUT_FLOAT>(p, nblk, grid, lds, stream); break;
+        case LCE_OUT_BITPACKED * 2 + 0: launch_mfma<2, lce::OUT_BITS>(p, nblk, grid, lds, stream); break;
+        case LCE_OUT_BITPACKED * 2 + 1: launch_mfma<4, lce::OUT_BITS>(p, nblk, grid, lds, stream); break;
+        case LCE_OUT_INT32 * 2 + 0: launch_mfma<2, lce::OUT_INT>(p, nblk, grid, lds, stream); break;
+        default: launch_mfma<4, lce::OUT_INT>(p, nblk, grid, lds, stream); break;
+    }
+    return check_launch("lce_bconv2d_mfma launch");
 }
 
 const char *lce_last_error(void) { return g_last_error.c_str(); }

@@ -1,0 +1,175 @@
+"""GPU parity of the matrix-core path (lce_bconv2d_mfma) against the oracle.
+
+The MFMA multiplies +-1 values as 4-bit floats and accumulates in fp32, so
+its dot is the exact integer the oracle computes: int32 and bitpacked outputs
+must match bit for bit, float outputs within 1e-6 relative.  Zero padding
+(0.0 at padded locations) is checked against the oracle's pad_value=0.
+"""
+import numpy as np
+import pytest
+
+import oracle
+from tests.layer_util import (assert_match, clamp_of, dev, gpu_input, gpu_pack_weights,
+                              oracle_signs, poisoned_out)
+from workloads import Layer, config, make_layer_inputs
+
+pytestmark = pytest.mark.gpu
+
+
+@pytest.fixture(scope="module", autouse=True)
+def gpu():
+    import torch
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    import paper_2011_09398_amd as lce
+    lce.lib()
+    yield
+    torch.cuda.synchronize()
+
+
+def sync_np(t):
+    import torch
+    torch.cuda.synchronize()
+    return t.cpu().numpy()
+
+
+def mfma_run(layer, inp, *, pad_value="one", x_packed=None, w_packed=None, thresholds=None,
+             flip=None):
+    import paper_2011_09398_amd as lce
+    x_packed = gpu_input(inp) if x_packed is None else x_packed
+    w_packed = gpu_pack_weights(inp) if w_packed is None else w_packed
+    wf = lce.mfma_weights(w_packed, layer.c_in)
+    kw = {}
+    if layer.out == "float":
+        kw = dict(multiplier=dev(inp.mult), bias=dev(inp.bias))
+    elif layer.out == "bitpacked":
+        kw = dict(thresholds=dev(inp.thr if thresholds is None else thresholds),
+                  flip=None if flip is None else dev(flip))
+    return lce.bconv2d_mfma(x_packed, wf, layer.c_in, layer.c_out, (layer.kh, layer.kw),
+                            stride=layer.strides, padding=layer.padding, pad_value=pad_value,
+                            clamp=layer.clamp, out_type=layer.out, out=poisoned_out(layer), **kw)
+
+
+def oracle_run(layer, inp, a_signs, pad_value=1):
+    return oracle.bconv2d(a_signs, inp.w_sign, stride=layer.strides, padding=layer.padding,
+                          clamp_range=clamp_of(layer), out=layer.out, mult=inp.mult,
+                          bias=inp.bias, thr=inp.thr, pad_value=pad_value)
+
+
+def mfma_cases():
+    rng = np.random.default_rng(5150)
+    cases = []
+    for i in range(60):
+        k = int(rng.choice([1, 2, 3, 3, 3, 5, 7]))
+        kw = k if rng.random() < 0.8 else int(rng.choice([1, 3]))
+        s = int(rng.choice([1, 1, 2, 3]))
+        sw_ = s if rng.random() < 0.8 else int(rng.choice([1, 2]))
+        padding = "same" if rng.random() < 0.75 else "valid"
+        h, w = int(rng.integers(1, 13)), int(rng.integers(1, 13))
+        if padding == "valid":
+            h, w = max(h, k), max(w, kw)
+        c_in = int(rng.choice([1, 7, 32, 33, 64, 96, 100, 128, 160, 256, 512]))
+        c_out = int(rng.choice([1, 5, 8, 13, 32, 40, 64, 100, 128, 200]))
+        n = int(rng.integers(1, 5))
+        out = ["float", "bitpacked", "int32"][i % 3]
+        kk = k * kw * c_in
+        clamp = [None, (-kk, kk), (0, kk), (-3, 3), (0, 0)][int(rng.integers(0, 5))]
+        cases.append(Layer(f"mf{i}", n, h, w, c_in, c_out, kh=k, kw=kw, stride=s,
+                           stride_w=sw_, padding=padding, out=out, clamp=clamp,
+                           input_kind=["float", "bits"][i % 2]))
+    return cases
+
+
+@pytest.mark.parametrize("pad_value", ["one", "zero"])
+@pytest.mark.parametrize("layer", mfma_cases(), ids=lambda l: l.name)
+def test_mfma_sweep(layer, pad_value):
+    inp = make_layer_inputs(layer, 11, 97, int(layer.name[2:]))
+    got = sync_np(mfma_run(layer, inp, pad_value=pad_value))
+    ref = oracle_run(layer, inp, oracle_signs(inp), 0 if pad_value == "zero" else 1)
+    assert_match(layer, got, ref, f"{layer.name} {pad_value}")
+
+
+@pytest.mark.parametrize("cfg", [1, 2, 3])
+def test_mfma_config_parity_full(cfg):
+    for i, layer in enumerate(config(cfg)):
+        inp = make_layer_inputs(layer, 0, cfg, i)
+        got = sync_np(mfma_run(layer, inp))
+        assert_match(layer, got, oracle_run(layer, inp, oracle_signs(inp)), layer.name)
+
+
+@pytest.mark.parametrize("nblk", [1, 2, 4])
+def test_mfma_config4_sampled_every_filter_split(monkeypatch, nblk):
+    """The batch-64 layers at full size, every filter-block split."""
+    monkeypatch.setenv("LCE_MFMA_NBLK", str(nblk))
+    sample = [0, 29, 63]
+    for i, layer in enumerate(config(4)):
+        inp = make_layer_inputs(layer, 0, 4, i)
+        got = sync_np(mfma_run(layer, inp))
+        ref = oracle_run(layer, inp, oracle_signs(inp, sample))
+        assert_match(layer, got[sample], ref, f"{layer.name} nblk={nblk}")
+
+
+def test_mfma_config5_chain_every_layer():
+    """The 12-layer batch-16 stack, each layer fed the previous MFMA output."""
+    layers = config(5)
+    prev_gpu = prev_ref = None
+    for i, layer in enumerate(layers):
+        inp = make_layer_inputs(layer, 0, 5, i)
+        if prev_gpu is None:
+            x, a = gpu_input(inp), oracle_signs(inp)
+        else:
+            x, a = prev_gpu, oracle.unpack(prev_ref, layer.c_in)
+        got = mfma_run(layer, inp, x_packed=x)
+        ref = oracle_run(layer, inp, a)
+        assert_match(layer, sync_np(got), ref, f"stack {layer.name}")
+        prev_gpu, prev_ref = got, ref
+
+
+def test_mfma_matches_xor_path_bit_for_bit():
+    """Both implementations of LceBConv2d give identical outputs."""
+    from tests.layer_util import gpu_layer
+    for layer in (Layer("eqf", 2, 9, 7, 96, 72, out="float", clamp=(-40, 50), input_kind="bits"),
+                  Layer("eqb", 3, 14, 14, 256, 256, out="bitpacked", input_kind="bits"),
+                  Layer("eqs", 2, 12, 12, 64, 128, stride=2, out="int32", input_kind="bits")):
+        inp = make_layer_inputs(layer, 2, 96, layer.c_out)
+        xp, wp = gpu_input(inp), gpu_pack_weights(inp)
+        a = sync_np(gpu_layer(layer, inp, x_packed=xp, w_packed=wp))
+        b = sync_np(mfma_run(layer, inp, x_packed=xp, w_packed=wp))
+        assert np.array_equal(a.view(np.uint32), b.view(np.uint32)), layer.name
+
+
+def test_mfma_flip_and_special_thresholds():
+    layer = Layer("mthr", 2, 9, 7, 64, 72, out="bitpacked", input_kind="bits", clamp=(-20, 30))
+    inp = make_layer_inputs(layer, 5, 95, 0)
+    inp.thr[:10] = [-20.0, -20.5, -19.5, 30.0, 30.5, 31.0, np.inf, -np.inf, np.nan, 0.0]
+    rng = np.random.default_rng(3)
+    fbits = rng.integers(0, 2, 72).astype(np.uint8)
+    words = np.zeros(3, np.uint32)
+    for co, b in enumerate(fbits):
+        if b:
+            words[co // 32] |= np.uint32(1) << np.uint32(co % 32)
+    words[2] |= np.uint32(0xFFFFFF00)                 # pad bits must be ignored
+    got = sync_np(mfma_run(layer, inp, flip=words.view(np.int32)))
+    ref = oracle.bconv2d(oracle_signs(inp), inp.w_sign, out="bitpacked", thr=inp.thr,
+                         clamp_range=(-20, 30), flip=fbits)
+    assert_match(layer, got, ref, layer.name)
+
+
+def test_mfma_weights_are_zero_past_the_real_channels_and_filters():
+    """Widened filters: +-1.0 codes for real weights, 0.0 for pad channels,
+    pad words and pad filters (checked against the oracle-side signs)."""
+    import paper_2011_09398_amd as lce
+    layer = Layer("wx", 1, 4, 4, 40, 13, kh=3, kw=3, input_kind="bits")
+    inp = make_layer_inputs(layer, 1, 94, 0)
+    raw = sync_np(lce.mfma_weights(gpu_pack_weights(inp), 40)).view(np.uint32)
+    cw, cwe, coutp, taps = 2, 2, 32, 9
+    codes = np.zeros((taps * cwe, coutp, 32), np.uint8)
+    words = raw.reshape(taps * cwe, coutp, 4)
+    for j in range(32):
+        codes[..., j] = (words[..., j // 8] >> np.uint32(4 * (j % 8))) & 0xF
+    want = np.zeros_like(codes)
+    w = inp.w_sign.reshape(13, taps, 40)
+    for t in range(taps):
+        for c in range(40):
+            want[t * cwe + c // 32, :13, c % 32] = np.where(w[:, t, c] > 0, 0x2, 0xA)
+    assert np.array_equal(codes, want)
