@@ -18,9 +18,10 @@
 // word (32 channels of one tap) widened to 16 bytes; the filter side is
 // widened the same way once per filter tensor (mfma_expand_weights_kernel).
 //
-// Work decomposition: a workgroup (4 waves) owns 128 consecutive output
-// pixels and 32*NBLK filters; wave w computes pixels [32w, 32w+32) of them
-// against all the workgroup's filters (NBLK 32x32 accumulator blocks).
+// Work decomposition: a workgroup (4 waves) owns 128*MB consecutive output
+// pixels and 32*NBLK filters; each wave computes MB blocks of 32 pixels
+// against all the workgroup's filters (MB x NBLK 32x32 accumulator blocks),
+// so every B operand it reads from LDS feeds MB matrix products.
 //   * A: the input region the 128 pixels read (rows of the batch stacked as
 //     padded images, all padded columns) is widened once per channel chunk
 //     of CC words into LDS; every tap of the im2col is then an address
@@ -42,7 +43,7 @@
 
 namespace lce {
 
-constexpr int kMfmaPix = 128;      // output pixels per workgroup (32 per wave)
+constexpr int kMfmaPixMax = 256;   // output pixels per workgroup (32 or 64 per wave)
 
 // 16 bytes as a native vector (HIP's uint4 is a class, which keeps arrays of
 // it out of registers)
@@ -70,7 +71,8 @@ struct MfmaParams {
     int32_t lo, hi, m;
     int32_t tile_rows;               // stacked padded rows staged per workgroup
     int32_t pad_zero;                // 1: padded locations are 0.0
-    FastDiv div_ohw, div_ow, div_ph, div_pw;
+    int32_t region_vec;              // words per DMA lane when staging the region: 4 or 1
+    FastDiv div_ohw, div_ow, div_ph, div_pw, div_cw;
 };
 
 typedef int mfma_v8i __attribute__((ext_vector_type(8)));
@@ -103,16 +105,19 @@ __device__ __forceinline__ mfma_v16f mfma_fp4(u32x4 a, u32x4 b, mfma_v16f c) {
     return __builtin_amdgcn_mfma_scale_f32_32x32x64_f8f6f4(av, bv, c, 4, 4, 0, 127, 0, 127);
 }
 
-// Threshold as a bound on the unclamped dot: bit = clamp(dot) < thr becomes
-// dot < T with T = ceil(thr) inside (lo, hi], kAlways-like INT32_MAX when
-// ceil(thr) > hi, never (INT32_MIN) when ceil(thr) <= lo or thr is NaN.
-__device__ inline int32_t thr_to_dot_bound(float thr, int lo, int hi) {
+// Threshold as a bound on the unclamped dot, as a float: bit = clamp(dot) <
+// thr becomes dot < T with T = ceil(thr) inside (lo, hi] (|T| <= 2^24 there
+// is not needed: T only meets exact integer dots below 2^24), +infinity when
+// ceil(thr) > hi (always), -infinity when ceil(thr) <= lo or thr is NaN
+// (never).  The fp32 accumulator holds the dot exactly, so the compare is
+// one v_cmp_lt_f32 whose lane mask is the output bits.
+__device__ inline float thr_to_dot_bound_f(float thr, int lo, int hi) {
     const double t = (double)thr;
-    if (t != t) return INT32_MIN;
+    if (t != t) return -INFINITY;
     const double tc = ceil(t);
-    if (tc <= (double)lo) return INT32_MIN;
-    if (tc > (double)hi) return INT32_MAX;
-    return (int32_t)tc;
+    if (tc <= (double)lo) return -INFINITY;
+    if (tc > (double)hi) return INFINITY;
+    return (float)tc;
 }
 
 // Stacked padded row of output pixel m's window origin, and its column.
@@ -138,197 +143,267 @@ __device__ __forceinline__ void wait_vmcnt() {
     __builtin_amdgcn_s_waitcnt((N & 0xF) | ((N >> 4) << 14) | 0x70 | 0xF00);
 }
 
-constexpr int kMfmaDepth = 4;       // B stages in flight (registers) ahead of the one in use
+// s_waitcnt lgkmcnt(0) alone (vmcnt and expcnt fields at their maxima).
+__device__ __forceinline__ void wait_lgkmcnt0() { __builtin_amdgcn_s_waitcnt(0xC07F); }
 
-template <int CC, int OUT, int NBLK>
+// Workgroup barrier for the pipelined loop: this wave's LDS accesses done
+// (lgkmcnt), then s_barrier.  Unlike __syncthreads() it carries no memory
+// fence, whose release semantics would make the compiler wait for every LDS
+// DMA in flight; the DMA stages the loop needs are waited for explicitly
+// (vmcnt) before it.  Without a fence nothing stops the compiler from
+// moving an LDS read above the barrier, so the barrier returns an opaque
+// zero, produced after it, that every read of barrier-protected LDS adds to
+// its address.
+__device__ __forceinline__ int lds_barrier() {
+    int zero;
+    asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier\n\tv_mov_b32 %0, 0"
+                 : "=v"(zero) : : "memory");
+    return zero;
+}
+
+template <int CC, int OUT, int NBLK, int MB>
 __global__ __launch_bounds__(kMfmaThreads) void bconv2d_mfma_kernel(MfmaParams p) {
     constexpr int BN = 32 * NBLK;
+    constexpr int BM = 32 * MB * 4;                                   // pixels per workgroup
     constexpr int kStage = CC * BN;                                   // u32x4 per B stage
-    constexpr int kBPer = (kStage + kMfmaThreads - 1) / kMfmaThreads; // u32x4 per thread
+    constexpr int kDmaPerStage = kStage / 64;                         // 1 KB instructions
+    constexpr int kDmaPerWave = (kDmaPerStage + 3) / 4;
+    // B stages: four separate arrays, so that the compiler can tell the
+    // stage being read from the ones being written by DMA
+    __shared__ __attribute__((aligned(16))) u32x4 bslot0[kStage];
+    __shared__ __attribute__((aligned(16))) u32x4 bslot1[kStage];
+    __shared__ __attribute__((aligned(16))) u32x4 bslot2[kStage];
+    __shared__ __attribute__((aligned(16))) u32x4 bslot3[kStage];
     extern __shared__ __attribute__((aligned(16))) u32x4 smem[];
     const int tid = threadIdx.x;
     const int lane = tid & 63, half = lane >> 5, l32 = lane & 31;
     const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
-    const int m0 = blockIdx.x * kMfmaPix;
+    const int m0 = blockIdx.x * BM;
     const int n_base = blockIdx.y * BN;
     const int taps = p.kh * p.kw;
     const int chunks = p.cwe / CC;
     const int stages = chunks * taps;
     const int TR = p.tile_rows, PW = p.pw, plane = TR * PW;
     const int bits_words = plane * p.cw;                      // packed input region
-    u32x4 *bbuf = smem;                                       // [2][CC][BN]
-    u32x4 *atile = bbuf + 2 * kStage;                         // [CC][TR][PW] e2m1
+    u32x4 *atile = smem;                                      // [CC][TR][PW] e2m1
     uint32_t *abits = reinterpret_cast<uint32_t *>(atile + CC * plane);   // [TR][PW][Cw]
+    uint8_t *rowok = reinterpret_cast<uint8_t *>(abits + bits_words + 256);  // [TR]
 
     int row0, col0;
     mfma_pixel(p, m0, row0, col0);
-    const int mp = min(m0 + wave * 32 + l32, p.m - 1);
-    int prow, pcol;
-    mfma_pixel(p, mp, prow, pcol);
-    const int a_base = (half * TR + (prow - row0)) * PW + pcol;
-
-    // ---- the packed input region, by LDS DMA: tile word e = (r*PW + c)*Cw + j;
-    // padding reads the zero buffer.  The last instruction's extra lanes land
-    // in the slack of the LDS allocation.
-    for (int u = wave; u * 64 < bits_words; u += 4) {
-        const int e = min(u * 64 + lane, bits_words - 1);
-        const int rc = e / p.cw, j = e - (e / p.cw) * p.cw;
-        const int r = (int)fast_div((uint32_t)rc, p.div_pw);
-        const int c = rc - r * PW;
-        const int R = row0 + r;
-        const int img = (int)fast_div((uint32_t)R, p.div_ph);
-        const int yy = R - img * p.ph - p.pt, xx = c - p.pl;
-        const bool inside = img < p.n && (unsigned)yy < (unsigned)p.h &&
-                            (unsigned)xx < (unsigned)p.w;
-        const uint32_t *src = inside ? p.x + (((size_t)img * p.h + yy) * p.w + xx) * p.cw + j
-                                     : g_mfma_zero;
-        __builtin_amdgcn_global_load_lds((mfma_global_void *)src,
-                                         (mfma_lds_void *)(abits + u * 64), 4, 0, 0);
+    // A rows of this lane: pixel blocks b = 0..MB-1 of the wave
+    int a_base[MB];
+#pragma unroll
+    for (int b = 0; b < MB; ++b) {
+        const int mp = min(m0 + (wave * MB + b) * 32 + l32, p.m - 1);
+        int prow, pcol;
+        mfma_pixel(p, mp, prow, pcol);
+        a_base[b] = (half * TR + (prow - row0)) * PW + pcol;
     }
 
-    // ---- B stage s = (chunk s / taps, tap s % taps): words [c0, c0+CC) of the
-    // tap, filters [n_base, n_base + BN), u32x4 e = j*BN + f of the stage.
-    // Loads are unconditional (past the last stage they re-read it, and a
-    // thread past the stage re-reads its last element), so each lands
-    // straight in its ring register and the compiler's wait for it can be
-    // deferred to the store that needs it.
-    auto load_b = [&](int s, u32x4 (&r)[kBPer]) __attribute__((always_inline)) {
-        s = min(s, stages - 1);
-        const int c0 = (s / taps) * CC, t = s - (s / taps) * taps;
-#pragma unroll
-        for (int i = 0; i < kBPer; ++i) {
-            const int e = min(tid + i * kMfmaThreads, kStage - 1);
-            const int j = e / BN, f = e - (e / BN) * BN;
-            const int co = min(n_base + f, p.coutp - 1);
-            r[i] = p.wexp[(size_t)(t * p.cwe + c0 + j) * p.coutp + co];
-        }
-    };
-    auto store_b = [&](int s, const u32x4 (&r)[kBPer]) __attribute__((always_inline)) {
-        u32x4 *slot = bbuf + (s & 1) * kStage;     // (past the last stage: unused data)
-#pragma unroll
-        for (int i = 0; i < kBPer; ++i) {
-            const int e = tid + i * kMfmaThreads;
-            if (e < kStage) slot[e] = r[i];
-        }
-    };
-
-    u32x4 breg[kMfmaDepth][kBPer];
-#pragma unroll
-    for (int d = 0; d < kMfmaDepth; ++d) load_b(d, breg[d]);
-    wait_vmcnt<0>();                 // this wave's input words (and the first B stages)
-    store_b(0, breg[0]);
-    __syncthreads();
-
-    mfma_v16f acc[NBLK];
-#pragma unroll
-    for (int i = 0; i < NBLK; ++i)
-#pragma unroll
-        for (int v = 0; v < 16; ++v) acc[i][v] = 0.0f;
-
-    const uint32_t pad_lut = p.pad_zero ? 0u : kFp4PlusMinusLut;
-    auto widen_chunk = [&](int c0) __attribute__((always_inline)) {
-        for (int e = tid; e < CC * plane; e += kMfmaThreads) {
-            const int j = e / plane;
-            const int rc = e - j * plane;
+    // ---- the packed input region by LDS DMA: region word e = (r*PW + c)*Cw + j;
+    // padding reads the zero buffer.  Each lane moves region_vec words (16
+    // bytes when Cw is a multiple of 4); the last instruction's extra lanes
+    // land in the 256-word slack after the region.
+    auto stage_region = [&](auto vec_c) __attribute__((always_inline)) {
+        constexpr int V = decltype(vec_c)::value;
+        for (int u = wave; u * 64 * V < bits_words; u += 4) {
+            const int e = min(u * 64 + lane, bits_words / V - 1) * V;
+            const int rc = (int)fast_div((uint32_t)e, p.div_cw);
+            const int j = e - rc * p.cw;
             const int r = (int)fast_div((uint32_t)rc, p.div_pw);
             const int c = rc - r * PW;
             const int R = row0 + r;
             const int img = (int)fast_div((uint32_t)R, p.div_ph);
             const int yy = R - img * p.ph - p.pt, xx = c - p.pl;
-            const int word = c0 + j;
             const bool inside = img < p.n && (unsigned)yy < (unsigned)p.h &&
                                 (unsigned)xx < (unsigned)p.w;
-            uint32_t bits = 0u, lut = pad_lut;
-            if (word < p.cw && inside) {
-                bits = abits[rc * p.cw + word];
-                lut = kFp4PlusMinusLut;
+            const uint32_t *src =
+                inside ? p.x + (((size_t)img * p.h + yy) * p.w + xx) * p.cw + j : g_mfma_zero;
+            if constexpr (V == 4)
+                __builtin_amdgcn_global_load_lds((mfma_global_void *)src,
+                                                 (mfma_lds_void *)(abits + u * 64 * V), 16, 0, 0);
+            else
+                __builtin_amdgcn_global_load_lds((mfma_global_void *)src,
+                                                 (mfma_lds_void *)(abits + u * 64 * V), 4, 0, 0);
+        }
+    };
+    if (p.region_vec == 4)
+        stage_region(std::integral_constant<int, 4>{});
+    else
+        stage_region(std::integral_constant<int, 1>{});
+    // rows of the region that are image rows (zero padding needs them)
+    for (int r = tid; r < TR; r += kMfmaThreads) {
+        const int R = row0 + r;
+        const int img = (int)fast_div((uint32_t)R, p.div_ph);
+        const int yy = R - img * p.ph - p.pt;
+        rowok[r] = (uint8_t)(img < p.n && (unsigned)yy < (unsigned)p.h);
+    }
+
+    // ---- B stage s = (chunk s / taps, tap s % taps) by LDS DMA into `slot`:
+    // words [c0, c0+CC) of the tap, filters [n_base, n_base + BN); DMA
+    // instruction u moves elements e = 64u + lane, e = j*BN + f.  Stages past
+    // the last re-read it (the loop below always issues the same number of
+    // instructions, which keeps the vmcnt accounting exact).
+    auto issue_b = [&](int s, u32x4 *slot) __attribute__((always_inline)) {
+        s = min(s, stages - 1);
+        const int c0 = (s / taps) * CC, t = s - (s / taps) * taps;
+#pragma unroll
+        for (int i = 0; i < kDmaPerWave; ++i) {
+            const int u = wave + 4 * i;
+            if (u < kDmaPerStage) {
+                const int e = u * 64 + lane;
+                const int j = e / BN, f = e - (e / BN) * BN;
+                const int co = min(n_base + f, p.coutp - 1);
+                const u32x4 *src = p.wexp + (size_t)(t * p.cwe + c0 + j) * p.coutp + co;
+                __builtin_amdgcn_global_load_lds((mfma_global_void *)src,
+                                                 (mfma_lds_void *)(slot + u * 64), 16, 0, 0);
             }
-            atile[e] = widen_word(bits, lut);
+        }
+    };
+    issue_b(0, bslot0);
+    issue_b(1, bslot1);
+    issue_b(2, bslot2);
+
+    // per-lane output-transform parameters of the NBLK filters this lane
+    // stores (loaded now, used after the last stage)
+    float ep_a[NBLK], ep_b[NBLK];
+#pragma unroll
+    for (int i = 0; i < NBLK; ++i) {
+        const int co = min(n_base + 32 * i + l32, p.cout - 1);
+        if constexpr (OUT == OUT_BITS) {
+            ep_a[i] = p.thr[co];
+            ep_b[i] = 0.0f;
+        } else if constexpr (OUT == OUT_FLOAT) {
+            ep_a[i] = p.mult ? p.mult[co] : 1.0f;
+            ep_b[i] = p.bias ? p.bias[co] : 0.0f;
+        } else {
+            ep_a[i] = ep_b[i] = 0.0f;
+        }
+    }
+
+    mfma_v16f acc[MB][NBLK];
+#pragma unroll
+    for (int b = 0; b < MB; ++b)
+#pragma unroll
+        for (int i = 0; i < NBLK; ++i)
+#pragma unroll
+            for (int v = 0; v < 16; ++v) acc[b][i][v] = 0.0f;
+
+    // widen words [c0, c0+CC) of the region into the A tile (LDS -> LDS);
+    // padding locations are 0 words, i.e. +1.0, unless zero padding asks 0.0
+    auto widen_chunk = [&](int c0, int z) __attribute__((always_inline)) {
+#pragma unroll
+        for (int j = 0; j < CC; ++j) {
+            const int word = c0 + j;
+            for (int rc = tid; rc < plane; rc += kMfmaThreads) {
+                uint32_t bits = 0u, lut = kFp4PlusMinusLut;
+                if (word < p.cw) bits = abits[rc * p.cw + word + z];
+                if (p.pad_zero) {
+                    const int r = (int)fast_div((uint32_t)rc, p.div_pw);
+                    const int xx = rc - r * PW - p.pl;
+                    if (!(rowok[r + z] && (unsigned)xx < (unsigned)p.w)) lut = 0u;
+                }
+                atile[j * plane + rc] = widen_word(bits, lut);
+            }
         }
     };
 
-    // One stage: (at a chunk's first tap) widen the chunk, then the MFMAs of
-    // stage s against LDS slot s & 1; stage s+1 goes to the other slot and
-    // stage s + kMfmaDepth starts loading into the registers s freed.  The
-    // loop runs a multiple of four stages with no branch around any of them
-    // (a branch would let the compiler sink each load down to its use): a
-    // stage past the last one reads in-bounds data and feeds the MFMA a zero
-    // A operand, which adds nothing.
-    auto stage = [&](int s, u32x4 (&mine)[kBPer], u32x4 (&next)[kBPer]) __attribute__((always_inline)) {
+    // One stage: this wave's DMA of stage s has landed once at most the two
+    // later stages' instructions are outstanding; after the barrier every
+    // wave's has, and the slot of stage s-1 is free for stage s+3.  At a
+    // chunk's first tap the chunk is widened first.  The loop runs a multiple
+    // of four stages without branches around them; a stage past the last one
+    // feeds the MFMA a zero A operand, which adds nothing.
+    auto stage = [&](int s, const u32x4 *cur, u32x4 *refill) __attribute__((always_inline)) {
         const int ch = s / taps, t = s - ch * taps;
         const bool live = s < stages;
+        wait_vmcnt<2 * kDmaPerWave>();
         if (t == 0 && live) {
-            widen_chunk(ch * CC);
-            __syncthreads();
+            const int z = lds_barrier();     // the A tile is free (and the region landed)
+            widen_chunk(ch * CC, z);
         }
-        load_b(s + kMfmaDepth, mine);
+        const int z = lds_barrier();
+        issue_b(s + 3, refill);
         const int ky = t / p.kw, kx = t - (t / p.kw) * p.kw;
-        const int a_tap = a_base + ky * PW + kx;
-        const u32x4 *bt = bbuf + (s & 1) * kStage;
-        const u32x4 zero = u32x4{0u, 0u, 0u, 0u};
+        const int tap_off = ky * PW + kx;
+        const u32x4 zero = {0u, 0u, 0u, 0u};
 #pragma unroll
         for (int q = 0; q < CC / 2; ++q) {
-            u32x4 a = atile[a_tap + 2 * q * plane];
-            if (!live) a = zero;
-            u32x4 b[NBLK];
+            u32x4 a[MB];
 #pragma unroll
-            for (int i = 0; i < NBLK; ++i) b[i] = bt[(2 * q + half) * BN + 32 * i + l32];
+            for (int b = 0; b < MB; ++b) {
+                a[b] = atile[a_base[b] + tap_off + 2 * q * plane + z];
+                if (!live) a[b] = zero;
+            }
+            u32x4 bv[NBLK];
 #pragma unroll
-            for (int i = 0; i < NBLK; ++i) acc[i] = mfma_fp4(a, b[i], acc[i]);
+            for (int i = 0; i < NBLK; ++i) bv[i] = cur[(2 * q + half) * BN + 32 * i + l32 + z];
+#pragma unroll
+            for (int i = 0; i < NBLK; ++i)
+#pragma unroll
+                for (int b = 0; b < MB; ++b) acc[b][i] = mfma_fp4(a[b], bv[i], acc[b][i]);
         }
-        store_b(s + 1, next);
-        __syncthreads();
+        // Keep the stage's matrix products in the stage: they touch no memory,
+        // so without this the compiler gathers several stages' operands (and
+        // their registers) before issuing any.  The empty volatile asm stays
+        // in order with the barrier's, and takes the accumulators as operands.
+#pragma unroll
+        for (int b = 0; b < MB; ++b)
+#pragma unroll
+            for (int i = 0; i < NBLK; ++i) asm volatile("" : "+a"(acc[b][i]));
     };
-    static_assert(kMfmaDepth == 4, "the stage loop below is unrolled by four");
     for (int s = 0; s < stages; s += 4) {
-        stage(s, breg[0], breg[1]);
-        stage(s + 1, breg[1], breg[2]);
-        stage(s + 2, breg[2], breg[3]);
-        stage(s + 3, breg[3], breg[0]);
+        stage(s, bslot0, bslot3);
+        stage(s + 1, bslot1, bslot0);
+        stage(s + 2, bslot2, bslot1);
+        stage(s + 3, bslot3, bslot2);
     }
     const int nblk = min(NBLK, (p.coutp - n_base) >> 5);
 
-    // ---- epilogue: accumulator value v of block i is pixel
-    // (v/4)*8 + half*4 + v%4 of the wave and filter n_base + 32i + l32.
-    const int mw = m0 + wave * 32;
+    // ---- epilogue: accumulator value v of block (b, i) is pixel
+    // (v/4)*8 + half*4 + v%4 of pixel block b and filter n_base + 32i + l32.
 #pragma unroll
     for (int i = 0; i < NBLK; ++i) {
         if (i >= nblk) break;
         const int co = n_base + 32 * i + l32;
         const bool co_ok = co < p.cout;
-        if constexpr (OUT == OUT_BITS) {
-            const int32_t T = co_ok ? thr_to_dot_bound(p.thr[co], p.lo, p.hi) : INT32_MIN;
-            uint32_t fbit = 0;
-            if (p.flip && co_ok) fbit = (p.flip[co >> 5] >> (co & 31)) & 1u;
-            uint32_t word = 0;
 #pragma unroll
-            for (int v = 0; v < 16; ++v) {
-                const int dot = (int)acc[i][v];
-                const uint32_t bit = (uint32_t)(dot < T) ^ fbit;
-                const uint64_t mask = __ballot(bit);
-                const int r0 = (v >> 2) * 8 + (v & 3);          // pixel of lanes 0-31
-                if (lane == r0) word = (uint32_t)mask;
-                if (lane == r0 + 4) word = (uint32_t)(mask >> 32);
-            }
-            const int m = mw + lane;
-            if (lane < 32 && m < p.m)
-                reinterpret_cast<uint32_t *>(p.out)[(size_t)m * p.cwo + (co >> 5)] = word;
-        } else {
-            float mu = 1.0f, bi = 0.0f;
-            if constexpr (OUT == OUT_FLOAT) {
-                if (co_ok && p.mult) mu = p.mult[co];
-                if (co_ok && p.bias) bi = p.bias[co];
-            }
+        for (int b = 0; b < MB; ++b) {
+            const int mw = m0 + (wave * MB + b) * 32;
+            if constexpr (OUT == OUT_BITS) {
+                const float T = co_ok ? thr_to_dot_bound_f(ep_a[i], p.lo, p.hi) : -INFINITY;
+                // flip bits of the block's 32 filters, for both lane halves
+                uint64_t fmask = 0;
+                if (p.flip) {
+                    const uint32_t fw = p.flip[(n_base >> 5) + i];
+                    const uint32_t valid = co_ok ? 1u : 0u;
+                    const uint32_t fv = (uint32_t)__ballot(valid) & fw;   // filters < cout
+                    fmask = (uint64_t)fv | ((uint64_t)fv << 32);
+                }
+                uint32_t word = 0;
 #pragma unroll
-            for (int v = 0; v < 16; ++v) {
-                const int m = mw + (v >> 2) * 8 + half * 4 + (v & 3);
-                const int c = min(max((int)acc[i][v], p.lo), p.hi);
-                if (co_ok && m < p.m) {
-                    if constexpr (OUT == OUT_FLOAT)
-                        reinterpret_cast<float *>(p.out)[(size_t)m * p.cout + co] =
-                            __builtin_fmaf((float)c, mu, bi);
-                    else
-                        reinterpret_cast<int32_t *>(p.out)[(size_t)m * p.cout + co] = c;
+                for (int v = 0; v < 16; ++v) {
+                    const uint64_t mask = __ballot(acc[b][i][v] < T) ^ fmask;
+                    const int r0 = (v >> 2) * 8 + (v & 3);      // pixel of lanes 0-31
+                    if (lane == r0) word = (uint32_t)mask;
+                    if (lane == r0 + 4) word = (uint32_t)(mask >> 32);
+                }
+                const int m = mw + lane;
+                if (lane < 32 && m < p.m)
+                    reinterpret_cast<uint32_t *>(p.out)[(size_t)m * p.cwo + (co >> 5)] = word;
+            } else {
+#pragma unroll
+                for (int v = 0; v < 16; ++v) {
+                    const int m = mw + (v >> 2) * 8 + half * 4 + (v & 3);
+                    const int c = min(max((int)acc[b][i][v], p.lo), p.hi);
+                    if (co_ok && m < p.m) {
+                        if constexpr (OUT == OUT_FLOAT)
+                            reinterpret_cast<float *>(p.out)[(size_t)m * p.cout + co] =
+                                __builtin_fmaf((float)c, ep_a[i], ep_b[i]);
+                        else
+                            reinterpret_cast<int32_t *>(p.out)[(size_t)m * p.cout + co] = c;
+                    }
                 }
             }
         }

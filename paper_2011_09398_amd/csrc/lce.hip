@@ -323,12 +323,12 @@ int device_max_lds() {
     return cache[dev];
 }
 
-// Stacked padded rows a 128-pixel workgroup reads, maximized over the
+// Stacked padded rows a workgroup of `bm` pixels reads, maximized over the
 // workgroups (the span repeats with the image, so one period suffices).
-int mfma_tile_rows(const lce::MfmaParams &p) {
+int mfma_tile_rows(const lce::MfmaParams &p, int bm) {
     const int64_t per_img = (int64_t)p.oh * p.ow;
-    const int64_t blocks = ((int64_t)p.m + lce::kMfmaPix - 1) / lce::kMfmaPix;
-    int64_t g = per_img, b = lce::kMfmaPix;
+    const int64_t blocks = ((int64_t)p.m + bm - 1) / bm;
+    int64_t g = per_img, b = bm;
     while (b) { const int64_t t = g % b; g = b; b = t; }
     const int64_t period = per_img / g;           // blocks until the pattern repeats
     auto row_of = [&](int64_t m) {
@@ -337,22 +337,31 @@ int mfma_tile_rows(const lce::MfmaParams &p) {
     };
     int64_t best = 0;
     for (int64_t i = 0; i < std::min(blocks, period + 1); ++i) {
-        const int64_t first = i * lce::kMfmaPix;
-        const int64_t last = std::min(first + lce::kMfmaPix - 1, (int64_t)p.m - 1);
+        const int64_t first = i * bm;
+        const int64_t last = std::min(first + bm - 1, (int64_t)p.m - 1);
         best = std::max(best, row_of(last) - row_of(first) + p.kh);
     }
     return (int)best;
 }
 
-template <int CC, int OUT>
-void launch_mfma(const lce::MfmaParams &p, int nblk, dim3 grid, size_t lds, hipStream_t s) {
+template <int CC, int OUT, int MB>
+void launch_mfma_mb(const lce::MfmaParams &p, int nblk, dim3 grid, size_t lds, hipStream_t s) {
     const dim3 block(lce::kMfmaThreads);
     if (nblk == 4)
-        hipLaunchKernelGGL((lce::bconv2d_mfma_kernel<CC, OUT, 4>), grid, block, lds, s, p);
+        hipLaunchKernelGGL((lce::bconv2d_mfma_kernel<CC, OUT, 4, MB>), grid, block, lds, s, p);
     else if (nblk == 2)
-        hipLaunchKernelGGL((lce::bconv2d_mfma_kernel<CC, OUT, 2>), grid, block, lds, s, p);
+        hipLaunchKernelGGL((lce::bconv2d_mfma_kernel<CC, OUT, 2, MB>), grid, block, lds, s, p);
     else
-        hipLaunchKernelGGL((lce::bconv2d_mfma_kernel<CC, OUT, 1>), grid, block, lds, s, p);
+        hipLaunchKernelGGL((lce::bconv2d_mfma_kernel<CC, OUT, 1, MB>), grid, block, lds, s, p);
+}
+
+template <int CC, int OUT>
+void launch_mfma(const lce::MfmaParams &p, int nblk, int mb, dim3 grid, size_t lds,
+                 hipStream_t s) {
+    if (mb == 2)
+        launch_mfma_mb<CC, OUT, 2>(p, nblk, grid, lds, s);
+    else
+        launch_mfma_mb<CC, OUT, 1>(p, nblk, grid, lds, s);
 }
 
 }  // namespace
@@ -669,7 +678,7 @@ lce_status lce_bconv2d_mfma(const lce_bconv2d_desc *desc, const int32_t *x_packe
         (multiplier && !aligned(multiplier, 4)) || (bias && !aligned(bias, 4)) ||
         (thresholds && !aligned(thresholds, 4)) || (flip && !aligned(flip, 4)))
         return fail(LCE_EALIGN, "tensor pointers must be 4-byte aligned (w_fp4 16-byte)");
-    if ((int64_t)d.n * g.oh * g.ow > INT32_MAX - lce::kMfmaPix)
+    if ((int64_t)d.n * g.oh * g.ow > INT32_MAX - lce::kMfmaPixMax)
         return fail(LCE_EINVAL, "too many output pixels for the matrix-core path");
     const int64_t k = (int64_t)d.kh * d.kw * d.c_in;
     if (k >= (1 << 24))
@@ -697,39 +706,59 @@ lce_status lce_bconv2d_mfma(const lce_bconv2d_desc *desc, const int32_t *x_packe
     p.lo = d.clamp_min; p.hi = d.clamp_max;
     p.m = d.n * g.oh * g.ow;
     p.pad_zero = d.pad_value == LCE_PAD_ZERO ? 1 : 0;
+    p.region_vec = (p.cw % 4 == 0 && aligned(x_packed, 16)) ? 4 : 1;
     p.div_ohw = lce::make_fastdiv((uint32_t)(g.oh * g.ow));
     p.div_ow = lce::make_fastdiv((uint32_t)g.ow);
     p.div_ph = lce::make_fastdiv((uint32_t)p.ph);
     p.div_pw = lce::make_fastdiv((uint32_t)p.pw);
-    p.tile_rows = mfma_tile_rows(p);
+    p.div_cw = lce::make_fastdiv((uint32_t)p.cw);
 
-    // filter blocks per workgroup: 4, unless that leaves CUs idle
-    const int64_t pix_groups = ((int64_t)p.m + lce::kMfmaPix - 1) / lce::kMfmaPix;
+    // Work split: MB pixel blocks of 32 per wave (128*MB pixels per
+    // workgroup) and NBLK filter blocks of 32.  The largest tiles reuse each
+    // operand read from LDS most; they are kept while the grid still covers
+    // every CU.
     const int64_t cus = device_simds() / 4;
     const int blocks32 = p.coutp / 32;
-    int nblk = blocks32 >= 4 ? 4 : blocks32 >= 2 ? 2 : 1;
-    while (nblk > 1 && pix_groups * ((blocks32 + nblk - 1) / nblk) < cus) nblk /= 2;
+    const int nmax = blocks32 >= 4 ? 4 : blocks32 >= 2 ? 2 : 1;
+    static const int kSplits[][2] = {{2, 4}, {1, 4}, {2, 2}, {1, 2}, {2, 1}, {1, 1}};
+    int mb = 1, nblk = 1;
+    int64_t best_wgs = -1;
+    for (const auto &o : kSplits) {
+        if (o[1] > nmax) continue;
+        const int64_t wgs = ((int64_t)p.m + 128 * o[0] - 1) / (128 * o[0]) *
+                            ((blocks32 + o[1] - 1) / o[1]);
+        if (wgs >= cus) { mb = o[0]; nblk = o[1]; break; }
+        if (wgs > best_wgs) { best_wgs = wgs; mb = o[0]; nblk = o[1]; }
+    }
     nblk = env_int("LCE_MFMA_NBLK", nblk);
+    mb = env_int("LCE_MFMA_MB", mb);
     if (nblk != 1 && nblk != 2 && nblk != 4) nblk = 4;
-    // LDS: two B stages, the widened A chunk, the packed input region (with
-    // the 64-word slack of its last DMA instruction)
+    if (mb != 1 && mb != 2) mb = 2;
+    const int bm = 128 * mb;
+    p.tile_rows = mfma_tile_rows(p, bm);
+    const int64_t pix_groups = ((int64_t)p.m + bm - 1) / bm;
+    // dynamic LDS: the widened A chunk, the packed input region (with the
+    // 256-word slack of its last DMA instruction), one byte per region row;
+    // the four B stages are static (4 x CC x 32*NBLK x 16 bytes)
     const size_t region_words = (size_t)p.tile_rows * p.pw * p.cw;
-    const size_t lds = (2 * (size_t)cc * 32 * nblk + (size_t)cc * p.tile_rows * p.pw) * 16 +
-                       (region_words + 64) * 4;
-    if (lds > (size_t)device_max_lds())
+    const size_t lds = (size_t)cc * p.tile_rows * p.pw * 16 + (region_words + 256) * 4 +
+                       ((size_t)p.tile_rows + 15) / 16 * 16;
+    const size_t lds_static = (size_t)4 * cc * 32 * nblk * 16;
+    if (lds + lds_static > (size_t)device_max_lds())
         return fail(LCE_EUNSUPPORTED,
                     "matrix-core tile of %zu bytes exceeds the %d bytes of LDS per workgroup "
-                    "(padded width %d, %d rows)", lds, device_max_lds(), p.pw, p.tile_rows);
+                    "(padded width %d, %d rows)", lds + lds_static, device_max_lds(), p.pw,
+                    p.tile_rows);
     if ((int64_t)p.tile_rows * p.pw * cc > INT32_MAX / 2)
         return fail(LCE_EUNSUPPORTED, "matrix-core tile too large");
     const dim3 grid((unsigned)pix_groups, (unsigned)((blocks32 + nblk - 1) / nblk));
     switch (d.out_type * 2 + (cc == 4)) {
-        case LCE_OUT_FLOAT32 * 2 + 0: launch_mfma<2, lce::OUT_FLOAT>(p, nblk, grid, lds, stream); break;
-        case LCE_OUT_FLOAT32 * 2 + 1: launch_mfma<4, lce::OUT_FLOAT>(p, nblk, grid, lds, stream); break;
-        case LCE_OUT_BITPACKED * 2 + 0: launch_mfma<2, lce::OUT_BITS>(p, nblk, grid, lds, stream); break;
-        case LCE_OUT_BITPACKED * 2 + 1: launch_mfma<4, lce::OUT_BITS>(p, nblk, grid, lds, stream); break;
-        case LCE_OUT_INT32 * 2 + 0: launch_mfma<2, lce::OUT_INT>(p, nblk, grid, lds, stream); break;
-        default: launch_mfma<4, lce::OUT_INT>(p, nblk, grid, lds, stream); break;
+        case LCE_OUT_FLOAT32 * 2 + 0: launch_mfma<2, lce::OUT_FLOAT>(p, nblk, mb, grid, lds, stream); break;
+        case LCE_OUT_FLOAT32 * 2 + 1: launch_mfma<4, lce::OUT_FLOAT>(p, nblk, mb, grid, lds, stream); break;
+        case LCE_OUT_BITPACKED * 2 + 0: launch_mfma<2, lce::OUT_BITS>(p, nblk, mb, grid, lds, stream); break;
+        case LCE_OUT_BITPACKED * 2 + 1: launch_mfma<4, lce::OUT_BITS>(p, nblk, mb, grid, lds, stream); break;
+        case LCE_OUT_INT32 * 2 + 0: launch_mfma<2, lce::OUT_INT>(p, nblk, mb, grid, lds, stream); break;
+        default: launch_mfma<4, lce::OUT_INT>(p, nblk, mb, grid, lds, stream); break;
     }
     return check_launch("lce_bconv2d_mfma launch");
 }
