@@ -4,6 +4,12 @@ Default workload (one step): the four batch-64 QuickNet-shaped binary 3x3
 convolutions with bitpacked input and output: 56x56x64->128 stride 2, whose
 output feeds 28x28x128->128, then 14x14x256->256 and 7x7x512->512.
 
+Each convolution has two implementations with identical results: the XOR +
+POPCOUNT kernel of the paper's method (lce_bconv2d, VALU) and the same dot
+on the matrix cores (lce_bconv2d_mfma, +-1 widened to 4-bit floats).  Both
+are timed per layer; the step uses the faster one for each layer (--kernel
+auto, the default) or the one named by --kernel xor|mfma.
+
 Measured on the launch stream with HIP events:
   * the timed region: K steps back to back (events at its two ends, plus
     wall clock around it, synchronized on both sides) -> value, ms_per_step;
@@ -45,6 +51,8 @@ CUS, LANES, CLOCK_HZ = 256, 64, 2.4e9
 VALU_LANE_OPS = CUS * LANES * CLOCK_HZ
 BINARY_OPS_PER_LANE_OP = 32
 PEAK_BINARY_TOPS = VALU_LANE_OPS * BINARY_OPS_PER_LANE_OP / 1e12      # 1258.3
+# Dense fp4 MFMA peak (MI355X): one +-1 MAC is one fp4 MAC, 2 ops.
+PEAK_FP4_TFLOPS = 10100.0
 HBM_PEAK_GBS = 8000.0
 
 
@@ -55,6 +63,8 @@ def parse():
     ap.add_argument("--warmup", type=int, default=50)
     ap.add_argument("--reps", type=int, default=100, help="launches per per-kernel timing")
     ap.add_argument("--workload", choices=("b64", "stack16"), default="b64")
+    ap.add_argument("--kernel", choices=("auto", "xor", "mfma"), default="auto",
+                    help="convolution implementation per layer (auto: the faster)")
     ap.add_argument("--no-cpu", action="store_true", help="skip the CPU oracle baseline")
     ap.add_argument("--no-batch1", action="store_true", help="skip the batch-1 lines")
     ap.add_argument("--no-probe", action="store_true", help="skip the VALU rate probe")
@@ -86,7 +96,8 @@ class Step:
         self.layers = config(cfg_idx)
         self.inputs = [make_layer_inputs(l, 0, cfg_idx, i) for i, l in enumerate(self.layers)]
         dev = lambda a: torch.from_numpy(np.ascontiguousarray(a)).cuda()
-        self.calls, self.packs, self.outs, self.keep = [], [], [], []
+        self.xor_calls, self.mfma_calls = [], []
+        self.packs, self.outs, self.keep = [], [], []
         for i, (layer, inp) in enumerate(zip(self.layers, self.inputs)):
             w_packed = lce.bitpack(dev(inp.w_float))          # 1-bit weight storage
             pack = None
@@ -108,12 +119,34 @@ class Step:
                 out = torch.empty((layer.n, oh, ow, layer.cw_out), dtype=torch.int32,
                                   device="cuda")
                 kw = dict(thresholds=dev(inp.thr))
-            self.calls.append(lce.PreparedBConv2d(
+            self.xor_calls.append(lce.PreparedBConv2d(
                 x_packed, w_packed, layer.c_in, out, stride=layer.strides,
                 padding=layer.padding, clamp=layer.clamp, out_type=layer.out, **kw))
+            w_fp4 = lce.mfma_weights(w_packed, layer.c_in)     # widened once per filter tensor
+            m = lce.PreparedBConv2dMfma(
+                x_packed, w_fp4, layer.c_in, layer.c_out, (layer.kh, layer.kw), out,
+                stride=layer.strides, padding=layer.padding, clamp=layer.clamp,
+                out_type=layer.out, **kw)
+            m.keep = m.keep + (w_fp4,)
+            self.mfma_calls.append(m)
             self.packs.append(pack)
             self.outs.append(out)
             self.keep.append((w_packed, x_packed, kw))
+        self.calls = list(self.xor_calls)
+        self.kinds = ["xor"] * len(self.calls)
+        self.times = [None] * len(self.calls)
+
+    def choose(self, mode: str, reps: int):
+        """Time both implementations of every layer; keep the faster (auto)
+        or the named one for the step."""
+        self.times = []
+        for i, (x, m) in enumerate(zip(self.xor_calls, self.mfma_calls)):
+            tx = time_repeated(x, reps, graph=False)
+            tm = time_repeated(m, reps, graph=False)
+            self.times.append((tx, tm))
+            kind = mode if mode != "auto" else ("mfma" if tm < tx else "xor")
+            self.kinds[i] = kind
+            self.calls[i] = m if kind == "mfma" else x
 
     def run(self):
         """One pass of the hot path: bitpack any float input, then every conv."""
@@ -169,14 +202,21 @@ def time_repeated(fn, reps: int, graph: bool) -> float:
     return e0.elapsed_time(e1) / reps
 
 
-def layer_record(layer, ms, probe_tops=None):
+def layer_record(layer, ms, probe_tops=None, kind="xor", times=None):
+    """One convolution launch: binary GOPS against the roofline of the unit
+    that ran it (VALU xor+popcount, or dense fp4 MFMA)."""
     ops = layer.binary_ops
     tops = ops / (ms * 1e-3) / 1e12
-    r = {"layer": layer.name, "batch": layer.n, "us": round(ms * 1e3, 3),
-         "binary_gops": round(tops * 1e3, 1), "valu_frac": round(tops / PEAK_BINARY_TOPS, 4),
-         "binary_ops": ops}
-    if probe_tops:
-        r["probe_frac"] = round(tops / probe_tops, 4)
+    r = {"layer": layer.name, "batch": layer.n, "kernel": kind, "us": round(ms * 1e3, 3),
+         "binary_gops": round(tops * 1e3, 1), "binary_ops": ops}
+    if kind == "xor":
+        r["valu_frac"] = round(tops / PEAK_BINARY_TOPS, 4)
+        if probe_tops:
+            r["probe_frac"] = round(tops / probe_tops, 4)
+    else:
+        r["mfma_fp4_frac"] = round(tops / PEAK_FP4_TFLOPS, 4)
+    if times is not None:
+        r["us_xor"], r["us_mfma"] = round(times[0] * 1e3, 3), round(times[1] * 1e3, 3)
     return r
 
 
@@ -261,18 +301,24 @@ def memory_bound_lines(reps: int):
 
 
 def zero_padding_lines(step, reps: int, probe_tops=None):
-    """The step's layers with zero padding (correction table prepared once)."""
+    """The step's layers with zero padding: the XOR path with its correction
+    table (prepared once), and the matrix-core path (padding widened to 0.0)."""
     import paper_2011_09398_amd as lce
     lines = []
-    for call, layer, (w_packed, x_packed, kw), out in zip(step.calls, step.layers, step.keep,
-                                                          step.outs):
+    for m, layer, (w_packed, x_packed, kw), out in zip(step.mfma_calls, step.layers,
+                                                       step.keep, step.outs):
         corr = lce.pad_correction(w_packed, layer.c_in)
         z = lce.PreparedBConv2d(x_packed, w_packed, layer.c_in, out, stride=layer.strides,
                                 padding=layer.padding, pad_value="zero", clamp=layer.clamp,
                                 out_type=layer.out, pad_correction=corr, **kw)
-        r = layer_record(layer, time_repeated(z, reps, graph=False), probe_tops)
-        r["padding"] = "zero"
-        lines.append(r)
+        zm = lce.PreparedBConv2dMfma(x_packed, m.keep[1], layer.c_in, layer.c_out,
+                                     (layer.kh, layer.kw), out, stride=layer.strides,
+                                     padding=layer.padding, pad_value="zero",
+                                     clamp=layer.clamp, out_type=layer.out, **kw)
+        for kind, call in (("xor", z), ("mfma", zm)):
+            r = layer_record(layer, time_repeated(call, reps, graph=False), probe_tops, kind)
+            r["padding"] = "zero"
+            lines.append(r)
     return lines
 
 
@@ -335,11 +381,13 @@ def cpu_baseline(cfg_idx: int, target_s: float):
             "cpu": platform.processor() or platform.machine()}
 
 
-def measured_traffic(layer_name):
+def measured_traffic(layer_name, kind):
     """HBM bytes per launch from the committed counter summary, or None when
     the kernel sources have changed since those counters were taken."""
     import hashlib
-    path = os.path.join(ROOT, "profiles", "bconv2d_qn-b64_traffic.json")
+    path = os.path.join(ROOT, "profiles",
+                        "bconv2d_qn-b64_traffic.json" if kind == "xor"
+                        else "bconv2d_mfma_qn-b64_traffic.json")
     if not os.path.exists(path):
         return None
     rec = json.load(open(path))
@@ -372,6 +420,8 @@ def main():
 
     cfg_idx = 4 if args.workload == "b64" else 5
     step = Step(cfg_idx)
+    log(f"choosing the convolution implementation per layer ({args.kernel})")
+    step.choose(args.kernel, max(args.reps // 2, 20))
     if args.profile_pass:
         src = torch.ones(128 * 2 ** 20, dtype=torch.float32, device="cuda")   # 512 MiB
         dst = torch.empty_like(src)
@@ -395,20 +445,29 @@ def main():
 
     log(f"per-launch timing, {args.reps} launches each")
     layers = []
-    for pack, call, layer in zip(step.packs, step.calls, step.layers):
+    for pack, call, layer, kind, times in zip(step.packs, step.calls, step.layers, step.kinds,
+                                              step.times):
         if pack is not None:
             layers.append(bitpack_record(layer, time_repeated(pack, args.reps, graph=False)))
-        layers.append(layer_record(layer, time_repeated(call, args.reps, graph=False), probe))
+        layers.append(layer_record(layer, time_repeated(call, args.reps, graph=False), probe,
+                                   kind, times))
     conv = [r for r in layers if "binary_ops" in r]
     dom = max(conv, key=lambda r: r["us"])
-    roofline = {"bound": "alu", "achieved": round(dom["binary_gops"] / 1e3, 2),
-                "peak": round(PEAK_BINARY_TOPS, 1), "unit": "TOP/s",
-                "frac": dom["valu_frac"],
-                "traffic": measured_traffic(dom["layer"]) if cfg_idx == 4 else None,
-                "kernel": f"bconv2d {dom['layer']} (batch {dom['batch']})",
-                "per_launch_binary_ops": dom["binary_ops"], "avg_launch_us": dom["us"],
-                "probe_peak": None if probe is None else round(probe, 1),
-                "probe_frac": dom.get("probe_frac")}
+    if dom["kernel"] == "xor":
+        roofline = {"bound": "alu", "achieved": round(dom["binary_gops"] / 1e3, 2),
+                    "peak": round(PEAK_BINARY_TOPS, 1), "unit": "TOP/s",
+                    "frac": dom["valu_frac"],
+                    "traffic": measured_traffic(dom["layer"], "xor") if cfg_idx == 4 else None,
+                    "kernel": f"bconv2d (xor+popcount) {dom['layer']} (batch {dom['batch']})",
+                    "probe_peak": None if probe is None else round(probe, 1),
+                    "probe_frac": dom.get("probe_frac")}
+    else:
+        roofline = {"bound": "mfma", "achieved": round(dom["binary_gops"] / 1e3, 2),
+                    "peak": PEAK_FP4_TFLOPS, "unit": "TFLOP/s",
+                    "frac": dom["mfma_fp4_frac"],
+                    "traffic": measured_traffic(dom["layer"], "mfma") if cfg_idx == 4 else None,
+                    "kernel": f"bconv2d_mfma (fp4) {dom['layer']} (batch {dom['batch']})"}
+    roofline.update({"per_launch_binary_ops": dom["binary_ops"], "avg_launch_us": dom["us"]})
 
     zero_pad = mem_lines = None
     if not args.no_extra:
@@ -422,9 +481,13 @@ def main():
         log("batch-1 layers (graph-captured repeats)")
         s1 = Step(3)
         batch1 = []
-        for pack, call, layer in zip(s1.packs, s1.calls, s1.layers):
+        for pack, x, m, layer in zip(s1.packs, s1.xor_calls, s1.mfma_calls, s1.layers):
             batch1.append(bitpack_record(layer, time_repeated(pack, args.reps, graph=True)))
-            batch1.append(layer_record(layer, time_repeated(call, args.reps, graph=True), probe))
+            tx = time_repeated(x, args.reps, graph=True)
+            tm = time_repeated(m, args.reps, graph=True)
+            kind = args.kernel if args.kernel != "auto" else ("mfma" if tm < tx else "xor")
+            batch1.append(layer_record(layer, tm if kind == "mfma" else tx, probe, kind,
+                                       (tx, tm)))
 
     cpu = None
     if not args.no_cpu:
@@ -440,6 +503,7 @@ def main():
                    + CONFIG_NAMES[cfg_idx],
                    "batch": step.layers[0].n,
                    "layers": [l.name for l in step.layers],
+                   "kernels": step.kinds,
                    "binary_ops_per_step": total_ops},
         "event_ms_per_step": round(ev_s * 1e3 / args.steps, 5),
         "roofline": roofline, "cpu_baseline": cpu, "layers": layers, "batch1": batch1,
