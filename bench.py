@@ -71,8 +71,8 @@ def parse():
     ap.add_argument("--no-extra", action="store_true",
                     help="skip the zero-padding and memory-bound operator lines")
     ap.add_argument("--profile-pass", action="store_true",
-                    help="short run for counter collection: a 512 MiB copy (the byte-counter "
-                         "calibration) then a few steps")
+                    help="short run for counter collection: 512 MiB copies (the byte-counter "
+                         "calibration) then three launches of each implementation per layer")
     ap.add_argument("--cpu-seconds", type=float, default=10.0,
                     help="target wall time of the CPU baseline sample")
     return ap.parse_args()
@@ -420,18 +420,25 @@ def main():
 
     cfg_idx = 4 if args.workload == "b64" else 5
     step = Step(cfg_idx)
-    log(f"choosing the convolution implementation per layer ({args.kernel})")
-    step.choose(args.kernel, max(args.reps // 2, 20))
     if args.profile_pass:
+        # Counter runs: the byte-counter calibration copies, then every layer
+        # in order, three launches of each implementation (xor, then mfma).
         src = torch.ones(128 * 2 ** 20, dtype=torch.float32, device="cuda")   # 512 MiB
         dst = torch.empty_like(src)
         for _ in range(3):
             dst.copy_(src)
-        for _ in range(3):
-            step.run()
+        for pack, x, m in zip(step.packs, step.xor_calls, step.mfma_calls):
+            if pack is not None:
+                pack()
+            for call in (x, m):
+                for _ in range(3):
+                    call()
         torch.cuda.synchronize()
-        log("profile pass done: 3 copies of 512 MiB, 3 steps")
+        log("profile pass done: 3 copies of 512 MiB, then 3 launches of each "
+            "implementation per layer")
         return
+    log(f"choosing the convolution implementation per layer ({args.kernel})")
+    step.choose(args.kernel, max(args.reps // 2, 20))
     log(f"timing config {cfg_idx}: {args.warmup} warmup + {args.steps} steps")
     wall, ev_s = time_steps(step, args.steps, args.warmup)
     ms_per_step = wall * 1e3 / args.steps

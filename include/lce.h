@@ -204,6 +204,10 @@ lce_status lce_bconv2d_mfma_weights(const lce_bconv2d_desc *desc, const int32_t 
  * lce_bconv2d (multiplier/bias for FLOAT32, thresholds and optional flip for
  * BITPACKED), with the widened filters in place of w_packed and either
  * pad_value (no correction table).
+ * The work is split by shape between two schedules, pixels across the waves
+ * of a workgroup or K across them (long K); the environment variables
+ * LCE_MFMA_KS (1 / 0), LCE_MFMA_MB and LCE_MFMA_NBLK force a schedule and a
+ * tile for testing and tuning.  Every choice gives the identical output.
  * Errors: as lce_bconv2d, plus LCE_EUNSUPPORTED when K = KH*KW*C_in >= 2^24
  * or when the input region a workgroup stages exceeds the LDS of one
  * workgroup (very wide images); w_fp4 must be 16-byte aligned. */

@@ -28,8 +28,8 @@
 //     offset into it, so a word is widened once, not once per tap.
 //     Padding locations widen to +1.0 (one-padding, Section 3.2) or 0.0
 //     (zero padding): zero padding costs nothing on this path.
-//   * B: the widened filters of one tap and chunk, staged in LDS (two
-//     buffers, the next tap's copy in flight during the current tap).
+//   * B: the widened filters of one tap and chunk (a stage), streamed into
+//     LDS by DMA through four slots, three stages ahead of the one in use.
 //   * Epilogue: the fp32 accumulator is the exact integer dot; the fused
 //     activation clamp and the float transform or threshold compare follow
 //     as on the XOR path.  Bitpacked output gathers each pixel's 32 filter
@@ -72,7 +72,10 @@ struct MfmaParams {
     int32_t tile_rows;               // stacked padded rows staged per workgroup
     int32_t pad_zero;                // 1: padded locations are 0.0
     int32_t region_vec;              // words per DMA lane when staging the region: 4 or 1
-    FastDiv div_ohw, div_ow, div_ph, div_pw, div_cw;
+    FastDiv div_ohw, div_ow, div_ph, div_pw;
+    FastDiv div_plane;               // tile_rows * pw: region locations
+    FastDiv div_cwh, div_kw;         // cwe / 2 (word pairs per tap), kw
+    FastDiv div_groups;              // region_vec-word groups per location
 };
 
 typedef int mfma_v8i __attribute__((ext_vector_type(8)));
@@ -185,8 +188,11 @@ __global__ __launch_bounds__(kMfmaThreads) void bconv2d_mfma_kernel(MfmaParams p
     const int stages = chunks * taps;
     const int TR = p.tile_rows, PW = p.pw, plane = TR * PW;
     const int bits_words = plane * p.cw;                      // packed input region
+    const int V = p.region_vec;
     u32x4 *atile = smem;                                      // [CC][TR][PW] e2m1
-    uint32_t *abits = reinterpret_cast<uint32_t *>(atile + CC * plane);   // [TR][PW][Cw]
+    // packed region, word-group major: [Cw/V][TR][PW][V], so that the lanes
+    // widening one word of consecutive locations read consecutive addresses
+    uint32_t *abits = reinterpret_cast<uint32_t *>(atile + CC * plane);
     uint8_t *rowok = reinterpret_cast<uint8_t *>(abits + bits_words + 256);  // [TR]
 
     int row0, col0;
@@ -201,16 +207,18 @@ __global__ __launch_bounds__(kMfmaThreads) void bconv2d_mfma_kernel(MfmaParams p
         a_base[b] = (half * TR + (prow - row0)) * PW + pcol;
     }
 
-    // ---- the packed input region by LDS DMA: region word e = (r*PW + c)*Cw + j;
-    // padding reads the zero buffer.  Each lane moves region_vec words (16
-    // bytes when Cw is a multiple of 4); the last instruction's extra lanes
-    // land in the 256-word slack after the region.
+    // ---- the packed input region by LDS DMA: element q = g*plane + rc holds
+    // words [g*V, g*V + V) of region location rc = r*PW + c; padding reads
+    // the zero buffer.  Each lane moves one element (16 bytes when Cw is a
+    // multiple of 4); the last instruction's extra lanes land in the 256-word
+    // slack after the region.
     auto stage_region = [&](auto vec_c) __attribute__((always_inline)) {
         constexpr int V = decltype(vec_c)::value;
         for (int u = wave; u * 64 * V < bits_words; u += 4) {
-            const int e = min(u * 64 + lane, bits_words / V - 1) * V;
-            const int rc = (int)fast_div((uint32_t)e, p.div_cw);
-            const int j = e - rc * p.cw;
+            const int q = min(u * 64 + lane, bits_words / V - 1);
+            const int g = (int)fast_div((uint32_t)q, p.div_plane);
+            const int rc = q - g * plane;
+            const int j = g * V;
             const int r = (int)fast_div((uint32_t)rc, p.div_pw);
             const int c = rc - r * PW;
             const int R = row0 + r;
@@ -292,34 +300,38 @@ __global__ __launch_bounds__(kMfmaThreads) void bconv2d_mfma_kernel(MfmaParams p
 
     // widen words [c0, c0+CC) of the region into the A tile (LDS -> LDS);
     // padding locations are 0 words, i.e. +1.0, unless zero padding asks 0.0
+    // (with 16-byte elements a chunk is exactly one element: CC = 4 = V)
     auto widen_chunk = [&](int c0, int z) __attribute__((always_inline)) {
-#pragma unroll
-        for (int j = 0; j < CC; ++j) {
-            const int word = c0 + j;
-            for (int rc = tid; rc < plane; rc += kMfmaThreads) {
-                uint32_t bits = 0u, lut = kFp4PlusMinusLut;
-                if (word < p.cw) bits = abits[rc * p.cw + word + z];
-                if (p.pad_zero) {
-                    const int r = (int)fast_div((uint32_t)rc, p.div_pw);
-                    const int xx = rc - r * PW - p.pl;
-                    if (!(rowok[r + z] && (unsigned)xx < (unsigned)p.w)) lut = 0u;
-                }
-                atile[j * plane + rc] = widen_word(bits, lut);
+        for (int rc = tid; rc < plane; rc += kMfmaThreads) {
+            uint32_t lut = kFp4PlusMinusLut;
+            if (p.pad_zero) {
+                const int r = (int)fast_div((uint32_t)rc, p.div_pw);
+                const int xx = rc - r * PW - p.pl;
+                if (!(rowok[r + z] && (unsigned)xx < (unsigned)p.w)) lut = 0u;
             }
+            uint32_t bits[CC];
+            if (CC == 4 && V == 4) {
+                const u32x4 b4 = reinterpret_cast<const u32x4 *>(abits)[(c0 >> 2) * plane + rc + z];
+#pragma unroll
+                for (int j = 0; j < CC; ++j) bits[j] = b4[j];
+            } else {
+#pragma unroll
+                for (int j = 0; j < CC; ++j)
+                    bits[j] = c0 + j < p.cw ? abits[(c0 + j) * plane + rc + z] : 0u;
+            }
+#pragma unroll
+            for (int j = 0; j < CC; ++j) atile[j * plane + rc] = widen_word(bits[j], lut);
         }
     };
 
     // One stage: this wave's DMA of stage s has landed once at most the two
     // later stages' instructions are outstanding; after the barrier every
     // wave's has, and the slot of stage s-1 is free for stage s+3.  At a
-    // chunk's first tap the chunk is widened first.  The loop runs a multiple
-    // of four stages without branches around them; a stage past the last one
-    // feeds the MFMA a zero A operand, which adds nothing.
+    // chunk's first tap the chunk is widened first.
     auto stage = [&](int s, const u32x4 *cur, u32x4 *refill) __attribute__((always_inline)) {
         const int ch = s / taps, t = s - ch * taps;
-        const bool live = s < stages;
         wait_vmcnt<2 * kDmaPerWave>();
-        if (t == 0 && live) {
+        if (t == 0) {
             const int z = lds_barrier();     // the A tile is free (and the region landed)
             widen_chunk(ch * CC, z);
         }
@@ -327,15 +339,11 @@ __global__ __launch_bounds__(kMfmaThreads) void bconv2d_mfma_kernel(MfmaParams p
         issue_b(s + 3, refill);
         const int ky = t / p.kw, kx = t - (t / p.kw) * p.kw;
         const int tap_off = ky * PW + kx;
-        const u32x4 zero = {0u, 0u, 0u, 0u};
 #pragma unroll
         for (int q = 0; q < CC / 2; ++q) {
             u32x4 a[MB];
 #pragma unroll
-            for (int b = 0; b < MB; ++b) {
-                a[b] = atile[a_base[b] + tap_off + 2 * q * plane + z];
-                if (!live) a[b] = zero;
-            }
+            for (int b = 0; b < MB; ++b) a[b] = atile[a_base[b] + tap_off + 2 * q * plane + z];
             u32x4 bv[NBLK];
 #pragma unroll
             for (int i = 0; i < NBLK; ++i) bv[i] = cur[(2 * q + half) * BN + 32 * i + l32 + z];
@@ -353,12 +361,19 @@ __global__ __launch_bounds__(kMfmaThreads) void bconv2d_mfma_kernel(MfmaParams p
 #pragma unroll
             for (int i = 0; i < NBLK; ++i) asm volatile("" : "+a"(acc[b][i]));
     };
-    for (int s = 0; s < stages; s += 4) {
+    // Four stages per iteration (the slot of a stage is fixed by s % 4), then
+    // the one to three left over, under uniform branches.
+    int s = 0;
+    for (; s + 4 <= stages; s += 4) {
         stage(s, bslot0, bslot3);
         stage(s + 1, bslot1, bslot0);
         stage(s + 2, bslot2, bslot1);
         stage(s + 3, bslot3, bslot2);
     }
+    if (s < stages) stage(s, bslot0, bslot3);
+    if (s + 1 < stages) stage(s + 1, bslot1, bslot0);
+    if (s + 2 < stages) stage(s + 2, bslot2, bslot1);
+    wait_vmcnt<0>();   // the trailing prefetches land before the workgroup ends
     const int nblk = min(NBLK, (p.coutp - n_base) >> 5);
 
     // ---- epilogue: accumulator value v of block (b, i) is pixel
@@ -404,6 +419,250 @@ __global__ __launch_bounds__(kMfmaThreads) void bconv2d_mfma_kernel(MfmaParams p
                         else
                             reinterpret_cast<int32_t *>(p.out)[(size_t)m * p.cout + co] = c;
                     }
+                }
+            }
+        }
+    }
+}
+
+// K-split schedule, for layers whose output tile per workgroup is small
+// next to K (few pixels, many channels).  The four waves of a workgroup
+// compute the same 32*MBW pixels x 32*NBLK filters, each over a quarter of
+// the K steps (one K step = one tap and one pair of packed words = 64
+// channels), and add their partial sums at the end.
+//   * A: every packed word of the input region is widened into LDS once,
+//     up front (cwe planes of the region), so any wave can take any K step.
+//   * B: each wave loads the widened filters of its own K steps straight
+//     into registers, kRing - 1 steps ahead; the waves never wait for each
+//     other inside the loop.
+//   * Reduction: in three rounds each wave hands its partial sums of the
+//     blocks another wave owns to that wave through LDS (block j belongs to
+//     wave j % 4); the owner adds them (fp32 adds of integers below 2^24
+//     are exact in any order) and applies the output transform.
+constexpr int kRing = 4;
+
+template <int OUT, int NBLK, int MBW>
+__global__ __launch_bounds__(kMfmaThreads) void bconv2d_mfma_ks_kernel(MfmaParams p) {
+    constexpr int BN = 32 * NBLK;
+    constexpr int BM = 32 * MBW;
+    constexpr int kBlocks = MBW * NBLK;
+    extern __shared__ __attribute__((aligned(16))) u32x4 smem[];
+    const int tid = threadIdx.x;
+    const int lane = tid & 63, half = lane >> 5, l32 = lane & 31;
+    const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+    const int m0 = blockIdx.x * BM;
+    const int n_base = blockIdx.y * BN;
+    const int cwh = p.cwe >> 1;
+    const int ksteps = p.kh * p.kw * cwh;
+    const int TR = p.tile_rows, PW = p.pw, plane = TR * PW;
+    u32x4 *atile = smem;                                 // [cwe][TR][PW] e2m1
+
+    int row0, col0;
+    mfma_pixel(p, m0, row0, col0);
+    int a_lane[MBW];                                     // this lane's A offset per pixel block
+#pragma unroll
+    for (int b = 0; b < MBW; ++b) {
+        const int mp = min(m0 + b * 32 + l32, p.m - 1);
+        int prow, pcol;
+        mfma_pixel(p, mp, prow, pcol);
+        a_lane[b] = half * plane + (prow - row0) * PW + pcol;
+    }
+
+    // output-transform parameters of the NBLK filter blocks
+    float ep_a[NBLK], ep_b[NBLK];
+#pragma unroll
+    for (int i = 0; i < NBLK; ++i) {
+        const int co = min(n_base + 32 * i + l32, p.cout - 1);
+        if constexpr (OUT == OUT_BITS) {
+            ep_a[i] = p.thr[co];
+            ep_b[i] = 0.0f;
+        } else if constexpr (OUT == OUT_FLOAT) {
+            ep_a[i] = p.mult ? p.mult[co] : 1.0f;
+            ep_b[i] = p.bias ? p.bias[co] : 0.0f;
+        } else {
+            ep_a[i] = ep_b[i] = 0.0f;
+        }
+    }
+
+    // B of this wave's local step i (K step wave + 4i, clamped: steps past
+    // the last re-read it): word row t*cwe + 2*jp + half, NBLK blocks of 32
+    // filters, 16 bytes per lane per block.
+    const u32x4 *wcol[NBLK];
+#pragma unroll
+    for (int ib = 0; ib < NBLK; ++ib)
+        wcol[ib] = p.wexp + (size_t)half * p.coutp + min(n_base + 32 * ib + l32, p.coutp - 1);
+    auto load_b = [&](int i, u32x4 (&dst)[NBLK]) __attribute__((always_inline)) {
+        const int ks = min(wave + 4 * i, ksteps - 1);
+        const int t = (int)fast_div((uint32_t)ks, p.div_cwh);
+        const int jp = ks - t * cwh;
+        const size_t row = (size_t)(t * p.cwe + 2 * jp) * p.coutp;
+#pragma unroll
+        for (int ib = 0; ib < NBLK; ++ib) dst[ib] = wcol[ib][row];
+    };
+    u32x4 ring[kRing][NBLK];
+#pragma unroll
+    for (int r = 0; r < kRing - 1; ++r) load_b(r, ring[r]);
+
+    // ---- widen the whole region: element e = rc * groups + g holds words
+    // [g*V, g*V + V) of location rc; padding locations are 0 words (+1.0),
+    // or 0.0 under zero padding; words past Cw are +1.0 (their filter
+    // values are 0.0).  Loads are unconditional (padding reads zeros), four
+    // per thread in flight.
+    {
+        constexpr int U = 4;
+        const int V = p.region_vec;
+        const int groups = p.div_groups.d;
+        const int total = plane * groups;
+        for (int e0 = 0; e0 < total; e0 += U * kMfmaThreads) {
+            u32x4 v[U];
+            int dst[U];
+            uint32_t luts[U];
+#pragma unroll
+            for (int u = 0; u < U; ++u) {
+                const int e = min(e0 + u * kMfmaThreads + tid, total - 1);
+                const int rc = (int)fast_div((uint32_t)e, p.div_groups);
+                const int g = e - rc * groups;
+                const int r = (int)fast_div((uint32_t)rc, p.div_pw);
+                const int c = rc - r * PW;
+                const int R = row0 + r;
+                const int img = (int)fast_div((uint32_t)R, p.div_ph);
+                const int yy = R - img * p.ph - p.pt, xx = c - p.pl;
+                const bool inside = img < p.n && (unsigned)yy < (unsigned)p.h &&
+                                    (unsigned)xx < (unsigned)p.w;
+                const bool load = inside && g * V < p.cw;
+                const uint32_t *src =
+                    load ? p.x + (((size_t)img * p.h + yy) * p.w + xx) * p.cw + g * V
+                         : g_mfma_zero;
+                if (V == 4)
+                    v[u] = *reinterpret_cast<const u32x4 *>(src);
+                else
+                    v[u] = u32x4{*src, 0u, 0u, 0u};
+                dst[u] = g * V * plane + rc;
+                luts[u] = (p.pad_zero && !inside) ? 0u : kFp4PlusMinusLut;
+            }
+#pragma unroll
+            for (int u = 0; u < U; ++u) {
+                if (e0 + u * kMfmaThreads + tid >= total) continue;
+                if (V == 4) {
+#pragma unroll
+                    for (int j = 0; j < 4; ++j)
+                        atile[dst[u] + j * plane] = widen_word(v[u][j], luts[u]);
+                } else {
+                    atile[dst[u]] = widen_word(v[u][0], luts[u]);
+                }
+            }
+        }
+    }
+    int z = lds_barrier();                               // the A planes are complete
+
+    mfma_v16f acc[MBW][NBLK];
+#pragma unroll
+    for (int b = 0; b < MBW; ++b)
+#pragma unroll
+        for (int i = 0; i < NBLK; ++i)
+#pragma unroll
+            for (int v = 0; v < 16; ++v) acc[b][i][v] = 0.0f;
+
+    // Local step i with its filters in `cur`; the ring entry of step i-1
+    // (`next`) takes step i + kRing - 1.
+    auto step = [&](int i, u32x4 (&cur)[NBLK], u32x4 (&next)[NBLK])
+                    __attribute__((always_inline)) {
+        load_b(i + kRing - 1, next);
+        const int ks = wave + 4 * i;
+        const int t = (int)fast_div((uint32_t)ks, p.div_cwh);
+        const int jp = ks - t * cwh;
+        const int ky = (int)fast_div((uint32_t)t, p.div_kw);
+        const int off = 2 * jp * plane + ky * PW + (t - ky * p.kw) + z;
+        u32x4 a[MBW];
+#pragma unroll
+        for (int b = 0; b < MBW; ++b) a[b] = atile[a_lane[b] + off];
+#pragma unroll
+        for (int ib = 0; ib < NBLK; ++ib)
+#pragma unroll
+            for (int b = 0; b < MBW; ++b) acc[b][ib] = mfma_fp4(a[b], cur[ib], acc[b][ib]);
+#pragma unroll
+        for (int b = 0; b < MBW; ++b)
+#pragma unroll
+            for (int ib = 0; ib < NBLK; ++ib) asm volatile("" : "+a"(acc[b][ib]));
+    };
+    const int nsteps = ksteps > wave ? (ksteps - wave + 3) >> 2 : 0;
+    int i = 0;
+    for (; i + kRing <= nsteps; i += kRing) {
+#pragma unroll
+        for (int u = 0; u < kRing; ++u) step(i + u, ring[u], ring[(u + kRing - 1) % kRing]);
+    }
+#pragma unroll
+    for (int u = 0; u < kRing - 1; ++u)
+        if (i + u < nsteps) step(i + u, ring[u], ring[(u + kRing - 1) % kRing]);
+
+    // ---- reduction: in round r every wave w stores its partial sums of the
+    // blocks of wave (w + r) % 4 into red[(j*16 + v)*64 + lane] (one writer
+    // per block and round), and every wave adds those of its own blocks.
+    float *red = reinterpret_cast<float *>(smem);
+#pragma unroll
+    for (int r = 1; r < 4; ++r) {
+        z = lds_barrier();                               // the A planes / last round are read
+        const int to = (wave + r) & 3;
+#pragma unroll
+        for (int j = 0; j < kBlocks; ++j) {
+            if ((j & 3) != to) continue;
+#pragma unroll
+            for (int v = 0; v < 16; ++v)
+                red[(j * 16 + v) * 64 + lane + z] = acc[j / NBLK][j % NBLK][v];
+        }
+        z = lds_barrier();
+#pragma unroll
+        for (int j = 0; j < kBlocks; ++j) {
+            if ((j & 3) != wave) continue;
+#pragma unroll
+            for (int v = 0; v < 16; ++v)
+                acc[j / NBLK][j % NBLK][v] += red[(j * 16 + v) * 64 + lane + z];
+        }
+    }
+
+    // ---- epilogue on this wave's blocks.  Value v of block (b, ib) is
+    // pixel (v/4)*8 + half*4 + v%4 of pixel block b and filter
+    // n_base + 32*ib + l32.
+    const int nblk = min(NBLK, (p.coutp - n_base) >> 5);
+#pragma unroll
+    for (int j = 0; j < kBlocks; ++j) {
+        if ((j & 3) != wave) continue;
+        const int b = j / NBLK, ib = j % NBLK;
+        if (ib >= nblk) continue;
+        const mfma_v16f val = acc[b][ib];
+        const int co = n_base + 32 * ib + l32;
+        const bool co_ok = co < p.cout;
+        const int mw = m0 + b * 32;
+        if constexpr (OUT == OUT_BITS) {
+            const float T = co_ok ? thr_to_dot_bound_f(ep_a[ib], p.lo, p.hi) : -INFINITY;
+            uint64_t fmask = 0;
+            if (p.flip) {
+                const uint32_t fw = p.flip[(n_base >> 5) + ib];
+                const uint32_t fv = (uint32_t)__ballot(co_ok ? 1u : 0u) & fw;
+                fmask = (uint64_t)fv | ((uint64_t)fv << 32);
+            }
+            uint32_t word = 0;
+#pragma unroll
+            for (int v = 0; v < 16; ++v) {
+                const uint64_t mask = __ballot(val[v] < T) ^ fmask;
+                const int r0 = (v >> 2) * 8 + (v & 3);
+                if (lane == r0) word = (uint32_t)mask;
+                if (lane == r0 + 4) word = (uint32_t)(mask >> 32);
+            }
+            const int m = mw + lane;
+            if (lane < 32 && m < p.m)
+                reinterpret_cast<uint32_t *>(p.out)[(size_t)m * p.cwo + (co >> 5)] = word;
+        } else {
+#pragma unroll
+            for (int v = 0; v < 16; ++v) {
+                const int m = mw + (v >> 2) * 8 + half * 4 + (v & 3);
+                const int c = min(max((int)val[v], p.lo), p.hi);
+                if (co_ok && m < p.m) {
+                    if constexpr (OUT == OUT_FLOAT)
+                        reinterpret_cast<float *>(p.out)[(size_t)m * p.cout + co] =
+                            __builtin_fmaf((float)c, ep_a[ib], ep_b[ib]);
+                    else
+                        reinterpret_cast<int32_t *>(p.out)[(size_t)m * p.cout + co] = c;
                 }
             }
         }

@@ -4,6 +4,12 @@ The MFMA multiplies +-1 values as 4-bit floats and accumulates in fp32, so
 its dot is the exact integer the oracle computes: int32 and bitpacked outputs
 must match bit for bit, float outputs within 1e-6 relative.  Zero padding
 (0.0 at padded locations) is checked against the oracle's pad_value=0.
+
+Every test runs under both schedules of the path, forced through the
+environment: the K-split one (the four waves of a workgroup share one output
+tile and divide K; LCE_MFMA_KS=1, used where its LDS fits) and the
+pixel-split one (LCE_MFMA_KS=0).  Unforced, the library takes the K-split
+schedule for long K only.
 """
 import numpy as np
 import pytest
@@ -25,6 +31,12 @@ def gpu():
     lce.lib()
     yield
     torch.cuda.synchronize()
+
+
+@pytest.fixture(autouse=True, params=["ks", "pixel"])
+def schedule(request, monkeypatch):
+    monkeypatch.setenv("LCE_MFMA_KS", "1" if request.param == "ks" else "0")
+    return request.param
 
 
 def sync_np(t):
@@ -107,6 +119,40 @@ def test_mfma_config4_sampled_every_filter_split(monkeypatch, nblk):
         got = sync_np(mfma_run(layer, inp))
         ref = oracle_run(layer, inp, oracle_signs(inp, sample))
         assert_match(layer, got[sample], ref, f"{layer.name} nblk={nblk}")
+
+
+@pytest.mark.parametrize("mbw,nblk", [(4, 2), (2, 4), (2, 2), (4, 1), (1, 4), (2, 1), (1, 2),
+                                      (1, 1)])
+def test_mfma_every_tile_shape(monkeypatch, schedule, mbw, nblk):
+    """Every tile of either schedule: the batch-64 7x7x512 layer (sampled), a
+    ragged float layer and a stride-2 layer with zero padding."""
+    if schedule == "pixel" and mbw == 4:
+        pytest.skip("the pixel-split schedule takes 1 or 2 pixel blocks per wave")
+    monkeypatch.setenv("LCE_MFMA_MB", str(mbw))
+    monkeypatch.setenv("LCE_MFMA_NBLK", str(nblk))
+    layer = config(4)[3]
+    inp = make_layer_inputs(layer, 0, 4, 3)
+    sample = [1, 62]
+    got = sync_np(mfma_run(layer, inp))
+    assert_match(layer, got[sample], oracle_run(layer, inp, oracle_signs(inp, sample)),
+                 f"{layer.name} mb={mbw} nblk={nblk}")
+    for lay, pv in ((Layer("rag", 3, 11, 9, 100, 200, out="float", clamp=(-60, 90),
+                           input_kind="float"), "one"),
+                    (Layer("s2z", 2, 13, 10, 96, 72, stride=2, out="bitpacked",
+                           input_kind="bits"), "zero")):
+        inp = make_layer_inputs(lay, 4, 93, nblk * 10 + mbw)
+        got = sync_np(mfma_run(lay, inp, pad_value=pv))
+        ref = oracle_run(lay, inp, oracle_signs(inp), 0 if pv == "zero" else 1)
+        assert_match(lay, got, ref, f"{lay.name} mb={mbw} nblk={nblk}")
+
+
+def test_mfma_wide_region_falls_back_to_the_pixel_split(monkeypatch):
+    """A region too wide for the K-split schedule's LDS (every word of a
+    2048-channel, 60-column region) runs on the pixel-split schedule."""
+    layer = Layer("wide", 1, 5, 60, 2048, 40, out="int32", input_kind="bits")
+    inp = make_layer_inputs(layer, 6, 92, 0)
+    got = sync_np(mfma_run(layer, inp))
+    assert_match(layer, got, oracle_run(layer, inp, oracle_signs(inp)), layer.name)
 
 
 def test_mfma_config5_chain_every_layer():
