@@ -23,7 +23,9 @@ Measured on the launch stream with HIP events:
   * the memory-bound operators at sizes beyond the 256 MB last-level cache,
     inputs (or outputs) rotated over buffers totalling more than 512 MB:
     bitpack (LceQuantize), binary max pooling (LceBMaxPool2d) and
-    dequantize (LceDequantize), in GB/s of algorithmic bytes vs 8 TB/s.
+    dequantize (LceDequantize), in GB/s of algorithmic bytes vs 8 TB/s;
+  * the convolution sweep of Section 4.1 (48 batch-1 layers, 3x3 and 5x5,
+    bitpacked in, float out), both kernels from captured graphs.
 Then the CPU oracle, as it stands, on a bounded sample of the same step.
 
     python bench.py [--steps K] [--warmup W] [--no-cpu] [--workload b64|stack16]
@@ -67,6 +69,8 @@ def parse():
                     help="convolution implementation per layer (auto: the faster)")
     ap.add_argument("--no-cpu", action="store_true", help="skip the CPU oracle baseline")
     ap.add_argument("--no-batch1", action="store_true", help="skip the batch-1 lines")
+    ap.add_argument("--no-sweep", action="store_true",
+                    help="skip the convolution-sweep lines (48 batch-1 layers)")
     ap.add_argument("--no-probe", action="store_true", help="skip the VALU rate probe")
     ap.add_argument("--no-extra", action="store_true",
                     help="skip the zero-padding and memory-bound operator lines")
@@ -496,6 +500,19 @@ def main():
             batch1.append(layer_record(layer, tm if kind == "mfma" else tx, probe, kind,
                                        (tx, tm)))
 
+    sweep = None
+    if not args.no_sweep:
+        log("convolution sweep (graph-captured repeats, both kernels)")
+        s6 = Step(6)
+        sweep = []
+        for x, m, layer in zip(s6.xor_calls, s6.mfma_calls, s6.layers):
+            tx = time_repeated(x, args.reps, graph=True)
+            tm = time_repeated(m, args.reps, graph=True)
+            kind = args.kernel if args.kernel != "auto" else ("mfma" if tm < tx else "xor")
+            r = layer_record(layer, tm if kind == "mfma" else tx, probe, kind, (tx, tm))
+            r["macs"] = layer.macs
+            sweep.append(r)
+
     cpu = None
     if not args.no_cpu:
         log("CPU oracle sample")
@@ -514,7 +531,7 @@ def main():
                    "binary_ops_per_step": total_ops},
         "event_ms_per_step": round(ev_s * 1e3 / args.steps, 5),
         "roofline": roofline, "cpu_baseline": cpu, "layers": layers, "batch1": batch1,
-        "zero_padding": zero_pad, "memory_bound": mem_lines,
+        "zero_padding": zero_pad, "memory_bound": mem_lines, "conv_sweep": sweep,
         "device": torch.cuda.get_device_name(0),
     }
     print(json.dumps(line), flush=True)

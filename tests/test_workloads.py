@@ -44,3 +44,18 @@ def test_random_words_pad_bits_zero():
     assert not (x[..., 1] >> 8).any()
     ones = np.unpackbits(np.ascontiguousarray(x[..., 0]).view(np.uint8)).mean()
     assert 0.4 < ones < 0.6
+
+
+def test_conv_sweep_shapes():
+    """Section 4.1's sweep: 6 channel counts x 4 sizes x 2 kernels = 48
+    shape-preserving convolutions, 0.59 M to 6.7 G MACs (the listed
+    dimensions; the paper's printed upper bound is garbled)."""
+    c6 = config(6)
+    assert len(c6) == 48
+    assert len({(l.h, l.c_in, l.kh) for l in c6}) == 48
+    for l in c6:
+        assert l.n == 1 and l.h == l.w and l.c_in == l.c_out and l.kh == l.kw
+        assert l.strides == (1, 1) and l.padding == "same" and l.out_hw() == (l.h, l.w)
+    macs = sorted(l.macs for l in c6)
+    assert macs[0] == 8 * 8 * 32 * 32 * 9 == 589_824
+    assert macs[-1] == 64 * 64 * 256 * 256 * 25 == 6_710_886_400

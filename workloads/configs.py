@@ -1,8 +1,9 @@
 """The binary-convolution workloads: layer shapes and epilogues.
 
-Shapes come from the paper's workloads: the ResNet18 3x3 convolutions of
-Section 4.1 and the QuickNet stage widths of Table 3 (Section 5.1).  Every
-layer is a 3x3 binary convolution with one-padding (Section 3.2, LceBConv2d).
+Shapes come from the paper's workloads: the ResNet18 3x3 convolutions and
+the convolution sweep of Section 4.1, and the QuickNet stage widths of
+Table 3 (Section 5.1).  Every layer is a binary convolution with one-padding
+(Section 3.2, LceBConv2d), 3x3 except the sweep's 5x5 half.
 
 This module holds shapes only; it performs none of the method's arithmetic.
 """
@@ -128,7 +129,22 @@ def _cfg5():
     return layers
 
 
-CONFIGS = {1: _cfg1, 2: _cfg2, 3: _cfg3, 4: _cfg4, 5: _cfg5}
+SWEEP_CHANNELS = (32, 64, 96, 128, 160, 256)
+SWEEP_SIZES = (8, 16, 32, 64)
+SWEEP_KERNELS = (3, 5)
+
+
+def _cfg6():
+    # The convolution sweep of Section 4.1: every combination of channels,
+    # square input size and square kernel, stride 1, equal padding, input
+    # and output channels equal, one image.  The layer takes bitpacked
+    # activations and writes floats through the fused multiplier and bias.
+    return [Layer(f"{hw}x{hw}x{c}->{c} k{k}", 1, hw, hw, c, c, kh=k, kw=k, out="float",
+                  input_kind="bits")
+            for k in SWEEP_KERNELS for hw in SWEEP_SIZES for c in SWEEP_CHANNELS]
+
+
+CONFIGS = {1: _cfg1, 2: _cfg2, 3: _cfg3, 4: _cfg4, 5: _cfg5, 6: _cfg6}
 
 CONFIG_NAMES = {
     1: "bconv 1x8x8x64->64 3x3 s1 same, float out",
@@ -136,6 +152,7 @@ CONFIG_NAMES = {
     3: "QuickNet-shaped bconv sweep, batch 1, bitpacked out",
     4: "QuickNet-shaped bconv sweep, batch 64, pre-bitpacked in, bitpacked out",
     5: "12-layer QuickNet-like stack, batch 16, bitpacked chain, float last",
+    6: "conv sweep: C in {32..256}, H=W in {8..64}, 3x3 / 5x5, batch 1, bitpacked in, float out",
 }
 
 
