@@ -38,6 +38,7 @@
 
 #include <hip/hip_runtime.h>
 #include <stdint.h>
+#include <utility>
 
 #include "bconv.hpp"   // FastDiv, OutKind, thr_to_padz-style bounds
 
@@ -121,6 +122,48 @@ __device__ inline float thr_to_dot_bound_f(float thr, int lo, int hi) {
     if (tc <= (double)lo) return -INFINITY;
     if (tc > (double)hi) return INFINITY;
     return (float)tc;
+}
+
+// Bitpacked output of one 32x32 accumulator block.  Value v of the block is
+// pixel (v/4)*8 + half*4 + v%4 and filter lane % 32, so one ballot of
+// "value < T" over the wave gives the 32 filter bits of two pixels (lanes
+// 0-31 and 32-63); v_writelane drops each 32-bit half into the lane of its
+// pixel.  fmask (wave-uniform) flips chosen filters.  Lane l < 32 returns
+// the word of pixel l.
+//
+// The SGPR a v_writelane reads may have just been written by a VALU
+// instruction (the compare itself, when there is no flip mask).  CDNA3/4
+// require two wait states between the two that the hardware does not
+// insert, and the compiler's hazard recognizer does not look inside inline
+// asm, so each v_writelane carries its own s_nop 1.
+template <int V>
+__device__ __forceinline__ void block_bits_step(const mfma_v16f &val, float T, uint64_t fmask,
+                                                uint32_t &word) {
+    constexpr int r0 = (V >> 2) * 8 + (V & 3);
+    const uint64_t mask = __ballot(val[V] < T) ^ fmask;
+    asm("s_nop 1\n\tv_writelane_b32 %0, %1, %2" : "+v"(word) : "s"((uint32_t)mask), "i"(r0));
+    asm("s_nop 1\n\tv_writelane_b32 %0, %1, %2"
+        : "+v"(word) : "s"((uint32_t)(mask >> 32)), "i"(r0 + 4));
+}
+template <int... V>
+__device__ __forceinline__ uint32_t block_bits_impl(const mfma_v16f &val, float T,
+                                                    uint64_t fmask,
+                                                    std::integer_sequence<int, V...>) {
+    uint32_t word = 0;
+    (block_bits_step<V>(val, T, fmask, word), ...);
+    return word;
+}
+__device__ __forceinline__ uint32_t block_bits(const mfma_v16f &val, float T, uint64_t fmask) {
+    return block_bits_impl(val, T, fmask, std::make_integer_sequence<int, 16>{});
+}
+
+// Flip mask of a block of 32 filters for both lane halves, wave-uniform:
+// flip word `fw` restricted to the filters below C_out (co_ok per lane).
+__device__ __forceinline__ uint64_t block_flip(const uint32_t *flip, int word_index, bool co_ok) {
+    if (!flip) return 0;
+    const uint32_t fw = __builtin_amdgcn_readfirstlane(flip[word_index]);
+    const uint32_t fv = (uint32_t)__ballot(co_ok ? 1u : 0u) & fw;
+    return (uint64_t)fv | ((uint64_t)fv << 32);
 }
 
 // Stacked padded row of output pixel m's window origin, and its column.
@@ -324,11 +367,50 @@ __global__ __launch_bounds__(kMfmaThreads) void bconv2d_mfma_kernel(MfmaParams p
         }
     };
 
+    // Operands of one stage in registers, double-buffered: stage s reads its
+    // A and B operands from LDS and then issues the matrix products of stage
+    // s-1, whose operands arrived during the previous stage, so that the LDS
+    // reads of one stage overlap the matrix products of the other.
+    typedef u32x4 OpsA[CC / 2][MB];
+    typedef u32x4 OpsB[CC / 2][NBLK];
+    OpsA oa0, oa1;
+    OpsB ob0, ob1;
+    auto load_ops = [&](int t, const u32x4 *cur, int z, OpsA &oa, OpsB &ob)
+                        __attribute__((always_inline)) {
+        const int ky = t / p.kw, kx = t - (t / p.kw) * p.kw;
+        const int tap_off = ky * PW + kx;
+#pragma unroll
+        for (int q = 0; q < CC / 2; ++q) {
+#pragma unroll
+            for (int b = 0; b < MB; ++b) oa[q][b] = atile[a_base[b] + tap_off + 2 * q * plane + z];
+#pragma unroll
+            for (int i = 0; i < NBLK; ++i) ob[q][i] = cur[(2 * q + half) * BN + 32 * i + l32 + z];
+        }
+    };
+    // Keep a stage's matrix products where they are issued: they touch no
+    // memory, so without this the compiler gathers several stages' operands
+    // (and their registers) before issuing any.  The empty volatile asm stays
+    // in order with the barriers', and takes the accumulators as operands.
+    auto mma = [&](OpsA &oa, OpsB &ob) __attribute__((always_inline)) {
+#pragma unroll
+        for (int q = 0; q < CC / 2; ++q)
+#pragma unroll
+            for (int i = 0; i < NBLK; ++i)
+#pragma unroll
+                for (int b = 0; b < MB; ++b) acc[b][i] = mfma_fp4(oa[q][b], ob[q][i], acc[b][i]);
+#pragma unroll
+        for (int b = 0; b < MB; ++b)
+#pragma unroll
+            for (int i = 0; i < NBLK; ++i) asm volatile("" : "+a"(acc[b][i]));
+    };
+
     // One stage: this wave's DMA of stage s has landed once at most the two
     // later stages' instructions are outstanding; after the barrier every
     // wave's has, and the slot of stage s-1 is free for stage s+3.  At a
-    // chunk's first tap the chunk is widened first.
-    auto stage = [&](int s, const u32x4 *cur, u32x4 *refill) __attribute__((always_inline)) {
+    // chunk's first tap the chunk is widened first (the barrier before it
+    // also retires every wave's reads of the previous chunk).
+    auto stage = [&](int s, const u32x4 *cur, u32x4 *refill, OpsA &oa, OpsB &ob, OpsA &pa,
+                     OpsB &pb, bool first) __attribute__((always_inline)) {
         const int ch = s / taps, t = s - ch * taps;
         wait_vmcnt<2 * kDmaPerWave>();
         if (t == 0) {
@@ -337,42 +419,37 @@ __global__ __launch_bounds__(kMfmaThreads) void bconv2d_mfma_kernel(MfmaParams p
         }
         const int z = lds_barrier();
         issue_b(s + 3, refill);
-        const int ky = t / p.kw, kx = t - (t / p.kw) * p.kw;
-        const int tap_off = ky * PW + kx;
+        load_ops(t, cur, z, oa, ob);
+        if (!first) mma(pa, pb);
+    };
+    // Stage 0 alone, then four stages per iteration (the slot of a stage is
+    // fixed by s % 4, its register buffer by s % 2), then the one to three
+    // left over under uniform branches, then the last stage's products.
+    stage(0, bslot0, bslot3, oa0, ob0, oa1, ob1, true);
+    int s = 1;
+    for (; s + 4 <= stages; s += 4) {
+        stage(s, bslot1, bslot0, oa1, ob1, oa0, ob0, false);
+        stage(s + 1, bslot2, bslot1, oa0, ob0, oa1, ob1, false);
+        stage(s + 2, bslot3, bslot2, oa1, ob1, oa0, ob0, false);
+        stage(s + 3, bslot0, bslot3, oa0, ob0, oa1, ob1, false);
+    }
+    if (s < stages) stage(s, bslot1, bslot0, oa1, ob1, oa0, ob0, false);
+    if (s + 1 < stages) stage(s + 1, bslot2, bslot1, oa0, ob0, oa1, ob1, false);
+    if (s + 2 < stages) stage(s + 2, bslot3, bslot2, oa1, ob1, oa0, ob0, false);
+    {
+        // the last stage's operands sit in buffer (stages - 1) % 2
+        const bool odd = (stages - 1) & 1;
+        OpsA fa;
+        OpsB fb;
 #pragma unroll
         for (int q = 0; q < CC / 2; ++q) {
-            u32x4 a[MB];
 #pragma unroll
-            for (int b = 0; b < MB; ++b) a[b] = atile[a_base[b] + tap_off + 2 * q * plane + z];
-            u32x4 bv[NBLK];
+            for (int b = 0; b < MB; ++b) fa[q][b] = odd ? oa1[q][b] : oa0[q][b];
 #pragma unroll
-            for (int i = 0; i < NBLK; ++i) bv[i] = cur[(2 * q + half) * BN + 32 * i + l32 + z];
-#pragma unroll
-            for (int i = 0; i < NBLK; ++i)
-#pragma unroll
-                for (int b = 0; b < MB; ++b) acc[b][i] = mfma_fp4(a[b], bv[i], acc[b][i]);
+            for (int i = 0; i < NBLK; ++i) fb[q][i] = odd ? ob1[q][i] : ob0[q][i];
         }
-        // Keep the stage's matrix products in the stage: they touch no memory,
-        // so without this the compiler gathers several stages' operands (and
-        // their registers) before issuing any.  The empty volatile asm stays
-        // in order with the barrier's, and takes the accumulators as operands.
-#pragma unroll
-        for (int b = 0; b < MB; ++b)
-#pragma unroll
-            for (int i = 0; i < NBLK; ++i) asm volatile("" : "+a"(acc[b][i]));
-    };
-    // Four stages per iteration (the slot of a stage is fixed by s % 4), then
-    // the one to three left over, under uniform branches.
-    int s = 0;
-    for (; s + 4 <= stages; s += 4) {
-        stage(s, bslot0, bslot3);
-        stage(s + 1, bslot1, bslot0);
-        stage(s + 2, bslot2, bslot1);
-        stage(s + 3, bslot3, bslot2);
+        mma(fa, fb);
     }
-    if (s < stages) stage(s, bslot0, bslot3);
-    if (s + 1 < stages) stage(s + 1, bslot1, bslot0);
-    if (s + 2 < stages) stage(s + 2, bslot2, bslot1);
     wait_vmcnt<0>();   // the trailing prefetches land before the workgroup ends
     const int nblk = min(NBLK, (p.coutp - n_base) >> 5);
 
@@ -388,22 +465,10 @@ __global__ __launch_bounds__(kMfmaThreads) void bconv2d_mfma_kernel(MfmaParams p
             const int mw = m0 + (wave * MB + b) * 32;
             if constexpr (OUT == OUT_BITS) {
                 const float T = co_ok ? thr_to_dot_bound_f(ep_a[i], p.lo, p.hi) : -INFINITY;
-                // flip bits of the block's 32 filters, for both lane halves
-                uint64_t fmask = 0;
-                if (p.flip) {
-                    const uint32_t fw = p.flip[(n_base >> 5) + i];
-                    const uint32_t valid = co_ok ? 1u : 0u;
-                    const uint32_t fv = (uint32_t)__ballot(valid) & fw;   // filters < cout
-                    fmask = (uint64_t)fv | ((uint64_t)fv << 32);
-                }
-                uint32_t word = 0;
-#pragma unroll
-                for (int v = 0; v < 16; ++v) {
-                    const uint64_t mask = __ballot(acc[b][i][v] < T) ^ fmask;
-                    const int r0 = (v >> 2) * 8 + (v & 3);      // pixel of lanes 0-31
-                    if (lane == r0) word = (uint32_t)mask;
-                    if (lane == r0 + 4) word = (uint32_t)(mask >> 32);
-                }
+                // (no flip mask: a separate instance without the XOR chain)
+                const uint32_t word =
+                    p.flip ? block_bits(acc[b][i], T, block_flip(p.flip, (n_base >> 5) + i, co_ok))
+                           : block_bits(acc[b][i], T, 0);
                 const int m = mw + lane;
                 if (lane < 32 && m < p.m)
                     reinterpret_cast<uint32_t *>(p.out)[(size_t)m * p.cwo + (co >> 5)] = word;
@@ -635,20 +700,9 @@ __global__ __launch_bounds__(kMfmaThreads) void bconv2d_mfma_ks_kernel(MfmaParam
         const int mw = m0 + b * 32;
         if constexpr (OUT == OUT_BITS) {
             const float T = co_ok ? thr_to_dot_bound_f(ep_a[ib], p.lo, p.hi) : -INFINITY;
-            uint64_t fmask = 0;
-            if (p.flip) {
-                const uint32_t fw = p.flip[(n_base >> 5) + ib];
-                const uint32_t fv = (uint32_t)__ballot(co_ok ? 1u : 0u) & fw;
-                fmask = (uint64_t)fv | ((uint64_t)fv << 32);
-            }
-            uint32_t word = 0;
-#pragma unroll
-            for (int v = 0; v < 16; ++v) {
-                const uint64_t mask = __ballot(val[v] < T) ^ fmask;
-                const int r0 = (v >> 2) * 8 + (v & 3);
-                if (lane == r0) word = (uint32_t)mask;
-                if (lane == r0 + 4) word = (uint32_t)(mask >> 32);
-            }
+            const uint32_t word =
+                p.flip ? block_bits(val, T, block_flip(p.flip, (n_base >> 5) + ib, co_ok))
+                       : block_bits(val, T, 0);
             const int m = mw + lane;
             if (lane < 32 && m < p.m)
                 reinterpret_cast<uint32_t *>(p.out)[(size_t)m * p.cwo + (co >> 5)] = word;
