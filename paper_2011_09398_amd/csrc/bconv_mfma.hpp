@@ -500,10 +500,10 @@ __global__ __launch_bounds__(kMfmaThreads) void bconv2d_mfma_kernel(MfmaParams p
 //   * B: each wave loads the widened filters of its own K steps straight
 //     into registers, kRing - 1 steps ahead; the waves never wait for each
 //     other inside the loop.
-//   * Reduction: in three rounds each wave hands its partial sums of the
-//     blocks another wave owns to that wave through LDS (block j belongs to
-//     wave j % 4); the owner adds them (fp32 adds of integers below 2^24
-//     are exact in any order) and applies the output transform.
+//   * Reduction: every wave hands its partial sums of the blocks another
+//     wave owns to that wave through LDS in one exchange (block j belongs to
+//     wave j % 4); the owner adds them (fp32 adds of integers below 2^24 are
+//     exact in any order) and applies the output transform.
 constexpr int kRing = 4;
 
 template <int OUT, int NBLK, int MBW>
@@ -628,23 +628,31 @@ __global__ __launch_bounds__(kMfmaThreads) void bconv2d_mfma_ks_kernel(MfmaParam
 #pragma unroll
             for (int v = 0; v < 16; ++v) acc[b][i][v] = 0.0f;
 
-    // Local step i with its filters in `cur`; the ring entry of step i-1
-    // (`next`) takes step i + kRing - 1.
-    auto step = [&](int i, u32x4 (&cur)[NBLK], u32x4 (&next)[NBLK])
-                    __attribute__((always_inline)) {
-        load_b(i + kRing - 1, next);
-        const int ks = wave + 4 * i;
+    // A operands of local step i (clamped like the filters), double-buffered
+    // in registers: step i reads the A of step i+1 before issuing its own
+    // matrix products, so that the LDS latency hides behind them.
+    auto load_a = [&](int i, u32x4 (&dst)[MBW]) __attribute__((always_inline)) {
+        const int ks = min(wave + 4 * i, ksteps - 1);
         const int t = (int)fast_div((uint32_t)ks, p.div_cwh);
         const int jp = ks - t * cwh;
         const int ky = (int)fast_div((uint32_t)t, p.div_kw);
         const int off = 2 * jp * plane + ky * PW + (t - ky * p.kw) + z;
-        u32x4 a[MBW];
 #pragma unroll
-        for (int b = 0; b < MBW; ++b) a[b] = atile[a_lane[b] + off];
+        for (int b = 0; b < MBW; ++b) dst[b] = atile[a_lane[b] + off];
+    };
+    u32x4 abuf[2][MBW];
+    load_a(0, abuf[0]);
+
+    // Local step i with its filters in `cur` and its A in `acur`; the ring
+    // entry of step i-1 (`next`) takes step i + kRing - 1.
+    auto step = [&](int i, u32x4 (&cur)[NBLK], u32x4 (&next)[NBLK], u32x4 (&acur)[MBW],
+                    u32x4 (&anext)[MBW]) __attribute__((always_inline)) {
+        load_b(i + kRing - 1, next);
+        load_a(i + 1, anext);
 #pragma unroll
         for (int ib = 0; ib < NBLK; ++ib)
 #pragma unroll
-            for (int b = 0; b < MBW; ++b) acc[b][ib] = mfma_fp4(a[b], cur[ib], acc[b][ib]);
+            for (int b = 0; b < MBW; ++b) acc[b][ib] = mfma_fp4(acur[b], cur[ib], acc[b][ib]);
 #pragma unroll
         for (int b = 0; b < MBW; ++b)
 #pragma unroll
@@ -654,35 +662,46 @@ __global__ __launch_bounds__(kMfmaThreads) void bconv2d_mfma_ks_kernel(MfmaParam
     int i = 0;
     for (; i + kRing <= nsteps; i += kRing) {
 #pragma unroll
-        for (int u = 0; u < kRing; ++u) step(i + u, ring[u], ring[(u + kRing - 1) % kRing]);
+        for (int u = 0; u < kRing; ++u)
+            step(i + u, ring[u], ring[(u + kRing - 1) % kRing], abuf[u % 2], abuf[(u + 1) % 2]);
     }
 #pragma unroll
     for (int u = 0; u < kRing - 1; ++u)
-        if (i + u < nsteps) step(i + u, ring[u], ring[(u + kRing - 1) % kRing]);
+        if (i + u < nsteps)
+            step(i + u, ring[u], ring[(u + kRing - 1) % kRing], abuf[u % 2], abuf[(u + 1) % 2]);
 
-    // ---- reduction: in round r every wave w stores its partial sums of the
-    // blocks of wave (w + r) % 4 into red[(j*16 + v)*64 + lane] (one writer
-    // per block and round), and every wave adds those of its own blocks.
-    float *red = reinterpret_cast<float *>(smem);
+    // ---- reduction: block j belongs to wave j % 4.  Every other wave stores
+    // its partial sums of block j into a slot of its own (slot = (writer -
+    // owner - 1) % 4, 0..2), four values per lane as one 16-byte row:
+    // red[((j*3 + slot)*4 + v/4)*64 + lane] = values 4(v/4) .. +3; after one
+    // barrier each owner adds its blocks' three partials.
+    typedef float f32x4 __attribute__((ext_vector_type(4)));
+    f32x4 *red = reinterpret_cast<f32x4 *>(smem);
+    z = lds_barrier();                                   // every wave is done with the A planes
 #pragma unroll
-    for (int r = 1; r < 4; ++r) {
-        z = lds_barrier();                               // the A planes / last round are read
-        const int to = (wave + r) & 3;
+    for (int j = 0; j < kBlocks; ++j) {
+        const int owner = j & 3;
+        if (owner == wave) continue;
+        const int slot = (wave - owner - 1) & 3;
 #pragma unroll
-        for (int j = 0; j < kBlocks; ++j) {
-            if ((j & 3) != to) continue;
-#pragma unroll
-            for (int v = 0; v < 16; ++v)
-                red[(j * 16 + v) * 64 + lane + z] = acc[j / NBLK][j % NBLK][v];
+        for (int vq = 0; vq < 4; ++vq) {
+            const mfma_v16f &a = acc[j / NBLK][j % NBLK];
+            red[((j * 3 + slot) * 4 + vq) * 64 + lane + z] =
+                f32x4{a[4 * vq], a[4 * vq + 1], a[4 * vq + 2], a[4 * vq + 3]};
         }
-        z = lds_barrier();
+    }
+    z = lds_barrier();
 #pragma unroll
-        for (int j = 0; j < kBlocks; ++j) {
-            if ((j & 3) != wave) continue;
+    for (int j = 0; j < kBlocks; ++j) {
+        if ((j & 3) != wave) continue;
 #pragma unroll
-            for (int v = 0; v < 16; ++v)
-                acc[j / NBLK][j % NBLK][v] += red[(j * 16 + v) * 64 + lane + z];
-        }
+        for (int slot = 0; slot < 3; ++slot)
+#pragma unroll
+            for (int vq = 0; vq < 4; ++vq) {
+                const f32x4 r = red[((j * 3 + slot) * 4 + vq) * 64 + lane + z];
+#pragma unroll
+                for (int e = 0; e < 4; ++e) acc[j / NBLK][j % NBLK][4 * vq + e] += r[e];
+            }
     }
 
     // ---- epilogue on this wave's blocks.  Value v of block (b, ib) is

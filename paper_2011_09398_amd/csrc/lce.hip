@@ -389,10 +389,11 @@ void launch_mfma_ks(const lce::MfmaParams &p, int nblk, int mbw, dim3 grid, size
 }
 
 // LDS of the K-split kernel: every widened word of the region, or the
-// reduction buffer, which reuses it.
+// reduction buffer (three partial copies of every 32x32 block), which
+// reuses it.
 size_t mfma_ks_lds(const lce::MfmaParams &p, int mbw, int nblk, int tile_rows) {
     const size_t a = (size_t)p.cwe * tile_rows * p.pw * 16;
-    const size_t red = (size_t)mbw * nblk * 16 * 64 * 4;
+    const size_t red = (size_t)mbw * nblk * 3 * 16 * 64 * 4;
     return std::max(a, red);
 }
 
