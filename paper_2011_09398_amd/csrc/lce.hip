@@ -161,8 +161,15 @@ void launch_generic(const BconvParams &p, dim3 grid, hipStream_t s) {
                        s, p);
 }
 
+// Shapes with a specialized instance: 3x3 and 5x5 filters over the word
+// counts of 32 to 512 (3x3) or 256 (5x5) channels that networks and the
+// paper's convolution sweep use; every other shape runs the generic kernel.
 bool has_static(int cw, int kh, int kw) {
-    return kh == 3 && kw == 3 && (cw == 1 || cw == 2 || cw == 4 || cw == 8 || cw == 16);
+    if (kh == 3 && kw == 3)
+        return (cw >= 1 && cw <= 6) || cw == 8 || cw == 16;
+    if (kh == 5 && kw == 5)
+        return (cw >= 1 && cw <= 6) || cw == 8;
+    return false;
 }
 
 template <int OUT, bool PADZ>
@@ -171,9 +178,23 @@ void dispatch(const BconvParams &p, dim3 grid, hipStream_t s, int vec) {
         switch (p.cw) {
             case 1: launch_static<1, 3, 3, OUT, PADZ>(p, grid, s, vec); return;
             case 2: launch_static<2, 3, 3, OUT, PADZ>(p, grid, s, vec); return;
+            case 3: launch_static<3, 3, 3, OUT, PADZ>(p, grid, s, vec); return;
             case 4: launch_static<4, 3, 3, OUT, PADZ>(p, grid, s, vec); return;
+            case 5: launch_static<5, 3, 3, OUT, PADZ>(p, grid, s, vec); return;
+            case 6: launch_static<6, 3, 3, OUT, PADZ>(p, grid, s, vec); return;
             case 8: launch_static<8, 3, 3, OUT, PADZ>(p, grid, s, vec); return;
             case 16: launch_static<16, 3, 3, OUT, PADZ>(p, grid, s, vec); return;
+            default: break;
+        }
+    } else if (p.kh == 5 && p.kw == 5) {
+        switch (p.cw) {
+            case 1: launch_static<1, 5, 5, OUT, PADZ>(p, grid, s, vec); return;
+            case 2: launch_static<2, 5, 5, OUT, PADZ>(p, grid, s, vec); return;
+            case 3: launch_static<3, 5, 5, OUT, PADZ>(p, grid, s, vec); return;
+            case 4: launch_static<4, 5, 5, OUT, PADZ>(p, grid, s, vec); return;
+            case 5: launch_static<5, 5, 5, OUT, PADZ>(p, grid, s, vec); return;
+            case 6: launch_static<6, 5, 5, OUT, PADZ>(p, grid, s, vec); return;
+            case 8: launch_static<8, 5, 5, OUT, PADZ>(p, grid, s, vec); return;
             default: break;
         }
     }

@@ -279,6 +279,22 @@ def test_graph_replay_matches_eager():
 SCHEDULES = [(1, 1), (2, 1), (3, 1), (4, 1), (1, 2), (1, 4)]
 
 
+STATIC = [(3, cw) for cw in (1, 2, 3, 4, 5, 6, 8, 16)] + [(5, cw) for cw in (1, 2, 3, 4, 5, 6, 8)]
+
+
+@pytest.mark.parametrize("k,cw", STATIC)
+@pytest.mark.parametrize("out", ["float", "bitpacked", "int32"])
+@pytest.mark.parametrize("stride", [1, 2])
+def test_every_static_instance(k, cw, out, stride):
+    """Every shape-specialized XOR kernel (3x3 and 5x5 filters, each word
+    count with a compile-time unrolled k loop) against the oracle, on a
+    channel count that leaves pad bits in the last word."""
+    layer = Layer(f"st{k}{cw}{out}{stride}", 2, 9, 11, 32 * cw - 7, 45, kh=k, kw=k,
+                  stride=stride, out=out, input_kind="bits",
+                  clamp=(-150, 120) if out != "bitpacked" else None)
+    run_case(layer, make_layer_inputs(layer, 10 * k + cw, 59, stride))
+
+
 @pytest.mark.parametrize("nb,ks", SCHEDULES)
 @pytest.mark.parametrize("shape", [
     # (n, h, w, c_in, c_out, stride, out)
@@ -287,14 +303,17 @@ SCHEDULES = [(1, 1), (2, 1), (3, 1), (4, 1), (1, 2), (1, 4)]
     (1, 7, 7, 512, 96, 1, "int32"),
     (2, 5, 6, 256, 130, 1, "bitpacked"),
     (1, 6, 6, 32, 100, 1, "float"),
+    (2, 7, 9, 160, 70, 1, "bitpacked", 5),
+    (1, 8, 8, 96, 64, 1, "float", 5),
 ])
 def test_every_schedule_matches_oracle(monkeypatch, nb, ks, shape):
     """Every work split of the shape-specialized kernel (filter blocks per
     wave, K split across waves) gives the oracle's result."""
-    n, h, w, c_in, c_out, s, out = shape
+    n, h, w, c_in, c_out, s, out = shape[:7]
+    k = shape[7] if len(shape) > 7 else 3
     monkeypatch.setenv("LCE_BCONV_NB", str(nb))
     monkeypatch.setenv("LCE_BCONV_KS", str(ks))
-    layer = Layer(f"sched{nb}{ks}", n, h, w, c_in, c_out, stride=s, out=out,
+    layer = Layer(f"sched{nb}{ks}", n, h, w, c_in, c_out, kh=k, kw=k, stride=s, out=out,
                   clamp=(-50, 60) if out != "bitpacked" else None, input_kind="bits")
     run_case(layer, make_layer_inputs(layer, nb * 10 + ks, 60, c_out))
 

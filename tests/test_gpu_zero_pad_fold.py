@@ -119,13 +119,17 @@ def test_zero_padding_sweep(layer):
     assert_match(layer, got, ref, layer.name)
 
 
-@pytest.mark.parametrize("cw", [1, 2, 4, 8, 16])
+STATIC = [(3, cw) for cw in (1, 2, 3, 4, 5, 6, 8, 16)] + [(5, cw) for cw in (1, 2, 3, 4, 5, 6, 8)]
+
+
+@pytest.mark.parametrize("k,cw", STATIC)
 @pytest.mark.parametrize("out", ["float", "bitpacked", "int32"])
-def test_zero_padding_every_static_width(cw, out):
-    """3x3 kernels with a compile-time word count stage the table in LDS."""
-    layer = Layer(f"zs{cw}{out}", 2, 9, 11, 32 * cw, 40, out=out, input_kind="bits",
-                  clamp=(-100, 90) if out != "bitpacked" else None)
-    inp = make_layer_inputs(layer, cw, 97, len(out))
+def test_zero_padding_every_static_width(k, cw, out):
+    """Kernels with a compile-time filter size and word count (3x3, 5x5)
+    stage the table in LDS."""
+    layer = Layer(f"zs{k}{cw}{out}", 2, 9, 11, 32 * cw, 40, kh=k, kw=k, out=out,
+                  input_kind="bits", clamp=(-100, 90) if out != "bitpacked" else None)
+    inp = make_layer_inputs(layer, cw + 20 * k, 97, len(out))
     got = sync_np(gpu_run(layer, inp))
     assert_match(layer, got, oracle_run(layer, inp, oracle_signs(inp)), layer.name)
 
