@@ -71,6 +71,9 @@ def parse():
     ap.add_argument("--no-batch1", action="store_true", help="skip the batch-1 lines")
     ap.add_argument("--no-sweep", action="store_true",
                     help="skip the convolution-sweep lines (48 batch-1 layers)")
+    ap.add_argument("--sweep-only", action="store_true",
+                    help="time only the convolution sweep (for kernel traces); prints the "
+                         "sweep lines instead of the benchmark line")
     ap.add_argument("--no-probe", action="store_true", help="skip the VALU rate probe")
     ap.add_argument("--no-extra", action="store_true",
                     help="skip the zero-padding and memory-bound operator lines")
@@ -326,6 +329,21 @@ def zero_padding_lines(step, reps: int, probe_tops=None):
     return lines
 
 
+def sweep_lines(args, probe=None):
+    """The convolution sweep (48 batch-1 layers): both kernels per layer,
+    each from a captured graph of R launches (5 eager warmups first)."""
+    s6 = Step(6)
+    out = []
+    for x, m, layer in zip(s6.xor_calls, s6.mfma_calls, s6.layers):
+        tx = time_repeated(x, args.reps, graph=True)
+        tm = time_repeated(m, args.reps, graph=True)
+        kind = args.kernel if args.kernel != "auto" else ("mfma" if tm < tx else "xor")
+        r = layer_record(layer, tm if kind == "mfma" else tx, probe, kind, (tx, tm))
+        r["macs"] = layer.macs
+        out.append(r)
+    return out
+
+
 def valu_probe():
     """Achievable xor+popcount rate in binary TOP/s (a pair covers 32 MACs = 64 ops)."""
     import torch
@@ -422,6 +440,12 @@ def main():
     from workloads import CONFIG_NAMES
     lce.lib()
 
+    if args.sweep_only:
+        # diagnostic run (kernel traces of the sweep): no step, no contract line
+        log("convolution sweep only")
+        print(json.dumps({"conv_sweep": sweep_lines(args)}), flush=True)
+        return
+
     cfg_idx = 4 if args.workload == "b64" else 5
     step = Step(cfg_idx)
     if args.profile_pass:
@@ -503,15 +527,7 @@ def main():
     sweep = None
     if not args.no_sweep:
         log("convolution sweep (graph-captured repeats, both kernels)")
-        s6 = Step(6)
-        sweep = []
-        for x, m, layer in zip(s6.xor_calls, s6.mfma_calls, s6.layers):
-            tx = time_repeated(x, args.reps, graph=True)
-            tm = time_repeated(m, args.reps, graph=True)
-            kind = args.kernel if args.kernel != "auto" else ("mfma" if tm < tx else "xor")
-            r = layer_record(layer, tm if kind == "mfma" else tx, probe, kind, (tx, tm))
-            r["macs"] = layer.macs
-            sweep.append(r)
+        sweep = sweep_lines(args, probe)
 
     cpu = None
     if not args.no_cpu:
