@@ -194,8 +194,10 @@ lce_status lce_bconv2d_mfma_weights_size(const lce_bconv2d_desc *desc, int64_t *
 
 /* Widen packed filters w_packed (as for lce_bconv2d, device, 4-byte aligned)
  * into w_fp4 (device, 16-byte aligned, lce_bconv2d_mfma_weights_size bytes),
- * asynchronously on `stream`.  Channels past C_in and filters past C_out
- * widen to 0.0.  Run once per filter tensor.
+ * asynchronously on `stream`.  Layout: 16-byte element (t*Cw' + j)*C_out' + co
+ * holds word j of tap t of filter co as 32 e2m1 codes (+1.0 = 0x2,
+ * -1.0 = 0xA), channel 32j + c in 32-bit word c % 4, nibble c / 4.  Channels
+ * past C_in and filters past C_out widen to 0.0.  Run once per filter tensor.
  * Errors: LCE_EINVAL, LCE_EALIGN, LCE_EHIP. */
 lce_status lce_bconv2d_mfma_weights(const lce_bconv2d_desc *desc, const int32_t *w_packed,
                                     void *w_fp4, hipStream_t stream);
@@ -204,10 +206,15 @@ lce_status lce_bconv2d_mfma_weights(const lce_bconv2d_desc *desc, const int32_t 
  * lce_bconv2d (multiplier/bias for FLOAT32, thresholds and optional flip for
  * BITPACKED), with the widened filters in place of w_packed and either
  * pad_value (no correction table).
- * The work is split by shape between two schedules, pixels across the waves
- * of a workgroup or K across them (long K); the environment variables
- * LCE_MFMA_KS (1 / 0), LCE_MFMA_MB and LCE_MFMA_NBLK force a schedule and a
- * tile for testing and tuning.  Every choice gives the identical output.
+ * The work is split by shape between three schedules: filter-stationary
+ * (each wave keeps its filters in registers and runs through about one
+ * CU's share of pixel blocks; up to 36 K steps of 64 channels), K-split
+ * (the waves of a workgroup divide K; long K) and pixel-split (the rest).
+ * The environment variables LCE_MFMA_FS (0 turns the first off),
+ * LCE_MFMA_FS_KS / LCE_MFMA_FS_S (its instance), LCE_MFMA_FS_PAD (one
+ * workgroup per CU by LDS size), LCE_MFMA_KS (1 / 0: K-split / pixel-split),
+ * LCE_MFMA_MB and LCE_MFMA_NBLK force a schedule and a tile for testing and
+ * tuning.  Every choice gives the identical output.
  * Errors: as lce_bconv2d, plus LCE_EUNSUPPORTED when K = KH*KW*C_in >= 2^24
  * or when the input region a workgroup stages exceeds the LDS of one
  * workgroup (very wide images); w_fp4 must be 16-byte aligned. */

@@ -51,11 +51,11 @@ constexpr int kMfmaPixMax = 256;   // output pixels per workgroup (32 or 64 per 
 typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
 constexpr int kMfmaThreads = 256;
 
-// e2m1 codes: +1.0 = 0x2, -1.0 = 0xA.  Byte for two bits (lo, hi):
-// code(lo) | code(hi) << 4, indexed by lo | hi << 1.
-constexpr uint32_t kFp4PlusMinusLut = 0xAAA22A22u;
-// Byte for two validity bits: 0xF for each valid half, 0x0 otherwise.
-constexpr uint32_t kFp4ValidLut = 0xFFF00F00u;
+// e2m1 codes: +1.0 = 0x2, -1.0 = 0xA (the sign is bit 3 of the nibble).
+// A widened word fills all eight nibbles of each 32-bit lane word with
+// +1.0 before the sign bits are ORed in; zero padding fills them with 0.0.
+constexpr uint32_t kFp4PlusOne = 0x22222222u;
+constexpr uint32_t kFp4SignBits = 0x88888888u;
 
 struct MfmaParams {
     const uint32_t *x;      // [N][H][W][Cw] bitpacked activations
@@ -71,6 +71,7 @@ struct MfmaParams {
     int32_t ph, pw;                  // padded image: (OH-1)*sh + KH rows, (OW-1)*sw + KW cols
     int32_t lo, hi, m;
     int32_t tile_rows;               // stacked padded rows staged per workgroup
+    int32_t fs_pixels;               // output pixels per workgroup (filter-stationary)
     int32_t pad_zero;                // 1: padded locations are 0.0
     int32_t region_vec;              // words per DMA lane when staging the region: 4 or 1
     FastDiv div_ohw, div_ow, div_ph, div_pw;
@@ -83,22 +84,30 @@ typedef int mfma_v8i __attribute__((ext_vector_type(8)));
 typedef float mfma_v16f __attribute__((ext_vector_type(16)));
 
 
-// One packed byte -> four bytes holding its 2-bit groups (bits 2i, 2i+1 of
-// x land in bits 0-1 of byte i).
-__device__ __forceinline__ uint32_t spread_pairs(uint32_t x) {
-    uint32_t t = ((x << 12) | x) & 0x000F000Fu;
-    return ((t << 6) | t) & 0x03030303u;
+// Packed word -> 32 e2m1 codes (16 bytes).  The order of k inside an MFMA
+// operand is free as long as both operands use the same one, so channel c of
+// the word goes where it is cheapest: 32-bit word c % 4, nibble c / 4.  Then
+// word d of the result is the packed word shifted so that channels d, d+4,
+// ... land on the nibbles' sign bits, masked, over a field of +1.0 codes:
+// two ALU operations per 32-bit word.  `fill` is kFp4PlusOne (bit 0 -> +1.0,
+// bit 1 -> -1.0), or 0 for an all-0.0 location (zero padding; its bits are 0).
+__device__ __forceinline__ u32x4 widen_word(uint32_t w, uint32_t fill) {
+    u32x4 o;
+    o.x = ((w << 3) & kFp4SignBits) | fill;
+    o.y = ((w << 2) & kFp4SignBits) | fill;
+    o.z = ((w << 1) & kFp4SignBits) | fill;
+    o.w = (w & kFp4SignBits) | fill;
+    return o;
 }
 
-// Packed word -> 32 e2m1 codes (16 bytes), channel c in nibble c of the
-// result (little-endian): the lookup `lut` maps each 2-bit group to a byte
-// (kFp4PlusMinusLut for +-1.0, 0 for all 0.0).
-__device__ __forceinline__ u32x4 widen_word(uint32_t w, uint32_t lut) {
+// Mask of the nibbles a widened word may keep: nibble c/4 of 32-bit word
+// c % 4 is 0xF for every channel c whose bit is set in `valid`.
+__device__ __forceinline__ u32x4 widen_valid_mask(uint32_t valid) {
     u32x4 o;
-    o.x = __builtin_amdgcn_perm(lut, lut, spread_pairs(w & 0xFFu));
-    o.y = __builtin_amdgcn_perm(lut, lut, spread_pairs((w >> 8) & 0xFFu));
-    o.z = __builtin_amdgcn_perm(lut, lut, spread_pairs((w >> 16) & 0xFFu));
-    o.w = __builtin_amdgcn_perm(lut, lut, spread_pairs(w >> 24));
+    o.x = (((valid << 3) & kFp4SignBits) >> 3) * 0xFu;
+    o.y = (((valid << 2) & kFp4SignBits) >> 3) * 0xFu;
+    o.z = (((valid << 1) & kFp4SignBits) >> 3) * 0xFu;
+    o.w = ((valid & kFp4SignBits) >> 3) * 0xFu;
     return o;
 }
 
@@ -346,11 +355,11 @@ __global__ __launch_bounds__(kMfmaThreads) void bconv2d_mfma_kernel(MfmaParams p
     // (with 16-byte elements a chunk is exactly one element: CC = 4 = V)
     auto widen_chunk = [&](int c0, int z) __attribute__((always_inline)) {
         for (int rc = tid; rc < plane; rc += kMfmaThreads) {
-            uint32_t lut = kFp4PlusMinusLut;
+            uint32_t fill = kFp4PlusOne;
             if (p.pad_zero) {
                 const int r = (int)fast_div((uint32_t)rc, p.div_pw);
                 const int xx = rc - r * PW - p.pl;
-                if (!(rowok[r + z] && (unsigned)xx < (unsigned)p.w)) lut = 0u;
+                if (!(rowok[r + z] && (unsigned)xx < (unsigned)p.w)) fill = 0u;
             }
             uint32_t bits[CC];
             if (CC == 4 && V == 4) {
@@ -363,7 +372,7 @@ __global__ __launch_bounds__(kMfmaThreads) void bconv2d_mfma_kernel(MfmaParams p
                     bits[j] = c0 + j < p.cw ? abits[(c0 + j) * plane + rc + z] : 0u;
             }
 #pragma unroll
-            for (int j = 0; j < CC; ++j) atile[j * plane + rc] = widen_word(bits[j], lut);
+            for (int j = 0; j < CC; ++j) atile[j * plane + rc] = widen_word(bits[j], fill);
         }
     };
 
@@ -490,6 +499,69 @@ __global__ __launch_bounds__(kMfmaThreads) void bconv2d_mfma_kernel(MfmaParams p
     }
 }
 
+// Widen the packed input region of a workgroup into LDS, every word of it:
+// atile[j*plane + rc] = word j of region location rc (rc = r*PW + c over
+// TR stacked padded rows from row0).  Padding locations are 0 words (+1.0),
+// or 0.0 under zero padding; words past Cw are +1.0 (their filter values
+// are 0.0).  Loads are unconditional (padding reads zeros), four per thread
+// in flight.
+__device__ __forceinline__ void widen_region(const MfmaParams &p, u32x4 *atile, int row0,
+                                             int plane, int tid) {
+    constexpr int U = 4;
+    const int V = p.region_vec;
+    const int groups = p.div_groups.d;
+    const int total = plane * groups;
+    const int PW = p.pw;
+    for (int e0 = 0; e0 < total; e0 += U * kMfmaThreads) {
+        u32x4 v[U];
+        int dst[U];
+        uint32_t fills[U];
+#pragma unroll
+        for (int u = 0; u < U; ++u) {
+            const int e = min(e0 + u * kMfmaThreads + tid, total - 1);
+            const int rc = (int)fast_div((uint32_t)e, p.div_groups);
+            const int g = e - rc * groups;
+            const int r = (int)fast_div((uint32_t)rc, p.div_pw);
+            const int c = rc - r * PW;
+            const int R = row0 + r;
+            const int img = (int)fast_div((uint32_t)R, p.div_ph);
+            const int yy = R - img * p.ph - p.pt, xx = c - p.pl;
+            const bool inside = img < p.n && (unsigned)yy < (unsigned)p.h &&
+                                (unsigned)xx < (unsigned)p.w;
+            const bool load = inside && g * V < p.cw;
+            const uint32_t *src =
+                load ? p.x + (((size_t)img * p.h + yy) * p.w + xx) * p.cw + g * V : g_mfma_zero;
+            if (V == 4)
+                v[u] = *reinterpret_cast<const u32x4 *>(src);
+            else
+                v[u] = u32x4{*src, 0u, 0u, 0u};
+            dst[u] = g * V * plane + rc;
+            fills[u] = (p.pad_zero && !inside) ? 0u : kFp4PlusOne;
+        }
+#pragma unroll
+        for (int u = 0; u < U; ++u) {
+            if (e0 + u * kMfmaThreads + tid >= total) continue;
+            if (V == 4) {
+#pragma unroll
+                for (int j = 0; j < 4; ++j) atile[dst[u] + j * plane] = widen_word(v[u][j], fills[u]);
+            } else {
+                atile[dst[u]] = widen_word(v[u][0], fills[u]);
+            }
+        }
+    }
+}
+
+// The four values 4*VQ .. 4*VQ+3 of an accumulator block as output bits
+// (see block_bits): pixels VQ*8 .. VQ*8+7 of the block.
+template <int VQ>
+__device__ __forceinline__ void quad_bits(const mfma_v16f &val, float T, uint64_t fmask,
+                                          uint32_t &word) {
+    block_bits_step<4 * VQ>(val, T, fmask, word);
+    block_bits_step<4 * VQ + 1>(val, T, fmask, word);
+    block_bits_step<4 * VQ + 2>(val, T, fmask, word);
+    block_bits_step<4 * VQ + 3>(val, T, fmask, word);
+}
+
 // K-split schedule, for layers whose output tile per workgroup is small
 // next to K (few pixels, many channels).  The four waves of a workgroup
 // compute the same 32*MBW pixels x 32*NBLK filters, each over a quarter of
@@ -568,56 +640,8 @@ __global__ __launch_bounds__(kMfmaThreads) void bconv2d_mfma_ks_kernel(MfmaParam
 #pragma unroll
     for (int r = 0; r < kRing - 1; ++r) load_b(r, ring[r]);
 
-    // ---- widen the whole region: element e = rc * groups + g holds words
-    // [g*V, g*V + V) of location rc; padding locations are 0 words (+1.0),
-    // or 0.0 under zero padding; words past Cw are +1.0 (their filter
-    // values are 0.0).  Loads are unconditional (padding reads zeros), four
-    // per thread in flight.
-    {
-        constexpr int U = 4;
-        const int V = p.region_vec;
-        const int groups = p.div_groups.d;
-        const int total = plane * groups;
-        for (int e0 = 0; e0 < total; e0 += U * kMfmaThreads) {
-            u32x4 v[U];
-            int dst[U];
-            uint32_t luts[U];
-#pragma unroll
-            for (int u = 0; u < U; ++u) {
-                const int e = min(e0 + u * kMfmaThreads + tid, total - 1);
-                const int rc = (int)fast_div((uint32_t)e, p.div_groups);
-                const int g = e - rc * groups;
-                const int r = (int)fast_div((uint32_t)rc, p.div_pw);
-                const int c = rc - r * PW;
-                const int R = row0 + r;
-                const int img = (int)fast_div((uint32_t)R, p.div_ph);
-                const int yy = R - img * p.ph - p.pt, xx = c - p.pl;
-                const bool inside = img < p.n && (unsigned)yy < (unsigned)p.h &&
-                                    (unsigned)xx < (unsigned)p.w;
-                const bool load = inside && g * V < p.cw;
-                const uint32_t *src =
-                    load ? p.x + (((size_t)img * p.h + yy) * p.w + xx) * p.cw + g * V
-                         : g_mfma_zero;
-                if (V == 4)
-                    v[u] = *reinterpret_cast<const u32x4 *>(src);
-                else
-                    v[u] = u32x4{*src, 0u, 0u, 0u};
-                dst[u] = g * V * plane + rc;
-                luts[u] = (p.pad_zero && !inside) ? 0u : kFp4PlusMinusLut;
-            }
-#pragma unroll
-            for (int u = 0; u < U; ++u) {
-                if (e0 + u * kMfmaThreads + tid >= total) continue;
-                if (V == 4) {
-#pragma unroll
-                    for (int j = 0; j < 4; ++j)
-                        atile[dst[u] + j * plane] = widen_word(v[u][j], luts[u]);
-                } else {
-                    atile[dst[u]] = widen_word(v[u][0], luts[u]);
-                }
-            }
-        }
-    }
+    // ---- widen the whole region (every word of every location)
+    widen_region(p, atile, row0, plane, tid);
     int z = lds_barrier();                               // the A planes are complete
 
     mfma_v16f acc[MBW][NBLK];
@@ -742,10 +766,465 @@ __global__ __launch_bounds__(kMfmaThreads) void bconv2d_mfma_ks_kernel(MfmaParam
     }
 }
 
+// Filter-stationary schedule.  Each wave keeps the widened filters of one
+// block of 32 filters for its KS K steps in registers for the whole kernel
+// (16 bytes per lane per step, loaded once); the workgroup stages its input
+// region in LDS by DMA, widens it there once, and then runs through its
+// pixel blocks two at a time, reading only the A operands from LDS.
+// Nothing is staged inside the loop, and the loop is software-pipelined
+// across pixel-block pairs:
+//   * a ring of A operands runs a few K steps ahead of the matrix products,
+//     into the next pair;
+//   * the previous pair is finished (partial-sum exchange and output
+//     transform) in small pieces between the current pair's products, so
+//     that the matrix pipe never waits for the epilogue;
+//   * compiler and scheduling barriers at every K step keep that order (the
+//     compiler would otherwise hoist every LDS read of a pair to its top).
+// F = 4/S filter blocks per workgroup; S = 2 waves share a filter block
+// when K is long, each taking KS consecutive K steps (one K step = one tap
+// and one pair of packed words = 64 channels; steps past the last add 0.0
+// filters).  Their partial sums meet in LDS once per pair (one barrier, two
+// alternating buffers), each wave finishing one block of the pair.  The host
+// gives each workgroup the same number of pixel blocks and about one
+// workgroup per CU.
+// Ring depth: K step i of every pair uses slot i % D, and the last steps of
+// a pair refill their slots with the first steps of the next, so D divides
+// KS (4 or 3 K steps, 5 for KS = 5).
+constexpr int fs_depth(int ks) { return ks % 4 == 0 ? 4 : ks % 3 == 0 ? 3 : ks; }
+
+// The packed input region of a workgroup by LDS DMA: element q = g*plane +
+// rc of `abits` holds words [g*V, g*V + V) of region location rc (V = 4 or
+// 1 words per lane); padding locations read zeros.  The last instruction's
+// extra lanes land in a slack of 64*V words after the region.  Nothing
+// reaches registers, so the loads stay in flight until the caller waits
+// for them (vmcnt) together with its other loads.
+__device__ __forceinline__ void dma_region(const MfmaParams &p, uint32_t *abits, int row0,
+                                           int plane, int wave, int lane) {
+    const int bits_words = plane * p.cw;
+    auto run = [&](auto vec_c) __attribute__((always_inline)) {
+        constexpr int V = decltype(vec_c)::value;
+        for (int u = wave; u * 64 * V < bits_words; u += kMfmaThreads / 64) {
+            const int q = min(u * 64 + lane, bits_words / V - 1);
+            const int g = (int)fast_div((uint32_t)q, p.div_plane);
+            const int rc = q - g * plane;
+            const int r = (int)fast_div((uint32_t)rc, p.div_pw);
+            const int c = rc - r * p.pw;
+            const int R = row0 + r;
+            const int img = (int)fast_div((uint32_t)R, p.div_ph);
+            const int yy = R - img * p.ph - p.pt, xx = c - p.pl;
+            const bool inside = img < p.n && (unsigned)yy < (unsigned)p.h &&
+                                (unsigned)xx < (unsigned)p.w;
+            const uint32_t *src =
+                inside ? p.x + (((size_t)img * p.h + yy) * p.w + xx) * p.cw + g * V : g_mfma_zero;
+            if constexpr (V == 4)
+                __builtin_amdgcn_global_load_lds((mfma_global_void *)src,
+                                                 (mfma_lds_void *)(abits + u * 64 * V), 16, 0, 0);
+            else
+                __builtin_amdgcn_global_load_lds((mfma_global_void *)src,
+                                                 (mfma_lds_void *)(abits + u * 64 * V), 4, 0, 0);
+        }
+    };
+    if (p.region_vec == 4)
+        run(std::integral_constant<int, 4>{});
+    else
+        run(std::integral_constant<int, 1>{});
+}
+
+// Widen the packed region (dma_region layout) into the A tile: atile[j*plane
+// + rc] = word j of location rc.  Words past Cw are +1.0 (their filter
+// values are 0.0); under zero padding, locations outside the image are
+// 0.0.  One straight-line path per staging width, four elements per thread
+// in flight (all reads before the writes):
+//   * V = 4: element e = g*plane + rc is one 16-byte group, widened into
+//     four A-tile words g*4 .. g*4+3;
+//   * V = 1: element e is word e / plane of location e % plane, at the
+//     same index in both arrays.
+__device__ __forceinline__ bool region_inside(const MfmaParams &p, int row0, int rc) {
+    const int r = (int)fast_div((uint32_t)rc, p.div_pw);
+    const int c = rc - r * p.pw;
+    const int R = row0 + r;
+    const int img = (int)fast_div((uint32_t)R, p.div_ph);
+    const int yy = R - img * p.ph - p.pt, xx = c - p.pl;
+    return img < p.n && (unsigned)yy < (unsigned)p.h && (unsigned)xx < (unsigned)p.w;
+}
+
+__device__ __forceinline__ void widen_region_lds(const MfmaParams &p, const uint32_t *abits,
+                                                 u32x4 *atile, int row0, int plane, int tid,
+                                                 int z) {
+    constexpr int U = 4;
+    if (p.region_vec == 4) {
+        const int total = plane * (p.cw >> 2);
+        const u32x4 *src = reinterpret_cast<const u32x4 *>(abits);
+        for (int e0 = 0; e0 < total; e0 += U * kMfmaThreads) {
+            u32x4 w[U];
+#pragma unroll
+            for (int u = 0; u < U; ++u) w[u] = src[min(e0 + u * kMfmaThreads + tid, total - 1) + z];
+#pragma unroll
+            for (int u = 0; u < U; ++u) {
+                const int e = e0 + u * kMfmaThreads + tid;
+                if (e >= total) break;
+                const int g = (int)fast_div((uint32_t)e, p.div_plane);
+                const int rc = e - g * plane;
+                const uint32_t fill = p.pad_zero && !region_inside(p, row0, rc) ? 0u : kFp4PlusOne;
+#pragma unroll
+                for (int k = 0; k < 4; ++k) atile[(4 * g + k) * plane + rc] = widen_word(w[u][k], fill);
+            }
+        }
+    } else {
+        const int total = plane * p.cw;
+        for (int e0 = 0; e0 < total; e0 += U * kMfmaThreads) {
+            uint32_t w[U];
+#pragma unroll
+            for (int u = 0; u < U; ++u) w[u] = abits[min(e0 + u * kMfmaThreads + tid, total - 1) + z];
+#pragma unroll
+            for (int u = 0; u < U; ++u) {
+                const int e = e0 + u * kMfmaThreads + tid;
+                if (e >= total) break;
+                uint32_t fill = kFp4PlusOne;
+                if (p.pad_zero) {
+                    const int j = (int)fast_div((uint32_t)e, p.div_plane);
+                    if (!region_inside(p, row0, e - j * plane)) fill = 0u;
+                }
+                atile[e] = widen_word(w[u], fill);
+            }
+        }
+    }
+    // words past Cw: +1.0 (0.0 outside the image under zero padding)
+    for (int e = plane * p.cw + tid; e < plane * p.cwe; e += kMfmaThreads) {
+        uint32_t fill = kFp4PlusOne;
+        if (p.pad_zero) {
+            const int j = (int)fast_div((uint32_t)e, p.div_plane);
+            if (!region_inside(p, row0, e - j * plane)) fill = 0u;
+        }
+        atile[e] = widen_word(0u, fill);
+    }
+}
+
+// Calls f(std::integral_constant<int, I>) for I = 0 .. N-1 in order.
+template <typename Fn, int... I>
+__device__ __forceinline__ void for_each_index(Fn &&f, std::integer_sequence<int, I...>) {
+    (f(std::integral_constant<int, I>{}), ...);
+}
+
+// Output bits of value V of an accumulator block (see block_bits): one
+// compare gives the lane masks of pixels r0 and r0 + 4 (r0 = (V/4)*8 +
+// V%4), and two v_writelane drop them into the lanes of their pixels.  The
+// s_nop 1 covers the VALU-written mask SGPRs (the compiler's hazard
+// recognizer does not look inside inline asm).  Nothing on the scalar unit
+// reads the masks: a scalar read of a VALU-written SGPR stalls the wave
+// until the compare retires, which the matrix products cannot hide.
+template <int V>
+__device__ __forceinline__ void bits_one_value(float a, float T, uint32_t &word) {
+    constexpr int r0 = (V >> 2) * 8 + (V & 3);
+    const uint64_t m = __ballot(a < T);
+    asm volatile(
+        "s_nop 1\n\t"
+        "v_writelane_b32 %0, %1, %3\n\t"
+        "v_writelane_b32 %0, %2, %4"
+        : "+v"(word)
+        : "s"((uint32_t)m), "s"((uint32_t)(m >> 32)), "i"(r0), "i"(r0 + 4));
+}
+
+// Filter-stationary instances: KS K steps per wave, S waves per filter
+// block (1 or 2).
+template <int KS, int S, int OUT>
+__global__ __launch_bounds__(kMfmaThreads) void bconv2d_mfma_fs_kernel(MfmaParams p) {
+    static_assert(S == 1 || S == 2, "one or two waves per filter block");
+    constexpr int F = 4 / S;
+    constexpr int D = fs_depth(KS);
+    static_assert(KS % D == 0 && D <= 5, "ring depth");
+    constexpr int NFB = S == 1 ? 2 : 1;                  // blocks of a pair this wave finishes
+    constexpr int NV = 16 * NFB;                         // values it finishes per pair
+    constexpr int kFirst = S == 1 ? 1 : 2;               // first K step that finishes values
+    constexpr int kPer = (NV + (KS - kFirst) - 1) / (KS - kFirst);         // values per step
+    static_assert(KS > kFirst, "too few K steps per wave");
+    typedef float f32x4 __attribute__((ext_vector_type(4)));
+    extern __shared__ __attribute__((aligned(16))) u32x4 smem[];
+    const int tid = threadIdx.x;
+    const int lane = tid & 63, half = lane >> 5, l32 = lane & 31;
+    const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+    const int fblk = wave % F, sk = wave / F;
+    const int m0 = blockIdx.x * p.fs_pixels;
+    const int m_end = min(m0 + p.fs_pixels, p.m);
+    const int nb = (m_end - m0 + 31) >> 5;
+    const int f0 = (blockIdx.y * F + fblk) * 32;         // this wave's first filter
+    const bool fvalid = f0 < p.coutp;
+    const int co = f0 + l32;
+    const bool co_ok = co < p.cout;
+    const int cwh = p.cwe >> 1;
+    const int ksteps = p.kh * p.kw * cwh;
+    const int TR = p.tile_rows, PW = p.pw, plane = TR * PW;
+    u32x4 *atile = smem;                                 // [cwe][TR][PW] e2m1
+    // past the A tile: the packed region (staged before the loop), and over
+    // it, once the A tile is complete, the exchange buffer
+    uint32_t *abits = reinterpret_cast<uint32_t *>(smem + p.cwe * plane);
+    f32x4 *red = reinterpret_cast<f32x4 *>(smem + p.cwe * plane);
+
+    // ---- per-lane output-transform parameters of filter co (loaded before
+    // the filters: memory counters retire in order).  A flipped filter
+    // (bitpacked output) is computed negated: its widened weights get their
+    // sign bits inverted, so the accumulator holds -dot, and the bit
+    // dot >= T becomes -dot < 1 - T (integers; +-infinity stay exact), the
+    // same compare as for every other filter.
+    float ep_a = 0.0f, ep_b = 0.0f;
+    bool flipped = false;
+    {
+        const int cc = min(co, p.cout - 1);
+        if constexpr (OUT == OUT_BITS) {
+            ep_a = p.thr[cc];
+            if (p.flip && fvalid) flipped = co_ok && ((p.flip[f0 >> 5] >> l32) & 1u);
+        } else if constexpr (OUT == OUT_FLOAT) {
+            ep_a = p.mult ? p.mult[cc] : 1.0f;
+            ep_b = p.bias ? p.bias[cc] : 0.0f;
+        }
+    }
+
+    int row0, col0;
+    mfma_pixel(p, m0, row0, col0);
+    dma_region(p, abits, row0, plane, wave, lane);
+
+    // ---- this wave's filters: step i is K step s = sk*KS + i = (tap t =
+    // s / (Cw'/2), word pair q = s % (Cw'/2)): word 2q + half of tap t of
+    // filter co, which is row 2s + half of the widened filters; and the
+    // offset of the same word and tap in the A tile (lane-dependent, so it
+    // stays in a VGPR).  The loads are unconditional (filters past C_out'
+    // read the last one and are never stored; steps past the last read the
+    // last row and are zeroed after the wait).
+    u32x4 breg[KS];
+    int aoff[KS];
+    {
+        const u32x4 *wcol = p.wexp + (size_t)half * p.coutp + min(co, p.coutp - 1);
+#pragma unroll
+        for (int i = 0; i < KS; ++i) {
+            const int s = min(sk * KS + i, ksteps - 1);
+            breg[i] = wcol[(size_t)(2 * s) * p.coutp];
+            const int t = (int)fast_div((uint32_t)s, p.div_cwh);
+            const int q = s - t * cwh;
+            const int ky = (int)fast_div((uint32_t)t, p.div_kw);
+            aoff[i] = (2 * q + half) * plane + ky * PW + (t - ky * p.kw);
+        }
+    }
+
+    wait_vmcnt<0>();                                     // region, filters, parameters
+#pragma unroll
+    for (int i = 0; i < KS; ++i)
+        if (sk * KS + i >= ksteps) breg[i] = u32x4{0u, 0u, 0u, 0u};
+    if constexpr (OUT == OUT_BITS) {
+        const uint32_t neg = flipped ? kFp4SignBits : 0u;
+#pragma unroll
+        for (int i = 0; i < KS; ++i) breg[i] ^= u32x4{neg, neg, neg, neg};
+    }
+    if constexpr (OUT == OUT_BITS) {
+        ep_a = co_ok ? thr_to_dot_bound_f(ep_a, p.lo, p.hi) : -INFINITY;
+        if (flipped) ep_a = 1.0f - ep_a;
+    }
+    int z = lds_barrier();                               // every wave's region DMA landed
+    widen_region_lds(p, abits, atile, row0, plane, tid, z);
+    z = lds_barrier();                                   // the A tile is complete (abits is free)
+
+    // A-tile offset of the window origin of pixel block b's 32 pixels
+    auto block_base = [&](int b) __attribute__((always_inline)) {
+        const int mp = min(m0 + b * 32 + l32, m_end - 1);
+        int prow, pcol;
+        mfma_pixel(p, mp, prow, pcol);
+        return (prow - row0) * PW + pcol;
+    };
+
+    // ---- finishing a pair (or the last single block).  S = 1: this wave
+    // finishes both blocks.  S = 2: wave sk finishes block sk, after the two
+    // waves of the filter block swap their partial sums of each other's
+    // block through LDS (red[((buf*F + fblk)*2 + block)*4 + quad] rows of 64
+    // lanes, two alternating buffers).  The values leave the accumulators
+    // (into fin, or into LDS for the other wave) before the next pair's
+    // first products overwrite them.
+    mfma_v16f acc[2];
+    float fin[NFB][16];
+    uint32_t word[NFB];
+    int fin_b0 = 0, fin_nbp = 2;
+    int buf = 0;
+    // (accumulator blocks are picked by uniform branches with constant
+    // indices: a runtime index would move them to scratch memory)
+    auto collect_prev = [&](int nbp) __attribute__((always_inline)) {
+        fin_nbp = nbp;
+        if constexpr (S == 2) {
+            auto move = [&](auto oc, auto jc) __attribute__((always_inline)) {
+                constexpr int O = decltype(oc)::value;   // the other wave's block
+                constexpr int J = decltype(jc)::value;   // this wave's block
+                if (O < nbp) {
+#pragma unroll
+                    for (int vq = 0; vq < 4; ++vq)
+                        red[(((buf * F + fblk) * 2 + O) * 4 + vq) * 64 + lane + z] =
+                            f32x4{acc[O][4 * vq], acc[O][4 * vq + 1], acc[O][4 * vq + 2],
+                                  acc[O][4 * vq + 3]};
+                }
+                if (J < nbp) {
+#pragma unroll
+                    for (int v = 0; v < 16; ++v) fin[0][v] = acc[J][v];
+                }
+            };
+            if (sk == 0)
+                move(std::integral_constant<int, 1>{}, std::integral_constant<int, 0>{});
+            else
+                move(std::integral_constant<int, 0>{}, std::integral_constant<int, 1>{});
+        } else {
+#pragma unroll
+            for (int j = 0; j < NFB; ++j)
+#pragma unroll
+                for (int v = 0; v < 16; ++v) fin[j][v] = acc[j][v];
+        }
+    };
+    // (S = 2) the other wave's partial sums of this wave's block
+    auto collect_partner = [&]() __attribute__((always_inline)) {
+        if constexpr (S == 2) {
+            z = lds_barrier();
+            if (sk < fin_nbp) {
+#pragma unroll
+                for (int vq = 0; vq < 4; ++vq) {
+                    const f32x4 r = red[(((buf * F + fblk) * 2 + sk) * 4 + vq) * 64 + lane + z];
+#pragma unroll
+                    for (int e = 0; e < 4; ++e) fin[0][4 * vq + e] += r[e];
+                }
+            }
+            buf ^= 1;
+        }
+    };
+    // value N of the finishing order: block N/16 of those this wave
+    // finishes, value N%16; a block's output is stored after its last value.
+    // No branch: values of a missing block (single last block) or of
+    // filters past C_out' are computed and not stored.
+    auto finish_one = [&](auto nc) __attribute__((always_inline)) {
+        constexpr int N = decltype(nc)::value;
+        constexpr int j = N / 16, v = N % 16;
+        const int blk = S == 1 ? j : sk;                 // block of the pair
+        const bool store = fvalid && blk < fin_nbp;
+        const int mw = m0 + (fin_b0 + blk) * 32;
+        if constexpr (OUT == OUT_BITS) {
+            if (v == 0) word[j] = 0u;
+            bits_one_value<v>(fin[j][v], ep_a, word[j]);
+            if (v == 15) {
+                const int m = mw + lane;
+                if (store && lane < 32 && m < m_end)
+                    reinterpret_cast<uint32_t *>(p.out)[(size_t)m * p.cwo + (f0 >> 5)] = word[j];
+            }
+        } else {
+            const int m = mw + (v >> 2) * 8 + half * 4 + (v & 3);
+            const int c = min(max((int)fin[j][v], p.lo), p.hi);
+            if (store && co_ok && m < m_end) {
+                if constexpr (OUT == OUT_FLOAT)
+                    reinterpret_cast<float *>(p.out)[(size_t)m * p.cout + co] =
+                        __builtin_fmaf((float)c, ep_a, ep_b);
+                else
+                    reinterpret_cast<int32_t *>(p.out)[(size_t)m * p.cout + co] = c;
+            }
+        }
+    };
+    // values [LO, HI) of the finishing order
+    auto finish_range = [&](auto loc, auto hic) __attribute__((always_inline)) {
+        constexpr int LO = decltype(loc)::value, HI = decltype(hic)::value;
+        if constexpr (LO < HI)
+            for_each_index([&](auto uc) __attribute__((always_inline)) {
+                finish_one(std::integral_constant<int, LO + decltype(uc)::value>{});
+            }, std::make_integer_sequence<int, HI - LO>{});
+    };
+    // finish the blocks in the accumulators at once (outside the pipeline)
+    auto finish_all = [&](int nbp) __attribute__((always_inline)) {
+        collect_prev(nbp);
+        collect_partner();
+        finish_range(std::integral_constant<int, 0>{}, std::integral_constant<int, NV>{});
+    };
+
+    // ---- the pipelined loop over pairs (and a last single block)
+    const int npairs = nb >> 1;
+    int base[2] = {block_base(0), block_base(min(1, nb - 1))};
+    u32x4 ring[D][2];
+#pragma unroll
+    for (int i = 0; i < D; ++i)
+#pragma unroll
+        for (int j = 0; j < 2; ++j) ring[i][j] = atile[base[j] + aoff[i < KS ? i : KS - 1] + z];
+
+    const mfma_v16f zero16 = {0.0f, 0.0f, 0.0f, 0.0f, 0.0f, 0.0f, 0.0f, 0.0f,
+                              0.0f, 0.0f, 0.0f, 0.0f, 0.0f, 0.0f, 0.0f, 0.0f};
+
+    // NBP (2 or 1) blocks from b0: K step i issues its products with a
+    // piece of the previous pair's finishing after each (the matrix pipe
+    // runs one product while the wave issues the piece), then refills its
+    // ring slot with step i + D (of these blocks, or of the next ones)
+    auto body = [&](auto nbp_c, auto prev_c, int b0) __attribute__((always_inline)) {
+        constexpr int NBP = decltype(nbp_c)::value;
+        constexpr bool has_prev = decltype(prev_c)::value;   // a compile-time branch per step
+        const int nxt = b0 + 2 < nb ? b0 + 2 : b0;
+        int next_base[2] = {base[0], base[1]};
+        if constexpr (NBP == 2) {
+            next_base[0] = block_base(nxt);
+            next_base[1] = block_base(min(nxt + 1, nb - 1));
+        }
+        if constexpr (has_prev) collect_prev(2);         // before the products overwrite them
+        auto step = [&](auto ic) __attribute__((always_inline)) {
+            constexpr int i = decltype(ic)::value;
+            // finishing pieces: values [lo, mid) after the first product,
+            // [mid, hi) after the second
+            constexpr int lo = i >= kFirst ? (i - kFirst) * kPer : NV;
+            constexpr int hi = lo + kPer < NV ? lo + kPer : NV;
+            constexpr int mid = NBP == 2 ? (lo + hi) / 2 : hi;
+#pragma unroll
+            for (int j = 0; j < NBP; ++j) {
+                acc[j] = mfma_fp4(ring[i % D][j], breg[i], i == 0 ? zero16 : acc[j]);
+                // pin the product here (it touches no memory and would move)
+                asm volatile("" : "+a"(acc[j]) : : "memory");
+                if constexpr (has_prev) {
+                    if (j == 0) {
+                        if constexpr (S == 2 && i == 1) collect_partner();
+                        finish_range(std::integral_constant<int, lo>{},
+                                     std::integral_constant<int, mid>{});
+                    } else {
+                        finish_range(std::integral_constant<int, mid>{},
+                                     std::integral_constant<int, hi>{});
+                    }
+                }
+                asm volatile("" ::: "memory");
+                __builtin_amdgcn_sched_barrier(0);
+            }
+            if constexpr (i + D < KS) {
+#pragma unroll
+                for (int j = 0; j < NBP; ++j) ring[i % D][j] = atile[base[j] + aoff[i + D] + z];
+            } else if constexpr (NBP == 2) {
+#pragma unroll
+                for (int j = 0; j < 2; ++j)
+                    ring[i % D][j] = atile[next_base[j] + aoff[i + D - KS] + z];
+            }
+            // keep the step's LDS reads here: a compiler memory barrier for
+            // the passes that move loads, a scheduling barrier for the
+            // machine scheduler
+            asm volatile("" ::: "memory");
+            __builtin_amdgcn_sched_barrier(0);
+        };
+        for_each_index(step, std::make_integer_sequence<int, KS>{});
+        base[0] = next_base[0];
+        base[1] = next_base[1];
+        fin_b0 = b0;
+    };
+    constexpr auto two = std::integral_constant<int, 2>{};
+    constexpr auto one = std::integral_constant<int, 1>{};
+    constexpr auto yes = std::integral_constant<bool, true>{};
+    constexpr auto no = std::integral_constant<bool, false>{};
+    if (npairs > 0) body(two, no, 0);
+    for (int pidx = 1; pidx < npairs; ++pidx) body(two, yes, 2 * pidx);
+    if (nb & 1) {
+        if (npairs > 0)
+            body(one, yes, nb - 1);
+        else
+            body(one, no, nb - 1);
+        finish_all(1);
+    } else if (npairs > 0) {
+        finish_all(2);
+    }
+}
+
 // Filters widened once per filter tensor into the B layout:
 //   wexp[(t*CwE + j)*CoutP + co] = 32 e2m1 codes of word j of tap t of
-//   filter co; channels past C_in, words past Cw and filters past Cout are
-//   0.0 (they then add nothing to any dot).
+//   filter co, in the order of widen_word (channel c of the word in 32-bit
+//   word c % 4, nibble c / 4); channels past C_in, words past Cw and filters
+//   past Cout are 0.0 (they then add nothing to any dot).
 __global__ __launch_bounds__(256) void mfma_expand_weights_kernel(const uint32_t *__restrict__ w,
                                                                   u32x4 *__restrict__ wexp,
                                                                   int cout, int coutp, int taps,
@@ -761,7 +1240,7 @@ __global__ __launch_bounds__(256) void mfma_expand_weights_kernel(const uint32_t
             const uint32_t bits = w[((size_t)co * taps + t) * cw + j];
             const int nvalid = min(32, cin - 32 * j);
             const uint32_t valid = nvalid >= 32 ? 0xFFFFFFFFu : (1u << nvalid) - 1u;
-            o = widen_word(bits, kFp4PlusMinusLut) & widen_word(valid, kFp4ValidLut);
+            o = widen_word(bits, kFp4PlusOne) & widen_valid_mask(valid);
         }
         wexp[idx] = o;
     }

@@ -409,6 +409,95 @@ void launch_mfma_ks(const lce::MfmaParams &p, int nblk, int mbw, dim3 grid, size
         launch_mfma_ks_mb<OUT, 1>(p, nblk, grid, lds, s);
 }
 
+// Filter-stationary instances: K steps per wave (KS) and waves sharing a
+// filter block (S).
+struct FsShape {
+    int ks, s;
+};
+constexpr FsShape kFsShapes[] = {{9, 1}, {18, 1}, {5, 2}, {9, 2}, {18, 2}};
+
+template <int KS, int S>
+void launch_mfma_fs_shape(const lce::MfmaParams &p, int out, dim3 grid, size_t lds,
+                          hipStream_t st) {
+    const dim3 block(lce::kMfmaThreads);
+    if (out == LCE_OUT_FLOAT32)
+        hipLaunchKernelGGL((lce::bconv2d_mfma_fs_kernel<KS, S, lce::OUT_FLOAT>), grid, block, lds,
+                           st, p);
+    else if (out == LCE_OUT_BITPACKED)
+        hipLaunchKernelGGL((lce::bconv2d_mfma_fs_kernel<KS, S, lce::OUT_BITS>), grid, block, lds,
+                           st, p);
+    else
+        hipLaunchKernelGGL((lce::bconv2d_mfma_fs_kernel<KS, S, lce::OUT_INT>), grid, block, lds,
+                           st, p);
+}
+
+void launch_mfma_fs(const lce::MfmaParams &p, FsShape sh, int out, dim3 grid, size_t lds,
+                    hipStream_t st) {
+    if (sh.ks == 9 && sh.s == 1) launch_mfma_fs_shape<9, 1>(p, out, grid, lds, st);
+    else if (sh.ks == 18 && sh.s == 1) launch_mfma_fs_shape<18, 1>(p, out, grid, lds, st);
+    else if (sh.ks == 5 && sh.s == 2) launch_mfma_fs_shape<5, 2>(p, out, grid, lds, st);
+    else if (sh.ks == 9 && sh.s == 2) launch_mfma_fs_shape<9, 2>(p, out, grid, lds, st);
+    else launch_mfma_fs_shape<18, 2>(p, out, grid, lds, st);
+}
+
+// LDS of the filter-stationary kernel: every widened word of the region,
+// then the larger of the packed region (staged before the loop, with the
+// 256-word slack of its last DMA instruction) and (S = 2) the partial-sum
+// exchange: two buffers x F filter blocks x two pixel blocks, 4 KB each.
+size_t mfma_fs_lds(const lce::MfmaParams &p, FsShape sh, int tile_rows) {
+    const size_t a = (size_t)p.cwe * tile_rows * p.pw * 16;
+    const size_t bits = ((size_t)tile_rows * p.pw * p.cw + 256) * 4;
+    const size_t red = sh.s > 1 ? (size_t)2 * (4 / sh.s) * 2 * 4096 : 0;
+    return a + std::max(bits, red);
+}
+
+struct FsPlan {
+    FsShape shape{0, 0};
+    int pixels = 0, tile_rows = 0;
+    int64_t groups = 0;
+    size_t lds = 0;
+};
+
+// The filter-stationary plan of a layer: among the instances whose K steps
+// cover the layer's with at most 1/8 padding (any, when forced), the one
+// with the fewest matrix products per wave (pixel blocks per workgroup x
+// KS, plus one per block for the exchange), with about one workgroup per
+// CU: each filter group gets CUs / filter groups workgroups, each an equal
+// whole number of pixel blocks.  shape.ks == 0: none fits.
+FsPlan plan_mfma_fs(const lce::MfmaParams &p, int64_t cus, int blocks32, int ksteps) {
+    FsPlan best;
+    int64_t best_cost = -1;
+    const int env_ks = env_int("LCE_MFMA_FS_KS", 0), env_s = env_int("LCE_MFMA_FS_S", 0);
+    for (const FsShape &sh : kFsShapes) {
+        if (env_ks && sh.ks != env_ks) continue;
+        if (env_s && sh.s != env_s) continue;
+        const int cover = sh.ks * sh.s;
+        if (cover < ksteps || cover - sh.ks >= ksteps) continue;   // every wave has work
+        if (!(env_ks && env_s) && (cover - ksteps) * 8 > ksteps) continue;
+        const int f = 4 / sh.s;
+        const int64_t fgroups = (blocks32 + f - 1) / f;
+        const int64_t pg = std::max<int64_t>(1, cus / fgroups);
+        int64_t px = ((int64_t)p.m + pg - 1) / pg;
+        px = (px + 31) / 32 * 32;
+        if (px > (1 << 20)) continue;
+        const int tr = mfma_tile_rows(p, (int)px);
+        const size_t lds = mfma_fs_lds(p, sh, tr);
+        if (lds > (size_t)device_max_lds()) continue;
+        if ((int64_t)tr * p.pw * p.cwe > INT32_MAX / 2) continue;
+        const int64_t nb = px / 32;
+        const int64_t cost = nb * sh.ks + (sh.s > 1 ? nb : 0);
+        if (best_cost < 0 || cost < best_cost) {
+            best_cost = cost;
+            best.shape = sh;
+            best.pixels = (int)px;
+            best.tile_rows = tr;
+            best.groups = ((int64_t)p.m + px - 1) / px;
+            best.lds = lds;
+        }
+    }
+    return best;
+}
+
 // LDS of the K-split kernel: every widened word of the region, or the
 // reduction buffer (three partial copies of every 32x32 block), which
 // reuses it.
@@ -783,6 +872,29 @@ lce_status lce_bconv2d_mfma(const lce_bconv2d_desc *desc, const int32_t *x_packe
     // either schedule (the K-split one where its LDS fits).
     const int64_t ksteps = (int64_t)d.kh * d.kw * (p.cwe / 2);
     const int ks_env = env_int("LCE_MFMA_KS", -1);
+
+    // Filter-stationary schedule: the default wherever an instance fits, up
+    // to 36 K steps (longer K runs on the K-split schedule below, measured
+    // faster there: its workgroups split K four ways); LCE_MFMA_FS=0 turns
+    // it off, LCE_MFMA_KS forces one of the others.
+    if (ks_env < 0 && env_int("LCE_MFMA_FS", 1) != 0 && ksteps <= 36) {
+        const FsPlan fp = plan_mfma_fs(p, cus, blocks32, (int)ksteps);
+        if (fp.shape.ks) {
+            p.tile_rows = fp.tile_rows;
+            p.fs_pixels = fp.pixels;
+            p.div_plane = lce::make_fastdiv((uint32_t)(fp.tile_rows * p.pw));
+            size_t lds = fp.lds;
+            // LCE_MFMA_FS_PAD=1: claim more than half of a CU's LDS, so that no
+            // CU holds two workgroups while another holds none
+            if (env_int("LCE_MFMA_FS_PAD", 0) == 1)
+                lds = std::max(lds, (size_t)device_max_lds() / 2 + 1024);
+            const dim3 grid((unsigned)fp.groups,
+                            (unsigned)((blocks32 + 4 / fp.shape.s - 1) / (4 / fp.shape.s)));
+            launch_mfma_fs(p, fp.shape, d.out_type, grid, lds, stream);
+            return check_launch("lce_bconv2d_mfma launch");
+        }
+    }
+
     if (ks_env == 1 || (ks_env != 0 && ksteps >= 48)) {
         static const int kTiles[][2] = {{4, 2}, {2, 4}, {2, 2}, {4, 1}, {1, 4},
                                         {2, 1}, {1, 2}, {1, 1}};

@@ -5,11 +5,13 @@ its dot is the exact integer the oracle computes: int32 and bitpacked outputs
 must match bit for bit, float outputs within 1e-6 relative.  Zero padding
 (0.0 at padded locations) is checked against the oracle's pad_value=0.
 
-Every test runs under both schedules of the path, forced through the
-environment: the K-split one (the four waves of a workgroup share one output
-tile and divide K; LCE_MFMA_KS=1, used where its LDS fits) and the
-pixel-split one (LCE_MFMA_KS=0).  Unforced, the library takes the K-split
-schedule for long K only.
+Every test runs under each schedule of the path, chosen through the
+environment: the filter-stationary one (each wave keeps its filters in
+registers and runs through the workgroup's pixel blocks; the default
+wherever one of its instances fits, LCE_MFMA_FS=1), the K-split one (the
+four waves of a workgroup share one output tile and divide K; LCE_MFMA_KS=1,
+used where its LDS fits) and the pixel-split one (LCE_MFMA_KS=0).  A layer no
+filter-stationary instance fits runs on one of the other two.
 """
 import numpy as np
 import pytest
@@ -33,9 +35,14 @@ def gpu():
     torch.cuda.synchronize()
 
 
-@pytest.fixture(autouse=True, params=["ks", "pixel"])
+@pytest.fixture(autouse=True, params=["fs", "ks", "pixel"])
 def schedule(request, monkeypatch):
-    monkeypatch.setenv("LCE_MFMA_KS", "1" if request.param == "ks" else "0")
+    for k in ("LCE_MFMA_KS", "LCE_MFMA_FS_KS", "LCE_MFMA_FS_S", "LCE_MFMA_FS_PAD"):
+        monkeypatch.delenv(k, raising=False)
+    if request.param == "fs":
+        monkeypatch.setenv("LCE_MFMA_FS", "1")
+    else:
+        monkeypatch.setenv("LCE_MFMA_KS", "1" if request.param == "ks" else "0")
     return request.param
 
 
@@ -128,6 +135,9 @@ def test_mfma_every_tile_shape(monkeypatch, schedule, mbw, nblk):
     ragged float layer and a stride-2 layer with zero padding."""
     if schedule == "pixel" and mbw == 4:
         pytest.skip("the pixel-split schedule takes 1 or 2 pixel blocks per wave")
+    if schedule == "fs":
+        pytest.skip("the filter-stationary schedule has no such tile (its instances are "
+                    "covered by test_mfma_fs_every_instance)")
     monkeypatch.setenv("LCE_MFMA_MB", str(mbw))
     monkeypatch.setenv("LCE_MFMA_NBLK", str(nblk))
     layer = config(4)[3]
@@ -144,6 +154,84 @@ def test_mfma_every_tile_shape(monkeypatch, schedule, mbw, nblk):
         got = sync_np(mfma_run(lay, inp, pad_value=pv))
         ref = oracle_run(lay, inp, oracle_signs(inp), 0 if pv == "zero" else 1)
         assert_match(lay, got, ref, f"{lay.name} mb={mbw} nblk={nblk}")
+
+
+# Filter-stationary instances (K steps per wave, waves per filter block) and,
+# for each, layers whose K steps (taps x ceil(Cw/2), Cw rounded up as the
+# widened filters are) need every wave of a filter block: ragged sizes,
+# stride 2, non-square filters, every output type, zero padding.
+FS_INSTANCES = [(9, 1), (18, 1), (5, 2), (9, 2), (18, 2)]
+
+
+def fs_layers(ks, s):
+    """Layers with (s-1)*ks < K steps <= s*ks."""
+    out = []
+    for kh, kw in ((3, 3), (1, 1), (5, 5), (3, 1), (2, 3), (1, 5), (7, 7)):
+        for cw in range(1, 17):
+            cwe = (cw + 1) // 2 * 2 if (cw + 1) // 2 * 2 < (cw + 3) // 4 * 4 else (cw + 3) // 4 * 4
+            steps = kh * kw * cwe // 2
+            if (s - 1) * ks < steps <= s * ks:
+                out.append((kh, kw, cw))
+    return out
+
+
+@pytest.mark.parametrize("ks,s", FS_INSTANCES, ids=lambda v: str(v))
+def test_mfma_fs_every_instance(monkeypatch, schedule, ks, s):
+    if schedule != "fs":
+        pytest.skip("filter-stationary instances")
+    monkeypatch.setenv("LCE_MFMA_FS_KS", str(ks))
+    monkeypatch.setenv("LCE_MFMA_FS_S", str(s))
+    shapes = fs_layers(ks, s)
+    assert shapes, (ks, s)
+    rng = np.random.default_rng(ks * 10 + s)
+    picks = [shapes[0], shapes[-1]] + [shapes[int(i)] for i in rng.integers(0, len(shapes), 2)]
+    for j, (kh, kw, cw) in enumerate(picks):
+        c_in = 32 * cw - int(rng.integers(0, 32))
+        c_out = int(rng.choice([13, 32, 64, 100, 128, 200]))
+        stride = int(rng.choice([1, 2]))
+        out = ["float", "bitpacked", "int32", "bitpacked"][j]
+        pv = ["one", "zero"][j % 2]
+        k = kh * kw * c_in
+        layer = Layer(f"fs{ks}x{s}_{j}", int(rng.integers(1, 4)), int(rng.integers(kh, 15)),
+                      int(rng.integers(kw, 15)), c_in, c_out, kh=kh, kw=kw, stride=stride,
+                      padding=["same", "valid"][j % 2], out=out,
+                      clamp=[None, (-k // 3, k // 2)][j % 2], input_kind="bits")
+        inp = make_layer_inputs(layer, 7, 91, ks * 100 + s * 10 + j)
+        flip = None
+        if out == "bitpacked" and j == 3:
+            flip = rng.integers(0, 2**31, (c_out + 31) // 32).astype(np.int32)
+        got = sync_np(mfma_run(layer, inp, pad_value=pv, flip=flip))
+        if flip is not None:
+            fbits = np.array([(int(flip[c // 32]) >> (c % 32)) & 1 for c in range(c_out)],
+                             np.uint8)
+            ref = oracle.bconv2d(oracle_signs(inp), inp.w_sign, stride=layer.strides,
+                                 padding=layer.padding, clamp_range=clamp_of(layer),
+                                 out="bitpacked", thr=inp.thr, flip=fbits,
+                                 pad_value=0 if pv == "zero" else 1)
+        else:
+            ref = oracle_run(layer, inp, oracle_signs(inp), 0 if pv == "zero" else 1)
+        assert_match(layer, got, ref, f"{layer.name} {kh}x{kw} cw={cw} {pv}")
+
+
+def test_mfma_fs_config4_every_instance_that_fits(monkeypatch, schedule):
+    """The batch-64 layers at full size (sampled images) on every
+    filter-stationary instance whose K steps fit the layer."""
+    if schedule != "fs":
+        pytest.skip("filter-stationary instances")
+    sample = [0, 37, 63]
+    for i, layer in enumerate(config(4)):
+        inp = make_layer_inputs(layer, 0, 4, i)
+        ref = None
+        steps = layer.kh * layer.kw * ((layer.cw + 1) // 2)
+        for ks, s in FS_INSTANCES:
+            if not ((s - 1) * ks < steps <= s * ks):
+                continue
+            monkeypatch.setenv("LCE_MFMA_FS_KS", str(ks))
+            monkeypatch.setenv("LCE_MFMA_FS_S", str(s))
+            got = sync_np(mfma_run(layer, inp))
+            if ref is None:
+                ref = oracle_run(layer, inp, oracle_signs(inp, sample))
+            assert_match(layer, got[sample], ref, f"{layer.name} fs {ks}x{s}")
 
 
 def test_mfma_wide_region_falls_back_to_the_pixel_split(monkeypatch):
@@ -211,8 +299,8 @@ def test_mfma_weights_are_zero_past_the_real_channels_and_filters():
     cw, cwe, coutp, taps = 2, 2, 32, 9
     codes = np.zeros((taps * cwe, coutp, 32), np.uint8)
     words = raw.reshape(taps * cwe, coutp, 4)
-    for j in range(32):
-        codes[..., j] = (words[..., j // 8] >> np.uint32(4 * (j % 8))) & 0xF
+    for j in range(32):                       # channel j: 32-bit word j % 4, nibble j // 4
+        codes[..., j] = (words[..., j % 4] >> np.uint32(4 * (j // 4))) & 0xF
     want = np.zeros_like(codes)
     w = inp.w_sign.reshape(13, taps, 40)
     for t in range(taps):
