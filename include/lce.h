@@ -208,11 +208,13 @@ lce_status lce_bconv2d_mfma_weights(const lce_bconv2d_desc *desc, const int32_t 
  * pad_value (no correction table).
  * The work is split by shape between three schedules: filter-stationary
  * (each wave keeps its filters in registers and runs through about one
- * CU's share of pixel blocks; up to 36 K steps of 64 channels), K-split
+ * CU's share of pixel blocks; by default up to 36 K steps of 64
+ * channels, up to 72 when an instance is forced), K-split
  * (the waves of a workgroup divide K; long K) and pixel-split (the rest).
  * The environment variables LCE_MFMA_FS (0 turns the first off),
- * LCE_MFMA_FS_KS / LCE_MFMA_FS_S (its instance), LCE_MFMA_FS_PAD (one
- * workgroup per CU by LDS size), LCE_MFMA_KS (1 / 0: K-split / pixel-split),
+ * LCE_MFMA_FS_KS / LCE_MFMA_FS_S (its instance), LCE_MFMA_FS_PAD (0: no
+ * LDS padding to one workgroup per CU), LCE_MFMA_KS (1 / 0: K-split /
+ * pixel-split),
  * LCE_MFMA_MB and LCE_MFMA_NBLK force a schedule and a tile for testing and
  * tuning.  Every choice gives the identical output.
  * Errors: as lce_bconv2d, plus LCE_EUNSUPPORTED when K = KH*KW*C_in >= 2^24

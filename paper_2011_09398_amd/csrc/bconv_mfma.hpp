@@ -929,7 +929,7 @@ __device__ __forceinline__ void bits_one_value(float a, float T, uint32_t &word)
 // block (1 or 2).
 template <int KS, int S, int OUT>
 __global__ __launch_bounds__(kMfmaThreads) void bconv2d_mfma_fs_kernel(MfmaParams p) {
-    static_assert(S == 1 || S == 2, "one or two waves per filter block");
+    static_assert(S == 1 || S == 2 || S == 4, "1, 2 or 4 waves per filter block");
     constexpr int F = 4 / S;
     constexpr int D = fs_depth(KS);
     static_assert(KS % D == 0 && D <= 5, "ring depth");
@@ -1005,7 +1005,14 @@ __global__ __launch_bounds__(kMfmaThreads) void bconv2d_mfma_fs_kernel(MfmaParam
         }
     }
 
-    wait_vmcnt<0>();                                     // region, filters, parameters
+    // The region DMA was issued before the KS filter loads and memory
+    // counters retire in order: once at most KS loads are outstanding, this
+    // wave's region words (and parameters) have landed, and the region is
+    // widened while the filters are still on their way.
+    wait_vmcnt<KS>();
+    int z = lds_barrier();                               // every wave's region DMA landed
+    widen_region_lds(p, abits, atile, row0, plane, tid, z);
+    wait_vmcnt<0>();                                     // the filters
 #pragma unroll
     for (int i = 0; i < KS; ++i)
         if (sk * KS + i >= ksteps) breg[i] = u32x4{0u, 0u, 0u, 0u};
@@ -1013,13 +1020,9 @@ __global__ __launch_bounds__(kMfmaThreads) void bconv2d_mfma_fs_kernel(MfmaParam
         const uint32_t neg = flipped ? kFp4SignBits : 0u;
 #pragma unroll
         for (int i = 0; i < KS; ++i) breg[i] ^= u32x4{neg, neg, neg, neg};
-    }
-    if constexpr (OUT == OUT_BITS) {
         ep_a = co_ok ? thr_to_dot_bound_f(ep_a, p.lo, p.hi) : -INFINITY;
         if (flipped) ep_a = 1.0f - ep_a;
     }
-    int z = lds_barrier();                               // every wave's region DMA landed
-    widen_region_lds(p, abits, atile, row0, plane, tid, z);
     z = lds_barrier();                                   // the A tile is complete (abits is free)
 
     // A-tile offset of the window origin of pixel block b's 32 pixels
@@ -1031,12 +1034,13 @@ __global__ __launch_bounds__(kMfmaThreads) void bconv2d_mfma_fs_kernel(MfmaParam
     };
 
     // ---- finishing a pair (or the last single block).  S = 1: this wave
-    // finishes both blocks.  S = 2: wave sk finishes block sk, after the two
-    // waves of the filter block swap their partial sums of each other's
-    // block through LDS (red[((buf*F + fblk)*2 + block)*4 + quad] rows of 64
-    // lanes, two alternating buffers).  The values leave the accumulators
-    // (into fin, or into LDS for the other wave) before the next pair's
-    // first products overwrite them.
+    // finishes both blocks.  S > 1: wave sk < 2 finishes block sk of the
+    // pair after the other S-1 waves of its filter block hand it their
+    // partial sums through LDS (red[(((buf*F + fblk)*2 + block)*(S-1) +
+    // slot)*4 + quad] rows of 64 lanes, slot = the writer's rank among the
+    // other waves, two alternating buffers); waves sk >= 2 finish nothing.
+    // The values leave the accumulators (into fin, or into LDS for another
+    // wave) before the next pair's first products overwrite them.
     mfma_v16f acc[2];
     float fin[NFB][16];
     uint32_t word[NFB];
@@ -1046,26 +1050,24 @@ __global__ __launch_bounds__(kMfmaThreads) void bconv2d_mfma_fs_kernel(MfmaParam
     // indices: a runtime index would move them to scratch memory)
     auto collect_prev = [&](int nbp) __attribute__((always_inline)) {
         fin_nbp = nbp;
-        if constexpr (S == 2) {
-            auto move = [&](auto oc, auto jc) __attribute__((always_inline)) {
-                constexpr int O = decltype(oc)::value;   // the other wave's block
-                constexpr int J = decltype(jc)::value;   // this wave's block
-                if (O < nbp) {
-#pragma unroll
-                    for (int vq = 0; vq < 4; ++vq)
-                        red[(((buf * F + fblk) * 2 + O) * 4 + vq) * 64 + lane + z] =
-                            f32x4{acc[O][4 * vq], acc[O][4 * vq + 1], acc[O][4 * vq + 2],
-                                  acc[O][4 * vq + 3]};
-                }
-                if (J < nbp) {
+        if constexpr (S > 1) {
+            auto move = [&](auto jc) __attribute__((always_inline)) {
+                constexpr int J = decltype(jc)::value;
+                if (J >= nbp) return;
+                if (J == sk) {
 #pragma unroll
                     for (int v = 0; v < 16; ++v) fin[0][v] = acc[J][v];
+                } else {
+                    const int slot = sk - (sk > J ? 1 : 0);
+#pragma unroll
+                    for (int vq = 0; vq < 4; ++vq)
+                        red[((((buf * F + fblk) * 2 + J) * (S - 1) + slot) * 4 + vq) * 64 + lane + z] =
+                            f32x4{acc[J][4 * vq], acc[J][4 * vq + 1], acc[J][4 * vq + 2],
+                                  acc[J][4 * vq + 3]};
                 }
             };
-            if (sk == 0)
-                move(std::integral_constant<int, 1>{}, std::integral_constant<int, 0>{});
-            else
-                move(std::integral_constant<int, 0>{}, std::integral_constant<int, 1>{});
+            move(std::integral_constant<int, 0>{});
+            move(std::integral_constant<int, 1>{});
         } else {
 #pragma unroll
             for (int j = 0; j < NFB; ++j)
@@ -1073,17 +1075,21 @@ __global__ __launch_bounds__(kMfmaThreads) void bconv2d_mfma_fs_kernel(MfmaParam
                 for (int v = 0; v < 16; ++v) fin[j][v] = acc[j][v];
         }
     };
-    // (S = 2) the other wave's partial sums of this wave's block
+    // (S > 1) the other waves' partial sums of this wave's block
     auto collect_partner = [&]() __attribute__((always_inline)) {
-        if constexpr (S == 2) {
+        if constexpr (S > 1) {
             z = lds_barrier();
             if (sk < fin_nbp) {
 #pragma unroll
-                for (int vq = 0; vq < 4; ++vq) {
-                    const f32x4 r = red[(((buf * F + fblk) * 2 + sk) * 4 + vq) * 64 + lane + z];
+                for (int slot = 0; slot < S - 1; ++slot)
 #pragma unroll
-                    for (int e = 0; e < 4; ++e) fin[0][4 * vq + e] += r[e];
-                }
+                    for (int vq = 0; vq < 4; ++vq) {
+                        const f32x4 r =
+                            red[((((buf * F + fblk) * 2 + sk) * (S - 1) + slot) * 4 + vq) * 64 +
+                                lane + z];
+#pragma unroll
+                        for (int e = 0; e < 4; ++e) fin[0][4 * vq + e] += r[e];
+                    }
             }
             buf ^= 1;
         }
@@ -1173,7 +1179,7 @@ __global__ __launch_bounds__(kMfmaThreads) void bconv2d_mfma_fs_kernel(MfmaParam
                 asm volatile("" : "+a"(acc[j]) : : "memory");
                 if constexpr (has_prev) {
                     if (j == 0) {
-                        if constexpr (S == 2 && i == 1) collect_partner();
+                        if constexpr (S > 1 && i == 1) collect_partner();
                         finish_range(std::integral_constant<int, lo>{},
                                      std::integral_constant<int, mid>{});
                     } else {

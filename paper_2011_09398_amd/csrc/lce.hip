@@ -414,7 +414,7 @@ void launch_mfma_ks(const lce::MfmaParams &p, int nblk, int mbw, dim3 grid, size
 struct FsShape {
     int ks, s;
 };
-constexpr FsShape kFsShapes[] = {{9, 1}, {18, 1}, {5, 2}, {9, 2}, {18, 2}};
+constexpr FsShape kFsShapes[] = {{9, 1}, {18, 1}, {5, 2}, {9, 2}, {18, 2}, {18, 4}};
 
 template <int KS, int S>
 void launch_mfma_fs_shape(const lce::MfmaParams &p, int out, dim3 grid, size_t lds,
@@ -437,17 +437,19 @@ void launch_mfma_fs(const lce::MfmaParams &p, FsShape sh, int out, dim3 grid, si
     else if (sh.ks == 18 && sh.s == 1) launch_mfma_fs_shape<18, 1>(p, out, grid, lds, st);
     else if (sh.ks == 5 && sh.s == 2) launch_mfma_fs_shape<5, 2>(p, out, grid, lds, st);
     else if (sh.ks == 9 && sh.s == 2) launch_mfma_fs_shape<9, 2>(p, out, grid, lds, st);
-    else launch_mfma_fs_shape<18, 2>(p, out, grid, lds, st);
+    else if (sh.ks == 18 && sh.s == 2) launch_mfma_fs_shape<18, 2>(p, out, grid, lds, st);
+    else launch_mfma_fs_shape<18, 4>(p, out, grid, lds, st);
 }
 
 // LDS of the filter-stationary kernel: every widened word of the region,
 // then the larger of the packed region (staged before the loop, with the
-// 256-word slack of its last DMA instruction) and (S = 2) the partial-sum
-// exchange: two buffers x F filter blocks x two pixel blocks, 4 KB each.
+// 256-word slack of its last DMA instruction) and (S > 1) the partial-sum
+// exchange: two buffers x F filter blocks x two pixel blocks x (S-1)
+// partials, 4 KB each.
 size_t mfma_fs_lds(const lce::MfmaParams &p, FsShape sh, int tile_rows) {
     const size_t a = (size_t)p.cwe * tile_rows * p.pw * 16;
     const size_t bits = ((size_t)tile_rows * p.pw * p.cw + 256) * 4;
-    const size_t red = sh.s > 1 ? (size_t)2 * (4 / sh.s) * 2 * 4096 : 0;
+    const size_t red = sh.s > 1 ? (size_t)2 * (4 / sh.s) * 2 * (sh.s - 1) * 4096 : 0;
     return a + std::max(bits, red);
 }
 
@@ -477,14 +479,15 @@ FsPlan plan_mfma_fs(const lce::MfmaParams &p, int64_t cus, int blocks32, int kst
         const int f = 4 / sh.s;
         const int64_t fgroups = (blocks32 + f - 1) / f;
         const int64_t pg = std::max<int64_t>(1, cus / fgroups);
-        int64_t px = ((int64_t)p.m + pg - 1) / pg;
-        px = (px + 31) / 32 * 32;
+        // (not rounded to whole blocks: the block count is the same, and an
+        // exact share often covers whole images or rows, with fewer rows)
+        const int64_t px = ((int64_t)p.m + pg - 1) / pg;
         if (px > (1 << 20)) continue;
         const int tr = mfma_tile_rows(p, (int)px);
         const size_t lds = mfma_fs_lds(p, sh, tr);
         if (lds > (size_t)device_max_lds()) continue;
         if ((int64_t)tr * p.pw * p.cwe > INT32_MAX / 2) continue;
-        const int64_t nb = px / 32;
+        const int64_t nb = (px + 31) / 32;
         const int64_t cost = nb * sh.ks + (sh.s > 1 ? nb : 0);
         if (best_cost < 0 || cost < best_cost) {
             best_cost = cost;
@@ -874,19 +877,26 @@ lce_status lce_bconv2d_mfma(const lce_bconv2d_desc *desc, const int32_t *x_packe
     const int ks_env = env_int("LCE_MFMA_KS", -1);
 
     // Filter-stationary schedule: the default wherever an instance fits, up
-    // to 36 K steps (longer K runs on the K-split schedule below, measured
-    // faster there: its workgroups split K four ways); LCE_MFMA_FS=0 turns
-    // it off, LCE_MFMA_KS forces one of the others.
-    if (ks_env < 0 && env_int("LCE_MFMA_FS", 1) != 0 && ksteps <= 36) {
+    // to 36 K steps.  Longer K runs on the K-split schedule below unless an
+    // instance is forced (LCE_MFMA_FS_KS / _S): with S = 4 waves per filter
+    // block every filter group re-widens the same input region and the
+    // partial sums add LDS traffic, measured slower than the K split on the
+    // 7x7x512 layer.  LCE_MFMA_FS=0 turns it off, LCE_MFMA_KS forces one of
+    // the others.
+    const bool fs_forced = env_int("LCE_MFMA_FS_KS", 0) && env_int("LCE_MFMA_FS_S", 0);
+    if (ks_env < 0 && env_int("LCE_MFMA_FS", 1) != 0 &&
+        (ksteps <= 36 || (fs_forced && ksteps <= 72))) {
         const FsPlan fp = plan_mfma_fs(p, cus, blocks32, (int)ksteps);
         if (fp.shape.ks) {
             p.tile_rows = fp.tile_rows;
             p.fs_pixels = fp.pixels;
             p.div_plane = lce::make_fastdiv((uint32_t)(fp.tile_rows * p.pw));
             size_t lds = fp.lds;
-            // LCE_MFMA_FS_PAD=1: claim more than half of a CU's LDS, so that no
-            // CU holds two workgroups while another holds none
-            if (env_int("LCE_MFMA_FS_PAD", 0) == 1)
+            // claim more than half of a CU's LDS when the grid fits the CUs,
+            // so that no CU holds two workgroups while another holds none
+            // (LCE_MFMA_FS_PAD=0 turns this off)
+            const int64_t wgs = fp.groups * ((blocks32 + 4 / fp.shape.s - 1) / (4 / fp.shape.s));
+            if (env_int("LCE_MFMA_FS_PAD", 1) == 1 && wgs <= cus)
                 lds = std::max(lds, (size_t)device_max_lds() / 2 + 1024);
             const dim3 grid((unsigned)fp.groups,
                             (unsigned)((blocks32 + 4 / fp.shape.s - 1) / (4 / fp.shape.s)));

@@ -160,7 +160,7 @@ def test_mfma_every_tile_shape(monkeypatch, schedule, mbw, nblk):
 # for each, layers whose K steps (taps x ceil(Cw/2), Cw rounded up as the
 # widened filters are) need every wave of a filter block: ragged sizes,
 # stride 2, non-square filters, every output type, zero padding.
-FS_INSTANCES = [(9, 1), (18, 1), (5, 2), (9, 2), (18, 2)]
+FS_INSTANCES = [(9, 1), (18, 1), (5, 2), (9, 2), (18, 2), (18, 4)]
 
 
 def fs_layers(ks, s):
