@@ -787,10 +787,13 @@ __global__ __launch_bounds__(kMfmaThreads) void bconv2d_mfma_ks_kernel(MfmaParam
 // alternating buffers), each wave finishing one block of the pair.  The host
 // gives each workgroup the same number of pixel blocks and about one
 // workgroup per CU.
-// Ring depth: K step i of every pair uses slot i % D, and the last steps of
-// a pair refill their slots with the first steps of the next, so D divides
-// KS (4 or 3 K steps, 5 for KS = 5).
-constexpr int fs_depth(int ks) { return ks % 4 == 0 ? 4 : ks % 3 == 0 ? 3 : ks; }
+// Ring of A operands: K step i of every pair uses slot i % D and, before
+// its products, refills the slot of step i-1 with step i + D - 1 (of this
+// pair, or of the next past its end), so D divides KS (4 or 3 K steps, 5
+// for KS = 5) and the reads run D - 1 steps ahead.  The refill comes first
+// in the step because the loop's pace is set by LDS: every read issued
+// later, behind the step's other work, would leave the LDS idle meanwhile.
+constexpr int fs_depth(int ks) { return ks % 6 == 0 ? 6 : ks % 4 == 0 ? 4 : ks % 3 == 0 ? 3 : ks; }
 
 // The packed input region of a workgroup by LDS DMA: element q = g*plane +
 // rc of `abits` holds words [g*V, g*V + V) of region location rc (V = 4 or
@@ -906,17 +909,18 @@ __device__ __forceinline__ void for_each_index(Fn &&f, std::integer_sequence<int
     (f(std::integral_constant<int, I>{}), ...);
 }
 
-// Output bits of value V of an accumulator block (see block_bits): one
-// compare gives the lane masks of pixels r0 and r0 + 4 (r0 = (V/4)*8 +
-// V%4), and two v_writelane drop them into the lanes of their pixels.  The
-// s_nop 1 covers the VALU-written mask SGPRs (the compiler's hazard
-// recognizer does not look inside inline asm).  Nothing on the scalar unit
-// reads the masks: a scalar read of a VALU-written SGPR stalls the wave
-// until the compare retires, which the matrix products cannot hide.
+// Output bits of value V of an accumulator block (see block_bits): the
+// lane mask `m` of "value < T" (one compare, issued a K step earlier) holds
+// pixels r0 (lanes 0-31) and r0 + 4 (lanes 32-63), r0 = (V/4)*8 + V%4, and
+// two v_writelane drop them into the lanes of their pixels.  A v_writelane
+// that reads the mask of a compare issued right before it stalls the wave
+// until the compare's SGPR write lands (measured: ~35 cycles per K step
+// next to the ring's LDS reads); a step later the mask is there.  The s_nop
+// 1 covers a VALU-written SGPR in any case (the compiler's hazard
+// recognizer does not look inside inline asm).
 template <int V>
-__device__ __forceinline__ void bits_one_value(float a, float T, uint32_t &word) {
+__device__ __forceinline__ void write_value_bits(uint64_t m, uint32_t &word) {
     constexpr int r0 = (V >> 2) * 8 + (V & 3);
-    const uint64_t m = __ballot(a < T);
     asm volatile(
         "s_nop 1\n\t"
         "v_writelane_b32 %0, %1, %3\n\t"
@@ -925,14 +929,12 @@ __device__ __forceinline__ void bits_one_value(float a, float T, uint32_t &word)
         : "s"((uint32_t)m), "s"((uint32_t)(m >> 32)), "i"(r0), "i"(r0 + 4));
 }
 
-// Filter-stationary instances: KS K steps per wave, S waves per filter
-// block (1 or 2).
 template <int KS, int S, int OUT>
 __global__ __launch_bounds__(kMfmaThreads) void bconv2d_mfma_fs_kernel(MfmaParams p) {
     static_assert(S == 1 || S == 2 || S == 4, "1, 2 or 4 waves per filter block");
     constexpr int F = 4 / S;
     constexpr int D = fs_depth(KS);
-    static_assert(KS % D == 0 && D <= 5, "ring depth");
+    static_assert(KS % D == 0 && D <= 6, "ring depth");
     constexpr int NFB = S == 1 ? 2 : 1;                  // blocks of a pair this wave finishes
     constexpr int NV = 16 * NFB;                         // values it finishes per pair
     constexpr int kFirst = S == 1 ? 1 : 2;               // first K step that finishes values
@@ -1097,22 +1099,19 @@ __global__ __launch_bounds__(kMfmaThreads) void bconv2d_mfma_fs_kernel(MfmaParam
     // value N of the finishing order: block N/16 of those this wave
     // finishes, value N%16; a block's output is stored after its last value.
     // No branch: values of a missing block (single last block) or of
-    // filters past C_out' are computed and not stored.
-    auto finish_one = [&](auto nc) __attribute__((always_inline)) {
+    // filters past C_out' are computed and not stored.  Bitpacked output
+    // finishes a value in two parts, the compare (finish_cmp) and, a K step
+    // later in the pipeline, the lane writes and the store (finish_write).
+    uint64_t mk[NV];
+    auto finish_cmp = [&](auto nc) __attribute__((always_inline)) {
         constexpr int N = decltype(nc)::value;
         constexpr int j = N / 16, v = N % 16;
-        const int blk = S == 1 ? j : sk;                 // block of the pair
-        const bool store = fvalid && blk < fin_nbp;
-        const int mw = m0 + (fin_b0 + blk) * 32;
         if constexpr (OUT == OUT_BITS) {
-            if (v == 0) word[j] = 0u;
-            bits_one_value<v>(fin[j][v], ep_a, word[j]);
-            if (v == 15) {
-                const int m = mw + lane;
-                if (store && lane < 32 && m < m_end)
-                    reinterpret_cast<uint32_t *>(p.out)[(size_t)m * p.cwo + (f0 >> 5)] = word[j];
-            }
+            mk[N] = __ballot(fin[j][v] < ep_a);
         } else {
+            const int blk = S == 1 ? j : sk;             // block of the pair
+            const bool store = fvalid && blk < fin_nbp;
+            const int mw = m0 + (fin_b0 + blk) * 32;
             const int m = mw + (v >> 2) * 8 + half * 4 + (v & 3);
             const int c = min(max((int)fin[j][v], p.lo), p.hi);
             if (store && co_ok && m < m_end) {
@@ -1124,19 +1123,35 @@ __global__ __launch_bounds__(kMfmaThreads) void bconv2d_mfma_fs_kernel(MfmaParam
             }
         }
     };
-    // values [LO, HI) of the finishing order
-    auto finish_range = [&](auto loc, auto hic) __attribute__((always_inline)) {
+    auto finish_write = [&](auto nc) __attribute__((always_inline)) {
+        constexpr int N = decltype(nc)::value;
+        constexpr int j = N / 16, v = N % 16;
+        if constexpr (OUT == OUT_BITS) {
+            const int blk = S == 1 ? j : sk;             // block of the pair
+            const bool store = fvalid && blk < fin_nbp;
+            if (v == 0) word[j] = 0u;
+            write_value_bits<v>(mk[N], word[j]);
+            if (v == 15) {
+                const int m = m0 + (fin_b0 + blk) * 32 + lane;
+                if (store && lane < 32 && m < m_end)
+                    reinterpret_cast<uint32_t *>(p.out)[(size_t)m * p.cwo + (f0 >> 5)] = word[j];
+            }
+        }
+    };
+    // values [LO, HI) of the finishing order, either part
+    auto finish_range = [&](auto fn, auto loc, auto hic) __attribute__((always_inline)) {
         constexpr int LO = decltype(loc)::value, HI = decltype(hic)::value;
         if constexpr (LO < HI)
             for_each_index([&](auto uc) __attribute__((always_inline)) {
-                finish_one(std::integral_constant<int, LO + decltype(uc)::value>{});
+                fn(std::integral_constant<int, LO + decltype(uc)::value>{});
             }, std::make_integer_sequence<int, HI - LO>{});
     };
     // finish the blocks in the accumulators at once (outside the pipeline)
     auto finish_all = [&](int nbp) __attribute__((always_inline)) {
         collect_prev(nbp);
         collect_partner();
-        finish_range(std::integral_constant<int, 0>{}, std::integral_constant<int, NV>{});
+        finish_range(finish_cmp, std::integral_constant<int, 0>{}, std::integral_constant<int, NV>{});
+        finish_range(finish_write, std::integral_constant<int, 0>{}, std::integral_constant<int, NV>{});
     };
 
     // ---- the pipelined loop over pairs (and a last single block)
@@ -1144,9 +1159,9 @@ __global__ __launch_bounds__(kMfmaThreads) void bconv2d_mfma_fs_kernel(MfmaParam
     int base[2] = {block_base(0), block_base(min(1, nb - 1))};
     u32x4 ring[D][2];
 #pragma unroll
-    for (int i = 0; i < D; ++i)
+    for (int i = 0; i < D - 1; ++i)
 #pragma unroll
-        for (int j = 0; j < 2; ++j) ring[i][j] = atile[base[j] + aoff[i < KS ? i : KS - 1] + z];
+        for (int j = 0; j < 2; ++j) ring[i][j] = atile[base[j] + aoff[i] + z];
 
     const mfma_v16f zero16 = {0.0f, 0.0f, 0.0f, 0.0f, 0.0f, 0.0f, 0.0f, 0.0f,
                               0.0f, 0.0f, 0.0f, 0.0f, 0.0f, 0.0f, 0.0f, 0.0f};
@@ -1167,11 +1182,25 @@ __global__ __launch_bounds__(kMfmaThreads) void bconv2d_mfma_fs_kernel(MfmaParam
         if constexpr (has_prev) collect_prev(2);         // before the products overwrite them
         auto step = [&](auto ic) __attribute__((always_inline)) {
             constexpr int i = decltype(ic)::value;
-            // finishing pieces: values [lo, mid) after the first product,
-            // [mid, hi) after the second
+            // refill slot (i + D - 1) % D, the one step i-1 used
+            constexpr int nxs = i + D - 1;
+            if constexpr (nxs < KS) {
+#pragma unroll
+                for (int j = 0; j < NBP; ++j) ring[nxs % D][j] = atile[base[j] + aoff[nxs] + z];
+            } else if constexpr (NBP == 2) {
+#pragma unroll
+                for (int j = 0; j < 2; ++j)
+                    ring[nxs % D][j] = atile[next_base[j] + aoff[nxs - KS] + z];
+            }
+            asm volatile("" ::: "memory");
+            __builtin_amdgcn_sched_barrier(0);
+            // finishing pieces: the compares of values [lo, hi) after the
+            // first product, the lane writes of the previous step's values
+            // [plo, phi) after the second (the last ones after the loop)
             constexpr int lo = i >= kFirst ? (i - kFirst) * kPer : NV;
             constexpr int hi = lo + kPer < NV ? lo + kPer : NV;
-            constexpr int mid = NBP == 2 ? (lo + hi) / 2 : hi;
+            constexpr int plo = i > kFirst ? (i - 1 - kFirst) * kPer : NV;
+            constexpr int phi = plo + kPer < NV ? plo + kPer : NV;
 #pragma unroll
             for (int j = 0; j < NBP; ++j) {
                 acc[j] = mfma_fp4(ring[i % D][j], breg[i], i == 0 ? zero16 : acc[j]);
@@ -1180,31 +1209,27 @@ __global__ __launch_bounds__(kMfmaThreads) void bconv2d_mfma_fs_kernel(MfmaParam
                 if constexpr (has_prev) {
                     if (j == 0) {
                         if constexpr (S > 1 && i == 1) collect_partner();
-                        finish_range(std::integral_constant<int, lo>{},
-                                     std::integral_constant<int, mid>{});
-                    } else {
-                        finish_range(std::integral_constant<int, mid>{},
+                        finish_range(finish_cmp, std::integral_constant<int, lo>{},
                                      std::integral_constant<int, hi>{});
                     }
+                    if (j == NBP - 1)
+                        finish_range(finish_write, std::integral_constant<int, plo>{},
+                                     std::integral_constant<int, phi>{});
                 }
+                // keep each piece here: a compiler memory barrier for the
+                // passes that move loads and stores, a scheduling barrier for
+                // the machine scheduler
                 asm volatile("" ::: "memory");
                 __builtin_amdgcn_sched_barrier(0);
             }
-            if constexpr (i + D < KS) {
-#pragma unroll
-                for (int j = 0; j < NBP; ++j) ring[i % D][j] = atile[base[j] + aoff[i + D] + z];
-            } else if constexpr (NBP == 2) {
-#pragma unroll
-                for (int j = 0; j < 2; ++j)
-                    ring[i % D][j] = atile[next_base[j] + aoff[i + D - KS] + z];
-            }
-            // keep the step's LDS reads here: a compiler memory barrier for
-            // the passes that move loads, a scheduling barrier for the
-            // machine scheduler
-            asm volatile("" ::: "memory");
-            __builtin_amdgcn_sched_barrier(0);
         };
         for_each_index(step, std::make_integer_sequence<int, KS>{});
+        if constexpr (has_prev) {                        // the last step's lane writes
+            constexpr int llo = KS - 1 >= kFirst ? (KS - 1 - kFirst) * kPer : NV;
+            constexpr int lhi = llo + kPer < NV ? llo + kPer : NV;
+            finish_range(finish_write, std::integral_constant<int, llo>{},
+                         std::integral_constant<int, lhi>{});
+        }
         base[0] = next_base[0];
         base[1] = next_base[1];
         fin_b0 = b0;
