@@ -57,6 +57,9 @@ constexpr int kMfmaThreads = 256;
 constexpr uint32_t kFp4PlusOne = 0x22222222u;
 constexpr uint32_t kFp4SignBits = 0x88888888u;
 
+// K steps (S*KS) a filter-stationary instance covers at most.
+constexpr int kFsMaxSteps = 72;
+
 struct MfmaParams {
     const uint32_t *x;      // [N][H][W][Cw] bitpacked activations
     const u32x4 *wexp;      // [KH*KW*CwE][CoutP] widened filters (16 bytes = 32 values)
@@ -78,6 +81,11 @@ struct MfmaParams {
     FastDiv div_plane;               // tile_rows * pw: region locations
     FastDiv div_cwh, div_kw;         // cwe / 2 (word pairs per tap), kw
     FastDiv div_groups;              // region_vec-word groups per location
+    // filter-stationary schedule: A-tile offset (in 16-byte words) of K step
+    // s = (tap t = ky*KW + kx, word pair q) from a pixel's window origin,
+    // 2q*plane + ky*PW + kx (plane = tile_rows*pw); steps past the last
+    // repeat the last one
+    int32_t fs_koff[kFsMaxSteps];
 };
 
 typedef int mfma_v8i __attribute__((ext_vector_type(8)));
@@ -197,9 +205,6 @@ __device__ __forceinline__ void wait_vmcnt() {
     static_assert(N >= 0 && N < 64, "vmcnt range");
     __builtin_amdgcn_s_waitcnt((N & 0xF) | ((N >> 4) << 14) | 0x70 | 0xF00);
 }
-
-// s_waitcnt lgkmcnt(0) alone (vmcnt and expcnt fields at their maxima).
-__device__ __forceinline__ void wait_lgkmcnt0() { __builtin_amdgcn_s_waitcnt(0xC07F); }
 
 // Workgroup barrier for the pipelined loop: this wave's LDS accesses done
 // (lgkmcnt), then s_barrier.  Unlike __syncthreads() it carries no memory
@@ -499,67 +504,112 @@ __global__ __launch_bounds__(kMfmaThreads) void bconv2d_mfma_kernel(MfmaParams p
     }
 }
 
-// Widen the packed input region of a workgroup into LDS, every word of it:
-// atile[j*plane + rc] = word j of region location rc (rc = r*PW + c over
-// TR stacked padded rows from row0).  Padding locations are 0 words (+1.0),
-// or 0.0 under zero padding; words past Cw are +1.0 (their filter values
-// are 0.0).  Loads are unconditional (padding reads zeros), four per thread
-// in flight.
-__device__ __forceinline__ void widen_region(const MfmaParams &p, u32x4 *atile, int row0,
-                                             int plane, int tid) {
-    constexpr int U = 4;
-    const int V = p.region_vec;
-    const int groups = p.div_groups.d;
-    const int total = plane * groups;
-    const int PW = p.pw;
-    for (int e0 = 0; e0 < total; e0 += U * kMfmaThreads) {
-        u32x4 v[U];
-        int dst[U];
-        uint32_t fills[U];
-#pragma unroll
-        for (int u = 0; u < U; ++u) {
-            const int e = min(e0 + u * kMfmaThreads + tid, total - 1);
-            const int rc = (int)fast_div((uint32_t)e, p.div_groups);
-            const int g = e - rc * groups;
+// The packed input region of a workgroup by LDS DMA: element q = g*plane +
+// rc of `abits` holds words [g*V, g*V + V) of region location rc (V = 4 or
+// 1 words per lane); padding locations read zeros.  The last instruction's
+// extra lanes land in a slack of 64*V words after the region.  Nothing
+// reaches registers, so the loads stay in flight until the caller waits
+// for them (vmcnt) together with its other loads.
+__device__ __forceinline__ void dma_region(const MfmaParams &p, uint32_t *abits, int row0,
+                                           int plane, int wave, int lane) {
+    const int bits_words = plane * p.cw;
+    auto run = [&](auto vec_c) __attribute__((always_inline)) {
+        constexpr int V = decltype(vec_c)::value;
+        for (int u = wave; u * 64 * V < bits_words; u += kMfmaThreads / 64) {
+            const int q = min(u * 64 + lane, bits_words / V - 1);
+            const int g = (int)fast_div((uint32_t)q, p.div_plane);
+            const int rc = q - g * plane;
             const int r = (int)fast_div((uint32_t)rc, p.div_pw);
-            const int c = rc - r * PW;
+            const int c = rc - r * p.pw;
             const int R = row0 + r;
             const int img = (int)fast_div((uint32_t)R, p.div_ph);
             const int yy = R - img * p.ph - p.pt, xx = c - p.pl;
             const bool inside = img < p.n && (unsigned)yy < (unsigned)p.h &&
                                 (unsigned)xx < (unsigned)p.w;
-            const bool load = inside && g * V < p.cw;
             const uint32_t *src =
-                load ? p.x + (((size_t)img * p.h + yy) * p.w + xx) * p.cw + g * V : g_mfma_zero;
-            if (V == 4)
-                v[u] = *reinterpret_cast<const u32x4 *>(src);
+                inside ? p.x + (((size_t)img * p.h + yy) * p.w + xx) * p.cw + g * V : g_mfma_zero;
+            if constexpr (V == 4)
+                __builtin_amdgcn_global_load_lds((mfma_global_void *)src,
+                                                 (mfma_lds_void *)(abits + u * 64 * V), 16, 0, 0);
             else
-                v[u] = u32x4{*src, 0u, 0u, 0u};
-            dst[u] = g * V * plane + rc;
-            fills[u] = (p.pad_zero && !inside) ? 0u : kFp4PlusOne;
+                __builtin_amdgcn_global_load_lds((mfma_global_void *)src,
+                                                 (mfma_lds_void *)(abits + u * 64 * V), 4, 0, 0);
         }
+    };
+    if (p.region_vec == 4)
+        run(std::integral_constant<int, 4>{});
+    else
+        run(std::integral_constant<int, 1>{});
+}
+
+// Widen the packed region (dma_region layout) into the A tile: atile[j*plane
+// + rc] = word j of location rc.  Words past Cw are +1.0 (their filter
+// values are 0.0); under zero padding, locations outside the image are
+// 0.0.  One straight-line path per staging width, four elements per thread
+// in flight (all reads before the writes):
+//   * V = 4: element e = g*plane + rc is one 16-byte group, widened into
+//     four A-tile words g*4 .. g*4+3;
+//   * V = 1: element e is word e / plane of location e % plane, at the
+//     same index in both arrays.
+__device__ __forceinline__ bool region_inside(const MfmaParams &p, int row0, int rc) {
+    const int r = (int)fast_div((uint32_t)rc, p.div_pw);
+    const int c = rc - r * p.pw;
+    const int R = row0 + r;
+    const int img = (int)fast_div((uint32_t)R, p.div_ph);
+    const int yy = R - img * p.ph - p.pt, xx = c - p.pl;
+    return img < p.n && (unsigned)yy < (unsigned)p.h && (unsigned)xx < (unsigned)p.w;
+}
+
+__device__ __forceinline__ void widen_region_lds(const MfmaParams &p, const uint32_t *abits,
+                                                 u32x4 *atile, int row0, int plane, int tid,
+                                                 int z) {
+    constexpr int U = 4;
+    if (p.region_vec == 4) {
+        const int total = plane * (p.cw >> 2);
+        const u32x4 *src = reinterpret_cast<const u32x4 *>(abits);
+        for (int e0 = 0; e0 < total; e0 += U * kMfmaThreads) {
+            u32x4 w[U];
 #pragma unroll
-        for (int u = 0; u < U; ++u) {
-            if (e0 + u * kMfmaThreads + tid >= total) continue;
-            if (V == 4) {
+            for (int u = 0; u < U; ++u) w[u] = src[min(e0 + u * kMfmaThreads + tid, total - 1) + z];
 #pragma unroll
-                for (int j = 0; j < 4; ++j) atile[dst[u] + j * plane] = widen_word(v[u][j], fills[u]);
-            } else {
-                atile[dst[u]] = widen_word(v[u][0], fills[u]);
+            for (int u = 0; u < U; ++u) {
+                const int e = e0 + u * kMfmaThreads + tid;
+                if (e >= total) break;
+                const int g = (int)fast_div((uint32_t)e, p.div_plane);
+                const int rc = e - g * plane;
+                const uint32_t fill = p.pad_zero && !region_inside(p, row0, rc) ? 0u : kFp4PlusOne;
+#pragma unroll
+                for (int k = 0; k < 4; ++k) atile[(4 * g + k) * plane + rc] = widen_word(w[u][k], fill);
+            }
+        }
+    } else {
+        const int total = plane * p.cw;
+        for (int e0 = 0; e0 < total; e0 += U * kMfmaThreads) {
+            uint32_t w[U];
+#pragma unroll
+            for (int u = 0; u < U; ++u) w[u] = abits[min(e0 + u * kMfmaThreads + tid, total - 1) + z];
+#pragma unroll
+            for (int u = 0; u < U; ++u) {
+                const int e = e0 + u * kMfmaThreads + tid;
+                if (e >= total) break;
+                uint32_t fill = kFp4PlusOne;
+                if (p.pad_zero) {
+                    const int j = (int)fast_div((uint32_t)e, p.div_plane);
+                    if (!region_inside(p, row0, e - j * plane)) fill = 0u;
+                }
+                atile[e] = widen_word(w[u], fill);
             }
         }
     }
-}
-
-// The four values 4*VQ .. 4*VQ+3 of an accumulator block as output bits
-// (see block_bits): pixels VQ*8 .. VQ*8+7 of the block.
-template <int VQ>
-__device__ __forceinline__ void quad_bits(const mfma_v16f &val, float T, uint64_t fmask,
-                                          uint32_t &word) {
-    block_bits_step<4 * VQ>(val, T, fmask, word);
-    block_bits_step<4 * VQ + 1>(val, T, fmask, word);
-    block_bits_step<4 * VQ + 2>(val, T, fmask, word);
-    block_bits_step<4 * VQ + 3>(val, T, fmask, word);
+    // words past Cw: +1.0 (0.0 outside the image under zero padding)
+    for (int e = plane * p.cw + tid; e < plane * p.cwe; e += kMfmaThreads) {
+        uint32_t fill = kFp4PlusOne;
+        if (p.pad_zero) {
+            const int j = (int)fast_div((uint32_t)e, p.div_plane);
+            if (!region_inside(p, row0, e - j * plane)) fill = 0u;
+        }
+        atile[e] = widen_word(0u, fill);
+    }
 }
 
 // K-split schedule, for layers whose output tile per workgroup is small
@@ -621,6 +671,11 @@ __global__ __launch_bounds__(kMfmaThreads) void bconv2d_mfma_ks_kernel(MfmaParam
         }
     }
 
+    // the packed input region by LDS DMA, past the A tile (issued before
+    // the filter loads below: memory counters retire in order)
+    uint32_t *abits = reinterpret_cast<uint32_t *>(smem + p.cwe * plane);
+    dma_region(p, abits, row0, plane, wave, lane);
+
     // B of this wave's local step i (K step wave + 4i, clamped: steps past
     // the last re-read it): word row t*cwe + 2*jp + half, NBLK blocks of 32
     // filters, 16 bytes per lane per block.
@@ -640,9 +695,13 @@ __global__ __launch_bounds__(kMfmaThreads) void bconv2d_mfma_ks_kernel(MfmaParam
 #pragma unroll
     for (int r = 0; r < kRing - 1; ++r) load_b(r, ring[r]);
 
-    // ---- widen the whole region (every word of every location)
-    widen_region(p, atile, row0, plane, tid);
-    int z = lds_barrier();                               // the A planes are complete
+    // ---- widen the whole region (every word of every location) once this
+    // wave's DMA has landed (at most the ring's loads still outstanding) and
+    // every wave's has (barrier), while the filter ring is still arriving
+    wait_vmcnt<(kRing - 1) * NBLK>();
+    int z = lds_barrier();
+    widen_region_lds(p, abits, atile, row0, plane, tid, z);
+    z = lds_barrier();                                   // the A planes are complete
 
     mfma_v16f acc[MBW][NBLK];
 #pragma unroll
@@ -795,114 +854,6 @@ __global__ __launch_bounds__(kMfmaThreads) void bconv2d_mfma_ks_kernel(MfmaParam
 // later, behind the step's other work, would leave the LDS idle meanwhile.
 constexpr int fs_depth(int ks) { return ks % 6 == 0 ? 6 : ks % 4 == 0 ? 4 : ks % 3 == 0 ? 3 : ks; }
 
-// The packed input region of a workgroup by LDS DMA: element q = g*plane +
-// rc of `abits` holds words [g*V, g*V + V) of region location rc (V = 4 or
-// 1 words per lane); padding locations read zeros.  The last instruction's
-// extra lanes land in a slack of 64*V words after the region.  Nothing
-// reaches registers, so the loads stay in flight until the caller waits
-// for them (vmcnt) together with its other loads.
-__device__ __forceinline__ void dma_region(const MfmaParams &p, uint32_t *abits, int row0,
-                                           int plane, int wave, int lane) {
-    const int bits_words = plane * p.cw;
-    auto run = [&](auto vec_c) __attribute__((always_inline)) {
-        constexpr int V = decltype(vec_c)::value;
-        for (int u = wave; u * 64 * V < bits_words; u += kMfmaThreads / 64) {
-            const int q = min(u * 64 + lane, bits_words / V - 1);
-            const int g = (int)fast_div((uint32_t)q, p.div_plane);
-            const int rc = q - g * plane;
-            const int r = (int)fast_div((uint32_t)rc, p.div_pw);
-            const int c = rc - r * p.pw;
-            const int R = row0 + r;
-            const int img = (int)fast_div((uint32_t)R, p.div_ph);
-            const int yy = R - img * p.ph - p.pt, xx = c - p.pl;
-            const bool inside = img < p.n && (unsigned)yy < (unsigned)p.h &&
-                                (unsigned)xx < (unsigned)p.w;
-            const uint32_t *src =
-                inside ? p.x + (((size_t)img * p.h + yy) * p.w + xx) * p.cw + g * V : g_mfma_zero;
-            if constexpr (V == 4)
-                __builtin_amdgcn_global_load_lds((mfma_global_void *)src,
-                                                 (mfma_lds_void *)(abits + u * 64 * V), 16, 0, 0);
-            else
-                __builtin_amdgcn_global_load_lds((mfma_global_void *)src,
-                                                 (mfma_lds_void *)(abits + u * 64 * V), 4, 0, 0);
-        }
-    };
-    if (p.region_vec == 4)
-        run(std::integral_constant<int, 4>{});
-    else
-        run(std::integral_constant<int, 1>{});
-}
-
-// Widen the packed region (dma_region layout) into the A tile: atile[j*plane
-// + rc] = word j of location rc.  Words past Cw are +1.0 (their filter
-// values are 0.0); under zero padding, locations outside the image are
-// 0.0.  One straight-line path per staging width, four elements per thread
-// in flight (all reads before the writes):
-//   * V = 4: element e = g*plane + rc is one 16-byte group, widened into
-//     four A-tile words g*4 .. g*4+3;
-//   * V = 1: element e is word e / plane of location e % plane, at the
-//     same index in both arrays.
-__device__ __forceinline__ bool region_inside(const MfmaParams &p, int row0, int rc) {
-    const int r = (int)fast_div((uint32_t)rc, p.div_pw);
-    const int c = rc - r * p.pw;
-    const int R = row0 + r;
-    const int img = (int)fast_div((uint32_t)R, p.div_ph);
-    const int yy = R - img * p.ph - p.pt, xx = c - p.pl;
-    return img < p.n && (unsigned)yy < (unsigned)p.h && (unsigned)xx < (unsigned)p.w;
-}
-
-__device__ __forceinline__ void widen_region_lds(const MfmaParams &p, const uint32_t *abits,
-                                                 u32x4 *atile, int row0, int plane, int tid,
-                                                 int z) {
-    constexpr int U = 4;
-    if (p.region_vec == 4) {
-        const int total = plane * (p.cw >> 2);
-        const u32x4 *src = reinterpret_cast<const u32x4 *>(abits);
-        for (int e0 = 0; e0 < total; e0 += U * kMfmaThreads) {
-            u32x4 w[U];
-#pragma unroll
-            for (int u = 0; u < U; ++u) w[u] = src[min(e0 + u * kMfmaThreads + tid, total - 1) + z];
-#pragma unroll
-            for (int u = 0; u < U; ++u) {
-                const int e = e0 + u * kMfmaThreads + tid;
-                if (e >= total) break;
-                const int g = (int)fast_div((uint32_t)e, p.div_plane);
-                const int rc = e - g * plane;
-                const uint32_t fill = p.pad_zero && !region_inside(p, row0, rc) ? 0u : kFp4PlusOne;
-#pragma unroll
-                for (int k = 0; k < 4; ++k) atile[(4 * g + k) * plane + rc] = widen_word(w[u][k], fill);
-            }
-        }
-    } else {
-        const int total = plane * p.cw;
-        for (int e0 = 0; e0 < total; e0 += U * kMfmaThreads) {
-            uint32_t w[U];
-#pragma unroll
-            for (int u = 0; u < U; ++u) w[u] = abits[min(e0 + u * kMfmaThreads + tid, total - 1) + z];
-#pragma unroll
-            for (int u = 0; u < U; ++u) {
-                const int e = e0 + u * kMfmaThreads + tid;
-                if (e >= total) break;
-                uint32_t fill = kFp4PlusOne;
-                if (p.pad_zero) {
-                    const int j = (int)fast_div((uint32_t)e, p.div_plane);
-                    if (!region_inside(p, row0, e - j * plane)) fill = 0u;
-                }
-                atile[e] = widen_word(w[u], fill);
-            }
-        }
-    }
-    // words past Cw: +1.0 (0.0 outside the image under zero padding)
-    for (int e = plane * p.cw + tid; e < plane * p.cwe; e += kMfmaThreads) {
-        uint32_t fill = kFp4PlusOne;
-        if (p.pad_zero) {
-            const int j = (int)fast_div((uint32_t)e, p.div_plane);
-            if (!region_inside(p, row0, e - j * plane)) fill = 0u;
-        }
-        atile[e] = widen_word(0u, fill);
-    }
-}
-
 // Calls f(std::integral_constant<int, I>) for I = 0 .. N-1 in order.
 template <typename Fn, int... I>
 __device__ __forceinline__ void for_each_index(Fn &&f, std::integer_sequence<int, I...>) {
@@ -932,6 +883,15 @@ __device__ __forceinline__ void write_value_bits(uint64_t m, uint32_t &word) {
 template <int KS, int S, int OUT>
 __global__ __launch_bounds__(kMfmaThreads) void bconv2d_mfma_fs_kernel(MfmaParams p) {
     static_assert(S == 1 || S == 2 || S == 4, "1, 2 or 4 waves per filter block");
+    // Every cache line of the kernel arguments this kernel reads, fetched in
+    // one round trip up front: the compiler would otherwise load the fields
+    // in several dependent batches (behind branches), each first touch of a
+    // line a full memory latency.
+    {
+        const int ks0 = __builtin_amdgcn_readfirstlane((int)(threadIdx.x >> 6)) / (4 / S) * KS;
+        asm volatile("" ::"s"(p.x), "s"(p.oh), "s"(p.m), "s"(p.div_pw.d), "s"(p.fs_koff[ks0]),
+                     "s"(p.fs_koff[ks0 + KS / 2]), "s"(p.fs_koff[ks0 + KS - 1]));
+    }
     constexpr int F = 4 / S;
     constexpr int D = fs_depth(KS);
     static_assert(KS % D == 0 && D <= 6, "ring depth");
@@ -991,19 +951,20 @@ __global__ __launch_bounds__(kMfmaThreads) void bconv2d_mfma_fs_kernel(MfmaParam
     // offset of the same word and tap in the A tile (lane-dependent, so it
     // stays in a VGPR).  The loads are unconditional (filters past C_out'
     // read the last one and are never stored; steps past the last read the
-    // last row and are zeroed after the wait).
+    // last row and are zeroed on arrival).  Nothing waits for them here: the
+    // first pair's K step i waits for its own (memory counters retire in
+    // order), so the first products start while later filters still arrive.
+    static_assert(S * KS <= kFsMaxSteps, "offset table");
     u32x4 breg[KS];
     int aoff[KS];
     {
         const u32x4 *wcol = p.wexp + (size_t)half * p.coutp + min(co, p.coutp - 1);
+        const int hp = half * plane;
 #pragma unroll
         for (int i = 0; i < KS; ++i) {
             const int s = min(sk * KS + i, ksteps - 1);
             breg[i] = wcol[(size_t)(2 * s) * p.coutp];
-            const int t = (int)fast_div((uint32_t)s, p.div_cwh);
-            const int q = s - t * cwh;
-            const int ky = (int)fast_div((uint32_t)t, p.div_kw);
-            aoff[i] = (2 * q + half) * plane + ky * PW + (t - ky * p.kw);
+            aoff[i] = p.fs_koff[sk * KS + i] + hp;       // (word 2q + half)
         }
     }
 
@@ -1014,14 +975,10 @@ __global__ __launch_bounds__(kMfmaThreads) void bconv2d_mfma_fs_kernel(MfmaParam
     wait_vmcnt<KS>();
     int z = lds_barrier();                               // every wave's region DMA landed
     widen_region_lds(p, abits, atile, row0, plane, tid, z);
-    wait_vmcnt<0>();                                     // the filters
-#pragma unroll
-    for (int i = 0; i < KS; ++i)
-        if (sk * KS + i >= ksteps) breg[i] = u32x4{0u, 0u, 0u, 0u};
+    // sign bits of a flipped filter, applied to each step's filters as they
+    // arrive (first pair)
+    const uint32_t neg = OUT == OUT_BITS && flipped ? kFp4SignBits : 0u;
     if constexpr (OUT == OUT_BITS) {
-        const uint32_t neg = flipped ? kFp4SignBits : 0u;
-#pragma unroll
-        for (int i = 0; i < KS; ++i) breg[i] ^= u32x4{neg, neg, neg, neg};
         ep_a = co_ok ? thr_to_dot_bound_f(ep_a, p.lo, p.hi) : -INFINITY;
         if (flipped) ep_a = 1.0f - ep_a;
     }
@@ -1194,6 +1151,13 @@ __global__ __launch_bounds__(kMfmaThreads) void bconv2d_mfma_fs_kernel(MfmaParam
             }
             asm volatile("" ::: "memory");
             __builtin_amdgcn_sched_barrier(0);
+            // first pair: this step's filters have landed (the compiler waits
+            // for exactly this load); they take the flip, or 0.0 past the
+            // last K step
+            if constexpr (!has_prev) {
+                const uint32_t keep = sk * KS + i < ksteps ? ~0u : 0u;
+                breg[i] = (breg[i] ^ u32x4{neg, neg, neg, neg}) & u32x4{keep, keep, keep, keep};
+            }
             // finishing pieces: the compares of values [lo, hi) after the
             // first product, the lane writes of the previous step's values
             // [plo, phi) after the second (the last ones after the loop)
@@ -1238,16 +1202,21 @@ __global__ __launch_bounds__(kMfmaThreads) void bconv2d_mfma_fs_kernel(MfmaParam
     constexpr auto one = std::integral_constant<int, 1>{};
     constexpr auto yes = std::integral_constant<bool, true>{};
     constexpr auto no = std::integral_constant<bool, false>{};
-    if (npairs > 0) body(two, no, 0);
-    for (int pidx = 1; pidx < npairs; ++pidx) body(two, yes, 2 * pidx);
-    if (nb & 1) {
-        if (npairs > 0)
+    // (the bodies after the first are reached only through it, so that the
+    // compiler's counter waits find every filter load retired there, and
+    // wait for nothing, stores included, inside them)
+    if (npairs > 0) {
+        body(two, no, 0);
+        for (int pidx = 1; pidx < npairs; ++pidx) body(two, yes, 2 * pidx);
+        if (nb & 1) {
             body(one, yes, nb - 1);
-        else
-            body(one, no, nb - 1);
+            finish_all(1);
+        } else {
+            finish_all(2);
+        }
+    } else if (nb & 1) {
+        body(one, no, nb - 1);
         finish_all(1);
-    } else if (npairs > 0) {
-        finish_all(2);
     }
 }
 

@@ -501,13 +501,15 @@ FsPlan plan_mfma_fs(const lce::MfmaParams &p, int64_t cus, int blocks32, int kst
     return best;
 }
 
-// LDS of the K-split kernel: every widened word of the region, or the
-// reduction buffer (three partial copies of every 32x32 block), which
-// reuses it.
+// LDS of the K-split kernel: every widened word of the region followed by
+// the packed region it is widened from (with the 256-word slack of its last
+// DMA instruction), or the reduction buffer (three partial copies of every
+// 32x32 block), which reuses them.
 size_t mfma_ks_lds(const lce::MfmaParams &p, int mbw, int nblk, int tile_rows) {
     const size_t a = (size_t)p.cwe * tile_rows * p.pw * 16;
+    const size_t bits = ((size_t)tile_rows * p.pw * p.cw + 256) * 4;
     const size_t red = (size_t)mbw * nblk * 3 * 16 * 64 * 4;
-    return std::max(a, red);
+    return std::max(a + bits, red);
 }
 
 }  // namespace
@@ -891,6 +893,12 @@ lce_status lce_bconv2d_mfma(const lce_bconv2d_desc *desc, const int32_t *x_packe
             p.tile_rows = fp.tile_rows;
             p.fs_pixels = fp.pixels;
             p.div_plane = lce::make_fastdiv((uint32_t)(fp.tile_rows * p.pw));
+            const int plane = fp.tile_rows * p.pw, cwh = p.cwe / 2;
+            for (int s = 0; s < lce::kFsMaxSteps; ++s) {
+                const int sc = std::min<int>(s, (int)ksteps - 1);
+                const int t = sc / cwh, q = sc % cwh;
+                p.fs_koff[s] = 2 * q * plane + (t / d.kw) * p.pw + t % d.kw;
+            }
             size_t lds = fp.lds;
             // claim more than half of a CU's LDS when the grid fits the CUs,
             // so that no CU holds two workgroups while another holds none
