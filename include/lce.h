@@ -186,9 +186,10 @@ lce_status lce_fold_thresholds(const float *multiplier, const float *bias, int32
  * buffer (lce_bconv2d_mfma_weights).  Zero padding needs no correction table
  * there: padded locations simply widen to 0.0. */
 
-/* Bytes of the widened filter buffer of `desc` (16 bytes per 32 weights:
+/* Bytes of the widened filter buffer of `desc` (20 bytes per 32 weights:
  * KH*KW x Cw' words x C_out' filters, Cw' = ceil(C_in/32) rounded up to an
- * even word count or a multiple of 4, C_out' = C_out rounded up to 32).
+ * even word count or a multiple of 4, C_out' = C_out rounded up to 32; 16
+ * bytes widened and 4 bytes packed per word).
  * Errors: LCE_EINVAL (null pointer, bad field). */
 lce_status lce_bconv2d_mfma_weights_size(const lce_bconv2d_desc *desc, int64_t *bytes);
 
@@ -197,7 +198,11 @@ lce_status lce_bconv2d_mfma_weights_size(const lce_bconv2d_desc *desc, int64_t *
  * asynchronously on `stream`.  Layout: 16-byte element (t*Cw' + j)*C_out' + co
  * holds word j of tap t of filter co as 32 e2m1 codes (+1.0 = 0x2,
  * -1.0 = 0xA), channel 32j + c in 32-bit word c % 4, nibble c / 4.  Channels
- * past C_in and filters past C_out widen to 0.0.  Run once per filter tensor.
+ * past C_in and filters past C_out widen to 0.0.  Then, from byte
+ * 16*KH*KW*Cw'*C_out' on, the same elements as packed 32-bit words (bit 1 =
+ * -1; channels past C_in, words past Cw and filters past C_out 0): where
+ * C_in = 32*Cw', the filter-stationary schedule loads these and widens
+ * them itself.  Run once per filter tensor.
  * Errors: LCE_EINVAL, LCE_EALIGN, LCE_EHIP. */
 lce_status lce_bconv2d_mfma_weights(const lce_bconv2d_desc *desc, const int32_t *w_packed,
                                     void *w_fp4, hipStream_t stream);
@@ -213,7 +218,8 @@ lce_status lce_bconv2d_mfma_weights(const lce_bconv2d_desc *desc, const int32_t 
  * (the waves of a workgroup divide K; long K) and pixel-split (the rest).
  * The environment variables LCE_MFMA_FS (0 turns the first off),
  * LCE_MFMA_FS_KS / LCE_MFMA_FS_S (its instance), LCE_MFMA_FS_PAD (0: no
- * LDS padding to one workgroup per CU), LCE_MFMA_KS (1 / 0: K-split /
+ * LDS padding to one workgroup per CU), LCE_MFMA_FS_PK (0: load the widened
+ * filters even where the packed copy would do), LCE_MFMA_KS (1 / 0: K-split /
  * pixel-split),
  * LCE_MFMA_MB and LCE_MFMA_NBLK force a schedule and a tile for testing and
  * tuning.  Every choice gives the identical output.

@@ -63,6 +63,7 @@ constexpr int kFsMaxSteps = 72;
 struct MfmaParams {
     const uint32_t *x;      // [N][H][W][Cw] bitpacked activations
     const u32x4 *wexp;      // [KH*KW*CwE][CoutP] widened filters (16 bytes = 32 values)
+    const uint32_t *wpk;    // [KH*KW*CwE][CoutP] the same filters packed (4 bytes = 32 values)
     const float *mult;      // [Cout] or null (float output)
     const float *bias;      // [Cout] or null (float output)
     const float *thr;       // [Cout] (bitpacked output)
@@ -880,7 +881,7 @@ __device__ __forceinline__ void write_value_bits(uint64_t m, uint32_t &word) {
         : "s"((uint32_t)m), "s"((uint32_t)(m >> 32)), "i"(r0), "i"(r0 + 4));
 }
 
-template <int KS, int S, int OUT>
+template <int KS, int S, int OUT, bool PK>
 __global__ __launch_bounds__(kMfmaThreads) void bconv2d_mfma_fs_kernel(MfmaParams p) {
     static_assert(S == 1 || S == 2 || S == 4, "1, 2 or 4 waves per filter block");
     // Every cache line of the kernel arguments this kernel reads, fetched in
@@ -888,7 +889,7 @@ __global__ __launch_bounds__(kMfmaThreads) void bconv2d_mfma_fs_kernel(MfmaParam
     // in several dependent batches (behind branches), each first touch of a
     // line a full memory latency.
     {
-        const int ks0 = __builtin_amdgcn_readfirstlane((int)(threadIdx.x >> 6)) / (4 / S) * KS;
+        const int ks0 = S == 1 ? 0 : __builtin_amdgcn_readfirstlane((int)(threadIdx.x >> 6)) / (4 / S) * KS;
         asm volatile("" ::"s"(p.x), "s"(p.oh), "s"(p.m), "s"(p.div_pw.d), "s"(p.fs_koff[ks0]),
                      "s"(p.fs_koff[ks0 + KS / 2]), "s"(p.fs_koff[ks0 + KS - 1]));
     }
@@ -905,7 +906,10 @@ __global__ __launch_bounds__(kMfmaThreads) void bconv2d_mfma_fs_kernel(MfmaParam
     const int tid = threadIdx.x;
     const int lane = tid & 63, half = lane >> 5, l32 = lane & 31;
     const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
-    const int fblk = wave % F, sk = wave / F;
+    // (S = 1: sk is 0 at compile time, which keeps the argument-table
+    // index below constant; a runtime index the compiler cannot resolve
+    // makes it copy the kernel arguments to scratch memory)
+    const int fblk = wave % F, sk = S == 1 ? 0 : wave / F;
     const int m0 = blockIdx.x * p.fs_pixels;
     const int m_end = min(m0 + p.fs_pixels, p.m);
     const int nb = (m_end - m0 + 31) >> 5;
@@ -954,16 +958,22 @@ __global__ __launch_bounds__(kMfmaThreads) void bconv2d_mfma_fs_kernel(MfmaParam
     // last row and are zeroed on arrival).  Nothing waits for them here: the
     // first pair's K step i waits for its own (memory counters retire in
     // order), so the first products start while later filters still arrive.
+    // PK: every channel of every word is valid, and the packed words are
+    // loaded instead (a quarter of the bytes) and widened on arrival.
     static_assert(S * KS <= kFsMaxSteps, "offset table");
     u32x4 breg[KS];
+    uint32_t bpk[PK ? KS : 1];
     int aoff[KS];
     {
-        const u32x4 *wcol = p.wexp + (size_t)half * p.coutp + min(co, p.coutp - 1);
+        const size_t col = (size_t)half * p.coutp + min(co, p.coutp - 1);
         const int hp = half * plane;
 #pragma unroll
         for (int i = 0; i < KS; ++i) {
             const int s = min(sk * KS + i, ksteps - 1);
-            breg[i] = wcol[(size_t)(2 * s) * p.coutp];
+            if constexpr (PK)
+                bpk[i] = p.wpk[col + (size_t)(2 * s) * p.coutp];
+            else
+                breg[i] = p.wexp[col + (size_t)(2 * s) * p.coutp];
             aoff[i] = p.fs_koff[sk * KS + i] + hp;       // (word 2q + half)
         }
     }
@@ -975,9 +985,9 @@ __global__ __launch_bounds__(kMfmaThreads) void bconv2d_mfma_fs_kernel(MfmaParam
     wait_vmcnt<KS>();
     int z = lds_barrier();                               // every wave's region DMA landed
     widen_region_lds(p, abits, atile, row0, plane, tid, z);
-    // sign bits of a flipped filter, applied to each step's filters as they
-    // arrive (first pair)
-    const uint32_t neg = OUT == OUT_BITS && flipped ? kFp4SignBits : 0u;
+    // sign bits of a flipped filter (in the widened or the packed form),
+    // applied to each step's filters as they arrive (first pair)
+    const uint32_t neg = OUT == OUT_BITS && flipped ? (PK ? ~0u : kFp4SignBits) : 0u;
     if constexpr (OUT == OUT_BITS) {
         ep_a = co_ok ? thr_to_dot_bound_f(ep_a, p.lo, p.hi) : -INFINITY;
         if (flipped) ep_a = 1.0f - ep_a;
@@ -1153,10 +1163,13 @@ __global__ __launch_bounds__(kMfmaThreads) void bconv2d_mfma_fs_kernel(MfmaParam
             __builtin_amdgcn_sched_barrier(0);
             // first pair: this step's filters have landed (the compiler waits
             // for exactly this load); they take the flip, or 0.0 past the
-            // last K step
+            // last K step (PK: and are widened here)
             if constexpr (!has_prev) {
                 const uint32_t keep = sk * KS + i < ksteps ? ~0u : 0u;
-                breg[i] = (breg[i] ^ u32x4{neg, neg, neg, neg}) & u32x4{keep, keep, keep, keep};
+                if constexpr (PK)
+                    breg[i] = widen_word((bpk[i] ^ neg) & keep, kFp4PlusOne & keep);
+                else
+                    breg[i] = (breg[i] ^ u32x4{neg, neg, neg, neg}) & u32x4{keep, keep, keep, keep};
             }
             // finishing pieces: the compares of values [lo, hi) after the
             // first product, the lane writes of the previous step's values
@@ -1224,9 +1237,13 @@ __global__ __launch_bounds__(kMfmaThreads) void bconv2d_mfma_fs_kernel(MfmaParam
 //   wexp[(t*CwE + j)*CoutP + co] = 32 e2m1 codes of word j of tap t of
 //   filter co, in the order of widen_word (channel c of the word in 32-bit
 //   word c % 4, nibble c / 4); channels past C_in, words past Cw and filters
-//   past Cout are 0.0 (they then add nothing to any dot).
+//   past Cout are 0.0 (they then add nothing to any dot);
+//   wpk[same index] = the packed word itself (bits of channels past C_in
+//   cleared; words past Cw and filters past Cout 0), for kernels that
+//   widen the filters themselves where every channel is valid.
 __global__ __launch_bounds__(256) void mfma_expand_weights_kernel(const uint32_t *__restrict__ w,
                                                                   u32x4 *__restrict__ wexp,
+                                                                  uint32_t *__restrict__ wpk,
                                                                   int cout, int coutp, int taps,
                                                                   int cw, int cwe, int cin) {
     const int64_t total = (int64_t)taps * cwe * coutp;
@@ -1236,13 +1253,16 @@ __global__ __launch_bounds__(256) void mfma_expand_weights_kernel(const uint32_t
         const int co = (int)(idx - k * coutp);
         const int t = (int)(k / cwe), j = (int)(k - (int64_t)t * cwe);
         u32x4 o = {0u, 0u, 0u, 0u};
+        uint32_t packed = 0u;
         if (co < cout && j < cw) {
             const uint32_t bits = w[((size_t)co * taps + t) * cw + j];
             const int nvalid = min(32, cin - 32 * j);
             const uint32_t valid = nvalid >= 32 ? 0xFFFFFFFFu : (1u << nvalid) - 1u;
             o = widen_word(bits, kFp4PlusOne) & widen_valid_mask(valid);
+            packed = bits & valid;
         }
         wexp[idx] = o;
+        wpk[idx] = packed;
     }
 }
 

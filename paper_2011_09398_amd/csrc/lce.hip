@@ -327,7 +327,7 @@ int64_t mfma_weight_bytes(const lce_bconv2d_desc &d) {
     int cc, cwe;
     mfma_chunk(packed_words(d.c_in), &cc, &cwe);
     const int64_t coutp = (int64_t)(d.c_out + 31) / 32 * 32;
-    return (int64_t)d.kh * d.kw * cwe * coutp * 16;
+    return (int64_t)d.kh * d.kw * cwe * coutp * (16 + 4);   // widened, then packed
 }
 
 int device_max_lds() {
@@ -416,29 +416,40 @@ struct FsShape {
 };
 constexpr FsShape kFsShapes[] = {{9, 1}, {18, 1}, {5, 2}, {9, 2}, {18, 2}, {18, 4}};
 
-template <int KS, int S>
-void launch_mfma_fs_shape(const lce::MfmaParams &p, int out, dim3 grid, size_t lds,
-                          hipStream_t st) {
+template <int KS, int S, bool PK>
+void launch_mfma_fs_pk(const lce::MfmaParams &p, int out, dim3 grid, size_t lds,
+                       hipStream_t st) {
     const dim3 block(lce::kMfmaThreads);
     if (out == LCE_OUT_FLOAT32)
-        hipLaunchKernelGGL((lce::bconv2d_mfma_fs_kernel<KS, S, lce::OUT_FLOAT>), grid, block, lds,
-                           st, p);
+        hipLaunchKernelGGL((lce::bconv2d_mfma_fs_kernel<KS, S, lce::OUT_FLOAT, PK>), grid, block,
+                           lds, st, p);
     else if (out == LCE_OUT_BITPACKED)
-        hipLaunchKernelGGL((lce::bconv2d_mfma_fs_kernel<KS, S, lce::OUT_BITS>), grid, block, lds,
-                           st, p);
+        hipLaunchKernelGGL((lce::bconv2d_mfma_fs_kernel<KS, S, lce::OUT_BITS, PK>), grid, block,
+                           lds, st, p);
     else
-        hipLaunchKernelGGL((lce::bconv2d_mfma_fs_kernel<KS, S, lce::OUT_INT>), grid, block, lds,
-                           st, p);
+        hipLaunchKernelGGL((lce::bconv2d_mfma_fs_kernel<KS, S, lce::OUT_INT, PK>), grid, block,
+                           lds, st, p);
 }
 
-void launch_mfma_fs(const lce::MfmaParams &p, FsShape sh, int out, dim3 grid, size_t lds,
-                    hipStream_t st) {
-    if (sh.ks == 9 && sh.s == 1) launch_mfma_fs_shape<9, 1>(p, out, grid, lds, st);
-    else if (sh.ks == 18 && sh.s == 1) launch_mfma_fs_shape<18, 1>(p, out, grid, lds, st);
-    else if (sh.ks == 5 && sh.s == 2) launch_mfma_fs_shape<5, 2>(p, out, grid, lds, st);
-    else if (sh.ks == 9 && sh.s == 2) launch_mfma_fs_shape<9, 2>(p, out, grid, lds, st);
-    else if (sh.ks == 18 && sh.s == 2) launch_mfma_fs_shape<18, 2>(p, out, grid, lds, st);
-    else launch_mfma_fs_shape<18, 4>(p, out, grid, lds, st);
+template <int KS, int S>
+void launch_mfma_fs_shape(const lce::MfmaParams &p, bool pk, int out, dim3 grid, size_t lds,
+                          hipStream_t st) {
+    if (pk)
+        launch_mfma_fs_pk<KS, S, true>(p, out, grid, lds, st);
+    else
+        launch_mfma_fs_pk<KS, S, false>(p, out, grid, lds, st);
+}
+
+// pk: every channel of every packed word is valid (C_in = 32*Cw'), so the
+// kernel loads the packed copy of the filters and widens it itself
+void launch_mfma_fs(const lce::MfmaParams &p, FsShape sh, bool pk, int out, dim3 grid,
+                    size_t lds, hipStream_t st) {
+    if (sh.ks == 9 && sh.s == 1) launch_mfma_fs_shape<9, 1>(p, pk, out, grid, lds, st);
+    else if (sh.ks == 18 && sh.s == 1) launch_mfma_fs_shape<18, 1>(p, pk, out, grid, lds, st);
+    else if (sh.ks == 5 && sh.s == 2) launch_mfma_fs_shape<5, 2>(p, pk, out, grid, lds, st);
+    else if (sh.ks == 9 && sh.s == 2) launch_mfma_fs_shape<9, 2>(p, pk, out, grid, lds, st);
+    else if (sh.ks == 18 && sh.s == 2) launch_mfma_fs_shape<18, 2>(p, pk, out, grid, lds, st);
+    else launch_mfma_fs_shape<18, 4>(p, pk, out, grid, lds, st);
 }
 
 // LDS of the filter-stationary kernel: every widened word of the region,
@@ -806,8 +817,9 @@ lce_status lce_bconv2d_mfma_weights(const lce_bconv2d_desc *desc, const int32_t 
     if (blocks > 256 * 16) blocks = 256 * 16;
     hipLaunchKernelGGL(lce::mfma_expand_weights_kernel, dim3((unsigned)blocks), dim3(256), 0,
                        stream, reinterpret_cast<const uint32_t *>(w_packed),
-                       reinterpret_cast<lce::u32x4 *>(w_fp4), d.c_out, coutp, taps, cw, cwe,
-                       d.c_in);
+                       reinterpret_cast<lce::u32x4 *>(w_fp4),
+                       reinterpret_cast<uint32_t *>(reinterpret_cast<lce::u32x4 *>(w_fp4) + total),
+                       d.c_out, coutp, taps, cw, cwe, d.c_in);
     return check_launch("lce_bconv2d_mfma_weights launch");
 }
 
@@ -847,6 +859,8 @@ lce_status lce_bconv2d_mfma(const lce_bconv2d_desc *desc, const int32_t *x_packe
     mfma_chunk(p.cw, &cc, &cwe);
     p.cwe = cwe;
     p.oh = g.oh; p.ow = g.ow; p.cout = d.c_out; p.coutp = (d.c_out + 31) / 32 * 32;
+    // the packed copy follows the widened filters in the same buffer
+    p.wpk = reinterpret_cast<const uint32_t *>(p.wexp + (int64_t)d.kh * d.kw * cwe * p.coutp);
     p.cwo = packed_words(d.c_out);
     p.kh = d.kh; p.kw = d.kw; p.sh = d.stride_h; p.sw = d.stride_w; p.pt = g.pt; p.pl = g.pl;
     p.ph = (g.oh - 1) * d.stride_h + d.kh;
@@ -908,7 +922,8 @@ lce_status lce_bconv2d_mfma(const lce_bconv2d_desc *desc, const int32_t *x_packe
                 lds = std::max(lds, (size_t)device_max_lds() / 2 + 1024);
             const dim3 grid((unsigned)fp.groups,
                             (unsigned)((blocks32 + 4 / fp.shape.s - 1) / (4 / fp.shape.s)));
-            launch_mfma_fs(p, fp.shape, d.out_type, grid, lds, stream);
+            const bool pk = d.c_in == 32 * p.cwe && env_int("LCE_MFMA_FS_PK", 1) != 0;
+            launch_mfma_fs(p, fp.shape, pk, d.out_type, grid, lds, stream);
             return check_launch("lce_bconv2d_mfma launch");
         }
     }

@@ -37,7 +37,8 @@ def gpu():
 
 @pytest.fixture(autouse=True, params=["fs", "ks", "pixel"])
 def schedule(request, monkeypatch):
-    for k in ("LCE_MFMA_KS", "LCE_MFMA_FS_KS", "LCE_MFMA_FS_S", "LCE_MFMA_FS_PAD"):
+    for k in ("LCE_MFMA_KS", "LCE_MFMA_FS_KS", "LCE_MFMA_FS_S", "LCE_MFMA_FS_PAD",
+              "LCE_MFMA_FS_PK"):
         monkeypatch.delenv(k, raising=False)
     if request.param == "fs":
         monkeypatch.setenv("LCE_MFMA_FS", "1")
@@ -175,18 +176,27 @@ def fs_layers(ks, s):
     return out
 
 
+def cwe_of(cw):
+    e2, e4 = (cw + 1) // 2 * 2, (cw + 3) // 4 * 4
+    return e2 if e2 < e4 else e4
+
+
+@pytest.mark.parametrize("packed", [True, False], ids=["packed_filters", "widened_filters"])
 @pytest.mark.parametrize("ks,s", FS_INSTANCES, ids=lambda v: str(v))
-def test_mfma_fs_every_instance(monkeypatch, schedule, ks, s):
+def test_mfma_fs_every_instance(monkeypatch, schedule, ks, s, packed):
+    """packed: C_in fills every widened word (C_in = 32*Cw'), where the kernel
+    loads the packed filter copy and widens it itself; otherwise some
+    channels are padding and it loads the widened filters."""
     if schedule != "fs":
         pytest.skip("filter-stationary instances")
     monkeypatch.setenv("LCE_MFMA_FS_KS", str(ks))
     monkeypatch.setenv("LCE_MFMA_FS_S", str(s))
     shapes = fs_layers(ks, s)
     assert shapes, (ks, s)
-    rng = np.random.default_rng(ks * 10 + s)
+    rng = np.random.default_rng(ks * 10 + s + (1000 if packed else 0))
     picks = [shapes[0], shapes[-1]] + [shapes[int(i)] for i in rng.integers(0, len(shapes), 2)]
     for j, (kh, kw, cw) in enumerate(picks):
-        c_in = 32 * cw - int(rng.integers(0, 32))
+        c_in = 32 * cwe_of(cw) if packed else 32 * cw - int(rng.integers(1, 32))
         c_out = int(rng.choice([13, 32, 64, 100, 128, 200]))
         stride = int(rng.choice([1, 2]))
         out = ["float", "bitpacked", "int32", "bitpacked"][j]
@@ -213,11 +223,14 @@ def test_mfma_fs_every_instance(monkeypatch, schedule, ks, s):
         assert_match(layer, got, ref, f"{layer.name} {kh}x{kw} cw={cw} {pv}")
 
 
-def test_mfma_fs_config4_every_instance_that_fits(monkeypatch, schedule):
+@pytest.mark.parametrize("packed", ["1", "0"], ids=["packed_filters", "widened_filters"])
+def test_mfma_fs_config4_every_instance_that_fits(monkeypatch, schedule, packed):
     """The batch-64 layers at full size (sampled images) on every
-    filter-stationary instance whose K steps fit the layer."""
+    filter-stationary instance whose K steps fit the layer, loading the
+    packed filter copy (the default there) or the widened filters."""
     if schedule != "fs":
         pytest.skip("filter-stationary instances")
+    monkeypatch.setenv("LCE_MFMA_FS_PK", packed)
     sample = [0, 37, 63]
     for i, layer in enumerate(config(4)):
         inp = make_layer_inputs(layer, 0, 4, i)
@@ -291,14 +304,18 @@ def test_mfma_flip_and_special_thresholds():
 
 def test_mfma_weights_are_zero_past_the_real_channels_and_filters():
     """Widened filters: +-1.0 codes for real weights, 0.0 for pad channels,
-    pad words and pad filters (checked against the oracle-side signs)."""
+    pad words and pad filters (checked against the oracle-side signs); the
+    packed copy after them: bit 1 = -1, 0 for pad channels, words, filters."""
     import paper_2011_09398_amd as lce
     layer = Layer("wx", 1, 4, 4, 40, 13, kh=3, kw=3, input_kind="bits")
     inp = make_layer_inputs(layer, 1, 94, 0)
     raw = sync_np(lce.mfma_weights(gpu_pack_weights(inp), 40)).view(np.uint32)
     cw, cwe, coutp, taps = 2, 2, 32, 9
+    n = taps * cwe * coutp
+    assert raw.size == n * 4 + n
+    packed = raw[n * 4:].reshape(taps * cwe, coutp)
     codes = np.zeros((taps * cwe, coutp, 32), np.uint8)
-    words = raw.reshape(taps * cwe, coutp, 4)
+    words = raw[:n * 4].reshape(taps * cwe, coutp, 4)
     for j in range(32):                       # channel j: 32-bit word j % 4, nibble j // 4
         codes[..., j] = (words[..., j % 4] >> np.uint32(4 * (j // 4))) & 0xF
     want = np.zeros_like(codes)
@@ -307,3 +324,8 @@ def test_mfma_weights_are_zero_past_the_real_channels_and_filters():
         for c in range(40):
             want[t * cwe + c // 32, :13, c % 32] = np.where(w[:, t, c] > 0, 0x2, 0xA)
     assert np.array_equal(codes, want)
+    want_bits = np.zeros((taps * cwe, coutp), np.uint32)
+    for t in range(taps):
+        for c in range(40):
+            want_bits[t * cwe + c // 32, :13] |= (w[:, t, c] < 0).astype(np.uint32) << np.uint32(c % 32)
+    assert np.array_equal(packed, want_bits)
