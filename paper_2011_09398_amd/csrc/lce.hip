@@ -471,12 +471,27 @@ struct FsPlan {
     size_t lds = 0;
 };
 
+// Workgroups per CU the filter-stationary grid is sized for.  Two (two
+// waves per SIMD, each hiding the other's finishing work and LDS waits
+// behind its matrix products) where a wave's filters are few, KS <= 9 and
+// S = 1: measured about 1.1x faster on the 56x56x64->128/s2 layer (9 K
+// steps).  With KS = 18 the second workgroup's filter loads and widening
+// cost more than the overlap gains (measured slower on 28x28x128).  Every
+// instance with S = 1 and KS <= 9 keeps its registers within the 256 per
+// lane that two waves per SIMD leave.  LCE_MFMA_FS_WPC = 1 / 2 forces it.
+int fs_wgs_per_cu(FsShape sh) {
+    const int e = env_int("LCE_MFMA_FS_WPC", 0);
+    if (e == 1 || e == 2) return e;
+    return sh.s == 1 && sh.ks <= 9 ? 2 : 1;
+}
+
 // The filter-stationary plan of a layer: among the instances whose K steps
 // cover the layer's with at most 1/8 padding (any, when forced), the one
-// with the fewest matrix products per wave (pixel blocks per workgroup x
-// KS, plus one per block for the exchange), with about one workgroup per
-// CU: each filter group gets CUs / filter groups workgroups, each an equal
-// whole number of pixel blocks.  shape.ks == 0: none fits.
+// with the fewest matrix products per SIMD (pixel blocks per workgroup x
+// KS, plus one per block for the exchange, x workgroups per CU), with
+// about wpc workgroups per CU: each filter group gets wpc x CUs / filter
+// groups workgroups, each an equal share of the pixels.  shape.ks == 0:
+// none fits.
 FsPlan plan_mfma_fs(const lce::MfmaParams &p, int64_t cus, int blocks32, int ksteps) {
     FsPlan best;
     int64_t best_cost = -1;
@@ -489,7 +504,8 @@ FsPlan plan_mfma_fs(const lce::MfmaParams &p, int64_t cus, int blocks32, int kst
         if (!(env_ks && env_s) && (cover - ksteps) * 8 > ksteps) continue;
         const int f = 4 / sh.s;
         const int64_t fgroups = (blocks32 + f - 1) / f;
-        const int64_t pg = std::max<int64_t>(1, cus / fgroups);
+        const int wpc = fs_wgs_per_cu(sh);
+        const int64_t pg = std::max<int64_t>(1, cus * wpc / fgroups);
         // (not rounded to whole blocks: the block count is the same, and an
         // exact share often covers whole images or rows, with fewer rows)
         const int64_t px = ((int64_t)p.m + pg - 1) / pg;
@@ -499,7 +515,7 @@ FsPlan plan_mfma_fs(const lce::MfmaParams &p, int64_t cus, int blocks32, int kst
         if (lds > (size_t)device_max_lds()) continue;
         if ((int64_t)tr * p.pw * p.cwe > INT32_MAX / 2) continue;
         const int64_t nb = (px + 31) / 32;
-        const int64_t cost = nb * sh.ks + (sh.s > 1 ? nb : 0);
+        const int64_t cost = (nb * sh.ks + (sh.s > 1 ? nb : 0)) * wpc;   // per CU
         if (best_cost < 0 || cost < best_cost) {
             best_cost = cost;
             best.shape = sh;
@@ -914,12 +930,14 @@ lce_status lce_bconv2d_mfma(const lce_bconv2d_desc *desc, const int32_t *x_packe
                 p.fs_koff[s] = 2 * q * plane + (t / d.kw) * p.pw + t % d.kw;
             }
             size_t lds = fp.lds;
-            // claim more than half of a CU's LDS when the grid fits the CUs,
-            // so that no CU holds two workgroups while another holds none
-            // (LCE_MFMA_FS_PAD=0 turns this off)
+            // claim more than 1/(wpc+1) of a CU's LDS when the grid fits the
+            // CUs, so that no CU holds more than wpc workgroups while another
+            // holds fewer (LCE_MFMA_FS_PAD=0 turns this off)
             const int64_t wgs = fp.groups * ((blocks32 + 4 / fp.shape.s - 1) / (4 / fp.shape.s));
-            if (env_int("LCE_MFMA_FS_PAD", 1) == 1 && wgs <= cus)
-                lds = std::max(lds, (size_t)device_max_lds() / 2 + 1024);
+            const int wpc = fs_wgs_per_cu(fp.shape);
+            if (env_int("LCE_MFMA_FS_PAD", 1) == 1 && wgs <= cus * wpc &&
+                lds * (wpc + 1) <= (size_t)device_max_lds())
+                lds = std::max(lds, (size_t)device_max_lds() / (wpc + 1) + 1024);
             const dim3 grid((unsigned)fp.groups,
                             (unsigned)((blocks32 + 4 / fp.shape.s - 1) / (4 / fp.shape.s)));
             const bool pk = d.c_in == 32 * p.cwe && env_int("LCE_MFMA_FS_PK", 1) != 0;

@@ -38,7 +38,7 @@ def gpu():
 @pytest.fixture(autouse=True, params=["fs", "ks", "pixel"])
 def schedule(request, monkeypatch):
     for k in ("LCE_MFMA_KS", "LCE_MFMA_FS_KS", "LCE_MFMA_FS_S", "LCE_MFMA_FS_PAD",
-              "LCE_MFMA_FS_PK"):
+              "LCE_MFMA_FS_PK", "LCE_MFMA_FS_WPC"):
         monkeypatch.delenv(k, raising=False)
     if request.param == "fs":
         monkeypatch.setenv("LCE_MFMA_FS", "1")
@@ -221,6 +221,25 @@ def test_mfma_fs_every_instance(monkeypatch, schedule, ks, s, packed):
         else:
             ref = oracle_run(layer, inp, oracle_signs(inp), 0 if pv == "zero" else 1)
         assert_match(layer, got, ref, f"{layer.name} {kh}x{kw} cw={cw} {pv}")
+
+
+@pytest.mark.parametrize("wpc", ["1", "2"])
+@pytest.mark.parametrize("ks,s", [(9, 1), (18, 1), (9, 2)], ids=lambda v: str(v))
+def test_mfma_fs_workgroups_per_cu(monkeypatch, ks, s, wpc):
+    """One or two workgroups per CU (the grid and the pixel share per
+    workgroup change, the result does not): ragged layers, stride 2."""
+    monkeypatch.setenv("LCE_MFMA_FS", "1")
+    monkeypatch.setenv("LCE_MFMA_FS_KS", str(ks))
+    monkeypatch.setenv("LCE_MFMA_FS_S", str(s))
+    monkeypatch.setenv("LCE_MFMA_FS_WPC", wpc)
+    for j, (kh, kw, cw) in enumerate(fs_layers(ks, s)[:2]):
+        layer = Layer(f"wpc{ks}x{s}_{j}", 5, 19 - j, 23, 32 * cwe_of(cw) - 7 * j, 96 + 40 * j,
+                      kh=kh, kw=kw, stride=1 + j, out=["bitpacked", "float"][j],
+                      input_kind="bits")
+        inp = make_layer_inputs(layer, 3, 89, ks * 10 + s + j)
+        got = sync_np(mfma_run(layer, inp))
+        assert_match(layer, got, oracle_run(layer, inp, oracle_signs(inp)),
+                     f"{layer.name} wpc={wpc}")
 
 
 @pytest.mark.parametrize("packed", ["1", "0"], ids=["packed_filters", "widened_filters"])
