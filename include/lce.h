@@ -218,8 +218,9 @@ lce_status lce_bconv2d_mfma_weights(const lce_bconv2d_desc *desc, const int32_t 
  * (the waves of a workgroup divide K; long K) and pixel-split (the rest).
  * The environment variables LCE_MFMA_FS (0 turns the first off),
  * LCE_MFMA_FS_KS / LCE_MFMA_FS_S (its instance), LCE_MFMA_FS_PAD (0: no
- * LDS padding to one workgroup per CU), LCE_MFMA_FS_PK (0: load the widened
- * filters even where the packed copy would do), LCE_MFMA_KS (1 / 0: K-split /
+ * LDS padding to one workgroup per CU), LCE_MFMA_FS_WPC (1 / 2 workgroups
+ * per CU), LCE_MFMA_PK (0: load the widened filters even where the packed
+ * copy would do), LCE_MFMA_KS (1 / 0: K-split /
  * pixel-split),
  * LCE_MFMA_MB and LCE_MFMA_NBLK force a schedule and a tile for testing and
  * tuning.  Every choice gives the identical output.

@@ -82,6 +82,7 @@ struct MfmaParams {
     FastDiv div_plane;               // tile_rows * pw: region locations
     FastDiv div_cwh, div_kw;         // cwe / 2 (word pairs per tap), kw
     FastDiv div_groups;              // region_vec-word groups per location
+    FastDiv div_ks_gx;               // K-split schedule: pixel tiles (grid x)
     // filter-stationary schedule: A-tile offset (in 16-byte words) of K step
     // s = (tap t = ky*KW + kx, word pair q) from a pixel's window origin,
     // 2q*plane + ky*PW + kx (plane = tile_rows*pw); steps past the last
@@ -627,7 +628,14 @@ __device__ __forceinline__ void widen_region_lds(const MfmaParams &p, const uint
 //     wave owns to that wave through LDS in one exchange (block j belongs to
 //     wave j % 4); the owner adds them (fp32 adds of integers below 2^24 are
 //     exact in any order) and applies the output transform.
+//   (Loading the packed filter copy and widening it at use, as the
+//   filter-stationary schedule does, measured 10% slower here.)
+//   * Tiles are renumbered so that each of the 8 XCDs (which take the
+//     workgroups round-robin in launch order, each with its own L2) runs a
+//     contiguous range of them in filter-major order: its L2 then holds only
+//     its own filter tiles.
 constexpr int kRing = 4;
+constexpr unsigned kXcds = 8;
 
 template <int OUT, int NBLK, int MBW>
 __global__ __launch_bounds__(kMfmaThreads) void bconv2d_mfma_ks_kernel(MfmaParams p) {
@@ -638,8 +646,18 @@ __global__ __launch_bounds__(kMfmaThreads) void bconv2d_mfma_ks_kernel(MfmaParam
     const int tid = threadIdx.x;
     const int lane = tid & 63, half = lane >> 5, l32 = lane & 31;
     const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
-    const int m0 = blockIdx.x * BM;
-    const int n_base = blockIdx.y * BN;
+    int m0, n_base;
+    {
+        // launch index L goes to XCD L % 8 as its (L / 8)-th; XCD x runs
+        // tiles [x*q + min(x, rem), ...) of the T = q*8 + rem
+        const unsigned gx = gridDim.x, T = gx * gridDim.y;
+        const unsigned L = blockIdx.y * gx + blockIdx.x;
+        const unsigned q = T / kXcds, rem = T % kXcds, x = L % kXcds;
+        const unsigned t = x * q + min(x, rem) + L / kXcds;
+        const unsigned ty = fast_div(t, p.div_ks_gx);
+        m0 = (int)(t - ty * gx) * BM;
+        n_base = (int)ty * BN;
+    }
     const int cwh = p.cwe >> 1;
     const int ksteps = p.kh * p.kw * cwh;
     const int TR = p.tile_rows, PW = p.pw, plane = TR * PW;

@@ -940,7 +940,7 @@ lce_status lce_bconv2d_mfma(const lce_bconv2d_desc *desc, const int32_t *x_packe
                 lds = std::max(lds, (size_t)device_max_lds() / (wpc + 1) + 1024);
             const dim3 grid((unsigned)fp.groups,
                             (unsigned)((blocks32 + 4 / fp.shape.s - 1) / (4 / fp.shape.s)));
-            const bool pk = d.c_in == 32 * p.cwe && env_int("LCE_MFMA_FS_PK", 1) != 0;
+            const bool pk = d.c_in == 32 * p.cwe && env_int("LCE_MFMA_PK", 1) != 0;
             launch_mfma_fs(p, fp.shape, pk, d.out_type, grid, lds, stream);
             return check_launch("lce_bconv2d_mfma launch");
         }
@@ -969,6 +969,7 @@ lce_status lce_bconv2d_mfma(const lce_bconv2d_desc *desc, const int32_t *x_packe
             const size_t lds = mfma_ks_lds(p, mbw, knb, rows);
             const dim3 grid((unsigned)(((int64_t)p.m + 32 * mbw - 1) / (32 * mbw)),
                             (unsigned)((blocks32 + knb - 1) / knb));
+            p.div_ks_gx = lce::make_fastdiv(grid.x);
             switch (d.out_type) {
                 case LCE_OUT_FLOAT32: launch_mfma_ks<lce::OUT_FLOAT>(p, knb, mbw, grid, lds, stream); break;
                 case LCE_OUT_BITPACKED: launch_mfma_ks<lce::OUT_BITS>(p, knb, mbw, grid, lds, stream); break;

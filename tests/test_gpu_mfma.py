@@ -38,7 +38,7 @@ def gpu():
 @pytest.fixture(autouse=True, params=["fs", "ks", "pixel"])
 def schedule(request, monkeypatch):
     for k in ("LCE_MFMA_KS", "LCE_MFMA_FS_KS", "LCE_MFMA_FS_S", "LCE_MFMA_FS_PAD",
-              "LCE_MFMA_FS_PK", "LCE_MFMA_FS_WPC"):
+              "LCE_MFMA_PK", "LCE_MFMA_FS_WPC"):
         monkeypatch.delenv(k, raising=False)
     if request.param == "fs":
         monkeypatch.setenv("LCE_MFMA_FS", "1")
@@ -249,7 +249,7 @@ def test_mfma_fs_config4_every_instance_that_fits(monkeypatch, schedule, packed)
     packed filter copy (the default there) or the widened filters."""
     if schedule != "fs":
         pytest.skip("filter-stationary instances")
-    monkeypatch.setenv("LCE_MFMA_FS_PK", packed)
+    monkeypatch.setenv("LCE_MFMA_PK", packed)
     sample = [0, 37, 63]
     for i, layer in enumerate(config(4)):
         inp = make_layer_inputs(layer, 0, 4, i)
