@@ -143,37 +143,54 @@ __device__ inline float thr_to_dot_bound_f(float thr, int lo, int hi) {
     return (float)tc;
 }
 
+// Output bits of value V of an accumulator block (see block_bits): the
+// lane mask `m` of "value < T" holds pixels r0 (lanes 0-31) and r0 + 4
+// (lanes 32-63), r0 = (V/4)*8 + V%4, and two v_writelane drop them into the
+// lanes of their pixels.  A v_writelane that reads the mask of a compare
+// issued right before it stalls the wave until the compare's SGPR write
+// lands (measured: ~35 cycles per value next to LDS reads), so callers
+// issue the compares well ahead.  The s_nop 1 covers a VALU-written SGPR in
+// any case (the compiler's hazard recognizer does not look inside inline
+// asm).
+template <int V>
+__device__ __forceinline__ void write_value_bits(uint64_t m, uint32_t &word) {
+    constexpr int r0 = (V >> 2) * 8 + (V & 3);
+    asm volatile(
+        "s_nop 1\n\t"
+        "v_writelane_b32 %0, %1, %3\n\t"
+        "v_writelane_b32 %0, %2, %4"
+        : "+v"(word)
+        : "s"((uint32_t)m), "s"((uint32_t)(m >> 32)), "i"(r0), "i"(r0 + 4));
+}
+
 // Bitpacked output of one 32x32 accumulator block.  Value v of the block is
 // pixel (v/4)*8 + half*4 + v%4 and filter lane % 32, so one ballot of
 // "value < T" over the wave gives the 32 filter bits of two pixels (lanes
 // 0-31 and 32-63); v_writelane drops each 32-bit half into the lane of its
 // pixel.  fmask (wave-uniform) flips chosen filters.  Lane l < 32 returns
-// the word of pixel l.
-//
-// The SGPR a v_writelane reads may have just been written by a VALU
-// instruction (the compare itself, when there is no flip mask).  CDNA3/4
-// require two wait states between the two that the hardware does not
-// insert, and the compiler's hazard recognizer does not look inside inline
-// asm, so each v_writelane carries its own s_nop 1.
-template <int V>
-__device__ __forceinline__ void block_bits_step(const mfma_v16f &val, float T, uint64_t fmask,
-                                                uint32_t &word) {
-    constexpr int r0 = (V >> 2) * 8 + (V & 3);
-    const uint64_t mask = __ballot(val[V] < T) ^ fmask;
-    asm("s_nop 1\n\tv_writelane_b32 %0, %1, %2" : "+v"(word) : "s"((uint32_t)mask), "i"(r0));
-    asm("s_nop 1\n\tv_writelane_b32 %0, %1, %2"
-        : "+v"(word) : "s"((uint32_t)(mask >> 32)), "i"(r0 + 4));
-}
+// the word of pixel l.  All sixteen compares come first, so that no
+// v_writelane waits for the compare right before it.
 template <int... V>
 __device__ __forceinline__ uint32_t block_bits_impl(const mfma_v16f &val, float T,
                                                     uint64_t fmask,
                                                     std::integer_sequence<int, V...>) {
+    uint64_t m[16];
+    ((m[V] = __ballot(val[V] < T) ^ fmask), ...);
     uint32_t word = 0;
-    (block_bits_step<V>(val, T, fmask, word), ...);
+    (write_value_bits<V>(m[V], word), ...);
     return word;
 }
 __device__ __forceinline__ uint32_t block_bits(const mfma_v16f &val, float T, uint64_t fmask) {
     return block_bits_impl(val, T, fmask, std::make_integer_sequence<int, 16>{});
+}
+
+// Every cache line of the kernel arguments up to the K-split grid divisor
+// (one field per 64-byte line), fetched in one round trip at the top of a
+// kernel: the compiler would otherwise load the fields in several dependent
+// batches (behind branches), each first touch of a line a full memory
+// latency.
+__device__ __forceinline__ void fetch_arg_lines(const MfmaParams &p) {
+    asm volatile("" ::"s"(p.x), "s"(p.oh), "s"(p.m), "s"(p.div_pw.d), "s"(p.div_ks_gx.d));
 }
 
 // Flip mask of a block of 32 filters for both lane halves, wave-uniform:
@@ -225,6 +242,7 @@ __device__ __forceinline__ int lds_barrier() {
 
 template <int CC, int OUT, int NBLK, int MB>
 __global__ __launch_bounds__(kMfmaThreads) void bconv2d_mfma_kernel(MfmaParams p) {
+    fetch_arg_lines(p);
     constexpr int BN = 32 * NBLK;
     constexpr int BM = 32 * MB * 4;                                   // pixels per workgroup
     constexpr int kStage = CC * BN;                                   // u32x4 per B stage
@@ -646,6 +664,7 @@ __global__ __launch_bounds__(kMfmaThreads) void bconv2d_mfma_ks_kernel(MfmaParam
     const int tid = threadIdx.x;
     const int lane = tid & 63, half = lane >> 5, l32 = lane & 31;
     const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+    fetch_arg_lines(p);
     int m0, n_base;
     {
         // launch index L goes to XCD L % 8 as its (L / 8)-th; XCD x runs
@@ -879,37 +898,17 @@ __device__ __forceinline__ void for_each_index(Fn &&f, std::integer_sequence<int
     (f(std::integral_constant<int, I>{}), ...);
 }
 
-// Output bits of value V of an accumulator block (see block_bits): the
-// lane mask `m` of "value < T" (one compare, issued a K step earlier) holds
-// pixels r0 (lanes 0-31) and r0 + 4 (lanes 32-63), r0 = (V/4)*8 + V%4, and
-// two v_writelane drop them into the lanes of their pixels.  A v_writelane
-// that reads the mask of a compare issued right before it stalls the wave
-// until the compare's SGPR write lands (measured: ~35 cycles per K step
-// next to the ring's LDS reads); a step later the mask is there.  The s_nop
-// 1 covers a VALU-written SGPR in any case (the compiler's hazard
-// recognizer does not look inside inline asm).
-template <int V>
-__device__ __forceinline__ void write_value_bits(uint64_t m, uint32_t &word) {
-    constexpr int r0 = (V >> 2) * 8 + (V & 3);
-    asm volatile(
-        "s_nop 1\n\t"
-        "v_writelane_b32 %0, %1, %3\n\t"
-        "v_writelane_b32 %0, %2, %4"
-        : "+v"(word)
-        : "s"((uint32_t)m), "s"((uint32_t)(m >> 32)), "i"(r0), "i"(r0 + 4));
-}
 
 template <int KS, int S, int OUT, bool PK>
 __global__ __launch_bounds__(kMfmaThreads) void bconv2d_mfma_fs_kernel(MfmaParams p) {
     static_assert(S == 1 || S == 2 || S == 4, "1, 2 or 4 waves per filter block");
-    // Every cache line of the kernel arguments this kernel reads, fetched in
-    // one round trip up front: the compiler would otherwise load the fields
-    // in several dependent batches (behind branches), each first touch of a
-    // line a full memory latency.
+    // every argument line this kernel reads in one round trip, the tap
+    // offsets of this wave's K steps included
     {
         const int ks0 = S == 1 ? 0 : __builtin_amdgcn_readfirstlane((int)(threadIdx.x >> 6)) / (4 / S) * KS;
-        asm volatile("" ::"s"(p.x), "s"(p.oh), "s"(p.m), "s"(p.div_pw.d), "s"(p.fs_koff[ks0]),
-                     "s"(p.fs_koff[ks0 + KS / 2]), "s"(p.fs_koff[ks0 + KS - 1]));
+        fetch_arg_lines(p);
+        asm volatile("" ::"s"(p.fs_koff[ks0]), "s"(p.fs_koff[ks0 + KS / 2]),
+                     "s"(p.fs_koff[ks0 + KS - 1]));
     }
     constexpr int F = 4 / S;
     constexpr int D = fs_depth(KS);
