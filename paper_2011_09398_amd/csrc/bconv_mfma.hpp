@@ -565,11 +565,12 @@ __device__ __forceinline__ void dma_region(const MfmaParams &p, uint32_t *abits,
 // Widen the packed region (dma_region layout) into the A tile: atile[j*plane
 // + rc] = word j of location rc.  Words past Cw are +1.0 (their filter
 // values are 0.0); under zero padding, locations outside the image are
-// 0.0.  The staged groups (V = 4: 16 bytes, widened into A-tile words
-// 4g .. 4g+3; V = 1: one word, at the same index in both arrays) are
-// walked group by group (uniform), and within a group over the locations,
-// four per thread in flight (all reads before the writes): no division
-// and no multiply in the addresses.
+// 0.0.  One straight-line path per staging width, four elements per thread
+// in flight (all reads before the writes):
+//   * V = 4: element e = g*plane + rc is one 16-byte group, widened into
+//     four A-tile words g*4 .. g*4+3;
+//   * V = 1: element e is word e / plane of location e % plane, at the
+//     same index in both arrays.
 __device__ __forceinline__ bool region_inside(const MfmaParams &p, int row0, int rc) {
     const int r = (int)fast_div((uint32_t)rc, p.div_pw);
     const int c = rc - r * p.pw;
@@ -583,46 +584,52 @@ __device__ __forceinline__ void widen_region_lds(const MfmaParams &p, const uint
                                                  u32x4 *atile, int row0, int plane, int tid,
                                                  int z) {
     constexpr int U = 4;
-    auto fill_of = [&](int rc) __attribute__((always_inline)) {
-        return p.pad_zero && !region_inside(p, row0, rc) ? 0u : kFp4PlusOne;
-    };
     if (p.region_vec == 4) {
+        const int total = plane * (p.cw >> 2);
         const u32x4 *src = reinterpret_cast<const u32x4 *>(abits);
-        for (int g = 0; g < (p.cw >> 2); ++g, src += plane, atile += 4 * plane) {
-            for (int rc0 = 0; rc0 < plane; rc0 += U * kMfmaThreads) {
-                u32x4 w[U];
+        for (int e0 = 0; e0 < total; e0 += U * kMfmaThreads) {
+            u32x4 w[U];
 #pragma unroll
-                for (int u = 0; u < U; ++u)
-                    w[u] = src[min(rc0 + u * kMfmaThreads + tid, plane - 1) + z];
+            for (int u = 0; u < U; ++u) w[u] = src[min(e0 + u * kMfmaThreads + tid, total - 1) + z];
 #pragma unroll
-                for (int u = 0; u < U; ++u) {
-                    const int rc = rc0 + u * kMfmaThreads + tid;
-                    if (rc >= plane) break;
-                    const uint32_t fill = fill_of(rc);
+            for (int u = 0; u < U; ++u) {
+                const int e = e0 + u * kMfmaThreads + tid;
+                if (e >= total) break;
+                const int g = (int)fast_div((uint32_t)e, p.div_plane);
+                const int rc = e - g * plane;
+                const uint32_t fill = p.pad_zero && !region_inside(p, row0, rc) ? 0u : kFp4PlusOne;
 #pragma unroll
-                    for (int k = 0; k < 4; ++k) atile[k * plane + rc] = widen_word(w[u][k], fill);
-                }
+                for (int k = 0; k < 4; ++k) atile[(4 * g + k) * plane + rc] = widen_word(w[u][k], fill);
             }
         }
     } else {
-        for (int g = 0; g < p.cw; ++g, abits += plane, atile += plane) {
-            for (int rc0 = 0; rc0 < plane; rc0 += U * kMfmaThreads) {
-                uint32_t w[U];
+        const int total = plane * p.cw;
+        for (int e0 = 0; e0 < total; e0 += U * kMfmaThreads) {
+            uint32_t w[U];
 #pragma unroll
-                for (int u = 0; u < U; ++u) w[u] = abits[min(rc0 + u * kMfmaThreads + tid, plane - 1) + z];
+            for (int u = 0; u < U; ++u) w[u] = abits[min(e0 + u * kMfmaThreads + tid, total - 1) + z];
 #pragma unroll
-                for (int u = 0; u < U; ++u) {
-                    const int rc = rc0 + u * kMfmaThreads + tid;
-                    if (rc >= plane) break;
-                    atile[rc] = widen_word(w[u], fill_of(rc));
+            for (int u = 0; u < U; ++u) {
+                const int e = e0 + u * kMfmaThreads + tid;
+                if (e >= total) break;
+                uint32_t fill = kFp4PlusOne;
+                if (p.pad_zero) {
+                    const int j = (int)fast_div((uint32_t)e, p.div_plane);
+                    if (!region_inside(p, row0, e - j * plane)) fill = 0u;
                 }
+                atile[e] = widen_word(w[u], fill);
             }
         }
     }
-    // words past Cw: +1.0 (0.0 outside the image under zero padding); atile
-    // now points at word Cw
-    for (int g = p.cw; g < p.cwe; ++g, atile += plane)
-        for (int rc = tid; rc < plane; rc += kMfmaThreads) atile[rc] = widen_word(0u, fill_of(rc));
+    // words past Cw: +1.0 (0.0 outside the image under zero padding)
+    for (int e = plane * p.cw + tid; e < plane * p.cwe; e += kMfmaThreads) {
+        uint32_t fill = kFp4PlusOne;
+        if (p.pad_zero) {
+            const int j = (int)fast_div((uint32_t)e, p.div_plane);
+            if (!region_inside(p, row0, e - j * plane)) fill = 0u;
+        }
+        atile[e] = widen_word(0u, fill);
+    }
 }
 
 // K-split schedule, for layers whose output tile per workgroup is small
