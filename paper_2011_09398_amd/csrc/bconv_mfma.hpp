@@ -169,16 +169,18 @@ __device__ __forceinline__ void write_value_bits(uint64_t m, uint32_t &word) {
 // 0-31 and 32-63); v_writelane drops each 32-bit half into the lane of its
 // pixel.  fmask (wave-uniform) flips chosen filters.  Lane l < 32 returns
 // the word of pixel l.  All sixteen compares come first, so that no
-// v_writelane waits for the compare right before it.
+// v_writelane waits for the compare right before it, and the lane writes
+// alternate between four partial words (consecutive writes to one register
+// form a dependent chain).
 template <int... V>
 __device__ __forceinline__ uint32_t block_bits_impl(const mfma_v16f &val, float T,
                                                     uint64_t fmask,
                                                     std::integer_sequence<int, V...>) {
     uint64_t m[16];
     ((m[V] = __ballot(val[V] < T) ^ fmask), ...);
-    uint32_t word = 0;
-    (write_value_bits<V>(m[V], word), ...);
-    return word;
+    uint32_t w[4] = {0u, 0u, 0u, 0u};
+    (write_value_bits<V>(m[V], w[V & 3]), ...);
+    return (w[0] | w[1]) | (w[2] | w[3]);
 }
 __device__ __forceinline__ uint32_t block_bits(const mfma_v16f &val, float T, uint64_t fmask) {
     return block_bits_impl(val, T, fmask, std::make_integer_sequence<int, 16>{});
@@ -1029,7 +1031,9 @@ __global__ __launch_bounds__(kMfmaThreads) void bconv2d_mfma_fs_kernel(MfmaParam
     // wave) before the next pair's first products overwrite them.
     mfma_v16f acc[2];
     float fin[NFB][16];
-    uint32_t word[NFB];
+    // (two partial words per block, even and odd values: consecutive lane
+    // writes then go to different registers instead of one dependent chain)
+    uint32_t word[NFB][2];
     int fin_b0 = 0, fin_nbp = 2;
     int buf = 0;
     // (accumulator blocks are picked by uniform branches with constant
@@ -1113,12 +1117,13 @@ __global__ __launch_bounds__(kMfmaThreads) void bconv2d_mfma_fs_kernel(MfmaParam
         if constexpr (OUT == OUT_BITS) {
             const int blk = S == 1 ? j : sk;             // block of the pair
             const bool store = fvalid && blk < fin_nbp;
-            if (v == 0) word[j] = 0u;
-            write_value_bits<v>(mk[N], word[j]);
+            if (v < 2) word[j][v] = 0u;
+            write_value_bits<v>(mk[N], word[j][v & 1]);
             if (v == 15) {
                 const int m = m0 + (fin_b0 + blk) * 32 + lane;
                 if (store && lane < 32 && m < m_end)
-                    reinterpret_cast<uint32_t *>(p.out)[(size_t)m * p.cwo + (f0 >> 5)] = word[j];
+                    reinterpret_cast<uint32_t *>(p.out)[(size_t)m * p.cwo + (f0 >> 5)] =
+                        word[j][0] | word[j][1];
             }
         }
     };
