@@ -867,7 +867,9 @@ __global__ __launch_bounds__(kMfmaThreads) void bconv2d_mfma_ks_kernel(MfmaParam
 
 // Filter-stationary schedule.  Each wave keeps the widened filters of one
 // block of 32 filters for its KS K steps in registers for the whole kernel
-// (16 bytes per lane per step, loaded once); the workgroup stages its input
+// (16 bytes per lane per step, loaded once, from the packed copy where every
+// channel is valid, and waited for step by step in the first pair); the
+// workgroup stages its input
 // region in LDS by DMA, widens it there once, and then runs through its
 // pixel blocks two at a time, reading only the A operands from LDS.
 // Nothing is staged inside the loop, and the loop is software-pipelined
@@ -885,11 +887,11 @@ __global__ __launch_bounds__(kMfmaThreads) void bconv2d_mfma_ks_kernel(MfmaParam
 // filters).  Their partial sums meet in LDS once per pair (one barrier, two
 // alternating buffers), each wave finishing one block of the pair.  The host
 // gives each workgroup the same number of pixel blocks and about one
-// workgroup per CU.
+// workgroup per CU (two where a wave's filters are few).
 // Ring of A operands: K step i of every pair uses slot i % D and, before
 // its products, refills the slot of step i-1 with step i + D - 1 (of this
-// pair, or of the next past its end), so D divides KS (4 or 3 K steps, 5
-// for KS = 5) and the reads run D - 1 steps ahead.  The refill comes first
+// pair, or of the next past its end), so D divides KS (6, 4 or 3 K steps,
+// else KS itself) and the reads run D - 1 steps ahead.  The refill comes first
 // in the step because the loop's pace is set by LDS: every read issued
 // later, behind the step's other work, would leave the LDS idle meanwhile.
 constexpr int fs_depth(int ks) { return ks % 6 == 0 ? 6 : ks % 4 == 0 ? 4 : ks % 3 == 0 ? 3 : ks; }
