@@ -25,8 +25,17 @@ Measured on the launch stream with HIP events:
     bitpack (LceQuantize), binary max pooling (LceBMaxPool2d) and
     dequantize (LceDequantize), in GB/s of algorithmic bytes vs 8 TB/s;
   * the convolution sweep of Section 4.1 (48 batch-1 layers, 3x3 and 5x5,
-    bitpacked in, float out), both kernels from captured graphs.
-Then the CPU oracle, as it stands, on a bounded sample of the same step.
+    bitpacked in, float out), both kernels from captured graphs;
+  * configurations 1, 2 and 3 (batch 1) per layer from captured graphs, and
+    configuration 5 (the 12-layer batch-16 stack) end to end, from eager
+    launches and from one captured graph of the whole pass, with its
+    per-layer breakdown;
+  * the headline layers on the XOR+POPCOUNT kernel as well, reported against
+    the VALU peak (roofline_valu) next to the roofline of the kernel the
+    step uses.
+Then the CPU oracle, as it stands, on a bounded sample of the same step, on
+the whole configuration-5 stack, and on every batch-1 layer with one thread
+and with all host threads.
 
     python bench.py [--steps K] [--warmup W] [--no-cpu] [--workload b64|stack16]
 """
@@ -55,6 +64,9 @@ BINARY_OPS_PER_LANE_OP = 32
 PEAK_BINARY_TOPS = VALU_LANE_OPS * BINARY_OPS_PER_LANE_OP / 1e12      # 1258.3
 # Dense fp4 MFMA peak (MI355X): one +-1 MAC is one fp4 MAC, 2 ops.
 PEAK_FP4_TFLOPS = 10100.0
+# The arithmetic each implementation computes in (the bench line's dtype).
+DTYPES = {"xor": "u32 xor+popcount (VALU), int32 accumulate",
+          "mfma": "fp4 e2m1 MFMA, fp32 accumulate (integer-exact dot)"}
 HBM_PEAK_GBS = 8000.0
 
 
@@ -69,6 +81,8 @@ def parse():
                     help="convolution implementation per layer (auto: the faster)")
     ap.add_argument("--no-cpu", action="store_true", help="skip the CPU oracle baseline")
     ap.add_argument("--no-batch1", action="store_true", help="skip the batch-1 lines")
+    ap.add_argument("--no-stack", action="store_true",
+                    help="skip configuration 5 (the 12-layer batch-16 stack)")
     ap.add_argument("--no-sweep", action="store_true",
                     help="skip the convolution-sweep lines (48 batch-1 layers)")
     ap.add_argument("--sweep-only", action="store_true",
@@ -143,13 +157,14 @@ class Step:
         self.kinds = ["xor"] * len(self.calls)
         self.times = [None] * len(self.calls)
 
-    def choose(self, mode: str, reps: int):
+    def choose(self, mode: str, reps: int, graph: bool = False):
         """Time both implementations of every layer; keep the faster (auto)
-        or the named one for the step."""
+        or the named one for the step.  graph: time from captured graphs
+        (layers shorter than an eager launch)."""
         self.times = []
         for i, (x, m) in enumerate(zip(self.xor_calls, self.mfma_calls)):
-            tx = time_repeated(x, reps, graph=False)
-            tm = time_repeated(m, reps, graph=False)
+            tx = time_repeated(x, reps, graph=graph)
+            tm = time_repeated(m, reps, graph=graph)
             self.times.append((tx, tm))
             kind = mode if mode != "auto" else ("mfma" if tm < tx else "xor")
             self.kinds[i] = kind
@@ -177,6 +192,31 @@ def time_steps(step: Step, steps: int, warmup: int):
     torch.cuda.synchronize()
     wall = time.perf_counter() - t0
     return wall, e0.elapsed_time(e1) * 1e-3
+
+
+def time_graph_steps(step: Step, steps: int) -> float:
+    """Seconds per step when one step (every launch of the pass) is replayed
+    from a captured HIP graph, `steps` replays back to back between events."""
+    import torch
+    step.run()
+    torch.cuda.synchronize()
+    g = torch.cuda.CUDAGraph()
+    s = torch.cuda.Stream()
+    s.wait_stream(torch.cuda.current_stream())
+    with torch.cuda.stream(s):
+        with torch.cuda.graph(g, stream=s):
+            step.run()
+    torch.cuda.current_stream().wait_stream(s)
+    for _ in range(3):
+        g.replay()
+    torch.cuda.synchronize()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record()
+    for _ in range(steps):
+        g.replay()
+    e1.record()
+    torch.cuda.synchronize()
+    return e0.elapsed_time(e1) * 1e-3 / steps
 
 
 def time_repeated(fn, reps: int, graph: bool) -> float:
@@ -344,6 +384,120 @@ def sweep_lines(args, probe=None):
     return out
 
 
+def batch1_lines(args, probe=None):
+    """Configurations 1, 2 and 3 (batch 1, float input bitpacked on the
+    device first): per layer, bitpack and both convolution kernels, each
+    from a captured graph of R launches."""
+    out = []
+    for cfg in (1, 2, 3):
+        s = Step(cfg)
+        for pack, x, m, layer in zip(s.packs, s.xor_calls, s.mfma_calls, s.layers):
+            r = bitpack_record(layer, time_repeated(pack, args.reps, graph=True))
+            r["config"] = cfg
+            out.append(r)
+            tx = time_repeated(x, args.reps, graph=True)
+            tm = time_repeated(m, args.reps, graph=True)
+            kind = args.kernel if args.kernel != "auto" else ("mfma" if tm < tx else "xor")
+            r = layer_record(layer, tm if kind == "mfma" else tx, probe, kind, (tx, tm))
+            r["config"] = cfg
+            out.append(r)
+    return out
+
+
+def stack_lines(args, probe=None):
+    """Configuration 5, the 12-layer batch-16 stack (bitpack of the float
+    input, then the chain): end to end from eager launches and from a
+    captured graph, the per-layer breakdown (graph-captured repeats), and
+    the oracle's wall time on the same stack."""
+    s5 = Step(5)
+    s5.choose(args.kernel, max(args.reps // 2, 20), graph=True)
+    steps = max(args.steps // 5, 20)
+    wall, ev_s = time_steps(s5, steps, max(args.warmup // 5, 5))
+    graph_s = time_graph_steps(s5, steps)
+    ops = sum(l.binary_ops for l in s5.layers)
+    layers = []
+    for pack, call, layer, kind, times in zip(s5.packs, s5.calls, s5.layers, s5.kinds,
+                                              s5.times):
+        if pack is not None:
+            layers.append(bitpack_record(layer, time_repeated(pack, args.reps, graph=True)))
+        layers.append(layer_record(layer, time_repeated(call, args.reps, graph=True), probe,
+                                   kind, times))
+    rec = {"workload": "stack16: " + __import__("workloads").CONFIG_NAMES[5],
+           "binary_ops": ops, "steps": steps,
+           "eager_us": round(wall * 1e6 / steps, 2),
+           "eager_event_us": round(ev_s * 1e6 / steps, 2),
+           "graph_us": round(graph_s * 1e6, 2),
+           "binary_gops_eager": round(ops / (wall / steps) / 1e9, 1),
+           "binary_gops_graph": round(ops / graph_s / 1e9, 1),
+           "kernels": s5.kinds, "layers": layers}
+    if not args.no_cpu:
+        import oracle
+        t0 = time.perf_counter()
+        oracle_pass(5, s5.layers[0].n)
+        dt = time.perf_counter() - t0
+        rec["cpu_oracle"] = {"us": round(dt * 1e6, 1), "binary_gops": round(ops / dt / 1e9, 3),
+                             "cores": oracle.num_threads(), "kind": "oracle",
+                             "sample": "the whole stack, all 16 images, once"}
+    return rec
+
+
+def oracle_pass(cfg_idx: int, images: int):
+    """One pass of the oracle over a configuration's layers (its first
+    `images` images), chained like the device pass; returns binary ops."""
+    import oracle
+    from workloads import config, make_layer_inputs
+    layers = config(cfg_idx)
+    ops, prev = 0, None
+    for i, layer in enumerate(layers):
+        inp = make_layer_inputs(layer, 0, cfg_idx, i)
+        if layer.chained_from is not None:
+            a = oracle.unpack(prev, layer.c_in)
+        elif inp.x_float is not None:
+            a = oracle.binarize(inp.x_float[:images])
+        else:
+            a = oracle.unpack(inp.x_words[:images], layer.c_in)
+        prev = oracle.bconv2d(a, inp.w_sign, stride=layer.strides, padding=layer.padding,
+                              clamp_range=layer.clamp or (-(2 ** 31), 2 ** 31 - 1),
+                              out=layer.out, mult=inp.mult, bias=inp.bias, thr=inp.thr)
+        ops += layer.binary_ops // layer.n * images
+    return ops
+
+
+def cpu_batch1_lines():
+    """The oracle on every batch-1 layer (configurations 1, 2, 3), with one
+    thread and with every host thread: wall time of one pass each."""
+    import oracle
+    from workloads import config, make_layer_inputs
+    full = oracle.num_threads()
+    out = []
+    try:
+        for threads in (1, full):
+            oracle.set_num_threads(threads)
+            for cfg in (1, 2, 3):
+                for i, layer in enumerate(config(cfg)):
+                    inp = make_layer_inputs(layer, 0, cfg, i)
+                    t0 = time.perf_counter()
+                    reps = 0
+                    while True:
+                        a = oracle.binarize(inp.x_float)
+                        oracle.bconv2d(a, inp.w_sign, stride=layer.strides,
+                                       padding=layer.padding,
+                                       clamp_range=layer.clamp or (-(2 ** 31), 2 ** 31 - 1),
+                                       out=layer.out, mult=inp.mult, bias=inp.bias,
+                                       thr=inp.thr)
+                        reps += 1
+                        if time.perf_counter() - t0 > 0.2 or reps >= 50:
+                            break
+                    dt = (time.perf_counter() - t0) / reps
+                    out.append({"config": cfg, "layer": layer.name, "threads": threads,
+                                "us": round(dt * 1e6, 1),
+                                "binary_gops": round(layer.binary_ops / dt / 1e9, 3),
+                                "kind": "oracle"})
+    finally:
+        oracle.set_num_threads(full)
+    return out
+
+
 def valu_probe():
     """Achievable xor+popcount rate in binary TOP/s (a pair covers 32 MACs = 64 ops)."""
     import torch
@@ -366,28 +520,15 @@ def valu_probe():
 def cpu_baseline(cfg_idx: int, target_s: float):
     """The oracle, as it stands, on a bounded sample of the same step."""
     import oracle
-    from workloads import config, make_layer_inputs
+    from workloads import config
 
-    layers = config(cfg_idx)
-    inputs = [make_layer_inputs(l, 0, cfg_idx, i) for i, l in enumerate(layers)]
+    n = config(cfg_idx)[0].n
 
     def run(images):
-        ops, prev = 0, None
         t0 = time.perf_counter()
-        for layer, inp in zip(layers, inputs):
-            if layer.chained_from is not None:
-                a = oracle.unpack(prev, layer.c_in)
-            elif inp.x_float is not None:
-                a = oracle.binarize(inp.x_float[:images])
-            else:
-                a = oracle.unpack(inp.x_words[:images], layer.c_in)
-            prev = oracle.bconv2d(a, inp.w_sign, stride=layer.strides, padding=layer.padding,
-                                  clamp_range=layer.clamp or (-(2 ** 31), 2 ** 31 - 1),
-                                  out=layer.out, mult=inp.mult, bias=inp.bias, thr=inp.thr)
-            ops += layer.binary_ops // layer.n * images
+        ops = oracle_pass(cfg_idx, images)
         return time.perf_counter() - t0, ops
 
-    n = layers[0].n
     dt, ops = run(1)
     images = int(max(1, min(n, target_s / max(dt, 1e-6))))
     reps = 1
@@ -488,21 +629,16 @@ def main():
                                    kind, times))
     conv = [r for r in layers if "binary_ops" in r]
     dom = max(conv, key=lambda r: r["us"])
-    if dom["kernel"] == "xor":
-        roofline = {"bound": "alu", "achieved": round(dom["binary_gops"] / 1e3, 2),
-                    "peak": round(PEAK_BINARY_TOPS, 1), "unit": "TOP/s",
-                    "frac": dom["valu_frac"],
-                    "traffic": measured_traffic(dom["layer"], "xor") if cfg_idx == 4 else None,
-                    "kernel": f"bconv2d (xor+popcount) {dom['layer']} (batch {dom['batch']})",
-                    "probe_peak": None if probe is None else round(probe, 1),
-                    "probe_frac": dom.get("probe_frac")}
-    else:
-        roofline = {"bound": "mfma", "achieved": round(dom["binary_gops"] / 1e3, 2),
-                    "peak": PEAK_FP4_TFLOPS, "unit": "TFLOP/s",
-                    "frac": dom["mfma_fp4_frac"],
-                    "traffic": measured_traffic(dom["layer"], "mfma") if cfg_idx == 4 else None,
-                    "kernel": f"bconv2d_mfma (fp4) {dom['layer']} (batch {dom['batch']})"}
-    roofline.update({"per_launch_binary_ops": dom["binary_ops"], "avg_launch_us": dom["us"]})
+    roofline = roofline_record(dom, dom["kernel"], cfg_idx, probe)
+    # The paper's method (XOR + POPCOUNT on the VALU) on the same layers,
+    # against the VALU peak, whichever implementation the step uses.
+    xor_layers = []
+    for call, layer in zip(step.xor_calls, step.layers):
+        xor_layers.append(layer_record(layer, time_repeated(call, args.reps, graph=False),
+                                       probe, "xor"))
+    roofline_valu = roofline_record(max(xor_layers, key=lambda r: r["us"]), "xor", cfg_idx,
+                                    probe)
+    roofline_valu["layers_valu_frac"] = {r["layer"]: r["valu_frac"] for r in xor_layers}
 
     zero_pad = mem_lines = None
     if not args.no_extra:
@@ -513,31 +649,32 @@ def main():
 
     batch1 = None
     if not args.no_batch1:
-        log("batch-1 layers (graph-captured repeats)")
-        s1 = Step(3)
-        batch1 = []
-        for pack, x, m, layer in zip(s1.packs, s1.xor_calls, s1.mfma_calls, s1.layers):
-            batch1.append(bitpack_record(layer, time_repeated(pack, args.reps, graph=True)))
-            tx = time_repeated(x, args.reps, graph=True)
-            tm = time_repeated(m, args.reps, graph=True)
-            kind = args.kernel if args.kernel != "auto" else ("mfma" if tm < tx else "xor")
-            batch1.append(layer_record(layer, tm if kind == "mfma" else tx, probe, kind,
-                                       (tx, tm)))
+        log("batch-1 configurations 1, 2, 3 (graph-captured repeats)")
+        batch1 = batch1_lines(args, probe)
+
+    stack = None
+    if not args.no_stack:
+        log("configuration 5: the 12-layer batch-16 stack, eager and graph")
+        stack = stack_lines(args, probe)
 
     sweep = None
     if not args.no_sweep:
         log("convolution sweep (graph-captured repeats, both kernels)")
         sweep = sweep_lines(args, probe)
 
-    cpu = None
+    cpu = cpu_b1 = None
     if not args.no_cpu:
         log("CPU oracle sample")
         cpu = cpu_baseline(cfg_idx, args.cpu_seconds)
+        log("CPU oracle on the batch-1 layers, one thread and all threads")
+        cpu_b1 = cpu_batch1_lines()
 
+    kinds = set(step.kinds)
+    dtype = " + ".join(DTYPES[k] for k in sorted(kinds))
     line = {
         "metric": METRIC, "value": round(value, 1), "unit": "GOPS", "n_gpus": 1,
         "steps": args.steps, "warmup": args.warmup, "ms_per_step": round(ms_per_step, 5),
-        "higher_is_better": True, "scaling": "weak", "vs_baseline": None, "dtype": "u32",
+        "higher_is_better": True, "scaling": "weak", "vs_baseline": None, "dtype": dtype,
         "data": "synthetic",
         "config": {"workload": ("qn-b64: " if cfg_idx == 4 else "stack16: ")
                    + CONFIG_NAMES[cfg_idx],
@@ -546,11 +683,33 @@ def main():
                    "kernels": step.kinds,
                    "binary_ops_per_step": total_ops},
         "event_ms_per_step": round(ev_s * 1e3 / args.steps, 5),
-        "roofline": roofline, "cpu_baseline": cpu, "layers": layers, "batch1": batch1,
+        "roofline": roofline, "roofline_valu": roofline_valu, "cpu_baseline": cpu,
+        "layers": layers, "batch1": batch1, "stack16": stack, "cpu_batch1": cpu_b1,
         "zero_padding": zero_pad, "memory_bound": mem_lines, "conv_sweep": sweep,
+        "valu_probe": None if probe is None else {
+            "binary_tops": round(probe, 1), "spec_binary_tops": round(PEAK_BINARY_TOPS, 1)},
         "device": torch.cuda.get_device_name(0),
     }
     print(json.dumps(line), flush=True)
+
+
+def roofline_record(rec, kind, cfg_idx, probe):
+    """The roofline object of one launch record: binary ops per launch over
+    its average duration, against the peak of the unit that ran it."""
+    if kind == "xor":
+        r = {"bound": "alu", "achieved": round(rec["binary_gops"] / 1e3, 2),
+             "peak": round(PEAK_BINARY_TOPS, 1), "unit": "TOP/s", "frac": rec["valu_frac"],
+             "traffic": measured_traffic(rec["layer"], "xor") if cfg_idx == 4 else None,
+             "kernel": f"bconv2d (xor+popcount, VALU) {rec['layer']} (batch {rec['batch']})",
+             "probe_peak": None if probe is None else round(probe, 1),
+             "probe_frac": rec.get("probe_frac")}
+    else:
+        r = {"bound": "mfma", "achieved": round(rec["binary_gops"] / 1e3, 2),
+             "peak": PEAK_FP4_TFLOPS, "unit": "TFLOP/s", "frac": rec["mfma_fp4_frac"],
+             "traffic": measured_traffic(rec["layer"], "mfma") if cfg_idx == 4 else None,
+             "kernel": f"bconv2d_mfma (fp4 e2m1 MFMA) {rec['layer']} (batch {rec['batch']})"}
+    r.update({"per_launch_binary_ops": rec["binary_ops"], "avg_launch_us": rec["us"]})
+    return r
 
 
 if __name__ == "__main__":

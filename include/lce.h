@@ -82,12 +82,16 @@ typedef struct {
     int32_t out_type;               /* lce_out_type                           */
 } lce_bconv2d_desc;
 
-/* Number of 32-bit words holding `channels` packed channels: ceil(c/32).
- * Returns -1 when channels < 0. */
+/* Number of 32-bit words holding `channels` packed channels: ceil(c/32)
+ * (Section 3.2, LceQuantize: the channel count is padded up to a multiple of
+ * 32 and every 32 channels become one word).  Returns -1 when channels < 0. */
 int32_t lce_packed_words(int32_t channels);
 
-/* Output height/width of `desc` (TensorFlow SAME/VALID).  Validates the
- * descriptor exactly as lce_bconv2d does, except for pointers.
+/* Output height/width of `desc`.  LceBConv2d extends TensorFlow Lite's
+ * convolution (Section 3, Section 3.2), so its geometry is TensorFlow's:
+ * SAME gives ceil(H/stride) rows, VALID floor((H-KH)/stride)+1, and likewise
+ * for the width.  Validates the descriptor exactly as lce_bconv2d does,
+ * except for pointers.
  * Errors: LCE_EINVAL (null desc/oh/ow, bad field, no output). */
 lce_status lce_bconv2d_out_shape(const lce_bconv2d_desc *desc, int32_t *oh, int32_t *ow);
 
@@ -216,17 +220,17 @@ lce_status lce_bconv2d_mfma_weights(const lce_bconv2d_desc *desc, const int32_t 
  * CU's share of pixel blocks; by default up to 36 K steps of 64
  * channels, up to 72 when an instance is forced), K-split
  * (the waves of a workgroup divide K; long K) and pixel-split (the rest).
- * The environment variables LCE_MFMA_FS (0 turns the first off),
- * LCE_MFMA_FS_KS / LCE_MFMA_FS_S (its instance), LCE_MFMA_FS_PAD (0: no
- * LDS padding to one workgroup per CU), LCE_MFMA_FS_WPC (1 / 2 workgroups
- * per CU), LCE_MFMA_PK (0: load the widened filters even where the packed
- * copy would do), LCE_MFMA_KS (1 / 0: K-split /
- * pixel-split),
- * LCE_MFMA_MB and LCE_MFMA_NBLK force a schedule and a tile for testing and
- * tuning.  Every choice gives the identical output.
+ * lce_set_tuning can force a schedule, an instance or a tile for tests and
+ * tuning; every choice gives the identical output.
+ * w_fp4 must be the output of lce_bconv2d_mfma_weights for a descriptor with
+ * the same c_in, c_out, kh and kw, 16-byte aligned and at least
+ * lce_bconv2d_mfma_weights_size(desc) bytes: the kernels read the widened
+ * filters and the packed copy behind them at offsets derived from `desc`
+ * (the library cannot see the buffer's size; a smaller one is read past its
+ * end).
  * Errors: as lce_bconv2d, plus LCE_EUNSUPPORTED when K = KH*KW*C_in >= 2^24
  * or when the input region a workgroup stages exceeds the LDS of one
- * workgroup (very wide images); w_fp4 must be 16-byte aligned. */
+ * workgroup (very wide images). */
 lce_status lce_bconv2d_mfma(const lce_bconv2d_desc *desc, const int32_t *x_packed,
                             const void *w_fp4, const float *multiplier, const float *bias,
                             const float *thresholds, const int32_t *flip, void *out,
@@ -269,6 +273,38 @@ lce_status lce_bmaxpool2d(const lce_bmaxpool2d_desc *desc, const int32_t *x_pack
  *         LCE_EHIP. */
 lce_status lce_dequantize(const int32_t *x_packed, float *out, int64_t rows, int32_t channels,
                           hipStream_t stream);
+
+/* ---- Schedule overrides, for tests and tuning ----------------------------
+ *
+ * Every convolution picks its work split by itself.  These process-wide
+ * overrides force one instead; each choice gives the identical output, only
+ * the speed changes.  0 (the initial value of every key) restores the
+ * library's own choice.  Callers are tests, benchmarks and tuning scripts,
+ * not production code.  Values are read once per launch with atomic loads,
+ * so setting them while other threads launch is safe (a launch sees either
+ * the old or the new value).  An out-of-range value falls back to the
+ * automatic choice where the key's comment says so. */
+typedef enum {
+    LCE_TUNE_XOR_NB = 0,          /* lce_bconv2d: blocks of 8 filters per wave, 1..4    */
+    LCE_TUNE_XOR_KS = 1,          /* lce_bconv2d: waves sharing a block's K range 1/2/4 */
+    LCE_TUNE_MFMA_SCHEDULE = 2,   /* lce_bconv2d_mfma: 1 filter-stationary (where an
+                                     instance fits), 2 K split, 3 pixel split            */
+    LCE_TUNE_MFMA_FS_KS = 3,      /* filter-stationary instance: K steps per wave       */
+    LCE_TUNE_MFMA_FS_S = 4,       /* filter-stationary instance: waves per filter block */
+    LCE_TUNE_MFMA_FS_WPC = 5,     /* filter-stationary grid: 1 or 2 workgroups per CU   */
+    LCE_TUNE_MFMA_FS_PAD = 6,     /* -1: no LDS claim that spreads workgroups over CUs  */
+    LCE_TUNE_MFMA_PACKED = 7,     /* -1: load widened filters where packed ones would do */
+    LCE_TUNE_MFMA_TILE_M = 8,     /* K-split / pixel-split tile: 32-pixel blocks        */
+    LCE_TUNE_MFMA_TILE_N = 9,     /* K-split / pixel-split tile: 32-filter blocks       */
+    LCE_TUNE_COUNT = 10
+} lce_tuning_key;
+
+/* Set override `key` to `value` (0 = automatic).
+ * Errors: LCE_EINVAL (unknown key). */
+lce_status lce_set_tuning(int32_t key, int32_t value);
+
+/* Current value of override `key` (0 for an unknown key). */
+int32_t lce_get_tuning(int32_t key);
 
 /* Message describing the last error on the calling thread ("" if none). */
 const char *lce_last_error(void);

@@ -35,7 +35,13 @@ EXPORTS = ("lce_packed_words", "lce_bconv2d_out_shape", "lce_bitpack", "lce_bcon
            "lce_bconv2d_pad_correction_size", "lce_bconv2d_pad_correction",
            "lce_fold_thresholds", "lce_bmaxpool2d_out_shape", "lce_bmaxpool2d",
            "lce_dequantize", "lce_bconv2d_mfma_weights_size", "lce_bconv2d_mfma_weights",
-           "lce_bconv2d_mfma", "lce_last_error")
+           "lce_bconv2d_mfma", "lce_set_tuning", "lce_get_tuning", "lce_last_error")
+
+# lce_tuning_key values, by the names tuning() takes.
+TUNING_KEYS = {"xor_nb": 0, "xor_ks": 1, "mfma_schedule": 2, "mfma_fs_ks": 3, "mfma_fs_s": 4,
+               "mfma_fs_wpc": 5, "mfma_fs_pad": 6, "mfma_packed": 7, "mfma_tile_m": 8,
+               "mfma_tile_n": 9}
+MFMA_SCHEDULES = {"auto": 0, "fs": 1, "ksplit": 2, "pixel": 3}
 
 
 class Desc(ctypes.Structure):
@@ -97,6 +103,10 @@ def lib() -> ctypes.CDLL:
         L.lce_bconv2d_mfma_weights.restype = ctypes.c_int
         L.lce_bconv2d_mfma.argtypes = [ctypes.POINTER(Desc), vp, vp, vp, vp, vp, vp, vp, vp]
         L.lce_bconv2d_mfma.restype = ctypes.c_int
+        L.lce_set_tuning.argtypes = [i32, i32]
+        L.lce_set_tuning.restype = ctypes.c_int
+        L.lce_get_tuning.argtypes = [i32]
+        L.lce_get_tuning.restype = i32
         L.lce_last_error.argtypes = []
         L.lce_last_error.restype = ctypes.c_char_p
         _lib = L
@@ -110,6 +120,37 @@ def last_error() -> str:
 def _check(status: int) -> None:
     if status != LCE_OK:
         raise LceError(status, last_error())
+
+
+def set_tuning(**overrides) -> None:
+    """Schedule overrides (lce_set_tuning), e.g. set_tuning(xor_nb=2,
+    mfma_schedule="fs"); 0 restores the automatic choice.  Process-wide."""
+    for name, value in overrides.items():
+        if name not in TUNING_KEYS:
+            raise KeyError(f"unknown tuning key {name!r}")
+        if name == "mfma_schedule" and isinstance(value, str):
+            value = MFMA_SCHEDULES[value]
+        _check(lib().lce_set_tuning(TUNING_KEYS[name], int(value)))
+
+
+def get_tuning(name: str) -> int:
+    return int(lib().lce_get_tuning(TUNING_KEYS[name]))
+
+
+class tuning:
+    """Context manager: the given overrides inside, every key back to
+    automatic (0) on exit."""
+
+    def __init__(self, **overrides):
+        self.overrides = overrides
+
+    def __enter__(self):
+        set_tuning(**self.overrides)
+        return self
+
+    def __exit__(self, *exc):
+        set_tuning(**{k: 0 for k in TUNING_KEYS})
+        return False
 
 
 def packed_words(channels: int) -> int:
@@ -335,6 +376,13 @@ def dequantize(x_packed, channels: int, out=None):
     return out
 
 
+def mfma_weights_size(desc: Desc) -> int:
+    """Bytes of the widened filter buffer lce_bconv2d_mfma reads for `desc`."""
+    n = ctypes.c_int64()
+    _check(lib().lce_bconv2d_mfma_weights_size(ctypes.byref(desc), ctypes.byref(n)))
+    return n.value
+
+
 def mfma_weights(w_packed, c_in: int, out=None):
     """Widened filters for bconv2d_mfma: uint8 device buffer (16-byte aligned)."""
     import torch
@@ -364,12 +412,19 @@ def bconv2d_mfma(x_packed, w_fp4, c_in: int, c_out: int, kernel, *, stride=1,
     _require(x_packed, torch.int32, "x_packed")
     if not isinstance(w_fp4, torch.Tensor) or w_fp4.device.type != "cuda":
         raise TypeError("w_fp4 must be a device tensor")
+    if not w_fp4.is_contiguous():
+        raise ValueError("w_fp4 must be contiguous")
     n, h, w, cw = x_packed.shape
     if cw != packed_words(c_in):
         raise ValueError(f"packed channel words {cw} do not match c_in={c_in}")
     kh, kw = (kernel, kernel) if isinstance(kernel, int) else tuple(kernel)
     desc = make_desc(n, h, w, c_in, c_out, kh, kw, stride, padding, pad_value, clamp, out_type)
     oh, ow = out_shape(desc)
+    need = mfma_weights_size(desc)
+    if w_fp4.numel() * w_fp4.element_size() < need:
+        raise ValueError(f"w_fp4 holds {w_fp4.numel() * w_fp4.element_size()} bytes; these "
+                         f"filters widen to {need} (mfma_weights of the same c_in, c_out "
+                         f"and kernel)")
     ptrs = []
     for t, name, dtype, numel in ((multiplier, "multiplier", torch.float32, c_out),
                                   (bias, "bias", torch.float32, c_out),

@@ -4,6 +4,7 @@
 #include <hip/hip_runtime.h>
 
 #include <algorithm>
+#include <atomic>
 #include <climits>
 #include <cmath>
 #include <cstdarg>
@@ -209,25 +210,32 @@ void dispatch(const BconvParams &p, dim3 grid, hipStream_t s, int vec, bool padz
         dispatch<OUT, false>(p, grid, s, vec);
 }
 
-int env_int(const char *name, int fallback) {
-    const char *v = getenv(name);
-    return v && *v ? atoi(v) : fallback;
+// Schedule overrides (lce_set_tuning): 0 = the library's own choice.  Each
+// launch reads every value it uses once, with a relaxed atomic load, so a
+// concurrent lce_set_tuning is never a data race (a launch sees the old or
+// the new value).
+std::atomic<int32_t> g_tuning[LCE_TUNE_COUNT];
+
+int tuning(lce_tuning_key key) { return g_tuning[key].load(std::memory_order_relaxed); }
+
+// A device attribute, cached per device.  The cache entries are atomics: two
+// threads making their first launch together both query the attribute and
+// store the same value.
+template <hipDeviceAttribute_t ATTR>
+int device_attribute(int fallback) {
+    static std::atomic<int> cache[64];
+    int dev = 0;
+    if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= 64) return fallback;
+    int v = cache[dev].load(std::memory_order_relaxed);
+    if (v == 0) {
+        if (hipDeviceGetAttribute(&v, ATTR, dev) != hipSuccess || v <= 0) v = fallback;
+        cache[dev].store(v, std::memory_order_relaxed);
+    }
+    return v;
 }
 
-// SIMDs of the current device (4 per compute unit), cached per device.
-int device_simds() {
-    static int cache[64];
-    int dev = 0;
-    if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= 64) return 1024;
-    if (cache[dev] == 0) {
-        int cus = 0;
-        if (hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess ||
-            cus <= 0)
-            cus = 256;
-        cache[dev] = 4 * cus;
-    }
-    return cache[dev];
-}
+// SIMDs of the current device (4 per compute unit).
+int device_simds() { return 4 * device_attribute<hipDeviceAttributeMultiprocessorCount>(256); }
 
 // Work schedule of the shape-specialized kernel.  A unit is 64 pixels x 8
 // filters x the whole K range.  Each schedule (nb filter blocks per wave, or
@@ -263,8 +271,8 @@ void choose_schedule(BconvParams &p, int filters) {
             have = true; best_occupied = occupied; best_key = key; nb = onb; ks = oks;
         }
     }
-    ks = env_int("LCE_BCONV_KS", ks);
-    nb = env_int("LCE_BCONV_NB", nb);
+    if (const int t = tuning(LCE_TUNE_XOR_KS)) ks = t;
+    if (const int t = tuning(LCE_TUNE_XOR_NB)) nb = t;
     if (ks != 1 && ks != 2 && ks != 4) ks = 1;
     if (ks > 1) nb = 1;
     if (nb < 1) nb = 1;
@@ -330,19 +338,7 @@ int64_t mfma_weight_bytes(const lce_bconv2d_desc &d) {
     return (int64_t)d.kh * d.kw * cwe * coutp * (16 + 4);   // widened, then packed
 }
 
-int device_max_lds() {
-    static int cache[64];
-    int dev = 0;
-    if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= 64) return 65536;
-    if (cache[dev] == 0) {
-        int v = 0;
-        if (hipDeviceGetAttribute(&v, hipDeviceAttributeMaxSharedMemoryPerBlock, dev) !=
-                hipSuccess || v <= 0)
-            v = 65536;
-        cache[dev] = v;
-    }
-    return cache[dev];
-}
+int device_max_lds() { return device_attribute<hipDeviceAttributeMaxSharedMemoryPerBlock>(65536); }
 
 // Stacked padded rows a workgroup of `bm` pixels reads, maximized over the
 // workgroups (the span repeats with the image, so one period suffices).
@@ -480,7 +476,7 @@ struct FsPlan {
 // instance with S = 1 and KS <= 9 keeps its registers within the 256 per
 // lane that two waves per SIMD leave.  LCE_MFMA_FS_WPC = 1 / 2 forces it.
 int fs_wgs_per_cu(FsShape sh) {
-    const int e = env_int("LCE_MFMA_FS_WPC", 0);
+    const int e = tuning(LCE_TUNE_MFMA_FS_WPC);
     if (e == 1 || e == 2) return e;
     return sh.s == 1 && sh.ks <= 9 ? 2 : 1;
 }
@@ -495,7 +491,7 @@ int fs_wgs_per_cu(FsShape sh) {
 FsPlan plan_mfma_fs(const lce::MfmaParams &p, int64_t cus, int blocks32, int ksteps) {
     FsPlan best;
     int64_t best_cost = -1;
-    const int env_ks = env_int("LCE_MFMA_FS_KS", 0), env_s = env_int("LCE_MFMA_FS_S", 0);
+    const int env_ks = tuning(LCE_TUNE_MFMA_FS_KS), env_s = tuning(LCE_TUNE_MFMA_FS_S);
     for (const FsShape &sh : kFsShapes) {
         if (env_ks && sh.ks != env_ks) continue;
         if (env_s && sh.s != env_s) continue;
@@ -906,7 +902,8 @@ lce_status lce_bconv2d_mfma(const lce_bconv2d_desc *desc, const int32_t *x_packe
     // 1.5 workgroups, among those whose LDS fits.  LCE_MFMA_KS=1 / 0 force
     // either schedule (the K-split one where its LDS fits).
     const int64_t ksteps = (int64_t)d.kh * d.kw * (p.cwe / 2);
-    const int ks_env = env_int("LCE_MFMA_KS", -1);
+    const int sched = tuning(LCE_TUNE_MFMA_SCHEDULE);   // 0 auto, 1 fs, 2 K split, 3 pixel split
+    const int ks_env = sched == 2 ? 1 : sched == 3 ? 0 : -1;
 
     // Filter-stationary schedule: the default wherever an instance fits, up
     // to 36 K steps.  Longer K runs on the K-split schedule below unless an
@@ -915,8 +912,8 @@ lce_status lce_bconv2d_mfma(const lce_bconv2d_desc *desc, const int32_t *x_packe
     // partial sums add LDS traffic, measured slower than the K split on the
     // 7x7x512 layer.  LCE_MFMA_FS=0 turns it off, LCE_MFMA_KS forces one of
     // the others.
-    const bool fs_forced = env_int("LCE_MFMA_FS_KS", 0) && env_int("LCE_MFMA_FS_S", 0);
-    if (ks_env < 0 && env_int("LCE_MFMA_FS", 1) != 0 &&
+    const bool fs_forced = tuning(LCE_TUNE_MFMA_FS_KS) && tuning(LCE_TUNE_MFMA_FS_S);
+    if (ks_env < 0 &&
         (ksteps <= 36 || (fs_forced && ksteps <= 72))) {
         const FsPlan fp = plan_mfma_fs(p, cus, blocks32, (int)ksteps);
         if (fp.shape.ks) {
@@ -935,12 +932,12 @@ lce_status lce_bconv2d_mfma(const lce_bconv2d_desc *desc, const int32_t *x_packe
             // holds fewer (LCE_MFMA_FS_PAD=0 turns this off)
             const int64_t wgs = fp.groups * ((blocks32 + 4 / fp.shape.s - 1) / (4 / fp.shape.s));
             const int wpc = fs_wgs_per_cu(fp.shape);
-            if (env_int("LCE_MFMA_FS_PAD", 1) == 1 && wgs <= cus * wpc &&
+            if (tuning(LCE_TUNE_MFMA_FS_PAD) >= 0 && wgs <= cus * wpc &&
                 lds * (wpc + 1) <= (size_t)device_max_lds())
                 lds = std::max(lds, (size_t)device_max_lds() / (wpc + 1) + 1024);
             const dim3 grid((unsigned)fp.groups,
                             (unsigned)((blocks32 + 4 / fp.shape.s - 1) / (4 / fp.shape.s)));
-            const bool pk = d.c_in == 32 * p.cwe && env_int("LCE_MFMA_PK", 1) != 0;
+            const bool pk = d.c_in == 32 * p.cwe && tuning(LCE_TUNE_MFMA_PACKED) >= 0;
             launch_mfma_fs(p, fp.shape, pk, d.out_type, grid, lds, stream);
             return check_launch("lce_bconv2d_mfma launch");
         }
@@ -951,7 +948,7 @@ lce_status lce_bconv2d_mfma(const lce_bconv2d_desc *desc, const int32_t *x_packe
                                         {2, 1}, {1, 2}, {1, 1}};
         int mbw = 0, knb = 0, rows = 0;
         int64_t best_wgs = -1;
-        const int env_mb = env_int("LCE_MFMA_MB", 0), env_nb = env_int("LCE_MFMA_NBLK", 0);
+        const int env_mb = tuning(LCE_TUNE_MFMA_TILE_M), env_nb = tuning(LCE_TUNE_MFMA_TILE_N);
         for (const auto &o : kTiles) {
             if (o[1] > nmax) continue;
             if (env_mb && o[0] != env_mb) continue;
@@ -994,8 +991,8 @@ lce_status lce_bconv2d_mfma(const lce_bconv2d_desc *desc, const int32_t *x_packe
         if (wgs >= cus) { mb = o[0]; nblk = o[1]; break; }
         if (wgs > best_wgs) { best_wgs = wgs; mb = o[0]; nblk = o[1]; }
     }
-    nblk = env_int("LCE_MFMA_NBLK", nblk);
-    mb = env_int("LCE_MFMA_MB", mb);
+    if (const int t = tuning(LCE_TUNE_MFMA_TILE_N)) nblk = t;
+    if (const int t = tuning(LCE_TUNE_MFMA_TILE_M)) mb = t;
     if (nblk != 1 && nblk != 2 && nblk != 4) nblk = 4;
     if (mb != 1 && mb != 2) mb = 2;
     const int bm = 128 * mb;
@@ -1026,6 +1023,17 @@ lce_status lce_bconv2d_mfma(const lce_bconv2d_desc *desc, const int32_t *x_packe
         default: launch_mfma<4, lce::OUT_INT>(p, nblk, mb, grid, lds, stream); break;
     }
     return check_launch("lce_bconv2d_mfma launch");
+}
+
+lce_status lce_set_tuning(int32_t key, int32_t value) {
+    if (key < 0 || key >= LCE_TUNE_COUNT) return fail(LCE_EINVAL, "unknown tuning key %d", key);
+    g_tuning[key].store(value, std::memory_order_relaxed);
+    return ok();
+}
+
+int32_t lce_get_tuning(int32_t key) {
+    if (key < 0 || key >= LCE_TUNE_COUNT) return 0;
+    return g_tuning[key].load(std::memory_order_relaxed);
 }
 
 const char *lce_last_error(void) { return g_last_error.c_str(); }

@@ -6,12 +6,13 @@ the previous layer's output, and then the oracle uses its own previous output.
 """
 from __future__ import annotations
 
+import functools
 from typing import Optional, Sequence
 
 import numpy as np
 
 import oracle
-from workloads import INT32_MAX, INT32_MIN, Layer, LayerInputs
+from workloads import INT32_MAX, INT32_MIN, Layer, LayerInputs, config, make_layer_inputs
 
 POISON_I32 = -1431655766                      # 0xAAAAAAAA
 POISON_F32 = np.array([POISON_I32], np.int32).view(np.float32)[0]
@@ -99,3 +100,27 @@ def assert_match(layer: Layer, got: np.ndarray, ref: np.ndarray, what: str = "")
             raise AssertionError(f"{what}: {int((g != r).sum())} mismatches, e.g. "
                                  + ", ".join(f"{tuple(i)} got {g[tuple(i)]} want {r[tuple(i)]}"
                                              for i in diff))
+
+
+@functools.lru_cache(maxsize=None)
+def config4_reference(chain: bool = True, pad_value: int = 1):
+    """Oracle outputs of the four batch-64 layers over the whole batch,
+    computed once per process: tuple of (layer, inputs, reference).
+
+    chain=True: the 28x28x128 layer takes the oracle's own stride-2 output
+    (the chained configuration); chain=False: every layer its own input.
+    pad_value: 1 one-padding, 0 zero padding."""
+    out, prev = [], None
+    for i, layer in enumerate(config(4)):
+        inp = make_layer_inputs(layer, 0, 4, i)
+        if chain and layer.chained_from is not None:
+            a = oracle.unpack(prev, layer.c_in)
+        else:
+            a = oracle_signs(inp)
+        ref = oracle.bconv2d(a, inp.w_sign, stride=layer.strides, padding=layer.padding,
+                             clamp_range=clamp_of(layer), out=layer.out, mult=inp.mult,
+                             bias=inp.bias, thr=inp.thr, pad_value=pad_value)
+        ref.setflags(write=False)
+        out.append((layer, inp, ref))
+        prev = ref
+    return tuple(out)

@@ -230,3 +230,53 @@ def test_dequantize_validation_errors():
     assert L.lce_dequantize(P, P, 2 ** 62, 64, None) == lce.LCE_EINVAL
     assert L.lce_dequantize(P, P, 0, 32, None) == lce.LCE_OK
     assert L.lce_dequantize(None, None, 0, 32, None) == lce.LCE_OK     # empty: may be NULL
+
+
+def test_tuning_overrides_round_trip_and_reset():
+    L = lce.lib()
+    assert ctypes.sizeof(ctypes.c_int32) == 4
+    for name, key in lce.TUNING_KEYS.items():
+        assert lce.get_tuning(name) == 0, name          # every override starts automatic
+    with lce.tuning(xor_nb=3, mfma_schedule="pixel", mfma_packed=-1):
+        assert lce.get_tuning("xor_nb") == 3
+        assert lce.get_tuning("mfma_schedule") == lce.MFMA_SCHEDULES["pixel"]
+        assert lce.get_tuning("mfma_packed") == -1
+    assert all(lce.get_tuning(n) == 0 for n in lce.TUNING_KEYS)
+    assert L.lce_set_tuning(len(lce.TUNING_KEYS), 1) == lce.LCE_EINVAL
+    assert "tuning key" in lce.last_error()
+    assert L.lce_set_tuning(-1, 1) == lce.LCE_EINVAL
+    assert L.lce_get_tuning(99) == 0
+    with pytest.raises(KeyError):
+        lce.set_tuning(no_such_key=1)
+
+
+def test_tuning_keys_match_header_enum():
+    text = open(HEADER).read()
+    enum = dict((m.group(1).lower(), int(m.group(2)))
+                for m in re.finditer(r"LCE_TUNE_([A-Z0-9_]+)\s*=\s*(\d+)", text))
+    count = enum.pop("count")
+    assert enum == lce.TUNING_KEYS
+    assert count == len(lce.TUNING_KEYS)
+
+
+def test_tuning_set_from_many_threads():
+    """Overrides are atomics: concurrent sets and gets from many threads
+    leave one of the written values, never a torn or foreign one."""
+    import threading
+    L = lce.lib()
+    key = lce.TUNING_KEYS["xor_nb"]
+    seen = set()
+
+    def work(v):
+        for _ in range(2000):
+            L.lce_set_tuning(key, v)
+            seen.add(L.lce_get_tuning(key))
+
+    threads = [threading.Thread(target=work, args=(v,)) for v in (1, 2, 3, 4)]
+    for t in threads:
+        t.start()
+    for t in threads:
+        t.join()
+    assert seen <= {1, 2, 3, 4}
+    assert L.lce_get_tuning(key) in (1, 2, 3, 4)
+    lce.set_tuning(xor_nb=0)

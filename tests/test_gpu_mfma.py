@@ -5,20 +5,20 @@ its dot is the exact integer the oracle computes: int32 and bitpacked outputs
 must match bit for bit, float outputs within 1e-6 relative.  Zero padding
 (0.0 at padded locations) is checked against the oracle's pad_value=0.
 
-Every test runs under each schedule of the path, chosen through the
-environment: the filter-stationary one (each wave keeps its filters in
+Every test runs under each schedule of the path, forced through
+lce_set_tuning: the filter-stationary one (each wave keeps its filters in
 registers and runs through the workgroup's pixel blocks; the default
-wherever one of its instances fits, LCE_MFMA_FS=1), the K-split one (the
-four waves of a workgroup share one output tile and divide K; LCE_MFMA_KS=1,
-used where its LDS fits) and the pixel-split one (LCE_MFMA_KS=0).  A layer no
-filter-stationary instance fits runs on one of the other two.
+wherever one of its instances fits), the K-split one (the four waves of a
+workgroup share one output tile and divide K; used where its LDS fits) and
+the pixel-split one.  A layer no filter-stationary instance fits runs on
+one of the other two.  The batch-64 layers are compared over every output.
 """
 import numpy as np
 import pytest
 
 import oracle
-from tests.layer_util import (assert_match, clamp_of, dev, gpu_input, gpu_pack_weights,
-                              oracle_signs, poisoned_out)
+from tests.layer_util import (assert_match, clamp_of, config4_reference, dev, gpu_input,
+                              gpu_pack_weights, oracle_signs, poisoned_out)
 from workloads import Layer, config, make_layer_inputs
 
 pytestmark = pytest.mark.gpu
@@ -35,15 +35,14 @@ def gpu():
     torch.cuda.synchronize()
 
 
+SCHEDULE_NAMES = {"fs": "fs", "ks": "ksplit", "pixel": "pixel"}
+
+
 @pytest.fixture(autouse=True, params=["fs", "ks", "pixel"])
-def schedule(request, monkeypatch):
-    for k in ("LCE_MFMA_KS", "LCE_MFMA_FS_KS", "LCE_MFMA_FS_S", "LCE_MFMA_FS_PAD",
-              "LCE_MFMA_PK", "LCE_MFMA_FS_WPC"):
-        monkeypatch.delenv(k, raising=False)
-    if request.param == "fs":
-        monkeypatch.setenv("LCE_MFMA_FS", "1")
-    else:
-        monkeypatch.setenv("LCE_MFMA_KS", "1" if request.param == "ks" else "0")
+def schedule(request):
+    import paper_2011_09398_amd as lce
+    lce.set_tuning(**{k: 0 for k in lce.TUNING_KEYS})
+    lce.set_tuning(mfma_schedule=SCHEDULE_NAMES[request.param])
     return request.param
 
 
@@ -117,36 +116,56 @@ def test_mfma_config_parity_full(cfg):
         assert_match(layer, got, oracle_run(layer, inp, oracle_signs(inp)), layer.name)
 
 
+def test_mfma_config4_full_batch_chained(schedule):
+    """Batch 64 as timed, every output of every layer; the stride-2 layer's
+    output feeds the 28x28x128 layer on both sides."""
+    prev_gpu = None
+    for layer, inp, ref in config4_reference(chain=True):
+        x = prev_gpu if layer.chained_from is not None else None
+        got = mfma_run(layer, inp, x_packed=x)
+        assert_match(layer, sync_np(got), ref, f"{layer.name} {schedule}")
+        prev_gpu = got
+
+
+def test_mfma_config4_default_schedule_full(schedule):
+    """The library's own schedule choice (no override) on the batch-64
+    layers, every output: the configuration the benchmark times."""
+    import paper_2011_09398_amd as lce
+    if schedule != "fs":
+        pytest.skip("one run suffices: the schedule override is cleared here")
+    lce.set_tuning(mfma_schedule=0)
+    for layer, inp, ref in config4_reference(chain=False):
+        assert_match(layer, sync_np(mfma_run(layer, inp)), ref, f"{layer.name} auto")
+
+
 @pytest.mark.parametrize("nblk", [1, 2, 4])
-def test_mfma_config4_sampled_every_filter_split(monkeypatch, nblk):
-    """The batch-64 layers at full size, every filter-block split."""
-    monkeypatch.setenv("LCE_MFMA_NBLK", str(nblk))
-    sample = [0, 29, 63]
-    for i, layer in enumerate(config(4)):
-        inp = make_layer_inputs(layer, 0, 4, i)
+def test_mfma_config4_every_filter_split(schedule, nblk):
+    """The batch-64 layers at full size, every filter-block split, every
+    output."""
+    import paper_2011_09398_amd as lce
+    if schedule == "fs":
+        pytest.skip("the filter-stationary schedule has no filter-block split")
+    lce.set_tuning(mfma_tile_n=nblk)
+    for layer, inp, ref in config4_reference(chain=False):
         got = sync_np(mfma_run(layer, inp))
-        ref = oracle_run(layer, inp, oracle_signs(inp, sample))
-        assert_match(layer, got[sample], ref, f"{layer.name} nblk={nblk}")
+        assert_match(layer, got, ref, f"{layer.name} nblk={nblk}")
 
 
 @pytest.mark.parametrize("mbw,nblk", [(4, 2), (2, 4), (2, 2), (4, 1), (1, 4), (2, 1), (1, 2),
                                       (1, 1)])
-def test_mfma_every_tile_shape(monkeypatch, schedule, mbw, nblk):
-    """Every tile of either schedule: the batch-64 7x7x512 layer (sampled), a
-    ragged float layer and a stride-2 layer with zero padding."""
+def test_mfma_every_tile_shape(schedule, mbw, nblk):
+    """Every tile of either schedule: the batch-64 7x7x512 layer (every
+    output), a ragged float layer and a stride-2 layer with zero padding."""
+    import paper_2011_09398_amd as lce
     if schedule == "pixel" and mbw == 4:
         pytest.skip("the pixel-split schedule takes 1 or 2 pixel blocks per wave")
     if schedule == "fs":
         pytest.skip("the filter-stationary schedule has no such tile (its instances are "
                     "covered by test_mfma_fs_every_instance)")
-    monkeypatch.setenv("LCE_MFMA_MB", str(mbw))
-    monkeypatch.setenv("LCE_MFMA_NBLK", str(nblk))
-    layer = config(4)[3]
-    inp = make_layer_inputs(layer, 0, 4, 3)
-    sample = [1, 62]
+    lce.set_tuning(mfma_tile_m=mbw, mfma_tile_n=nblk)
+    layer, inp, ref = config4_reference(chain=False)[3]
     got = sync_np(mfma_run(layer, inp))
-    assert_match(layer, got[sample], oracle_run(layer, inp, oracle_signs(inp, sample)),
-                 f"{layer.name} mb={mbw} nblk={nblk}")
+    assert_match(layer, got, ref, f"{layer.name} mb={mbw} nblk={nblk}")
     for lay, pv in ((Layer("rag", 3, 11, 9, 100, 200, out="float", clamp=(-60, 90),
                            input_kind="float"), "one"),
                     (Layer("s2z", 2, 13, 10, 96, 72, stride=2, out="bitpacked",
@@ -183,14 +202,14 @@ def cwe_of(cw):
 
 @pytest.mark.parametrize("packed", [True, False], ids=["packed_filters", "widened_filters"])
 @pytest.mark.parametrize("ks,s", FS_INSTANCES, ids=lambda v: str(v))
-def test_mfma_fs_every_instance(monkeypatch, schedule, ks, s, packed):
+def test_mfma_fs_every_instance(schedule, ks, s, packed):
     """packed: C_in fills every widened word (C_in = 32*Cw'), where the kernel
     loads the packed filter copy and widens it itself; otherwise some
     channels are padding and it loads the widened filters."""
+    import paper_2011_09398_amd as lce
     if schedule != "fs":
         pytest.skip("filter-stationary instances")
-    monkeypatch.setenv("LCE_MFMA_FS_KS", str(ks))
-    monkeypatch.setenv("LCE_MFMA_FS_S", str(s))
+    lce.set_tuning(mfma_fs_ks=ks, mfma_fs_s=s)
     shapes = fs_layers(ks, s)
     assert shapes, (ks, s)
     rng = np.random.default_rng(ks * 10 + s + (1000 if packed else 0))
@@ -225,13 +244,13 @@ def test_mfma_fs_every_instance(monkeypatch, schedule, ks, s, packed):
 
 @pytest.mark.parametrize("wpc", ["1", "2"])
 @pytest.mark.parametrize("ks,s", [(9, 1), (18, 1), (9, 2)], ids=lambda v: str(v))
-def test_mfma_fs_workgroups_per_cu(monkeypatch, ks, s, wpc):
+def test_mfma_fs_workgroups_per_cu(schedule, ks, s, wpc):
     """One or two workgroups per CU (the grid and the pixel share per
     workgroup change, the result does not): ragged layers, stride 2."""
-    monkeypatch.setenv("LCE_MFMA_FS", "1")
-    monkeypatch.setenv("LCE_MFMA_FS_KS", str(ks))
-    monkeypatch.setenv("LCE_MFMA_FS_S", str(s))
-    monkeypatch.setenv("LCE_MFMA_FS_WPC", wpc)
+    import paper_2011_09398_amd as lce
+    if schedule != "fs":
+        pytest.skip("filter-stationary grids")
+    lce.set_tuning(mfma_fs_ks=ks, mfma_fs_s=s, mfma_fs_wpc=int(wpc))
     for j, (kh, kw, cw) in enumerate(fs_layers(ks, s)[:2]):
         layer = Layer(f"wpc{ks}x{s}_{j}", 5, 19 - j, 23, 32 * cwe_of(cw) - 7 * j, 96 + 40 * j,
                       kh=kh, kw=kw, stride=1 + j, out=["bitpacked", "float"][j],
@@ -243,30 +262,25 @@ def test_mfma_fs_workgroups_per_cu(monkeypatch, ks, s, wpc):
 
 
 @pytest.mark.parametrize("packed", ["1", "0"], ids=["packed_filters", "widened_filters"])
-def test_mfma_fs_config4_every_instance_that_fits(monkeypatch, schedule, packed):
-    """The batch-64 layers at full size (sampled images) on every
+def test_mfma_fs_config4_every_instance_that_fits(schedule, packed):
+    """The batch-64 layers at full size (every output) on every
     filter-stationary instance whose K steps fit the layer, loading the
     packed filter copy (the default there) or the widened filters."""
+    import paper_2011_09398_amd as lce
     if schedule != "fs":
         pytest.skip("filter-stationary instances")
-    monkeypatch.setenv("LCE_MFMA_PK", packed)
-    sample = [0, 37, 63]
-    for i, layer in enumerate(config(4)):
-        inp = make_layer_inputs(layer, 0, 4, i)
-        ref = None
+    lce.set_tuning(mfma_packed=1 if packed == "1" else -1)
+    for layer, inp, ref in config4_reference(chain=False):
         steps = layer.kh * layer.kw * ((layer.cw + 1) // 2)
         for ks, s in FS_INSTANCES:
             if not ((s - 1) * ks < steps <= s * ks):
                 continue
-            monkeypatch.setenv("LCE_MFMA_FS_KS", str(ks))
-            monkeypatch.setenv("LCE_MFMA_FS_S", str(s))
+            lce.set_tuning(mfma_fs_ks=ks, mfma_fs_s=s)
             got = sync_np(mfma_run(layer, inp))
-            if ref is None:
-                ref = oracle_run(layer, inp, oracle_signs(inp, sample))
-            assert_match(layer, got[sample], ref, f"{layer.name} fs {ks}x{s}")
+            assert_match(layer, got, ref, f"{layer.name} fs {ks}x{s}")
 
 
-def test_mfma_wide_region_falls_back_to_the_pixel_split(monkeypatch):
+def test_mfma_wide_region_falls_back_to_the_pixel_split():
     """A region too wide for the K-split schedule's LDS (every word of a
     2048-channel, 60-column region) runs on the pixel-split schedule."""
     layer = Layer("wide", 1, 5, 60, 2048, 40, out="int32", input_kind="bits")

@@ -8,8 +8,8 @@ import numpy as np
 import pytest
 
 import oracle
-from tests.layer_util import (POISON_I32, assert_match, dev, gpu_input, gpu_layer,
-                              gpu_pack_weights, oracle_layer, oracle_signs)
+from tests.layer_util import (POISON_I32, assert_match, config4_reference, dev, gpu_input,
+                              gpu_layer, gpu_pack_weights, oracle_layer, oracle_signs)
 from workloads import INT32_MAX, INT32_MIN, Layer, config, make_layer_inputs
 
 pytestmark = pytest.mark.gpu
@@ -93,26 +93,18 @@ def test_config_parity_full(cfg):
         assert_match(layer, got, ref, f"config {cfg} layer {layer.name}")
 
 
-def test_config4_full_batch_sampled_images():
-    """Batch 64, launched exactly as timed; the oracle checks sampled images.
-
-    The stride-2 layer's bitpacked output is fed to the 28x28x128 layer on
-    both sides (the chain)."""
-    layers = config(4)
-    sample = [0, 29, 63]
-    prev_gpu = prev_ref = None
-    for i, layer in enumerate(layers):
-        inp = make_layer_inputs(layer, 0, 4, i)
+def test_config4_full_batch_chained():
+    """Batch 64, launched exactly as timed, every output of every layer
+    compared with the oracle.  The stride-2 layer's bitpacked output feeds
+    the 28x28x128 layer on both sides (the chain)."""
+    prev_gpu = None
+    for layer, inp, ref in config4_reference(chain=True):
         if layer.chained_from is not None:
             got = gpu_layer(layer, inp, x_packed=prev_gpu)
-            a = oracle.unpack(prev_ref, layer.c_in)
         else:
             got = gpu_layer(layer, inp)
-            a = oracle_signs(inp, sample)
-        got_np = sync_np(got)
-        ref = oracle_layer(layer, inp, a)
-        assert_match(layer, got_np[sample], ref, f"config 4 layer {layer.name}")
-        prev_gpu, prev_ref = got, ref
+        assert_match(layer, sync_np(got), ref, f"config 4 layer {layer.name}")
+        prev_gpu = got
 
 
 def test_config5_chain_every_layer():
@@ -306,28 +298,24 @@ def test_every_static_instance(k, cw, out, stride):
     (2, 7, 9, 160, 70, 1, "bitpacked", 5),
     (1, 8, 8, 96, 64, 1, "float", 5),
 ])
-def test_every_schedule_matches_oracle(monkeypatch, nb, ks, shape):
+def test_every_schedule_matches_oracle(nb, ks, shape):
     """Every work split of the shape-specialized kernel (filter blocks per
     wave, K split across waves) gives the oracle's result."""
+    import paper_2011_09398_amd as lce
     n, h, w, c_in, c_out, s, out = shape[:7]
     k = shape[7] if len(shape) > 7 else 3
-    monkeypatch.setenv("LCE_BCONV_NB", str(nb))
-    monkeypatch.setenv("LCE_BCONV_KS", str(ks))
+    lce.set_tuning(xor_nb=nb, xor_ks=ks)
     layer = Layer(f"sched{nb}{ks}", n, h, w, c_in, c_out, kh=k, kw=k, stride=s, out=out,
                   clamp=(-50, 60) if out != "bitpacked" else None, input_kind="bits")
     run_case(layer, make_layer_inputs(layer, nb * 10 + ks, 60, c_out))
 
 
-def test_config4_every_schedule_sampled(monkeypatch):
-    sample = [0, 63]
-    for i, layer in enumerate(config(4)):
-        if layer.chained_from is not None:
-            continue
-        inp = make_layer_inputs(layer, 0, 4, i)
-        xp, wp = gpu_input(inp), gpu_pack_weights(inp)
-        ref = oracle_layer(layer, inp, oracle_signs(inp, sample))
-        for nb, ks in SCHEDULES:
-            monkeypatch.setenv("LCE_BCONV_NB", str(nb))
-            monkeypatch.setenv("LCE_BCONV_KS", str(ks))
-            got = sync_np(gpu_layer(layer, inp, x_packed=xp, w_packed=wp))
-            assert_match(layer, got[sample], ref, f"{layer.name} nb={nb} ks={ks}")
+@pytest.mark.parametrize("nb,ks", SCHEDULES)
+def test_config4_every_schedule_full(nb, ks):
+    """The batch-64 layers (each on its own input) under every XOR work
+    split, every output compared."""
+    import paper_2011_09398_amd as lce
+    lce.set_tuning(xor_nb=nb, xor_ks=ks)
+    for layer, inp, ref in config4_reference(chain=False):
+        got = sync_np(gpu_layer(layer, inp))
+        assert_match(layer, got, ref, f"{layer.name} nb={nb} ks={ks}")

@@ -4,7 +4,8 @@
 {32, 64, 96, 128, 160, 256} (96 and 160 give odd word counts), H = W in
 {8, 16, 32, 64}, 3x3 and 5x5 filters, stride 1, equal padding; bitpacked
 input, float output through the fused multiplier and bias.  Every layer runs
-on the XOR+POPCOUNT kernel and on both schedules of the matrix-core kernel,
+on the XOR+POPCOUNT kernel, on the matrix-core kernel with the library's own
+schedule choice (what the benchmark times) and with each schedule forced,
 each compared with the oracle over the whole output (1e-6 relative).
 """
 import functools
@@ -45,15 +46,18 @@ def sync_np(t):
     return t.cpu().numpy()
 
 
-@pytest.mark.parametrize("kernel", ["xor", "mfma-pixel", "mfma-ksplit"])
+@pytest.mark.parametrize("kernel", ["xor", "mfma-default", "mfma-fs", "mfma-pixel",
+                                    "mfma-ksplit"])
 @pytest.mark.parametrize("i", range(len(LAYERS)), ids=[l.name for l in LAYERS])
-def test_sweep_layer(monkeypatch, i, kernel):
+def test_sweep_layer(i, kernel):
     import paper_2011_09398_amd as lce
     layer, inp, ref = case(i)
     if kernel == "xor":
         got = sync_np(gpu_layer(layer, inp))
     else:
-        monkeypatch.setenv("LCE_MFMA_KS", "1" if kernel == "mfma-ksplit" else "0")
+        lce.set_tuning(mfma_schedule={"mfma-default": "auto", "mfma-fs": "fs",
+                                      "mfma-pixel": "pixel",
+                                      "mfma-ksplit": "ksplit"}[kernel])
         wf = lce.mfma_weights(gpu_pack_weights(inp), layer.c_in)
         got = sync_np(lce.bconv2d_mfma(
             gpu_input(inp), wf, layer.c_in, layer.c_out, (layer.kh, layer.kw),

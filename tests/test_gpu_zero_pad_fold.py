@@ -14,8 +14,8 @@ import numpy as np
 import pytest
 
 import oracle
-from tests.layer_util import (POISON_I32, assert_match, clamp_of, dev, gpu_input,
-                              gpu_pack_weights, oracle_signs, poisoned_out)
+from tests.layer_util import (POISON_I32, assert_match, clamp_of, config4_reference, dev,
+                              gpu_input, gpu_pack_weights, oracle_signs, poisoned_out)
 from workloads import INT32_MAX, INT32_MIN, Layer, config, make_layer_inputs
 
 pytestmark = pytest.mark.gpu
@@ -144,10 +144,10 @@ SCHEDULES = [(1, 1), (2, 1), (3, 1), (4, 1), (1, 2), (1, 4)]
     (1, 7, 7, 512, 96, 1, "int32"),
     (2, 5, 6, 256, 130, 1, "bitpacked"),
 ])
-def test_zero_padding_every_schedule(monkeypatch, nb, ks, shape):
+def test_zero_padding_every_schedule(nb, ks, shape):
+    import paper_2011_09398_amd as lce
     n, h, w, c_in, c_out, s, out = shape
-    monkeypatch.setenv("LCE_BCONV_NB", str(nb))
-    monkeypatch.setenv("LCE_BCONV_KS", str(ks))
+    lce.set_tuning(xor_nb=nb, xor_ks=ks)
     layer = Layer(f"zsched{nb}{ks}", n, h, w, c_in, c_out, stride=s, out=out,
                   clamp=(-50, 60) if out != "bitpacked" else None, input_kind="bits")
     inp = make_layer_inputs(layer, nb * 10 + ks, 61, c_out)
@@ -169,15 +169,17 @@ def test_zero_padding_special_thresholds():
 
 @pytest.mark.parametrize("cfg_layer", [(2, 0), (4, 0), (4, 1), (4, 2), (4, 3)])
 def test_zero_padding_config_layers(cfg_layer):
-    """The workload layers at full size with zero padding (batch-64 layers
-    checked on sampled images; the launch covers the whole batch)."""
+    """The workload layers at full size with zero padding, every output
+    (each batch-64 layer on its own input)."""
     cfg, li = cfg_layer
-    layer = config(cfg)[li]
-    inp = make_layer_inputs(layer, 0, cfg, li)
-    sample = [0, 37, layer.n - 1] if layer.n > 4 else None
+    if cfg == 4:
+        layer, inp, ref = config4_reference(chain=False, pad_value=0)[li]
+    else:
+        layer = config(cfg)[li]
+        inp = make_layer_inputs(layer, 0, cfg, li)
+        ref = oracle_run(layer, inp, oracle_signs(inp))
     got = sync_np(gpu_run(layer, inp))
-    ref = oracle_run(layer, inp, oracle_signs(inp, sample))
-    assert_match(layer, got if sample is None else got[sample], ref, layer.name)
+    assert_match(layer, got, ref, layer.name)
 
 
 def test_zero_padding_without_padded_taps_needs_no_table():

@@ -479,3 +479,58 @@ def test_sign_of_affine_exact():
         ref = [1 if Fraction(int(ci)) * Fraction(float(m32)) + Fraction(float(b32)) < 0 else 0
                for ci in c]
         assert bits.tolist() == ref, (m, b)
+
+
+# ---------------------------------------------------------------- per-channel direction (flip)
+
+def test_flip_hand_example():
+    """tests/golden/e6_flip.json: four filters with hand-computed dots,
+    thresholds on either side of them and a flip word."""
+    g = golden("e6_flip.json")
+    a = np.ones((1, 1, 1, 8), np.int8)
+    w = np.ones((4, 1, 1, 8), np.int8)
+    for f, k in enumerate(g["k"]):
+        w[f, 0, 0, :k] = -1
+    dot = oracle.bconv2d(a, w, out="int32")
+    assert dot.reshape(-1).tolist() == g["dot"]
+    thr = np.array(g["thresholds"], np.float32)
+    plain = oracle.bconv2d(a, w, out="bitpacked", thr=thr)
+    assert int(plain.reshape(-1)[0]) == sum(b << i for i, b in enumerate(g["below"]))
+    got = oracle.bconv2d(a, w, out="bitpacked", thr=thr, flip=np.array(g["flip"], np.uint8))
+    assert got.shape == (1, 1, 1, 1)
+    assert int(got.reshape(-1)[0]) == g["word"]
+
+
+@pytest.mark.parametrize("c_out", [1, 31, 32, 40, 64, 100])
+def test_flip_every_channel_complements_valid_bits(c_out):
+    """Flipping every channel inverts exactly the C_out valid bits of each
+    output word; the pad bits past C_out stay 0.  Flipping none changes
+    nothing."""
+    rng = np.random.default_rng(c_out)
+    a = rand_signs((2, 5, 6, 40), rng)
+    w = rand_signs((c_out, 3, 3, 40), rng)
+    thr = rng.normal(0.0, 6.0, c_out).astype(np.float32)
+    base = oracle.bconv2d(a, w, out="bitpacked", thr=thr)
+    none = oracle.bconv2d(a, w, out="bitpacked", thr=thr, flip=np.zeros(c_out, np.uint8))
+    assert np.array_equal(none, base)
+    allf = oracle.bconv2d(a, w, out="bitpacked", thr=thr, flip=np.ones(c_out, np.uint8))
+    cw = (c_out + 31) // 32
+    mask = np.array([(1 << min(32, c_out - 32 * j)) - 1 for j in range(cw)], np.uint64)
+    assert np.array_equal(allf.astype(np.uint64), (~base.astype(np.uint64)) & mask)
+
+
+def test_flip_equals_negated_filters_with_mirrored_thresholds():
+    """For integer thresholds t: NOT(dot < t) = (-dot < 1 - t), and negating
+    the filters negates dot (a +-1 product changes sign).  So flipping a
+    channel equals running its negated filter against 1 - t without a flip,
+    channel by channel."""
+    rng = np.random.default_rng(77)
+    a = rand_signs((3, 7, 5, 64), rng)
+    w = rand_signs((48, 3, 3, 64), rng)
+    thr = rng.integers(-30, 31, 48).astype(np.float32)
+    flip = rng.integers(0, 2, 48).astype(np.uint8)
+    got = oracle.bconv2d(a, w, out="bitpacked", thr=thr, flip=flip)
+    w2 = np.where(flip[:, None, None, None].astype(bool), -w, w).astype(np.int8)
+    thr2 = np.where(flip.astype(bool), 1.0 - thr, thr).astype(np.float32)
+    want = oracle.bconv2d(a, w2, out="bitpacked", thr=thr2)
+    assert np.array_equal(got, want)
