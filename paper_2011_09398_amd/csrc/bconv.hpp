@@ -660,38 +660,4 @@ __global__ __launch_bounds__(kThreads) void bconv2d_generic_kernel(BconvParams p
     epilogue<RN, OUT, PADZ>(p, acc, m, co0, bound + wave * RN, p.padc + co0, pw);
 }
 
-// The zero-padding table of one filter tensor:
-//   table[(y*NI + I)*Cout + co] = sum over ky < y, kx in I of S(co, ky, kx),
-//   S(co, ky, kx) = C_in - 2*popcount(W[co][ky][kx][:])  (the sum of the tap's
-//   +-1 weights; pad bits are 0 and count nothing),
-// for y in [0, KH] and the NI = KW(KW+1)/2 column intervals I = [x0, x1).
-// One thread per filter; a filter tensor needs it once.
-__device__ inline int tap_sum(const uint32_t *w, int co, int ky, int kx, int kh, int kw, int cw,
-                              int cin) {
-    const uint32_t *wt = w + (((size_t)co * kh + ky) * kw + kx) * cw;
-    int pc = 0;
-    for (int j = 0; j < cw; ++j) pc += __builtin_popcount(wt[j]);
-    return cin - 2 * pc;
-}
-
-__global__ __launch_bounds__(256) void pad_table_kernel(const uint32_t *__restrict__ w,
-                                                        int32_t *__restrict__ table, int cout,
-                                                        int kh, int kw, int cw, int cin) {
-    const int co = blockIdx.x * blockDim.x + threadIdx.x;
-    if (co >= cout) return;
-    const size_t ni = (size_t)interval_count(kw);
-    for (size_t i = 0; i < ni; ++i) table[i * cout + co] = 0;        // y = 0
-    for (int y = 1; y <= kh; ++y) {
-        for (int x0 = 0; x0 < kw; ++x0) {
-            int run = 0;
-            for (int x1 = x0 + 1; x1 <= kw; ++x1) {
-                run += tap_sum(w, co, y - 1, x1 - 1, kh, kw, cw, cin);
-                const size_t i = (size_t)interval_index(x0, x1, kw);
-                table[((size_t)y * ni + i) * cout + co] =
-                    table[((size_t)(y - 1) * ni + i) * cout + co] + run;
-            }
-        }
-    }
-}
-
 }  // namespace lce

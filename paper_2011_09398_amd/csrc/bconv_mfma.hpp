@@ -76,6 +76,8 @@ struct MfmaParams {
     int32_t lo, hi, m;
     int32_t tile_rows;               // stacked padded rows staged per workgroup
     int32_t fs_pixels;               // output pixels per workgroup (filter-stationary)
+    int32_t fs_thr_off;              // filter-stationary: float offset of the bounds in LDS
+                                     // from the end of the A tile
     int32_t pad_zero;                // 1: padded locations are 0.0
     int32_t region_vec;              // words per DMA lane when staging the region: 4 or 1
     FastDiv div_ohw, div_ow, div_ph, div_pw;
@@ -83,10 +85,11 @@ struct MfmaParams {
     FastDiv div_cwh, div_kw;         // cwe / 2 (word pairs per tap), kw
     FastDiv div_groups;              // region_vec-word groups per location
     FastDiv div_ks_gx;               // K-split schedule: pixel tiles (grid x)
-    // filter-stationary schedule: A-tile offset (in 16-byte words) of K step
+    // filter-stationary schedules: A-tile offset (in 16-byte words) of K step
     // s = (tap t = ky*KW + kx, word pair q) from a pixel's window origin,
-    // 2q*plane + ky*PW + kx (plane = tile_rows*pw); steps past the last
-    // repeat the last one
+    // 2q*plane + ky*PW + kx (plane = tile_rows*pw), in bits 0-23, and the
+    // number of real channels in the step's word pair, min(64, C_in - 64q),
+    // in bits 24-31; steps past the last repeat the last one
     int32_t fs_koff[kFsMaxSteps];
 };
 
@@ -548,8 +551,11 @@ __device__ __forceinline__ void dma_region(const MfmaParams &p, uint32_t *abits,
             const int yy = R - img * p.ph - p.pt, xx = c - p.pl;
             const bool inside = img < p.n && (unsigned)yy < (unsigned)p.h &&
                                 (unsigned)xx < (unsigned)p.w;
+            // (the input holds fewer than 2^31 words: 32-bit offsets)
             const uint32_t *src =
-                inside ? p.x + (((size_t)img * p.h + yy) * p.w + xx) * p.cw + g * V : g_mfma_zero;
+                inside ? p.x + (((uint32_t)img * (uint32_t)p.h + (uint32_t)yy) * (uint32_t)p.w +
+                                (uint32_t)xx) * (uint32_t)p.cw + (uint32_t)(g * V)
+                       : g_mfma_zero;
             if constexpr (V == 4)
                 __builtin_amdgcn_global_load_lds((mfma_global_void *)src,
                                                  (mfma_lds_void *)(abits + u * 64 * V), 16, 0, 0);
@@ -995,7 +1001,7 @@ __global__ __launch_bounds__(kMfmaThreads) void bconv2d_mfma_fs_kernel(MfmaParam
                 bpk[i] = p.wpk[col + (size_t)(2 * s) * p.coutp];
             else
                 breg[i] = p.wexp[col + (size_t)(2 * s) * p.coutp];
-            aoff[i] = p.fs_koff[sk * KS + i] + hp;       // (word 2q + half)
+            aoff[i] = (p.fs_koff[sk * KS + i] & 0xFFFFFF) + hp;   // (word 2q + half)
         }
     }
 
@@ -1009,11 +1015,37 @@ __global__ __launch_bounds__(kMfmaThreads) void bconv2d_mfma_fs_kernel(MfmaParam
     // sign bits of a flipped filter (in the widened or the packed form),
     // applied to each step's filters as they arrive (first pair)
     const uint32_t neg = OUT == OUT_BITS && flipped ? (PK ? ~0u : kFp4SignBits) : 0u;
+    // bitpacked output: the bounds of the workgroup's F filter blocks go to
+    // LDS after the exchange area (one copy per filter block)
+    float *thrs = reinterpret_cast<float *>(smem + p.cwe * plane) + p.fs_thr_off;
     if constexpr (OUT == OUT_BITS) {
         ep_a = co_ok ? thr_to_dot_bound_f(ep_a, p.lo, p.hi) : -INFINITY;
         if (flipped) ep_a = 1.0f - ep_a;
+        if (sk == 0 && half == 0) thrs[fblk * 32 + l32] = ep_a;
     }
     z = lds_barrier();                                   // the A tile is complete (abits is free)
+
+    // Bitpacked output: the products are transposed (filters as the row
+    // operand, pixels as the column operand: lane = pixel of the block, value
+    // v = filter (v/4)*8 + half*4 + v%4), and each accumulator a wave
+    // finishes starts at -bound instead of 0, so that the finished value is
+    // dot - bound and the output bit its sign: two ALU operations per bit
+    // and no lane writes.  With S > 1 only the wave that finishes a block
+    // starts it at -bound.
+    mfma_v16f tinit[2];
+    if constexpr (OUT == OUT_BITS) {
+#pragma unroll
+        for (int q = 0; q < 4; ++q) {
+            const float4 t =
+                reinterpret_cast<const float4 *>(thrs)[(fblk * 32 + q * 8 + half * 4 + z) >> 2];
+            const float tv[4] = {t.x, t.y, t.z, t.w};
+#pragma unroll
+            for (int e = 0; e < 4; ++e)
+#pragma unroll
+                for (int b = 0; b < 2; ++b)
+                    tinit[b][4 * q + e] = S == 1 || b == sk ? -tv[e] : 0.0f;
+        }
+    }
 
     // A-tile offset of the window origin of pixel block b's 32 pixels
     auto block_base = [&](int b) __attribute__((always_inline)) {
@@ -1092,12 +1124,32 @@ __global__ __launch_bounds__(kMfmaThreads) void bconv2d_mfma_fs_kernel(MfmaParam
     // filters past C_out' are computed and not stored.  Bitpacked output
     // finishes a value in two parts, the compare (finish_cmp) and, a K step
     // later in the pipeline, the lane writes and the store (finish_write).
-    uint64_t mk[NV];
     auto finish_cmp = [&](auto nc) __attribute__((always_inline)) {
         constexpr int N = decltype(nc)::value;
         constexpr int j = N / 16, v = N % 16;
         if constexpr (OUT == OUT_BITS) {
-            mk[N] = __ballot(fin[j][v] < ep_a);
+            // the bit of value v (dot - bound) is its sign, at bit
+            // (v/4)*8 + v%4 of the lane's word; after the last value the
+            // word moves to its lane half (shift by 4*half) and the two
+            // halves of the pixel (lanes l and l + 32) are merged.  Then
+            // lane < 32 stores block 0's word of pixel lane, lane >= 32 block
+            // 1's (S = 1); with S > 1 lanes < 32 store the wave's block.
+            constexpr int pos = (v >> 2) * 8 + (v & 3);
+            const uint32_t bit = (__float_as_uint(fin[j][v]) >> (31 - pos)) & (1u << pos);
+            uint32_t w = v == 0 ? bit : word[j][0] | bit;
+            if constexpr (v == 15) {
+                w <<= 4 * half;
+                const auto sw = __builtin_amdgcn_permlane32_swap(w, w, false, false);
+                w = w | sw[0] | sw[1];
+            }
+            word[j][0] = w;
+            if constexpr (v == 15 && j == NFB - 1) {
+                const int blk = S == 1 ? half : sk;      // block of the pair
+                const uint32_t out_word = NFB == 2 && half ? word[NFB - 1][0] : word[0][0];
+                const int m = m0 + (fin_b0 + blk) * 32 + l32;
+                if (fvalid && blk < fin_nbp && (S == 1 || lane < 32) && m < m_end)
+                    reinterpret_cast<uint32_t *>(p.out)[(size_t)m * p.cwo + (f0 >> 5)] = out_word;
+            }
         } else {
             const int blk = S == 1 ? j : sk;             // block of the pair
             const bool store = fvalid && blk < fin_nbp;
@@ -1113,22 +1165,9 @@ __global__ __launch_bounds__(kMfmaThreads) void bconv2d_mfma_fs_kernel(MfmaParam
             }
         }
     };
-    auto finish_write = [&](auto nc) __attribute__((always_inline)) {
-        constexpr int N = decltype(nc)::value;
-        constexpr int j = N / 16, v = N % 16;
-        if constexpr (OUT == OUT_BITS) {
-            const int blk = S == 1 ? j : sk;             // block of the pair
-            const bool store = fvalid && blk < fin_nbp;
-            if (v < 2) word[j][v] = 0u;
-            write_value_bits<v>(mk[N], word[j][v & 1]);
-            if (v == 15) {
-                const int m = m0 + (fin_b0 + blk) * 32 + lane;
-                if (store && lane < 32 && m < m_end)
-                    reinterpret_cast<uint32_t *>(p.out)[(size_t)m * p.cwo + (f0 >> 5)] =
-                        word[j][0] | word[j][1];
-            }
-        }
-    };
+    // (the second part of a value, a K step after the first: nothing is left
+    // for it since the bitpacked output needs no lane writes)
+    auto finish_write = [&](auto nc) __attribute__((always_inline)) { (void)nc; };
     // values [LO, HI) of the finishing order, either part
     auto finish_range = [&](auto fn, auto loc, auto hic) __attribute__((always_inline)) {
         constexpr int LO = decltype(loc)::value, HI = decltype(hic)::value;
@@ -1204,7 +1243,10 @@ __global__ __launch_bounds__(kMfmaThreads) void bconv2d_mfma_fs_kernel(MfmaParam
             constexpr int phi = plo + kPer < NV ? plo + kPer : NV;
 #pragma unroll
             for (int j = 0; j < NBP; ++j) {
-                acc[j] = mfma_fp4(ring[i % D][j], breg[i], i == 0 ? zero16 : acc[j]);
+                if constexpr (OUT == OUT_BITS)
+                    acc[j] = mfma_fp4(breg[i], ring[i % D][j], i == 0 ? tinit[j] : acc[j]);
+                else
+                    acc[j] = mfma_fp4(ring[i % D][j], breg[i], i == 0 ? zero16 : acc[j]);
                 // pin the product here (it touches no memory and would move)
                 asm volatile("" : "+a"(acc[j]) : : "memory");
                 if constexpr (has_prev) {
@@ -1254,39 +1296,6 @@ __global__ __launch_bounds__(kMfmaThreads) void bconv2d_mfma_fs_kernel(MfmaParam
     } else if (nb & 1) {
         body(one, no, nb - 1);
         finish_all(1);
-    }
-}
-
-// Filters widened once per filter tensor into the B layout:
-//   wexp[(t*CwE + j)*CoutP + co] = 32 e2m1 codes of word j of tap t of
-//   filter co, in the order of widen_word (channel c of the word in 32-bit
-//   word c % 4, nibble c / 4); channels past C_in, words past Cw and filters
-//   past Cout are 0.0 (they then add nothing to any dot);
-//   wpk[same index] = the packed word itself (bits of channels past C_in
-//   cleared; words past Cw and filters past Cout 0), for kernels that
-//   widen the filters themselves where every channel is valid.
-__global__ __launch_bounds__(256) void mfma_expand_weights_kernel(const uint32_t *__restrict__ w,
-                                                                  u32x4 *__restrict__ wexp,
-                                                                  uint32_t *__restrict__ wpk,
-                                                                  int cout, int coutp, int taps,
-                                                                  int cw, int cwe, int cin) {
-    const int64_t total = (int64_t)taps * cwe * coutp;
-    for (int64_t idx = (int64_t)blockIdx.x * 256 + threadIdx.x; idx < total;
-         idx += (int64_t)gridDim.x * 256) {
-        const int64_t k = idx / coutp;
-        const int co = (int)(idx - k * coutp);
-        const int t = (int)(k / cwe), j = (int)(k - (int64_t)t * cwe);
-        u32x4 o = {0u, 0u, 0u, 0u};
-        uint32_t packed = 0u;
-        if (co < cout && j < cw) {
-            const uint32_t bits = w[((size_t)co * taps + t) * cw + j];
-            const int nvalid = min(32, cin - 32 * j);
-            const uint32_t valid = nvalid >= 32 ? 0xFFFFFFFFu : (1u << nvalid) - 1u;
-            o = widen_word(bits, kFp4PlusOne) & widen_valid_mask(valid);
-            packed = bits & valid;
-        }
-        wexp[idx] = o;
-        wpk[idx] = packed;
     }
 }
 

@@ -19,6 +19,79 @@
 #include "bconv.hpp"
 #include "pool.hpp"
 #include "bconv_mfma.hpp"
+#include "launch.hpp"
+
+// Kernels that run once per filter tensor (not on the timed path).
+namespace lce {
+
+// The zero-padding table of one filter tensor:
+//   table[(y*NI + I)*Cout + co] = sum over ky < y, kx in I of S(co, ky, kx),
+//   S(co, ky, kx) = C_in - 2*popcount(W[co][ky][kx][:])  (the sum of the tap's
+//   +-1 weights; pad bits are 0 and count nothing),
+// for y in [0, KH] and the NI = KW(KW+1)/2 column intervals I = [x0, x1).
+// One thread per filter; a filter tensor needs it once.
+__device__ inline int tap_sum(const uint32_t *w, int co, int ky, int kx, int kh, int kw, int cw,
+                              int cin) {
+    const uint32_t *wt = w + (((size_t)co * kh + ky) * kw + kx) * cw;
+    int pc = 0;
+    for (int j = 0; j < cw; ++j) pc += __builtin_popcount(wt[j]);
+    return cin - 2 * pc;
+}
+
+__global__ __launch_bounds__(256) void pad_table_kernel(const uint32_t *__restrict__ w,
+                                                        int32_t *__restrict__ table, int cout,
+                                                        int kh, int kw, int cw, int cin) {
+    const int co = blockIdx.x * blockDim.x + threadIdx.x;
+    if (co >= cout) return;
+    const size_t ni = (size_t)interval_count(kw);
+    for (size_t i = 0; i < ni; ++i) table[i * cout + co] = 0;        // y = 0
+    for (int y = 1; y <= kh; ++y) {
+        for (int x0 = 0; x0 < kw; ++x0) {
+            int run = 0;
+            for (int x1 = x0 + 1; x1 <= kw; ++x1) {
+                run += tap_sum(w, co, y - 1, x1 - 1, kh, kw, cw, cin);
+                const size_t i = (size_t)interval_index(x0, x1, kw);
+                table[((size_t)y * ni + i) * cout + co] =
+                    table[((size_t)(y - 1) * ni + i) * cout + co] + run;
+            }
+        }
+    }
+}
+
+// Filters widened once per filter tensor into the B layout:
+//   wexp[(t*CwE + j)*CoutP + co] = 32 e2m1 codes of word j of tap t of
+//   filter co, in the order of widen_word (channel c of the word in 32-bit
+//   word c % 4, nibble c / 4); channels past C_in, words past Cw and filters
+//   past Cout are 0.0 (they then add nothing to any dot);
+//   wpk[same index] = the packed word itself (bits of channels past C_in
+//   cleared; words past Cw and filters past Cout 0), for kernels that
+//   widen the filters themselves where every channel is valid.
+__global__ __launch_bounds__(256) void mfma_expand_weights_kernel(const uint32_t *__restrict__ w,
+                                                                  u32x4 *__restrict__ wexp,
+                                                                  uint32_t *__restrict__ wpk,
+                                                                  int cout, int coutp, int taps,
+                                                                  int cw, int cwe, int cin) {
+    const int64_t total = (int64_t)taps * cwe * coutp;
+    for (int64_t idx = (int64_t)blockIdx.x * 256 + threadIdx.x; idx < total;
+         idx += (int64_t)gridDim.x * 256) {
+        const int64_t k = idx / coutp;
+        const int co = (int)(idx - k * coutp);
+        const int t = (int)(k / cwe), j = (int)(k - (int64_t)t * cwe);
+        u32x4 o = {0u, 0u, 0u, 0u};
+        uint32_t packed = 0u;
+        if (co < cout && j < cw) {
+            const uint32_t bits = w[((size_t)co * taps + t) * cw + j];
+            const int nvalid = min(32, cin - 32 * j);
+            const uint32_t valid = nvalid >= 32 ? 0xFFFFFFFFu : (1u << nvalid) - 1u;
+            o = widen_word(bits, kFp4PlusOne) & widen_valid_mask(valid);
+            packed = bits & valid;
+        }
+        wexp[idx] = o;
+        wpk[idx] = packed;
+    }
+}
+
+}  // namespace lce
 
 namespace {
 
@@ -361,48 +434,17 @@ int mfma_tile_rows(const lce::MfmaParams &p, int bm) {
     return (int)best;
 }
 
-template <int CC, int OUT, int MB>
-void launch_mfma_mb(const lce::MfmaParams &p, int nblk, dim3 grid, size_t lds, hipStream_t s) {
-    const dim3 block(lce::kMfmaThreads);
-    if (nblk == 4)
-        hipLaunchKernelGGL((lce::bconv2d_mfma_kernel<CC, OUT, 4, MB>), grid, block, lds, s, p);
-    else if (nblk == 2)
-        hipLaunchKernelGGL((lce::bconv2d_mfma_kernel<CC, OUT, 2, MB>), grid, block, lds, s, p);
-    else
-        hipLaunchKernelGGL((lce::bconv2d_mfma_kernel<CC, OUT, 1, MB>), grid, block, lds, s, p);
-}
-
-template <int CC, int OUT>
-void launch_mfma(const lce::MfmaParams &p, int nblk, int mb, dim3 grid, size_t lds,
-                 hipStream_t s) {
-    if (mb == 2)
-        launch_mfma_mb<CC, OUT, 2>(p, nblk, grid, lds, s);
-    else
-        launch_mfma_mb<CC, OUT, 1>(p, nblk, grid, lds, s);
-}
-
-// (tiles of at most eight 32x32 blocks: MBW = 4 takes NBLK <= 2)
-template <int OUT, int MBW>
-void launch_mfma_ks_mb(const lce::MfmaParams &p, int nblk, dim3 grid, size_t lds, hipStream_t s) {
-    const dim3 block(lce::kMfmaThreads);
-    constexpr int kWide = MBW == 4 ? 2 : 4;
-    if (nblk == 4)
-        hipLaunchKernelGGL((lce::bconv2d_mfma_ks_kernel<OUT, kWide, MBW>), grid, block, lds, s, p);
-    else if (nblk == 2)
-        hipLaunchKernelGGL((lce::bconv2d_mfma_ks_kernel<OUT, 2, MBW>), grid, block, lds, s, p);
-    else
-        hipLaunchKernelGGL((lce::bconv2d_mfma_ks_kernel<OUT, 1, MBW>), grid, block, lds, s, p);
-}
-
-template <int OUT>
-void launch_mfma_ks(const lce::MfmaParams &p, int nblk, int mbw, dim3 grid, size_t lds,
-                    hipStream_t s) {
-    if (mbw == 4)
-        launch_mfma_ks_mb<OUT, 4>(p, nblk, grid, lds, s);
-    else if (mbw == 2)
-        launch_mfma_ks_mb<OUT, 2>(p, nblk, grid, lds, s);
-    else
-        launch_mfma_ks_mb<OUT, 1>(p, nblk, grid, lds, s);
+// The filter-stationary step table: A-tile offset of K step s (tap t, word
+// pair q), 2q*plane + ky*PW + kx, with the real channels of the word pair,
+// min(64, C_in - 64q), in bits 24-31; steps past the last repeat it.
+void fill_step_table(lce::MfmaParams &p, const lce_bconv2d_desc &d, int plane, int ksteps) {
+    const int cwh = p.cwe / 2;
+    for (int s = 0; s < lce::kFsMaxSteps; ++s) {
+        const int sc = std::min(s, ksteps - 1);
+        const int t = sc / cwh, q = sc % cwh;
+        const int vc = std::min(64, std::max(0, d.c_in - 64 * q));
+        p.fs_koff[s] = (2 * q * plane + (t / d.kw) * p.pw + t % d.kw) | (vc << 24);
+    }
 }
 
 // Filter-stationary instances: K steps per wave (KS) and waves sharing a
@@ -412,52 +454,23 @@ struct FsShape {
 };
 constexpr FsShape kFsShapes[] = {{9, 1}, {18, 1}, {5, 2}, {9, 2}, {18, 2}, {18, 4}};
 
-template <int KS, int S, bool PK>
-void launch_mfma_fs_pk(const lce::MfmaParams &p, int out, dim3 grid, size_t lds,
-                       hipStream_t st) {
-    const dim3 block(lce::kMfmaThreads);
-    if (out == LCE_OUT_FLOAT32)
-        hipLaunchKernelGGL((lce::bconv2d_mfma_fs_kernel<KS, S, lce::OUT_FLOAT, PK>), grid, block,
-                           lds, st, p);
-    else if (out == LCE_OUT_BITPACKED)
-        hipLaunchKernelGGL((lce::bconv2d_mfma_fs_kernel<KS, S, lce::OUT_BITS, PK>), grid, block,
-                           lds, st, p);
-    else
-        hipLaunchKernelGGL((lce::bconv2d_mfma_fs_kernel<KS, S, lce::OUT_INT, PK>), grid, block,
-                           lds, st, p);
-}
-
-template <int KS, int S>
-void launch_mfma_fs_shape(const lce::MfmaParams &p, bool pk, int out, dim3 grid, size_t lds,
-                          hipStream_t st) {
-    if (pk)
-        launch_mfma_fs_pk<KS, S, true>(p, out, grid, lds, st);
-    else
-        launch_mfma_fs_pk<KS, S, false>(p, out, grid, lds, st);
-}
-
-// pk: every channel of every packed word is valid (C_in = 32*Cw'), so the
-// kernel loads the packed copy of the filters and widens it itself
-void launch_mfma_fs(const lce::MfmaParams &p, FsShape sh, bool pk, int out, dim3 grid,
-                    size_t lds, hipStream_t st) {
-    if (sh.ks == 9 && sh.s == 1) launch_mfma_fs_shape<9, 1>(p, pk, out, grid, lds, st);
-    else if (sh.ks == 18 && sh.s == 1) launch_mfma_fs_shape<18, 1>(p, pk, out, grid, lds, st);
-    else if (sh.ks == 5 && sh.s == 2) launch_mfma_fs_shape<5, 2>(p, pk, out, grid, lds, st);
-    else if (sh.ks == 9 && sh.s == 2) launch_mfma_fs_shape<9, 2>(p, pk, out, grid, lds, st);
-    else if (sh.ks == 18 && sh.s == 2) launch_mfma_fs_shape<18, 2>(p, pk, out, grid, lds, st);
-    else launch_mfma_fs_shape<18, 4>(p, pk, out, grid, lds, st);
-}
-
 // LDS of the filter-stationary kernel: every widened word of the region,
 // then the larger of the packed region (staged before the loop, with the
 // 256-word slack of its last DMA instruction) and (S > 1) the partial-sum
 // exchange: two buffers x F filter blocks x two pixel blocks x (S-1)
-// partials, 4 KB each.
-size_t mfma_fs_lds(const lce::MfmaParams &p, FsShape sh, int tile_rows) {
-    const size_t a = (size_t)p.cwe * tile_rows * p.pw * 16;
+// partials, 4 KB each; then the bounds of the F filter blocks (bitpacked
+// output).
+// Bytes from the end of the A tile to the bounds of a bitpacked output
+// (after the larger of the packed region and the exchange, 16-byte aligned).
+size_t mfma_fs_thr_offset(const lce::MfmaParams &p, FsShape sh, int tile_rows) {
     const size_t bits = ((size_t)tile_rows * p.pw * p.cw + 256) * 4;
     const size_t red = sh.s > 1 ? (size_t)2 * (4 / sh.s) * 2 * (sh.s - 1) * 4096 : 0;
-    return a + std::max(bits, red);
+    return (std::max(bits, red) + 15) / 16 * 16;
+}
+
+size_t mfma_fs_lds(const lce::MfmaParams &p, FsShape sh, int tile_rows) {
+    const size_t a = (size_t)p.cwe * tile_rows * p.pw * 16;
+    return a + mfma_fs_thr_offset(p, sh, tile_rows) + (4 / sh.s) * 32 * 4;
 }
 
 struct FsPlan {
@@ -902,7 +915,8 @@ lce_status lce_bconv2d_mfma(const lce_bconv2d_desc *desc, const int32_t *x_packe
     // 1.5 workgroups, among those whose LDS fits.  LCE_MFMA_KS=1 / 0 force
     // either schedule (the K-split one where its LDS fits).
     const int64_t ksteps = (int64_t)d.kh * d.kw * (p.cwe / 2);
-    const int sched = tuning(LCE_TUNE_MFMA_SCHEDULE);   // 0 auto, 1 fs, 2 K split, 3 pixel split
+    // 0 auto, 1 filter-stationary, 2 K split, 3 pixel split
+    const int sched = tuning(LCE_TUNE_MFMA_SCHEDULE);
     const int ks_env = sched == 2 ? 1 : sched == 3 ? 0 : -1;
 
     // Filter-stationary schedule: the default wherever an instance fits, up
@@ -919,13 +933,9 @@ lce_status lce_bconv2d_mfma(const lce_bconv2d_desc *desc, const int32_t *x_packe
         if (fp.shape.ks) {
             p.tile_rows = fp.tile_rows;
             p.fs_pixels = fp.pixels;
+            p.fs_thr_off = (int32_t)(mfma_fs_thr_offset(p, fp.shape, fp.tile_rows) / 4);
             p.div_plane = lce::make_fastdiv((uint32_t)(fp.tile_rows * p.pw));
-            const int plane = fp.tile_rows * p.pw, cwh = p.cwe / 2;
-            for (int s = 0; s < lce::kFsMaxSteps; ++s) {
-                const int sc = std::min<int>(s, (int)ksteps - 1);
-                const int t = sc / cwh, q = sc % cwh;
-                p.fs_koff[s] = 2 * q * plane + (t / d.kw) * p.pw + t % d.kw;
-            }
+            fill_step_table(p, d, fp.tile_rows * p.pw, (int)ksteps);
             size_t lds = fp.lds;
             // claim more than 1/(wpc+1) of a CU's LDS when the grid fits the
             // CUs, so that no CU holds more than wpc workgroups while another
@@ -938,7 +948,7 @@ lce_status lce_bconv2d_mfma(const lce_bconv2d_desc *desc, const int32_t *x_packe
             const dim3 grid((unsigned)fp.groups,
                             (unsigned)((blocks32 + 4 / fp.shape.s - 1) / (4 / fp.shape.s)));
             const bool pk = d.c_in == 32 * p.cwe && tuning(LCE_TUNE_MFMA_PACKED) >= 0;
-            launch_mfma_fs(p, fp.shape, pk, d.out_type, grid, lds, stream);
+            lce::launch_mfma_fs(p, fp.shape.ks, fp.shape.s, pk, d.out_type, grid, lds, stream);
             return check_launch("lce_bconv2d_mfma launch");
         }
     }
@@ -967,11 +977,7 @@ lce_status lce_bconv2d_mfma(const lce_bconv2d_desc *desc, const int32_t *x_packe
             const dim3 grid((unsigned)(((int64_t)p.m + 32 * mbw - 1) / (32 * mbw)),
                             (unsigned)((blocks32 + knb - 1) / knb));
             p.div_ks_gx = lce::make_fastdiv(grid.x);
-            switch (d.out_type) {
-                case LCE_OUT_FLOAT32: launch_mfma_ks<lce::OUT_FLOAT>(p, knb, mbw, grid, lds, stream); break;
-                case LCE_OUT_BITPACKED: launch_mfma_ks<lce::OUT_BITS>(p, knb, mbw, grid, lds, stream); break;
-                default: launch_mfma_ks<lce::OUT_INT>(p, knb, mbw, grid, lds, stream); break;
-            }
+            lce::launch_mfma_ksplit(p, d.out_type, knb, mbw, grid, lds, stream);
             return check_launch("lce_bconv2d_mfma launch");
         }
     }
@@ -1014,14 +1020,7 @@ lce_status lce_bconv2d_mfma(const lce_bconv2d_desc *desc, const int32_t *x_packe
     if ((int64_t)p.tile_rows * p.pw * cc > INT32_MAX / 2)
         return fail(LCE_EUNSUPPORTED, "matrix-core tile too large");
     const dim3 grid((unsigned)pix_groups, (unsigned)((blocks32 + nblk - 1) / nblk));
-    switch (d.out_type * 2 + (cc == 4)) {
-        case LCE_OUT_FLOAT32 * 2 + 0: launch_mfma<2, lce::OUT_FLOAT>(p, nblk, mb, grid, lds, stream); break;
-        case LCE_OUT_FLOAT32 * 2 + 1: launch_mfma<4, lce::OUT_FLOAT>(p, nblk, mb, grid, lds, stream); break;
-        case LCE_OUT_BITPACKED * 2 + 0: launch_mfma<2, lce::OUT_BITS>(p, nblk, mb, grid, lds, stream); break;
-        case LCE_OUT_BITPACKED * 2 + 1: launch_mfma<4, lce::OUT_BITS>(p, nblk, mb, grid, lds, stream); break;
-        case LCE_OUT_INT32 * 2 + 0: launch_mfma<2, lce::OUT_INT>(p, nblk, mb, grid, lds, stream); break;
-        default: launch_mfma<4, lce::OUT_INT>(p, nblk, mb, grid, lds, stream); break;
-    }
+    lce::launch_mfma_pixel(p, d.out_type, cc, nblk, mb, grid, lds, stream);
     return check_launch("lce_bconv2d_mfma launch");
 }
 
