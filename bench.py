@@ -93,7 +93,8 @@ def parse():
                     help="skip the zero-padding and memory-bound operator lines")
     ap.add_argument("--profile-pass", action="store_true",
                     help="short run for counter collection: 512 MiB copies (the byte-counter "
-                         "calibration) then three launches of each implementation per layer")
+                         "calibration), three launches of each implementation per layer, "
+                         "then the VALU probe")
     ap.add_argument("--cpu-seconds", type=float, default=10.0,
                     help="target wall time of the CPU baseline sample")
     return ap.parse_args()
@@ -603,8 +604,9 @@ def main():
                 for _ in range(3):
                     call()
         torch.cuda.synchronize()
-        log("profile pass done: 3 copies of 512 MiB, then 3 launches of each "
-            "implementation per layer")
+        probe = valu_probe()   # 5 warmup + 5 timed launches of the xor+popcount probe
+        log("profile pass done: 3 copies of 512 MiB, 3 launches of each implementation "
+            f"per layer, 10 launches of the VALU probe ({probe:.1f} binary TOP/s)")
         return
     log(f"choosing the convolution implementation per layer ({args.kernel})")
     step.choose(args.kernel, max(args.reps // 2, 20))
