@@ -15,9 +15,10 @@ Measured on the launch stream with HIP events:
     wall clock around it, synchronized on both sides) -> value, ms_per_step;
   * per launch: each layer launched R times back to back between two events
     -> average launch duration, the figure the roofline uses;
-  * batch-1 layers (float input: lce_bitpack timed as its own line) the same
-    way, but from a captured HIP graph of the R launches, since eager launch
-    cost exceeds their run time;
+  * batch-1 layers (float input: lce_bitpack timed as its own line, and each
+    whole layer as bitpack + either conv, or as one quantize-fused launch)
+    the same way, but from a captured HIP graph of the R launches, since
+    eager launch cost exceeds their run time;
   * a probe of the achievable xor+popcount VALU rate, next to the spec peak;
   * the same layers with zero padding (the correction-step variant);
   * the memory-bound operators at sizes beyond the 256 MB last-level cache,
@@ -66,7 +67,8 @@ PEAK_BINARY_TOPS = VALU_LANE_OPS * BINARY_OPS_PER_LANE_OP / 1e12      # 1258.3
 PEAK_FP4_TFLOPS = 10100.0
 # The arithmetic each implementation computes in (the bench line's dtype).
 DTYPES = {"xor": "u32 xor+popcount (VALU), int32 accumulate",
-          "mfma": "fp4 e2m1 MFMA, fp32 accumulate (integer-exact dot)"}
+          "mfma": "fp4 e2m1 MFMA, fp32 accumulate (integer-exact dot)",
+          "fused": "fp32 sign test + u32 xor+popcount (VALU), int32 accumulate"}
 HBM_PEAK_GBS = 8000.0
 
 
@@ -118,7 +120,7 @@ class Step:
         self.layers = config(cfg_idx)
         self.inputs = [make_layer_inputs(l, 0, cfg_idx, i) for i, l in enumerate(self.layers)]
         dev = lambda a: torch.from_numpy(np.ascontiguousarray(a)).cuda()
-        self.xor_calls, self.mfma_calls = [], []
+        self.xor_calls, self.mfma_calls, self.fused_calls = [], [], []
         self.packs, self.outs, self.keep = [], [], []
         for i, (layer, inp) in enumerate(zip(self.layers, self.inputs)):
             w_packed = lce.bitpack(dev(inp.w_float))          # 1-bit weight storage
@@ -151,6 +153,16 @@ class Step:
                 out_type=layer.out, **kw)
             m.keep = m.keep + (w_fp4,)
             self.mfma_calls.append(m)
+            fused = None
+            if pack is not None:      # float input: the quantize-fused launch, where covered
+                try:
+                    fused = lce.PreparedQuantBConv2d(
+                        xf, w_packed, out, stride=layer.strides, padding=layer.padding,
+                        clamp=layer.clamp, out_type=layer.out, **kw)
+                except lce.LceError as e:
+                    if e.status != lce.LCE_EUNSUPPORTED:
+                        raise
+            self.fused_calls.append(fused)
             self.packs.append(pack)
             self.outs.append(out)
             self.keep.append((w_packed, x_packed, kw))
@@ -158,24 +170,42 @@ class Step:
         self.kinds = ["xor"] * len(self.calls)
         self.times = [None] * len(self.calls)
 
+    def layer_call(self, i, kind):
+        """Layer i as one callable: bitpack (float input) then the named
+        convolution, or the quantize-fused launch."""
+        if kind == "fused":
+            return self.fused_calls[i]
+        conv = self.mfma_calls[i] if kind == "mfma" else self.xor_calls[i]
+        pack = self.packs[i]
+        if pack is None:
+            return conv
+
+        def both():
+            pack()
+            conv()
+        return both
+
     def choose(self, mode: str, reps: int, graph: bool = False):
-        """Time both implementations of every layer; keep the faster (auto)
-        or the named one for the step.  graph: time from captured graphs
-        (layers shorter than an eager launch)."""
+        """Time the implementations of every layer and keep the fastest (auto)
+        or the named one for the step: bitpack (float input) + XOR/POPCOUNT
+        conv, bitpack + matrix-core conv, or the quantize-fused launch.
+        graph: time from captured graphs (layers shorter than an eager
+        launch).  times[i] = (xor, mfma[, fused]) whole-layer ms."""
         self.times = []
-        for i, (x, m) in enumerate(zip(self.xor_calls, self.mfma_calls)):
-            tx = time_repeated(x, reps, graph=graph)
-            tm = time_repeated(m, reps, graph=graph)
-            self.times.append((tx, tm))
-            kind = mode if mode != "auto" else ("mfma" if tm < tx else "xor")
+        for i in range(len(self.layers)):
+            kinds = ["xor", "mfma"] + (["fused"] if self.fused_calls[i] is not None else [])
+            t = [time_repeated(self.layer_call(i, k), reps, graph=graph) for k in kinds]
+            self.times.append(tuple(t))
+            kind = mode if mode != "auto" else kinds[min(range(len(t)), key=t.__getitem__)]
+            if kind == "fused" and self.fused_calls[i] is None:
+                kind = "xor"
             self.kinds[i] = kind
-            self.calls[i] = m if kind == "mfma" else x
+            self.calls[i] = self.layer_call(i, kind)
 
     def run(self):
-        """One pass of the hot path: bitpack any float input, then every conv."""
-        for pack, call in zip(self.packs, self.calls):
-            if pack is not None:
-                pack()
+        """One pass of the hot path: every layer (bitpack of a float input
+        included) with its chosen implementation."""
+        for call in self.calls:
             call()
 
 
@@ -251,13 +281,18 @@ def time_repeated(fn, reps: int, graph: bool) -> float:
 
 
 def layer_record(layer, ms, probe_tops=None, kind="xor", times=None):
-    """One convolution launch: binary GOPS against the roofline of the unit
-    that ran it (VALU xor+popcount, or dense fp4 MFMA)."""
+    """One layer's launch(es): binary GOPS against the roofline of the unit
+    that ran it (VALU xor+popcount, or dense fp4 MFMA; "fused" is the
+    XOR+POPCOUNT kernel binarizing its float input itself).  For a float
+    input, `us` covers the whole layer: bitpack + conv, or the fused launch.
+    times: the (xor, mfma[, fused]) timings the choice was made from."""
     ops = layer.binary_ops
     tops = ops / (ms * 1e-3) / 1e12
     r = {"layer": layer.name, "batch": layer.n, "kernel": kind, "us": round(ms * 1e3, 3),
          "binary_gops": round(tops * 1e3, 1), "binary_ops": ops}
-    if kind == "xor":
+    if layer.input_kind == "float" and layer.chained_from is None:
+        r["input"] = "float32, binarized in the timed launches"
+    if kind in ("xor", "fused"):
         r["valu_frac"] = round(tops / PEAK_BINARY_TOPS, 4)
         if probe_tops:
             r["probe_frac"] = round(tops / probe_tops, 4)
@@ -265,6 +300,8 @@ def layer_record(layer, ms, probe_tops=None, kind="xor", times=None):
         r["mfma_fp4_frac"] = round(tops / PEAK_FP4_TFLOPS, 4)
     if times is not None:
         r["us_xor"], r["us_mfma"] = round(times[0] * 1e3, 3), round(times[1] * 1e3, 3)
+        if len(times) > 2:
+            r["us_fused"] = round(times[2] * 1e3, 3)
     return r
 
 
@@ -386,20 +423,26 @@ def sweep_lines(args, probe=None):
 
 
 def batch1_lines(args, probe=None):
-    """Configurations 1, 2 and 3 (batch 1, float input bitpacked on the
-    device first): per layer, bitpack and both convolution kernels, each
-    from a captured graph of R launches."""
+    """Configurations 1, 2 and 3 (batch 1, float input), each timing from a
+    captured graph of R launches: per layer, bitpack alone, each convolution
+    kernel alone, and the whole layer three ways (bitpack + XOR/POPCOUNT
+    conv, bitpack + matrix-core conv, the quantize-fused launch); the layer
+    line reports the fastest whole layer."""
     out = []
     for cfg in (1, 2, 3):
         s = Step(cfg)
-        for pack, x, m, layer in zip(s.packs, s.xor_calls, s.mfma_calls, s.layers):
+        for i, (pack, x, m, layer) in enumerate(zip(s.packs, s.xor_calls, s.mfma_calls,
+                                                    s.layers)):
             r = bitpack_record(layer, time_repeated(pack, args.reps, graph=True))
             r["config"] = cfg
             out.append(r)
-            tx = time_repeated(x, args.reps, graph=True)
-            tm = time_repeated(m, args.reps, graph=True)
-            kind = args.kernel if args.kernel != "auto" else ("mfma" if tm < tx else "xor")
-            r = layer_record(layer, tm if kind == "mfma" else tx, probe, kind, (tx, tm))
+            kinds = ["xor", "mfma"] + (["fused"] if s.fused_calls[i] is not None else [])
+            whole = [time_repeated(s.layer_call(i, k), args.reps, graph=True) for k in kinds]
+            best = min(range(len(kinds)), key=whole.__getitem__)
+            kind = args.kernel if args.kernel != "auto" else kinds[best]
+            r = layer_record(layer, whole[kinds.index(kind)], probe, kind, tuple(whole))
+            r["us_conv_xor"] = round(time_repeated(x, args.reps, graph=True) * 1e3, 3)
+            r["us_conv_mfma"] = round(time_repeated(m, args.reps, graph=True) * 1e3, 3)
             r["config"] = cfg
             out.append(r)
     return out
@@ -421,6 +464,7 @@ def stack_lines(args, probe=None):
                                               s5.times):
         if pack is not None:
             layers.append(bitpack_record(layer, time_repeated(pack, args.reps, graph=True)))
+        # a float-input layer's line covers bitpack + conv, or the fused launch
         layers.append(layer_record(layer, time_repeated(call, args.reps, graph=True), probe,
                                    kind, times))
     rec = {"workload": "stack16: " + __import__("workloads").CONFIG_NAMES[5],
@@ -625,7 +669,7 @@ def main():
     layers = []
     for pack, call, layer, kind, times in zip(step.packs, step.calls, step.layers, step.kinds,
                                               step.times):
-        if pack is not None:
+        if pack is not None:   # the layer's line below covers bitpack + conv
             layers.append(bitpack_record(layer, time_repeated(pack, args.reps, graph=False)))
         layers.append(layer_record(layer, time_repeated(call, args.reps, graph=False), probe,
                                    kind, times))
@@ -698,11 +742,12 @@ def main():
 def roofline_record(rec, kind, cfg_idx, probe):
     """The roofline object of one launch record: binary ops per launch over
     its average duration, against the peak of the unit that ran it."""
-    if kind == "xor":
+    if kind in ("xor", "fused"):
         r = {"bound": "alu", "achieved": round(rec["binary_gops"] / 1e3, 2),
              "peak": round(PEAK_BINARY_TOPS, 1), "unit": "TOP/s", "frac": rec["valu_frac"],
              "traffic": measured_traffic(rec["layer"], "xor") if cfg_idx == 4 else None,
-             "kernel": f"bconv2d (xor+popcount, VALU) {rec['layer']} (batch {rec['batch']})",
+             "kernel": f"bconv2d{' (quantize-fused)' if kind == 'fused' else ''} "
+                       f"(xor+popcount, VALU) {rec['layer']} (batch {rec['batch']})",
              "probe_peak": None if probe is None else round(probe, 1),
              "probe_frac": rec.get("probe_frac")}
     else:

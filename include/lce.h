@@ -137,6 +137,30 @@ lce_status lce_bconv2d(const lce_bconv2d_desc *desc,
                        const float *thresholds, const int32_t *flip,
                        const int32_t *pad_correction, void *out, hipStream_t stream);
 
+/* LceQuantize followed by the LceBConv2d that consumes it, in one launch
+ * (Section 3.2: the float activation is sign-binarized and bitpacked, then
+ * convolved).  The result equals lce_bitpack of x followed by lce_bconv2d
+ * on the packed tensor, bit for bit, with no packed copy written to memory:
+ * each workgroup binarizes the input rows its own windows read.  That work
+ * is repeated by every filter group, so this pays at small batches, where
+ * a separate lce_bitpack launch costs more than it.
+ *   x          float32 [N][H][W][C_in]  (device, 16-byte aligned); the sign
+ *              test is lce_bitpack's (x < 0.0f is a 1 bit = -1.0, so -0.0
+ *              and NaN give +1.0)
+ *   w_packed, multiplier, bias, thresholds, flip, out: as lce_bconv2d
+ * Covered: C_in a multiple of 32, 3x3 filters over 32 to 192, 256 or 512
+ * channels and 5x5 over 32 to 192 or 256, one padding (or a geometry with
+ * no padded taps), and an input band (the input rows that the windows of
+ * 64 consecutive output pixels read) that fits the LDS of a workgroup.
+ * Other requests return LCE_EUNSUPPORTED before anything is launched, and
+ * the caller runs lce_bitpack and lce_bconv2d instead.
+ * Errors: as lce_bconv2d, plus LCE_EUNSUPPORTED (above) and LCE_EALIGN for
+ *         an x that is not 16-byte aligned. */
+lce_status lce_quantize_bconv2d(const lce_bconv2d_desc *desc, const float *x,
+                                const int32_t *w_packed, const float *multiplier,
+                                const float *bias, const float *thresholds,
+                                const int32_t *flip, void *out, hipStream_t stream);
+
 /* Number of int32 elements of the zero-padding correction table of `desc`:
  * (KH+1) * KW*(KW+1)/2 * C_out.  Validates the descriptor as lce_bconv2d
  * does.

@@ -6,6 +6,7 @@ If the library is not built this module raises; there is no CPU fallback.
 
     bitpack(x)                        LceQuantize: float [..., C] -> int32 [..., ceil(C/32)]
     bconv2d(x_packed, w_packed, c_in) LceBConv2d with the fused output transform
+    quantize_bconv2d(x, w_packed)     LceQuantize + LceBConv2d in one launch (float input)
     pad_correction(w_packed, c_in)    zero-padding correction table of a filter tensor
     fold_thresholds(m, b, k, clamp)   float transform + binarization -> thresholds, flip
     mfma_weights(w_packed, c_in)      filters widened to 4-bit +-1.0 for the matrix-core path
@@ -35,7 +36,8 @@ EXPORTS = ("lce_packed_words", "lce_bconv2d_out_shape", "lce_bitpack", "lce_bcon
            "lce_bconv2d_pad_correction_size", "lce_bconv2d_pad_correction",
            "lce_fold_thresholds", "lce_bmaxpool2d_out_shape", "lce_bmaxpool2d",
            "lce_dequantize", "lce_bconv2d_mfma_weights_size", "lce_bconv2d_mfma_weights",
-           "lce_bconv2d_mfma", "lce_set_tuning", "lce_get_tuning", "lce_last_error")
+           "lce_bconv2d_mfma", "lce_quantize_bconv2d", "lce_set_tuning", "lce_get_tuning",
+           "lce_last_error")
 
 # lce_tuning_key values, by the names tuning() takes.
 TUNING_KEYS = {"xor_nb": 0, "xor_ks": 1, "mfma_schedule": 2, "mfma_fs_ks": 3, "mfma_fs_s": 4,
@@ -103,6 +105,8 @@ def lib() -> ctypes.CDLL:
         L.lce_bconv2d_mfma_weights.restype = ctypes.c_int
         L.lce_bconv2d_mfma.argtypes = [ctypes.POINTER(Desc), vp, vp, vp, vp, vp, vp, vp, vp]
         L.lce_bconv2d_mfma.restype = ctypes.c_int
+        L.lce_quantize_bconv2d.argtypes = [ctypes.POINTER(Desc), vp, vp, vp, vp, vp, vp, vp, vp]
+        L.lce_quantize_bconv2d.restype = ctypes.c_int
         L.lce_set_tuning.argtypes = [i32, i32]
         L.lce_set_tuning.restype = ctypes.c_int
         L.lce_get_tuning.argtypes = [i32]
@@ -264,6 +268,39 @@ def fold_thresholds(multiplier, bias, c_out: int, k: int,
     return thr, flip
 
 
+def _epilogue_args(cout, kh, kw, multiplier, bias, thresholds, flip, pad_correction=None):
+    """Check the optional per-channel tensors of a convolution; their pointers."""
+    import torch
+    ptrs = []
+    for t, name, dtype, numel in ((multiplier, "multiplier", torch.float32, cout),
+                                  (bias, "bias", torch.float32, cout),
+                                  (thresholds, "thresholds", torch.float32, cout),
+                                  (flip, "flip", torch.int32, packed_words(cout)),
+                                  (pad_correction, "pad_correction", torch.int32,
+                                   (kh + 1) * (kw * (kw + 1) // 2) * cout)):
+        if t is None:
+            ptrs.append(None)
+        else:
+            _require(t, dtype, name)
+            if t.numel() != numel:
+                raise ValueError(f"{name} must have {numel} elements")
+            ptrs.append(t.data_ptr())
+    return ptrs
+
+
+def _conv_out(out, out_type, n, oh, ow, cout, device):
+    """Check a caller's output tensor, or allocate one."""
+    import torch
+    oc = packed_words(cout) if out_type == "bitpacked" else cout
+    dt = torch.float32 if out_type == "float" else torch.int32
+    if out is None:
+        return torch.empty((n, oh, ow, oc), dtype=dt, device=device)
+    _require(out, dt, "out")
+    if out.numel() != n * oh * ow * oc:
+        raise ValueError(f"out must hold {n}x{oh}x{ow}x{oc} elements")
+    return out
+
+
 def bconv2d(x_packed, w_packed, c_in: int, *, stride: Union[int, Sequence[int]] = 1,
             padding: str = "same", pad_value: str = "one",
             clamp: Optional[Tuple[int, int]] = None, out_type: str = "float",
@@ -286,35 +323,37 @@ def bconv2d(x_packed, w_packed, c_in: int, *, stride: Union[int, Sequence[int]] 
         raise ValueError(f"packed channel words {cw}/{cw2} do not match c_in={c_in}")
     desc = make_desc(n, h, w, c_in, cout, kh, kw, stride, padding, pad_value, clamp, out_type)
     oh, ow = out_shape(desc)
-    ptrs = []
-    for t, name, dtype, numel in ((multiplier, "multiplier", torch.float32, cout),
-                                  (bias, "bias", torch.float32, cout),
-                                  (thresholds, "thresholds", torch.float32, cout),
-                                  (flip, "flip", torch.int32, packed_words(cout)),
-                                  (pad_correction, "pad_correction", torch.int32,
-                                   (kh + 1) * (kw * (kw + 1) // 2) * cout)):
-        if t is None:
-            ptrs.append(None)
-        else:
-            _require(t, dtype, name)
-            if t.numel() != numel:
-                raise ValueError(f"{name} must have {numel} elements")
-            ptrs.append(t.data_ptr())
-    oc = packed_words(cout) if out_type == "bitpacked" else cout
-    if out is not None:
-        _require(out, torch.float32 if out_type == "float" else torch.int32, "out")
-        if out.numel() != n * oh * ow * oc:
-            raise ValueError(f"out must hold {n}x{oh}x{ow}x{oc} elements")
-    else:
-        if out_type == "float":
-            out = torch.empty((n, oh, ow, cout), dtype=torch.float32, device=x_packed.device)
-        elif out_type == "bitpacked":
-            out = torch.empty((n, oh, ow, packed_words(cout)), dtype=torch.int32,
-                              device=x_packed.device)
-        else:
-            out = torch.empty((n, oh, ow, cout), dtype=torch.int32, device=x_packed.device)
+    ptrs = _epilogue_args(cout, kh, kw, multiplier, bias, thresholds, flip, pad_correction)
+    out = _conv_out(out, out_type, n, oh, ow, cout, x_packed.device)
     _check(lib().lce_bconv2d(ctypes.byref(desc), x_packed.data_ptr(), w_packed.data_ptr(),
                              *ptrs, out.data_ptr(), _stream_handle(x_packed)))
+    return out
+
+
+def quantize_bconv2d(x, w_packed, *, stride: Union[int, Sequence[int]] = 1,
+                     padding: str = "same", clamp: Optional[Tuple[int, int]] = None,
+                     out_type: str = "float", multiplier=None, bias=None, thresholds=None,
+                     flip=None, out=None):
+    """LceQuantize + LceBConv2d in one launch: x float32 [N,H,W,C_in] (C_in a
+    multiple of 32, 16-byte aligned), w_packed int32 [Cout,KH,KW,C_in/32].
+
+    The result equals bconv2d(bitpack(x), w_packed, C_in, ...) with one
+    padding.  Shapes the fused kernel does not cover raise LceError with
+    status LCE_EUNSUPPORTED (nothing is launched); run bitpack and bconv2d.
+    """
+    import torch
+    _require(x, torch.float32, "x")
+    _require(w_packed, torch.int32, "w_packed")
+    n, h, w, c_in = x.shape
+    cout, kh, kw, cw = w_packed.shape
+    if cw != packed_words(c_in):
+        raise ValueError(f"packed channel words {cw} do not match c_in={c_in}")
+    desc = make_desc(n, h, w, c_in, cout, kh, kw, stride, padding, "one", clamp, out_type)
+    oh, ow = out_shape(desc)
+    ptrs = _epilogue_args(cout, kh, kw, multiplier, bias, thresholds, flip)[:4]
+    out = _conv_out(out, out_type, n, oh, ow, cout, x.device)
+    _check(lib().lce_quantize_bconv2d(ctypes.byref(desc), x.data_ptr(), w_packed.data_ptr(),
+                                      *ptrs, out.data_ptr(), _stream_handle(x)))
     return out
 
 
@@ -507,6 +546,31 @@ class PreparedBConv2d:
                      ptr(thresholds), ptr(flip), ptr(pad_correction), out.data_ptr())
         self.keep = (x_packed, w_packed, multiplier, bias, thresholds, flip, pad_correction, out)
         self._fn = lib().lce_bconv2d
+
+    def __call__(self, stream=None):
+        st = self._fn(self._desc_ref, *self.args, _current_stream() if stream is None else stream)
+        if st != LCE_OK:
+            raise LceError(st, last_error())
+
+
+class PreparedQuantBConv2d:
+    """A quantize_bconv2d call marshalled once (see PreparedBConv2d)."""
+
+    def __init__(self, x, w_packed, out, *, stride=1, padding="same", clamp=None,
+                 out_type="float", multiplier=None, bias=None, thresholds=None, flip=None):
+        quantize_bconv2d(x, w_packed, stride=stride, padding=padding, clamp=clamp,
+                         out_type=out_type, multiplier=multiplier, bias=bias,
+                         thresholds=thresholds, flip=flip, out=out)
+        n, h, w, c_in = x.shape
+        cout, kh, kw, _ = w_packed.shape
+        self.desc = make_desc(n, h, w, c_in, cout, kh, kw, stride, padding, "one", clamp,
+                              out_type)
+        self._desc_ref = ctypes.byref(self.desc)
+        ptr = lambda t: None if t is None else t.data_ptr()
+        self.args = (x.data_ptr(), w_packed.data_ptr(), ptr(multiplier), ptr(bias),
+                     ptr(thresholds), ptr(flip), out.data_ptr())
+        self.keep = (x, w_packed, multiplier, bias, thresholds, flip, out)
+        self._fn = lib().lce_quantize_bconv2d
 
     def __call__(self, stream=None):
         st = self._fn(self._desc_ref, *self.args, _current_stream() if stream is None else stream)

@@ -113,6 +113,9 @@ struct BconvParams {
     const uint32_t *flip;   // [Cwo] or null: output bits to invert (bitpacked output)
     const int32_t *padc;    // zero padding: table T [(KH+1)*KW*(KW+1)/2][Cout]
     FastDiv div_fwg;        // static kernel, zero padding: flat table index -> row
+    const float *xf;        // quantize-fused kernel: float32 input [N][H][W][32*Cw]
+    int32_t band_rows;      // quantize-fused kernel: rows of the tallest input band
+    int32_t band_pack;      // quantize-fused kernel: LDS word offset of the packed band
 };
 
 // LDS row stride for a row of `words` words: a multiple of 4 (16-byte rows
@@ -537,6 +540,50 @@ __host__ inline int table_lds_words(int rows, int fwg) { return (rows * fwg + 63
 // fields at their maxima, i.e. not waited on.)
 __device__ __forceinline__ void wait_table() { __builtin_amdgcn_s_waitcnt(0x0F70); }
 
+// One lane's share of its im2col row (shape known at compile time): wave w
+// holds taps w, w+4, ... of its pixel, CW words each, read as VEC-word
+// vectors (the tensor aligned to 4*VEC bytes).  load() issues every global
+// load; a padded tap loads the image's first pixel (always in bounds) and
+// store() writes it as 0 words (one padding).
+template <int CW, int KH, int KW, int VEC>
+struct TapStage {
+    static constexpr int kTaps = KH * KW;
+    static constexpr int kIters = (kTaps + kWaves - 1) / kWaves;
+    static constexpr int kVecs = CW / VEC;
+    using Vec = typename VecOf<VEC>::type;
+    Vec v[kIters][kVecs];
+    bool in[kIters];
+
+    // ximg: the pixel's image; (iy0, ix0): its window origin
+    __device__ __forceinline__ void load(const BconvParams &p, const uint32_t *ximg, int wave,
+                                         bool px_ok, int iy0, int ix0) {
+#pragma unroll
+        for (int i = 0; i < kIters; ++i) {
+            const int t = min(wave + i * kWaves, kTaps - 1);
+            const int ky = t / KW, kx = t - (t / KW) * KW;
+            const int iy = iy0 + ky, ix = ix0 + kx;
+            in[i] = px_ok && (unsigned)iy < (unsigned)p.h && (unsigned)ix < (unsigned)p.wd;
+            const uint32_t off = in[i] ? ((uint32_t)iy * (uint32_t)p.wd + (uint32_t)ix) * CW : 0u;
+            const Vec *src = reinterpret_cast<const Vec *>(ximg + off);
+#pragma unroll
+            for (int c = 0; c < kVecs; ++c) v[i][c] = src[c];
+        }
+    }
+
+    // row: the lane's im2col row in LDS
+    __device__ __forceinline__ void store(uint32_t *row, int wave) const {
+#pragma unroll
+        for (int i = 0; i < kIters; ++i) {
+            const int t = wave + i * kWaves;
+            if (t < kTaps) {
+                Vec *dst = reinterpret_cast<Vec *>(row + t * CW);
+#pragma unroll
+                for (int c = 0; c < kVecs; ++c) dst[c] = in[i] ? v[i][c] : VecOf<VEC>::zero();
+            }
+        }
+    }
+};
+
 // Shape-specialized kernel: Cw, KH, KW known at compile time, so the whole
 // im2col row fits one LDS slab and the filter-row offsets are immediates.
 // VEC = words per global load when staging (needs x aligned to 4*VEC bytes).
@@ -563,40 +610,15 @@ __global__ __launch_bounds__(kThreads) void bconv2d_static_kernel(BconvParams p)
     if (px_ok) pixel_origin(p, m, img_off, iy0, ix0, CW);
 
     // ---- stage the im2col rows: wave w copies taps w, w+4, ... of every pixel.
-    // All global loads are issued before any LDS store; a padded tap loads
-    // from the image's first pixel (always in bounds) and is replaced by 0.
-    // The per-filter epilogue values (and, for zero padding, the correction
-    // table) are fetched while those loads are in flight.
+    // All global loads are issued before any LDS store.  The per-filter
+    // epilogue values (and, for zero padding, the correction table) are
+    // fetched while those loads are in flight.
     {
-        const uint32_t *ximg = p.x + img_off;
-        constexpr int kIters = (kTaps + kWaves - 1) / kWaves;
-        constexpr int kVecs = CW / VEC;
-        using Vec = typename VecOf<VEC>::type;
-        Vec v[kIters][kVecs];
-        bool in[kIters];
-#pragma unroll
-        for (int i = 0; i < kIters; ++i) {
-            const int t = min(wave + i * kWaves, kTaps - 1);
-            const int ky = t / KW, kx = t - (t / KW) * KW;
-            const int iy = iy0 + ky, ix = ix0 + kx;
-            in[i] = px_ok && (unsigned)iy < (unsigned)p.h && (unsigned)ix < (unsigned)p.wd;
-            const uint32_t off = in[i] ? ((uint32_t)iy * (uint32_t)p.wd + (uint32_t)ix) * CW : 0u;
-            const Vec *src = reinterpret_cast<const Vec *>(ximg + off);
-#pragma unroll
-            for (int c = 0; c < kVecs; ++c) v[i][c] = src[c];
-        }
+        TapStage<CW, KH, KW, VEC> taps;
+        taps.load(p, p.x + img_off, wave, px_ok, iy0, ix0);
         if constexpr (PADZ) stage_table<kTableRows>(p, co_wg, wave, lane, sat);
         load_bounds<OUT, PADZ>(p, co_wg, p.fwg, bound);
-        uint32_t *row = lds + lane * kRS;
-#pragma unroll
-        for (int i = 0; i < kIters; ++i) {
-            const int t = wave + i * kWaves;
-            if (t < kTaps) {
-                Vec *dst = reinterpret_cast<Vec *>(row + t * CW);
-#pragma unroll
-                for (int c = 0; c < kVecs; ++c) dst[c] = in[i] ? v[i][c] : VecOf<VEC>::zero();
-            }
-        }
+        taps.store(lds + lane * kRS, wave);
     }
     if constexpr (PADZ) wait_table();
     __syncthreads();

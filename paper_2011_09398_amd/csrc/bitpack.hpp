@@ -13,17 +13,12 @@
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
+#include "dpp.hpp"
+
 namespace lce {
 
 constexpr int kBitpackThreads = 256;
 constexpr int kBitpackUnroll = 4;   // 1 KiB chunks in flight per wave
-
-// DPP control for "row_shr:n": lane i reads lane i-n of its row of 16 lanes;
-// with bound_ctrl set, lanes whose source falls outside the row read 0.
-template <int N>
-__device__ __forceinline__ uint32_t row_shr(uint32_t v) {
-    return (uint32_t)__builtin_amdgcn_update_dpp(0, (int)v, 0x110 | N, 0xF, 0xF, true);
-}
 
 // Fast path: channels % 32 == 0 and x 16-byte aligned, so the tensor is a
 // flat sequence of 32-float groups, each packing into one word.

@@ -1,7 +1,8 @@
-// Launchers of the matrix-core kernels, one translation unit per kernel
-// family (compiled in parallel); the C ABI in lce.hip plans a launch and
-// calls one of these.  out_type takes lce_out_type values, which equal the
-// kernels' OutKind values.
+// Launchers of the kernels compiled in their own translation units (the
+// matrix-core kernels and the quantize-fused convolution, compiled in
+// parallel); the C ABI in lce.hip plans a launch and calls one of these.
+// out_type takes lce_out_type values, which equal the kernels' OutKind
+// values.
 #pragma once
 
 #include <hip/hip_runtime.h>
@@ -21,4 +22,10 @@ void launch_mfma_ksplit(const MfmaParams &p, int out_type, int nblk, int mbw, di
 // pk: load the packed filter copy
 void launch_mfma_fs(const MfmaParams &p, int ks, int s, bool pk, int out_type, dim3 grid,
                      size_t lds, hipStream_t stream);
+
+// quantize-fused XOR/POPCOUNT convolution (float input, Cw = C_in/32 words
+// per pixel): whether an instance exists, and its launch
+bool has_quant_instance(int cw, int kh, int kw);
+void launch_bconv2d_quant(const BconvParams &p, int out_type, dim3 grid, size_t lds,
+                          hipStream_t stream);
 }  // namespace lce

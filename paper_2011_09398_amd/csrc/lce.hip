@@ -12,6 +12,7 @@
 #include <cstdint>
 #include <cstdio>
 #include <cstring>
+#include <numeric>
 #include <string>
 
 #include "lce.h"
@@ -207,6 +208,65 @@ lce_status validate_desc(const lce_bconv2d_desc *d, Geometry *g) {
 }
 
 using lce::BconvParams;
+
+// The launch parameters of an XOR/POPCOUNT convolution that depend only on
+// the descriptor, the filters and the output transform (the input pointer,
+// the zero-padding table and the schedule are set by the caller).
+BconvParams bconv_params(const lce_bconv2d_desc &d, const Geometry &g, const int32_t *w_packed,
+                         const float *multiplier, const float *bias, const float *thresholds,
+                         const int32_t *flip, void *out) {
+    BconvParams p{};
+    p.w = reinterpret_cast<const uint32_t *>(w_packed);
+    p.mult = d.out_type == LCE_OUT_FLOAT32 ? multiplier : nullptr;
+    p.bias = d.out_type == LCE_OUT_FLOAT32 ? bias : nullptr;
+    p.thr = thresholds;
+    p.flip = d.out_type == LCE_OUT_BITPACKED ? reinterpret_cast<const uint32_t *>(flip) : nullptr;
+    p.out = out;
+    p.n = d.n; p.h = d.h; p.wd = d.w; p.cw = packed_words(d.c_in);
+    p.oh = g.oh; p.ow = g.ow; p.cout = d.c_out; p.cwo = packed_words(d.c_out);
+    p.kh = d.kh; p.kw = d.kw; p.sh = d.stride_h; p.sw = d.stride_w; p.pt = g.pt; p.pl = g.pl;
+    p.kwords = d.kh * d.kw * p.cw;
+    p.k = d.kh * d.kw * d.c_in;
+    p.lo = d.clamp_min; p.hi = d.clamp_max;
+    p.m = d.n * g.oh * g.ow;
+    p.out_vec4 = aligned(out, 16) ? 1 : 0;
+    p.div_ohw = lce::make_fastdiv((uint32_t)(g.oh * g.ow));
+    p.div_ow = lce::make_fastdiv((uint32_t)g.ow);
+    return p;
+}
+
+// The quantize-fused convolution: the tallest band of input rows that the
+// windows of one workgroup's 64 consecutive output pixels read (global rows
+// n*H + y, first in-image row of the first pixel to last of the last).  A
+// block's band depends only on its first pixel's offset within the image (a
+// block cut short by the end of the batch is no taller than a full one at
+// the same offset), and the offset repeats every ohw / gcd(64, ohw) blocks,
+// so one such period covers every block.
+int64_t quant_band_rows(const BconvParams &p) {
+    const int64_t ohw = (int64_t)p.oh * p.ow;
+    const int64_t blocks = ((int64_t)p.m + lce::kPix - 1) / lce::kPix;
+    const int64_t period = ohw / std::gcd<int64_t>(lce::kPix, ohw);
+    int64_t tallest = 0;
+    for (int64_t b = 0; b < std::min(blocks, period); ++b) {
+        const int64_t ma = b * lce::kPix, mb = std::min(ma + lce::kPix - 1, (int64_t)p.m - 1);
+        const int64_t ia = ma / ohw, oya = (ma - ia * ohw) / p.ow;
+        const int64_t ib = mb / ohw, oyb = (mb - ib * ohw) / p.ow;
+        const int64_t first = ia * p.h + std::max<int64_t>(0, oya * p.sh - p.pt);
+        const int64_t last =
+            ib * p.h + std::min<int64_t>(p.h - 1, oyb * p.sh - p.pt + p.kh - 1);
+        tallest = std::max(tallest, last - first + 1);
+    }
+    return tallest;
+}
+
+// Why lce_quantize_bconv2d does not cover a valid descriptor, or NULL.
+const char *quant_unsupported(const lce_bconv2d_desc &d, const Geometry &g) {
+    if (zero_padded(d, g)) return "zero padding is not fused";
+    if (d.c_in % 32 != 0) return "c_in is not a multiple of 32";
+    if (!lce::has_quant_instance(d.c_in / 32, d.kh, d.kw))
+        return "no fused instance for this filter size and channel count";
+    return nullptr;
+}
 
 template <int CW, int KH, int KW, int OUT, bool PADZ>
 void launch_static(const BconvParams &p, dim3 grid, hipStream_t s, int vec) {
@@ -617,25 +677,9 @@ lce_status lce_bconv2d(const lce_bconv2d_desc *desc, const int32_t *x_packed,
         (pad_correction && !aligned(pad_correction, 4)))
         return fail(LCE_EALIGN, "tensor pointers must be 4-byte aligned");
 
-    BconvParams p{};
+    BconvParams p = bconv_params(d, g, w_packed, multiplier, bias, thresholds, flip, out);
     p.x = reinterpret_cast<const uint32_t *>(x_packed);
-    p.w = reinterpret_cast<const uint32_t *>(w_packed);
-    p.mult = d.out_type == LCE_OUT_FLOAT32 ? multiplier : nullptr;
-    p.bias = d.out_type == LCE_OUT_FLOAT32 ? bias : nullptr;
-    p.thr = thresholds;
-    p.flip = d.out_type == LCE_OUT_BITPACKED ? reinterpret_cast<const uint32_t *>(flip) : nullptr;
     p.padc = padz ? pad_correction : nullptr;
-    p.out = out;
-    p.n = d.n; p.h = d.h; p.wd = d.w; p.cw = packed_words(d.c_in);
-    p.oh = g.oh; p.ow = g.ow; p.cout = d.c_out; p.cwo = packed_words(d.c_out);
-    p.kh = d.kh; p.kw = d.kw; p.sh = d.stride_h; p.sw = d.stride_w; p.pt = g.pt; p.pl = g.pl;
-    p.kwords = d.kh * d.kw * p.cw;
-    p.k = d.kh * d.kw * d.c_in;
-    p.lo = d.clamp_min; p.hi = d.clamp_max;
-    p.m = d.n * g.oh * g.ow;
-    p.out_vec4 = aligned(out, 16) ? 1 : 0;
-    p.div_ohw = lce::make_fastdiv((uint32_t)(g.oh * g.ow));
-    p.div_ow = lce::make_fastdiv((uint32_t)g.ow);
     p.slab = p.kwords < lce::kSlabWords ? p.kwords : lce::kSlabWords;
     p.rs = lce::row_stride(p.slab);
 
@@ -655,6 +699,81 @@ lce_status lce_bconv2d(const lce_bconv2d_desc *desc, const int32_t *x_packed,
         default: dispatch<lce::OUT_INT>(p, grid, stream, vec, padz); break;
     }
     return check_launch("lce_bconv2d launch");
+}
+
+// The quantize-fused kernel's schedule.  Every filter group binarizes its
+// band again, so a second workgroup on a compute unit doubles that work:
+// the smallest filter group (most groups, least GEMM per workgroup) whose
+// grid still has at most one workgroup per compute unit; with more pixel
+// blocks than compute units, one group of all filters (up to 128).
+void choose_quant_schedule(BconvParams &p, int filters) {
+    const long pix_blocks = (p.m + lce::kPix - 1) / lce::kPix;
+    const long cus = device_simds() / 4;
+    static const int kOptions[][2] = {{4, 1}, {2, 1}, {1, 1}, {1, 2}, {1, 4}};
+    int nb = std::min(lce::kMaxNB, (filters + 31) / 32), ks = 1;
+    for (const auto &o : kOptions) {
+        if (o[1] > 1 && p.kwords < 4 * o[1]) continue;
+        const long fwg = (lce::kWaves / o[1]) * o[0] * lce::kRN;
+        if (pix_blocks * ((filters + fwg - 1) / fwg) <= cus) { nb = o[0]; ks = o[1]; }
+    }
+    if (const int t = tuning(LCE_TUNE_XOR_KS)) ks = t;
+    if (const int t = tuning(LCE_TUNE_XOR_NB)) nb = t;
+    if (ks != 1 && ks != 2 && ks != 4) ks = 1;
+    if (ks > 1) nb = 1;
+    nb = std::max(1, std::min(nb, lce::kMaxNB));
+    p.ks = ks;
+    p.nb = nb;
+    p.fwg = (lce::kWaves / ks) * nb * lce::kRN;
+    p.ksplit = ((p.kwords + ks - 1) / ks + 3) / 4 * 4;
+}
+
+lce_status lce_quantize_bconv2d(const lce_bconv2d_desc *desc, const float *x,
+                                const int32_t *w_packed, const float *multiplier,
+                                const float *bias, const float *thresholds,
+                                const int32_t *flip, void *out, hipStream_t stream) {
+    Geometry g;
+    lce_status st = validate_desc(desc, &g);
+    if (st != LCE_OK) return st;
+    const lce_bconv2d_desc &d = *desc;
+    // shapes the fused kernel does not cover: nothing is launched
+    if (const char *why = quant_unsupported(d, g))
+        return fail(LCE_EUNSUPPORTED, "%s; run lce_bitpack, then lce_bconv2d", why);
+    if (!x || !w_packed || !out) return fail(LCE_EINVAL, "x/w_packed/out is NULL");
+    if (d.out_type == LCE_OUT_BITPACKED && !thresholds)
+        return fail(LCE_EINVAL, "bitpacked output needs thresholds");
+    if (!aligned(x, 16))
+        return fail(LCE_EALIGN, "x must be 16-byte aligned (it is read in 16-byte units)");
+    if (!aligned(w_packed, 4) || !aligned(out, 4) || (multiplier && !aligned(multiplier, 4)) ||
+        (bias && !aligned(bias, 4)) || (thresholds && !aligned(thresholds, 4)) ||
+        (flip && !aligned(flip, 4)))
+        return fail(LCE_EALIGN, "tensor pointers must be 4-byte aligned");
+
+    BconvParams p = bconv_params(d, g, w_packed, multiplier, bias, thresholds, flip, out);
+    p.xf = x;
+    const int filters = d.out_type == LCE_OUT_BITPACKED ? p.cwo * 32 : p.cout;
+    choose_quant_schedule(p, filters);
+    p.div_fwg = lce::make_fastdiv((uint32_t)p.fwg);
+
+    // Dynamic LDS: the im2col rows (later the K-split partial sums), then the
+    // packed band.
+    const int64_t rows = quant_band_rows(p);
+    const int64_t band_words = rows * d.w * p.cw;
+    const int64_t row_area = (int64_t)lce::kPix * lce::row_stride(p.kwords);
+    const int64_t red_area = (int64_t)lce::kWaves * lce::kRN * lce::kPix;
+    const int64_t first_area = (std::max(row_area, red_area) + 3) / 4 * 4;
+    const int64_t lds = (first_area + (band_words + 3) / 4 * 4) * 4;
+    const int64_t lds_static = (int64_t)lce::kMaxFiltersWG * 4;
+    if (lds + lds_static > device_max_lds())
+        return fail(LCE_EUNSUPPORTED,
+                    "the input band of %lld rows needs %lld bytes of LDS (limit %d); run "
+                    "lce_bitpack, then lce_bconv2d", (long long)rows,
+                    (long long)(lds + lds_static), device_max_lds());
+    p.band_rows = (int32_t)rows;
+    p.band_pack = (int32_t)first_area;
+    dim3 grid((unsigned)((p.m + lce::kPix - 1) / lce::kPix),
+              (unsigned)((filters + p.fwg - 1) / p.fwg));
+    lce::launch_bconv2d_quant(p, d.out_type, grid, (size_t)lds, stream);
+    return check_launch("lce_quantize_bconv2d launch");
 }
 
 lce_status lce_bconv2d_pad_correction_size(const lce_bconv2d_desc *desc, int64_t *elements) {

@@ -127,6 +127,43 @@ def test_bconv2d_validation_errors():
     assert call_bconv(desc(c_out=(1 << 20) + 1, c_in=32, h=1, w=1)) == lce.LCE_EINVAL
 
 
+def call_quant(d, x=P, w=P, m=None, b=None, t=P, flip=None, out=P):
+    return lce.lib().lce_quantize_bconv2d(ctypes.byref(d), x, w, m, b, t, flip, out, None)
+
+
+def test_quantize_bconv2d_validation_errors():
+    L = lce.lib()
+    assert L.lce_quantize_bconv2d(None, P, P, None, None, P, None, P, None) == lce.LCE_EINVAL
+    assert call_quant(desc(clamp=(5, 4))) == lce.LCE_EINVAL
+    # shapes the fused kernel does not cover come back before any pointer check
+    assert call_quant(desc(pad_value="zero"), x=None) == lce.LCE_EUNSUPPORTED
+    assert "zero padding" in lce.last_error()
+    assert call_quant(desc(c_in=40), x=None) == lce.LCE_EUNSUPPORTED
+    assert "multiple of 32" in lce.last_error()
+    for kh, kw, c_in in ((3, 5, 64), (1, 1, 64), (7, 7, 64), (3, 3, 224), (3, 3, 1024),
+                         (5, 5, 512)):
+        assert call_quant(desc(kh=kh, kw=kw, c_in=c_in), x=None) == lce.LCE_EUNSUPPORTED, \
+            (kh, kw, c_in)
+    # a VALID geometry never pads, so zero padding is not a reason to refuse it
+    assert call_quant(desc(pad_value="zero", padding="valid"), x=None) == lce.LCE_EINVAL
+    assert call_quant(desc(), x=None) == lce.LCE_EINVAL
+    assert call_quant(desc(), w=None) == lce.LCE_EINVAL
+    assert call_quant(desc(), out=None) == lce.LCE_EINVAL
+    assert call_quant(desc(out_type="bitpacked"), t=None) == lce.LCE_EINVAL
+    # the float input is read in 16-byte units
+    assert call_quant(desc(), x=P + 4) == lce.LCE_EALIGN
+    assert "16-byte" in lce.last_error()
+    assert call_quant(desc(), x=P + 8) == lce.LCE_EALIGN
+    assert call_quant(desc(), out=P + 2) == lce.LCE_EALIGN
+    assert call_quant(desc(out_type="bitpacked"), flip=P + 1) == lce.LCE_EALIGN
+    # a band too tall for LDS, refused before any launch (and on a GPU too,
+    # whose LDS is 160 KiB): with stride 8 a 6-pixel-wide image has one
+    # output column, so 64 output pixels span 64 output rows = 507 input rows
+    # x 6 pixels x 16 words = 195 KiB, plus 38 KiB of im2col rows
+    assert call_quant(desc(h=4096, w=6, c_in=512, stride=8)) == lce.LCE_EUNSUPPORTED
+    assert "LDS" in lce.last_error()
+
+
 def test_bitpack_validation_errors():
     L = lce.lib()
     assert L.lce_bitpack(None, P, 4, 32, None) == lce.LCE_EINVAL
