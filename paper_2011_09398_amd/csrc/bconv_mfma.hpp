@@ -113,6 +113,19 @@ __device__ __forceinline__ u32x4 widen_word(uint32_t w, uint32_t fill) {
     return o;
 }
 
+// widen_word with the sign-bit mask in a register (mask = kFp4SignBits held
+// in a VGPR): each 32-bit word is then one shift and one AND-OR, since a
+// VALU instruction here takes at most one scalar or literal operand and the
+// fill is scalar.
+__device__ __forceinline__ u32x4 widen_word_vm(uint32_t w, uint32_t fill, uint32_t mask) {
+    u32x4 o;
+    o.x = ((w << 3) & mask) | fill;
+    o.y = ((w << 2) & mask) | fill;
+    o.z = ((w << 1) & mask) | fill;
+    o.w = (w & mask) | fill;
+    return o;
+}
+
 // Mask of the nibbles a widened word may keep: nibble c/4 of 32-bit word
 // c % 4 is 0xF for every channel c whose bit is set in `valid`.
 __device__ __forceinline__ u32x4 widen_valid_mask(uint32_t valid) {
@@ -1018,6 +1031,15 @@ __global__ __launch_bounds__(kMfmaThreads) void bconv2d_mfma_fs_kernel(MfmaParam
     // bitpacked output: the bounds of the workgroup's F filter blocks go to
     // LDS after the exchange area (one copy per filter block)
     float *thrs = reinterpret_cast<float *>(smem + p.cwe * plane) + p.fs_thr_off;
+    // after the bounds: the A-tile offset of every pixel's window origin
+    // (the pixel blocks' bases in the loop: one LDS read each instead of
+    // the divisions of mfma_pixel)
+    int *btab = reinterpret_cast<int *>(thrs + F * 32);
+    for (int t = tid; t < nb * 32; t += kMfmaThreads) {
+        int prow, pcol;
+        mfma_pixel(p, min(m0 + t, m_end - 1), prow, pcol);
+        btab[t] = (prow - row0) * PW + pcol;
+    }
     if constexpr (OUT == OUT_BITS) {
         ep_a = co_ok ? thr_to_dot_bound_f(ep_a, p.lo, p.hi) : -INFINITY;
         if (flipped) ep_a = 1.0f - ep_a;
@@ -1049,10 +1071,7 @@ __global__ __launch_bounds__(kMfmaThreads) void bconv2d_mfma_fs_kernel(MfmaParam
 
     // A-tile offset of the window origin of pixel block b's 32 pixels
     auto block_base = [&](int b) __attribute__((always_inline)) {
-        const int mp = min(m0 + b * 32 + l32, m_end - 1);
-        int prow, pcol;
-        mfma_pixel(p, mp, prow, pcol);
-        return (prow - row0) * PW + pcol;
+        return btab[b * 32 + l32 + z];
     };
 
     // ---- finishing a pair (or the last single block).  S = 1: this wave
@@ -1065,9 +1084,7 @@ __global__ __launch_bounds__(kMfmaThreads) void bconv2d_mfma_fs_kernel(MfmaParam
     // wave) before the next pair's first products overwrite them.
     mfma_v16f acc[2];
     float fin[NFB][16];
-    // (two partial words per block, even and odd values: consecutive lane
-    // writes then go to different registers instead of one dependent chain)
-    uint32_t word[NFB][2];
+    uint32_t word[NFB];
     int fin_b0 = 0, fin_nbp = 2;
     int buf = 0;
     // (accumulator blocks are picked by uniform branches with constant
@@ -1128,24 +1145,28 @@ __global__ __launch_bounds__(kMfmaThreads) void bconv2d_mfma_fs_kernel(MfmaParam
         constexpr int N = decltype(nc)::value;
         constexpr int j = N / 16, v = N % 16;
         if constexpr (OUT == OUT_BITS) {
-            // the bit of value v (dot - bound) is its sign, at bit
-            // (v/4)*8 + v%4 of the lane's word; after the last value the
-            // word moves to its lane half (shift by 4*half) and the two
-            // halves of the pixel (lanes l and l + 32) are merged.  Then
-            // lane < 32 stores block 0's word of pixel lane, lane >= 32 block
-            // 1's (S = 1); with S > 1 lanes < 32 store the wave's block.
-            constexpr int pos = (v >> 2) * 8 + (v & 3);
-            const uint32_t bit = (__float_as_uint(fin[j][v]) >> (31 - pos)) & (1u << pos);
-            uint32_t w = v == 0 ? bit : word[j][0] | bit;
+            // the bit of a value (dot - bound) is its sign.  The values are
+            // taken last to first (value vv = 15 - v at step v), each sign
+            // shifted into the word from the right (one v_alignbit_b32), so
+            // that bit vv of the word ends as value vv's sign.  Value vv is
+            // filter (vv/4)*8 + half*4 + vv%4: after the last one, nibble q
+            // of the word moves to nibble 2q + half, and the two halves of
+            // the pixel (lanes l and l + 32) are merged.  Then lane < 32
+            // stores block 0's word of pixel lane, lane >= 32 block 1's
+            // (S = 1); with S > 1 lanes < 32 store the wave's block.
+            constexpr int vv = 15 - v;
+            const uint32_t u = __float_as_uint(fin[j][vv]);
+            uint32_t w = v == 0 ? u >> 31 : __builtin_amdgcn_alignbit(word[j], u, 31);
             if constexpr (v == 15) {
-                w <<= 4 * half;
+                w = (w | (w << 8)) & 0x00FF00FFu;
+                w = ((w | (w << 4)) & 0x0F0F0F0Fu) << (4 * half);
                 const auto sw = __builtin_amdgcn_permlane32_swap(w, w, false, false);
-                w = w | sw[0] | sw[1];
+                w = sw[0] | sw[1];
             }
-            word[j][0] = w;
+            word[j] = w;
             if constexpr (v == 15 && j == NFB - 1) {
                 const int blk = S == 1 ? half : sk;      // block of the pair
-                const uint32_t out_word = NFB == 2 && half ? word[NFB - 1][0] : word[0][0];
+                const uint32_t out_word = NFB == 2 && half ? word[NFB - 1] : word[0];
                 const int m = m0 + (fin_b0 + blk) * 32 + l32;
                 if (fvalid && blk < fin_nbp && (S == 1 || lane < 32) && m < m_end)
                     reinterpret_cast<uint32_t *>(p.out)[(size_t)m * p.cwo + (f0 >> 5)] = out_word;
@@ -1195,6 +1216,9 @@ __global__ __launch_bounds__(kMfmaThreads) void bconv2d_mfma_fs_kernel(MfmaParam
 
     const mfma_v16f zero16 = {0.0f, 0.0f, 0.0f, 0.0f, 0.0f, 0.0f, 0.0f, 0.0f,
                               0.0f, 0.0f, 0.0f, 0.0f, 0.0f, 0.0f, 0.0f, 0.0f};
+    // the widening's sign-bit mask in a VGPR (see widen_word_vm)
+    uint32_t vmask;
+    asm volatile("v_mov_b32 %0, 0x88888888" : "=v"(vmask));
 
     // NBP (2 or 1) blocks from b0: K step i issues its products with a
     // piece of the previous pair's finishing after each (the matrix pipe
@@ -1230,7 +1254,7 @@ __global__ __launch_bounds__(kMfmaThreads) void bconv2d_mfma_fs_kernel(MfmaParam
             if constexpr (!has_prev) {
                 const uint32_t keep = sk * KS + i < ksteps ? ~0u : 0u;
                 if constexpr (PK)
-                    breg[i] = widen_word((bpk[i] ^ neg) & keep, kFp4PlusOne & keep);
+                    breg[i] = widen_word_vm((bpk[i] ^ neg) & keep, kFp4PlusOne & keep, vmask);
                 else
                     breg[i] = (breg[i] ^ u32x4{neg, neg, neg, neg}) & u32x4{keep, keep, keep, keep};
             }

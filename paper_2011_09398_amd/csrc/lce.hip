@@ -519,7 +519,8 @@ constexpr FsShape kFsShapes[] = {{9, 1}, {18, 1}, {5, 2}, {9, 2}, {18, 2}, {18, 
 // 256-word slack of its last DMA instruction) and (S > 1) the partial-sum
 // exchange: two buffers x F filter blocks x two pixel blocks x (S-1)
 // partials, 4 KB each; then the bounds of the F filter blocks (bitpacked
-// output).
+// output) and the A-tile offset of each pixel's window origin (one int per
+// pixel of the workgroup's whole blocks).
 // Bytes from the end of the A tile to the bounds of a bitpacked output
 // (after the larger of the packed region and the exchange, 16-byte aligned).
 size_t mfma_fs_thr_offset(const lce::MfmaParams &p, FsShape sh, int tile_rows) {
@@ -528,9 +529,10 @@ size_t mfma_fs_thr_offset(const lce::MfmaParams &p, FsShape sh, int tile_rows) {
     return (std::max(bits, red) + 15) / 16 * 16;
 }
 
-size_t mfma_fs_lds(const lce::MfmaParams &p, FsShape sh, int tile_rows) {
+size_t mfma_fs_lds(const lce::MfmaParams &p, FsShape sh, int tile_rows, int pixels) {
     const size_t a = (size_t)p.cwe * tile_rows * p.pw * 16;
-    return a + mfma_fs_thr_offset(p, sh, tile_rows) + (4 / sh.s) * 32 * 4;
+    return a + mfma_fs_thr_offset(p, sh, tile_rows) + (4 / sh.s) * 32 * 4 +
+           (size_t)(pixels + 31) / 32 * 32 * 4;
 }
 
 struct FsPlan {
@@ -580,7 +582,7 @@ FsPlan plan_mfma_fs(const lce::MfmaParams &p, int64_t cus, int blocks32, int kst
         const int64_t px = ((int64_t)p.m + pg - 1) / pg;
         if (px > (1 << 20)) continue;
         const int tr = mfma_tile_rows(p, (int)px);
-        const size_t lds = mfma_fs_lds(p, sh, tr);
+        const size_t lds = mfma_fs_lds(p, sh, tr, (int)px);
         if (lds > (size_t)device_max_lds()) continue;
         if ((int64_t)tr * p.pw * p.cwe > INT32_MAX / 2) continue;
         const int64_t nb = (px + 31) / 32;
