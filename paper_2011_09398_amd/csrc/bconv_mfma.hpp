@@ -79,7 +79,7 @@ struct MfmaParams {
     int32_t fs_thr_off;              // filter-stationary: float offset of the bounds in LDS
                                      // from the end of the A tile
     int32_t pad_zero;                // 1: padded locations are 0.0
-    int32_t region_vec;              // words per DMA lane when staging the region: 4 or 1
+    int32_t region_vec;              // words per lane per load when staging the region: 4 or 1
     FastDiv div_ohw, div_ow, div_ph, div_pw;
     FastDiv div_plane;               // tile_rows * pw: region locations
     FastDiv div_cwh, div_kw;         // cwe / 2 (word pairs per tap), kw
@@ -542,56 +542,7 @@ __global__ __launch_bounds__(kMfmaThreads) void bconv2d_mfma_kernel(MfmaParams p
     }
 }
 
-// The packed input region of a workgroup by LDS DMA: element q = g*plane +
-// rc of `abits` holds words [g*V, g*V + V) of region location rc (V = 4 or
-// 1 words per lane); padding locations read zeros.  The last instruction's
-// extra lanes land in a slack of 64*V words after the region.  Nothing
-// reaches registers, so the loads stay in flight until the caller waits
-// for them (vmcnt) together with its other loads.
-__device__ __forceinline__ void dma_region(const MfmaParams &p, uint32_t *abits, int row0,
-                                           int plane, int wave, int lane) {
-    const int bits_words = plane * p.cw;
-    auto run = [&](auto vec_c) __attribute__((always_inline)) {
-        constexpr int V = decltype(vec_c)::value;
-        for (int u = wave; u * 64 * V < bits_words; u += kMfmaThreads / 64) {
-            const int q = min(u * 64 + lane, bits_words / V - 1);
-            const int g = (int)fast_div((uint32_t)q, p.div_plane);
-            const int rc = q - g * plane;
-            const int r = (int)fast_div((uint32_t)rc, p.div_pw);
-            const int c = rc - r * p.pw;
-            const int R = row0 + r;
-            const int img = (int)fast_div((uint32_t)R, p.div_ph);
-            const int yy = R - img * p.ph - p.pt, xx = c - p.pl;
-            const bool inside = img < p.n && (unsigned)yy < (unsigned)p.h &&
-                                (unsigned)xx < (unsigned)p.w;
-            // (the input holds fewer than 2^31 words: 32-bit offsets)
-            const uint32_t *src =
-                inside ? p.x + (((uint32_t)img * (uint32_t)p.h + (uint32_t)yy) * (uint32_t)p.w +
-                                (uint32_t)xx) * (uint32_t)p.cw + (uint32_t)(g * V)
-                       : g_mfma_zero;
-            if constexpr (V == 4)
-                __builtin_amdgcn_global_load_lds((mfma_global_void *)src,
-                                                 (mfma_lds_void *)(abits + u * 64 * V), 16, 0, 0);
-            else
-                __builtin_amdgcn_global_load_lds((mfma_global_void *)src,
-                                                 (mfma_lds_void *)(abits + u * 64 * V), 4, 0, 0);
-        }
-    };
-    if (p.region_vec == 4)
-        run(std::integral_constant<int, 4>{});
-    else
-        run(std::integral_constant<int, 1>{});
-}
-
-// Widen the packed region (dma_region layout) into the A tile: atile[j*plane
-// + rc] = word j of location rc.  Words past Cw are +1.0 (their filter
-// values are 0.0); under zero padding, locations outside the image are
-// 0.0.  One straight-line path per staging width, four elements per thread
-// in flight (all reads before the writes):
-//   * V = 4: element e = g*plane + rc is one 16-byte group, widened into
-//     four A-tile words g*4 .. g*4+3;
-//   * V = 1: element e is word e / plane of location e % plane, at the
-//     same index in both arrays.
+// Whether region location rc lies inside the image.
 __device__ __forceinline__ bool region_inside(const MfmaParams &p, int row0, int rc) {
     const int r = (int)fast_div((uint32_t)rc, p.div_pw);
     const int c = rc - r * p.pw;
@@ -601,49 +552,160 @@ __device__ __forceinline__ bool region_inside(const MfmaParams &p, int row0, int
     return img < p.n && (unsigned)yy < (unsigned)p.h && (unsigned)xx < (unsigned)p.w;
 }
 
-__device__ __forceinline__ void widen_region_lds(const MfmaParams &p, const uint32_t *abits,
-                                                 u32x4 *atile, int row0, int plane, int tid,
-                                                 int z) {
-    constexpr int U = 4;
+// A copy of the parameters whose geometry fields (the ones the region
+// staging and the pixel arithmetic read) are held in scalar registers: each
+// passes through an empty asm statement, so the compiler keeps the value
+// instead of reloading it from the kernel arguments wherever it is used (it
+// treats argument loads as free to repeat, and each repeat is a dependent
+// scalar-cache round trip in the set-up).
+__device__ __forceinline__ MfmaParams pinned_geometry(const MfmaParams &p) {
+    MfmaParams q = p;
+    asm volatile("" : "+s"(q.n), "+s"(q.h), "+s"(q.w), "+s"(q.cw), "+s"(q.cwe), "+s"(q.pw),
+                      "+s"(q.ph), "+s"(q.pt), "+s"(q.pl), "+s"(q.sh), "+s"(q.sw), "+s"(q.ow),
+                      "+s"(q.region_vec), "+s"(q.pad_zero), "+s"(q.m));
+    asm volatile("" : "+s"(q.div_plane.d), "+s"(q.div_plane.magic), "+s"(q.div_plane.shift),
+                      "+s"(q.div_pw.d), "+s"(q.div_pw.magic), "+s"(q.div_pw.shift),
+                      "+s"(q.div_ph.d), "+s"(q.div_ph.magic), "+s"(q.div_ph.shift),
+                      "+s"(q.div_ohw.d), "+s"(q.div_ohw.magic), "+s"(q.div_ohw.shift),
+                      "+s"(q.div_ow.magic), "+s"(q.div_ow.shift));
+    return q;
+}
+
+// Buffer resources (gfx9 raw buffers: base, byte size, no stride; the
+// fourth descriptor word selects 32-bit data).  A buffer load takes a
+// wave-uniform base and byte offset in scalar registers and a 32-bit lane
+// offset; offsets at or past the size read zeros, which the region loads
+// use for padding locations.  The host keeps every buffer below 2^31 bytes.
+constexpr int kBufDword3 = 0x00020000;
+constexpr int kBufOutside = (int)0x80000000u;      // a lane offset past any buffer
+
+__device__ __forceinline__ __amdgpu_buffer_rsrc_t buffer_of(const void *base, uint32_t bytes) {
+    return __builtin_amdgcn_make_buffer_rsrc(const_cast<void *>(base), (short)0, (int)bytes,
+                                             kBufDword3);
+}
+
+// the bitpacked input as a buffer
+__device__ __forceinline__ __amdgpu_buffer_rsrc_t input_buffer(const MfmaParams &p) {
+    return buffer_of(p.x, (uint32_t)p.n * p.h * p.w * p.cw * 4u);
+}
+
+// the widened (16 bytes per element) or packed (4 bytes) filters as a buffer
+__device__ __forceinline__ __amdgpu_buffer_rsrc_t filter_buffer(const MfmaParams &p, bool packed) {
+    const uint32_t elems = (uint32_t)p.kh * p.kw * p.cwe * p.coutp;
+    return packed ? buffer_of(p.wpk, elems * 4u) : buffer_of(p.wexp, elems * 16u);
+}
+
+// The packed region staged through registers (filter-stationary and K-split
+// schedules): each thread loads up to kRegU elements (an element is
+// region_vec words of one location), widens them in registers and writes
+// them to the A tile once (atile[j*plane + rc] = word j of location rc),
+// with no LDS round trip and no barrier in between.  region_load issues one
+// chunk's buffer loads (the caller issues its filter loads after it, so
+// that both latencies overlap; the compiler waits for the region words where
+// region_widen first uses them); a padding location's lane offset lies past
+// the input, so it reads zeros, and it is flagged in `out`.
+constexpr int kRegU = 4;
+
+struct RegionChunk {
+    u32x4 w[kRegU];
+    uint32_t out;                        // bit u: element u lies outside the image
+};
+
+// byte offset in the input of word `word` of region location rc
+// (kBufOutside when the location is outside the image)
+__device__ __forceinline__ int region_offset(const MfmaParams &p, int row0, int rc, int word,
+                                             bool &inside) {
+    const int r = (int)fast_div((uint32_t)rc, p.div_pw);
+    const int c = rc - r * p.pw;
+    const int R = row0 + r;
+    const int img = (int)fast_div((uint32_t)R, p.div_ph);
+    const int yy = R - img * p.ph - p.pt, xx = c - p.pl;
+    inside = img < p.n && (unsigned)yy < (unsigned)p.h && (unsigned)xx < (unsigned)p.w;
+    const uint32_t w = (((uint32_t)img * (uint32_t)p.h + (uint32_t)yy) * (uint32_t)p.w +
+                        (uint32_t)xx) * (uint32_t)p.cw + (uint32_t)word;
+    return inside ? (int)(w * 4u) : kBufOutside;
+}
+
+// elements of the region: plane * Cw / region_vec
+__device__ __forceinline__ int region_elements(const MfmaParams &p, int plane) {
+    return p.region_vec == 4 ? plane * (p.cw >> 2) : plane * p.cw;
+}
+
+template <int NT>
+__device__ __forceinline__ void region_load(const MfmaParams &p, int row0, int plane, int tid,
+                                            int e0, RegionChunk &ch) {
+    const int total = region_elements(p, plane);
+    const __amdgpu_buffer_rsrc_t xb = input_buffer(p);
+    ch.out = 0;
+    // (slots whose whole wave lies past the region are skipped, a uniform
+    // branch, and hold zeros)
+    const int wave_e0 = e0 + (tid & ~63);
     if (p.region_vec == 4) {
-        const int total = plane * (p.cw >> 2);
-        const u32x4 *src = reinterpret_cast<const u32x4 *>(abits);
-        for (int e0 = 0; e0 < total; e0 += U * kMfmaThreads) {
-            u32x4 w[U];
 #pragma unroll
-            for (int u = 0; u < U; ++u) w[u] = src[min(e0 + u * kMfmaThreads + tid, total - 1) + z];
-#pragma unroll
-            for (int u = 0; u < U; ++u) {
-                const int e = e0 + u * kMfmaThreads + tid;
-                if (e >= total) break;
-                const int g = (int)fast_div((uint32_t)e, p.div_plane);
-                const int rc = e - g * plane;
-                const uint32_t fill = p.pad_zero && !region_inside(p, row0, rc) ? 0u : kFp4PlusOne;
-#pragma unroll
-                for (int k = 0; k < 4; ++k) atile[(4 * g + k) * plane + rc] = widen_word(w[u][k], fill);
+        for (int u = 0; u < kRegU; ++u) {
+            if (wave_e0 + u * NT >= total) {
+                ch.w[u] = u32x4{0u, 0u, 0u, 0u};
+                continue;
             }
+            const int e = min(e0 + u * NT + tid, total - 1);
+            const int g = (int)fast_div((uint32_t)e, p.div_plane);
+            bool in;
+            const int off = region_offset(p, row0, e - g * plane, 4 * g, in);
+            ch.w[u] = __builtin_amdgcn_raw_buffer_load_b128(xb, off, 0, 0);
+            ch.out |= in ? 0u : 1u << u;
         }
     } else {
-        const int total = plane * p.cw;
-        for (int e0 = 0; e0 < total; e0 += U * kMfmaThreads) {
-            uint32_t w[U];
 #pragma unroll
-            for (int u = 0; u < U; ++u) w[u] = abits[min(e0 + u * kMfmaThreads + tid, total - 1) + z];
-#pragma unroll
-            for (int u = 0; u < U; ++u) {
-                const int e = e0 + u * kMfmaThreads + tid;
-                if (e >= total) break;
-                uint32_t fill = kFp4PlusOne;
-                if (p.pad_zero) {
-                    const int j = (int)fast_div((uint32_t)e, p.div_plane);
-                    if (!region_inside(p, row0, e - j * plane)) fill = 0u;
-                }
-                atile[e] = widen_word(w[u], fill);
+        for (int u = 0; u < kRegU; ++u) {
+            if (wave_e0 + u * NT >= total) {
+                ch.w[u] = u32x4{0u, 0u, 0u, 0u};
+                continue;
             }
+            const int e = min(e0 + u * NT + tid, total - 1);
+            const int j = (int)fast_div((uint32_t)e, p.div_plane);
+            bool in;
+            const int off = region_offset(p, row0, e - j * plane, j, in);
+            ch.w[u].x = __builtin_amdgcn_raw_buffer_load_b32(xb, off, 0, 0);
+            ch.out |= in ? 0u : 1u << u;
         }
     }
-    // words past Cw: +1.0 (0.0 outside the image under zero padding)
-    for (int e = plane * p.cw + tid; e < plane * p.cwe; e += kMfmaThreads) {
+}
+
+// Widen a loaded chunk into the A tile: +1.0/-1.0 from the bits, 0.0 at
+// padding locations under zero padding.
+template <int NT>
+__device__ __forceinline__ void region_widen(const MfmaParams &p, const RegionChunk &ch,
+                                             u32x4 *atile, int plane, int tid, int e0) {
+    const int total = region_elements(p, plane);
+#pragma unroll
+    for (int u = 0; u < kRegU; ++u) {
+        const int e = e0 + u * NT + tid;
+        if (e >= total) break;
+        const uint32_t fill = p.pad_zero && ((ch.out >> u) & 1u) ? 0u : kFp4PlusOne;
+        if (p.region_vec == 4) {
+            const int g = (int)fast_div((uint32_t)e, p.div_plane);
+            const int rc = e - g * plane;
+#pragma unroll
+            for (int k = 0; k < 4; ++k) atile[(4 * g + k) * plane + rc] = widen_word(ch.w[u][k], fill);
+        } else {
+            atile[e] = widen_word(ch.w[u].x, fill);
+        }
+    }
+}
+
+// The rest of the A tile after the first chunk (regions of more than
+// kRegU*NT elements: load, wait, widen), then the words past Cw: +1.0, or
+// 0.0 outside the image under zero padding.
+template <int NT>
+__device__ __forceinline__ void region_finish(const MfmaParams &p, u32x4 *atile, int row0,
+                                              int plane, int tid) {
+    const int total = region_elements(p, plane);
+    for (int e0 = kRegU * NT; e0 < total; e0 += kRegU * NT) {
+        RegionChunk ch;
+        region_load<NT>(p, row0, plane, tid, e0, ch);
+        region_widen<NT>(p, ch, atile, plane, tid, e0);
+    }
+    for (int e = plane * p.cw + tid; e < plane * p.cwe; e += NT) {
         uint32_t fill = kFp4PlusOne;
         if (p.pad_zero) {
             const int j = (int)fast_div((uint32_t)e, p.div_plane);
@@ -658,8 +720,9 @@ __device__ __forceinline__ void widen_region_lds(const MfmaParams &p, const uint
 // compute the same 32*MBW pixels x 32*NBLK filters, each over a quarter of
 // the K steps (one K step = one tap and one pair of packed words = 64
 // channels), and add their partial sums at the end.
-//   * A: every packed word of the input region is widened into LDS once,
-//     up front (cwe planes of the region), so any wave can take any K step.
+//   * A: every packed word of the input region is loaded into registers
+//     and widened into LDS once, up front (cwe planes of the region), so
+//     any wave can take any K step.
 //   * B: each wave loads the widened filters of its own K steps straight
 //     into registers, kRing - 1 steps ahead; the waves never wait for each
 //     other inside the loop.
@@ -703,64 +766,75 @@ __global__ __launch_bounds__(kMfmaThreads) void bconv2d_mfma_ks_kernel(MfmaParam
     const int TR = p.tile_rows, PW = p.pw, plane = TR * PW;
     u32x4 *atile = smem;                                 // [cwe][TR][PW] e2m1
 
+    const MfmaParams g = pinned_geometry(p);     // (geometry in scalar registers)
     int row0, col0;
-    mfma_pixel(p, m0, row0, col0);
+    mfma_pixel(g, m0, row0, col0);
     int a_lane[MBW];                                     // this lane's A offset per pixel block
 #pragma unroll
     for (int b = 0; b < MBW; ++b) {
         const int mp = min(m0 + b * 32 + l32, p.m - 1);
         int prow, pcol;
-        mfma_pixel(p, mp, prow, pcol);
+        mfma_pixel(g, mp, prow, pcol);
         a_lane[b] = half * plane + (prow - row0) * PW + pcol;
     }
 
-    // output-transform parameters of the NBLK filter blocks
+    // the region's first chunk (its loads before the filters': the widening
+    // needs it first)
+    RegionChunk rch;
+    region_load<kMfmaThreads>(g, row0, plane, tid, 0, rch);
+
+    // output-transform parameters of the NBLK filter blocks (buffer loads
+    // after the region's, so that its widening does not wait for them; an
+    // absent array reads zeros, replaced by the default)
     float ep_a[NBLK], ep_b[NBLK];
+    {
+        const uint32_t cb = (uint32_t)p.cout * 4u;
+        const __amdgpu_buffer_rsrc_t ab = buffer_of(OUT == OUT_BITS ? p.thr : p.mult,
+                                                    OUT == OUT_BITS || p.mult ? cb : 0u);
+        const __amdgpu_buffer_rsrc_t bb = buffer_of(p.bias, p.bias ? cb : 0u);
 #pragma unroll
-    for (int i = 0; i < NBLK; ++i) {
-        const int co = min(n_base + 32 * i + l32, p.cout - 1);
-        if constexpr (OUT == OUT_BITS) {
-            ep_a[i] = p.thr[co];
-            ep_b[i] = 0.0f;
-        } else if constexpr (OUT == OUT_FLOAT) {
-            ep_a[i] = p.mult ? p.mult[co] : 1.0f;
-            ep_b[i] = p.bias ? p.bias[co] : 0.0f;
-        } else {
+        for (int i = 0; i < NBLK; ++i) {
+            const int co4 = min(n_base + 32 * i + l32, p.cout - 1) * 4;
             ep_a[i] = ep_b[i] = 0.0f;
+            if constexpr (OUT == OUT_BITS) {
+                ep_a[i] = __uint_as_float(__builtin_amdgcn_raw_buffer_load_b32(ab, co4, 0, 0));
+            } else if constexpr (OUT == OUT_FLOAT) {
+                const float m = __uint_as_float(__builtin_amdgcn_raw_buffer_load_b32(ab, co4, 0, 0));
+                const float b = __uint_as_float(__builtin_amdgcn_raw_buffer_load_b32(bb, co4, 0, 0));
+                ep_a[i] = p.mult ? m : 1.0f;
+                ep_b[i] = p.bias ? b : 0.0f;
+            }
         }
     }
-
-    // the packed input region by LDS DMA, past the A tile (issued before
-    // the filter loads below: memory counters retire in order)
-    uint32_t *abits = reinterpret_cast<uint32_t *>(smem + p.cwe * plane);
-    dma_region(p, abits, row0, plane, wave, lane);
 
     // B of this wave's local step i (K step wave + 4i, clamped: steps past
     // the last re-read it): word row t*cwe + 2*jp + half, NBLK blocks of 32
     // filters, 16 bytes per lane per block.
-    const u32x4 *wcol[NBLK];
+    // (buffer loads: lane offset of the filter column, uniform byte offset
+    // of the row)
+    const __amdgpu_buffer_rsrc_t wb = filter_buffer(p, false);
+    int wcol[NBLK];
 #pragma unroll
     for (int ib = 0; ib < NBLK; ++ib)
-        wcol[ib] = p.wexp + (size_t)half * p.coutp + min(n_base + 32 * ib + l32, p.coutp - 1);
+        wcol[ib] = (half * p.coutp + min(n_base + 32 * ib + l32, p.coutp - 1)) * 16;
     auto load_b = [&](int i, u32x4 (&dst)[NBLK]) __attribute__((always_inline)) {
         const int ks = min(wave + 4 * i, ksteps - 1);
         const int t = (int)fast_div((uint32_t)ks, p.div_cwh);
         const int jp = ks - t * cwh;
-        const size_t row = (size_t)(t * p.cwe + 2 * jp) * p.coutp;
+        const int row = (t * p.cwe + 2 * jp) * p.coutp * 16;
 #pragma unroll
-        for (int ib = 0; ib < NBLK; ++ib) dst[ib] = wcol[ib][row];
+        for (int ib = 0; ib < NBLK; ++ib)
+            dst[ib] = __builtin_amdgcn_raw_buffer_load_b128(wb, wcol[ib], row, 0);
     };
     u32x4 ring[kRing][NBLK];
 #pragma unroll
     for (int r = 0; r < kRing - 1; ++r) load_b(r, ring[r]);
 
-    // ---- widen the whole region (every word of every location) once this
-    // wave's DMA has landed (at most the ring's loads still outstanding) and
-    // every wave's has (barrier), while the filter ring is still arriving
-    wait_vmcnt<(kRing - 1) * NBLK>();
-    int z = lds_barrier();
-    widen_region_lds(p, abits, atile, row0, plane, tid, z);
-    z = lds_barrier();                                   // the A planes are complete
+    // ---- widen the whole region (every word of every location) as its
+    // words arrive, while the filter ring is still arriving
+    region_widen<kMfmaThreads>(g, rch, atile, plane, tid, 0);
+    region_finish<kMfmaThreads>(g, atile, row0, plane, tid);
+    int z = lds_barrier();                               // the A planes are complete
 
     mfma_v16f acc[MBW][NBLK];
 #pragma unroll
@@ -888,8 +962,8 @@ __global__ __launch_bounds__(kMfmaThreads) void bconv2d_mfma_ks_kernel(MfmaParam
 // block of 32 filters for its KS K steps in registers for the whole kernel
 // (16 bytes per lane per step, loaded once, from the packed copy where every
 // channel is valid, and waited for step by step in the first pair); the
-// workgroup stages its input
-// region in LDS by DMA, widens it there once, and then runs through its
+// workgroup loads its input region into registers (buffer loads issued
+// before the filters'), widens it into LDS once, and then runs through its
 // pixel blocks two at a time, reading only the A operands from LDS.
 // Nothing is staged inside the loop, and the loop is software-pipelined
 // across pixel-block pairs:
@@ -961,33 +1035,44 @@ __global__ __launch_bounds__(kMfmaThreads) void bconv2d_mfma_fs_kernel(MfmaParam
     const int ksteps = p.kh * p.kw * cwh;
     const int TR = p.tile_rows, PW = p.pw, plane = TR * PW;
     u32x4 *atile = smem;                                 // [cwe][TR][PW] e2m1
-    // past the A tile: the packed region (staged before the loop), and over
-    // it, once the A tile is complete, the exchange buffer
-    uint32_t *abits = reinterpret_cast<uint32_t *>(smem + p.cwe * plane);
+    // past the A tile: the exchange buffer (S > 1)
     f32x4 *red = reinterpret_cast<f32x4 *>(smem + p.cwe * plane);
 
-    // ---- per-lane output-transform parameters of filter co (loaded before
-    // the filters: memory counters retire in order).  A flipped filter
-    // (bitpacked output) is computed negated: its widened weights get their
-    // sign bits inverted, so the accumulator holds -dot, and the bit
-    // dot >= T becomes -dot < 1 - T (integers; +-infinity stay exact), the
-    // same compare as for every other filter.
+    const MfmaParams g = pinned_geometry(p);     // (geometry in scalar registers)
+    int row0, col0;
+    mfma_pixel(g, m0, row0, col0);
+    // the region's first chunk (its loads before the filters': the widening
+    // needs it first)
+    RegionChunk rch;
+    region_load<kMfmaThreads>(g, row0, plane, tid, 0, rch);
+
+    // ---- per-lane output-transform parameters of filter co, as buffer
+    // loads issued between the region's and the filters' (so that waiting
+    // for them leaves the filters in flight), used once the region is
+    // widened (an
+    // absent array is an empty buffer: its loads read zeros, replaced by the
+    // default).  A flipped filter (bitpacked output) is computed negated:
+    // its widened weights get their sign bits inverted, so the accumulator
+    // holds -dot, and the bit dot >= T becomes -dot < 1 - T (integers;
+    // +-infinity stay exact), the same compare as for every other filter.
     float ep_a = 0.0f, ep_b = 0.0f;
-    bool flipped = false;
+    uint32_t flip_word = 0;
     {
-        const int cc = min(co, p.cout - 1);
+        const int cc4 = min(co, p.cout - 1) * 4;
+        const uint32_t cb = (uint32_t)p.cout * 4u;
         if constexpr (OUT == OUT_BITS) {
-            ep_a = p.thr[cc];
-            if (p.flip && fvalid) flipped = co_ok && ((p.flip[f0 >> 5] >> l32) & 1u);
+            ep_a = __uint_as_float(__builtin_amdgcn_raw_buffer_load_b32(buffer_of(p.thr, cb), cc4, 0, 0));
+            flip_word = __builtin_amdgcn_raw_buffer_load_b32(
+                buffer_of(p.flip, p.flip ? (uint32_t)p.cwo * 4u : 0u), (f0 >> 5) * 4, 0, 0);
         } else if constexpr (OUT == OUT_FLOAT) {
-            ep_a = p.mult ? p.mult[cc] : 1.0f;
-            ep_b = p.bias ? p.bias[cc] : 0.0f;
+            const float m = __uint_as_float(__builtin_amdgcn_raw_buffer_load_b32(
+                buffer_of(p.mult, p.mult ? cb : 0u), cc4, 0, 0));
+            const float b = __uint_as_float(__builtin_amdgcn_raw_buffer_load_b32(
+                buffer_of(p.bias, p.bias ? cb : 0u), cc4, 0, 0));
+            ep_a = p.mult ? m : 1.0f;
+            ep_b = p.bias ? b : 0.0f;
         }
     }
-
-    int row0, col0;
-    mfma_pixel(p, m0, row0, col0);
-    dma_region(p, abits, row0, plane, wave, lane);
 
     // ---- this wave's filters: step i is K step s = sk*KS + i = (tap t =
     // s / (Cw'/2), word pair q = s % (Cw'/2)): word 2q + half of tap t of
@@ -995,7 +1080,8 @@ __global__ __launch_bounds__(kMfmaThreads) void bconv2d_mfma_fs_kernel(MfmaParam
     // offset of the same word and tap in the A tile (lane-dependent, so it
     // stays in a VGPR).  The loads are unconditional (filters past C_out'
     // read the last one and are never stored; steps past the last read the
-    // last row and are zeroed on arrival).  Nothing waits for them here: the
+    // last row and are zeroed on arrival); each is a wave-uniform row
+    // address plus a 32-bit lane offset.  Nothing waits for them here: the
     // first pair's K step i waits for its own (memory counters retire in
     // order), so the first products start while later filters still arrive.
     // PK: every channel of every word is valid, and the packed words are
@@ -1005,56 +1091,60 @@ __global__ __launch_bounds__(kMfmaThreads) void bconv2d_mfma_fs_kernel(MfmaParam
     uint32_t bpk[PK ? KS : 1];
     int aoff[KS];
     {
-        const size_t col = (size_t)half * p.coutp + min(co, p.coutp - 1);
+        const __amdgpu_buffer_rsrc_t wb = filter_buffer(p, PK);
+        constexpr int kEl = PK ? 4 : 16;                 // bytes per filter element
+        const int col = (half * p.coutp + min(co, p.coutp - 1)) * kEl;
         const int hp = half * plane;
 #pragma unroll
         for (int i = 0; i < KS; ++i) {
-            const int s = min(sk * KS + i, ksteps - 1);
+            const int row = 2 * min(sk * KS + i, ksteps - 1) * p.coutp * kEl;   // uniform
             if constexpr (PK)
-                bpk[i] = p.wpk[col + (size_t)(2 * s) * p.coutp];
+                bpk[i] = __builtin_amdgcn_raw_buffer_load_b32(wb, col, row, 0);
             else
-                breg[i] = p.wexp[col + (size_t)(2 * s) * p.coutp];
+                breg[i] = __builtin_amdgcn_raw_buffer_load_b128(wb, col, row, 0);
             aoff[i] = (p.fs_koff[sk * KS + i] & 0xFFFFFF) + hp;   // (word 2q + half)
         }
     }
 
-    // The region DMA was issued before the KS filter loads and memory
-    // counters retire in order: once at most KS loads are outstanding, this
-    // wave's region words (and parameters) have landed, and the region is
-    // widened while the filters are still on their way.
-    wait_vmcnt<KS>();
-    int z = lds_barrier();                               // every wave's region DMA landed
-    widen_region_lds(p, abits, atile, row0, plane, tid, z);
-    // sign bits of a flipped filter (in the widened or the packed form),
-    // applied to each step's filters as they arrive (first pair)
-    const uint32_t neg = OUT == OUT_BITS && flipped ? (PK ? ~0u : kFp4SignBits) : 0u;
     // bitpacked output: the bounds of the workgroup's F filter blocks go to
-    // LDS after the exchange area (one copy per filter block)
+    // LDS after the exchange area (one copy per filter block); after them,
+    // the A-tile offset of every pixel's window origin (the pixel blocks'
+    // bases in the loop: one LDS read each instead of the divisions of
+    // mfma_pixel), computed while the region's loads are in flight
     float *thrs = reinterpret_cast<float *>(smem + p.cwe * plane) + p.fs_thr_off;
-    // after the bounds: the A-tile offset of every pixel's window origin
-    // (the pixel blocks' bases in the loop: one LDS read each instead of
-    // the divisions of mfma_pixel)
     int *btab = reinterpret_cast<int *>(thrs + F * 32);
     for (int t = tid; t < nb * 32; t += kMfmaThreads) {
         int prow, pcol;
-        mfma_pixel(p, min(m0 + t, m_end - 1), prow, pcol);
+        mfma_pixel(g, min(m0 + t, m_end - 1), prow, pcol);
         btab[t] = (prow - row0) * PW + pcol;
     }
+
+    // The region, widened as its words arrive (the compiler waits for them
+    // here, with the filter loads still outstanding), the rest of it if any,
+    // and the words past Cw.
+    region_widen<kMfmaThreads>(g, rch, atile, plane, tid, 0);
+    region_finish<kMfmaThreads>(g, atile, row0, plane, tid);
+    int z;
+    const bool flipped = OUT == OUT_BITS && fvalid && co_ok && ((flip_word >> l32) & 1u);
+    // sign bits of a flipped filter (in the widened or the packed form),
+    // applied to each step's filters as they arrive (first pair)
+    const uint32_t neg = OUT == OUT_BITS && flipped ? (PK ? ~0u : kFp4SignBits) : 0u;
     if constexpr (OUT == OUT_BITS) {
         ep_a = co_ok ? thr_to_dot_bound_f(ep_a, p.lo, p.hi) : -INFINITY;
         if (flipped) ep_a = 1.0f - ep_a;
         if (sk == 0 && half == 0) thrs[fblk * 32 + l32] = ep_a;
     }
-    z = lds_barrier();                                   // the A tile is complete (abits is free)
+    z = lds_barrier();                                   // the A tile is complete
 
     // Bitpacked output: the products are transposed (filters as the row
     // operand, pixels as the column operand: lane = pixel of the block, value
     // v = filter (v/4)*8 + half*4 + v%4), and each accumulator a wave
     // finishes starts at -bound instead of 0, so that the finished value is
-    // dot - bound and the output bit its sign: two ALU operations per bit
-    // and no lane writes.  With S > 1 only the wave that finishes a block
-    // starts it at -bound.
-    mfma_v16f tinit[2];
+    // dot - bound and the output bit its sign: one ALU operation per bit and
+    // no lane writes.  With S > 1 only the wave that finishes a block starts
+    // it at -bound (S = 1: both blocks of a pair start from one copy).
+    constexpr int NT = S == 1 ? 1 : 2;
+    mfma_v16f tinit[NT];
     if constexpr (OUT == OUT_BITS) {
 #pragma unroll
         for (int q = 0; q < 4; ++q) {
@@ -1064,7 +1154,7 @@ __global__ __launch_bounds__(kMfmaThreads) void bconv2d_mfma_fs_kernel(MfmaParam
 #pragma unroll
             for (int e = 0; e < 4; ++e)
 #pragma unroll
-                for (int b = 0; b < 2; ++b)
+                for (int b = 0; b < NT; ++b)
                     tinit[b][4 * q + e] = S == 1 || b == sk ? -tv[e] : 0.0f;
         }
     }
@@ -1075,20 +1165,29 @@ __global__ __launch_bounds__(kMfmaThreads) void bconv2d_mfma_fs_kernel(MfmaParam
     };
 
     // ---- finishing a pair (or the last single block).  S = 1: this wave
-    // finishes both blocks.  S > 1: wave sk < 2 finishes block sk of the
-    // pair after the other S-1 waves of its filter block hand it their
-    // partial sums through LDS (red[(((buf*F + fblk)*2 + block)*(S-1) +
-    // slot)*4 + quad] rows of 64 lanes, slot = the writer's rank among the
-    // other waves, two alternating buffers); waves sk >= 2 finish nothing.
-    // The values leave the accumulators (into fin, or into LDS for another
-    // wave) before the next pair's first products overwrite them.
-    mfma_v16f acc[2];
-    float fin[NFB][16];
+    // finishes both blocks, from two accumulator sets that alternate by
+    // pair: while a pair's products run on one set, the previous pair's
+    // values are read from the other in pieces between them, so no product
+    // waits for the finishing and no finishing waits for a product.  S > 1:
+    // one set; wave sk < 2 finishes block sk of the pair after the other S-1
+    // waves of its filter block hand it their partial sums through LDS
+    // (red[(((buf*F + fblk)*2 + block)*(S-1) + slot)*4 + quad] rows of 64
+    // lanes, slot = the writer's rank among the other waves, two alternating
+    // buffers); waves sk >= 2 finish nothing.  The values leave the
+    // accumulators (into fin, or into LDS for another wave) before the next
+    // pair's first products overwrite them.
+    // (accumulator blocks and sets are picked with constant indices only: a
+    // runtime index would move them to scratch memory)
+    constexpr int NSET = S == 1 ? 2 : 1;
+    mfma_v16f acc[NSET][2];
+    // (S > 1: zero-initialized, since a wave with no block of its own in a
+    // pass computes values it never stores, and reading an unassigned fin
+    // there would be undefined: the compiler then may, and did, rewrite the
+    // other waves' path wrongly)
+    float fin[S == 1 ? 1 : NFB][16] = {};
     uint32_t word[NFB];
     int fin_b0 = 0, fin_nbp = 2;
     int buf = 0;
-    // (accumulator blocks are picked by uniform branches with constant
-    // indices: a runtime index would move them to scratch memory)
     auto collect_prev = [&](int nbp) __attribute__((always_inline)) {
         fin_nbp = nbp;
         if constexpr (S > 1) {
@@ -1097,23 +1196,18 @@ __global__ __launch_bounds__(kMfmaThreads) void bconv2d_mfma_fs_kernel(MfmaParam
                 if (J >= nbp) return;
                 if (J == sk) {
 #pragma unroll
-                    for (int v = 0; v < 16; ++v) fin[0][v] = acc[J][v];
+                    for (int v = 0; v < 16; ++v) fin[0][v] = acc[0][J][v];
                 } else {
                     const int slot = sk - (sk > J ? 1 : 0);
 #pragma unroll
                     for (int vq = 0; vq < 4; ++vq)
                         red[((((buf * F + fblk) * 2 + J) * (S - 1) + slot) * 4 + vq) * 64 + lane + z] =
-                            f32x4{acc[J][4 * vq], acc[J][4 * vq + 1], acc[J][4 * vq + 2],
-                                  acc[J][4 * vq + 3]};
+                            f32x4{acc[0][J][4 * vq], acc[0][J][4 * vq + 1], acc[0][J][4 * vq + 2],
+                                  acc[0][J][4 * vq + 3]};
                 }
             };
             move(std::integral_constant<int, 0>{});
             move(std::integral_constant<int, 1>{});
-        } else {
-#pragma unroll
-            for (int j = 0; j < NFB; ++j)
-#pragma unroll
-                for (int v = 0; v < 16; ++v) fin[j][v] = acc[j][v];
         }
     };
     // (S > 1) the other waves' partial sums of this wave's block
@@ -1135,15 +1229,23 @@ __global__ __launch_bounds__(kMfmaThreads) void bconv2d_mfma_fs_kernel(MfmaParam
             buf ^= 1;
         }
     };
+    // value V of block J of those this wave finishes, from accumulator set
+    // PS (S = 1) or from fin (S > 1)
+    auto value = [&](auto jc, auto vc, auto psc) __attribute__((always_inline)) -> float {
+        constexpr int J = decltype(jc)::value, V = decltype(vc)::value;
+        if constexpr (S == 1)
+            return acc[decltype(psc)::value][J][V];
+        else
+            return fin[J][V];
+    };
     // value N of the finishing order: block N/16 of those this wave
     // finishes, value N%16; a block's output is stored after its last value.
     // No branch: values of a missing block (single last block) or of
-    // filters past C_out' are computed and not stored.  Bitpacked output
-    // finishes a value in two parts, the compare (finish_cmp) and, a K step
-    // later in the pipeline, the lane writes and the store (finish_write).
-    auto finish_cmp = [&](auto nc) __attribute__((always_inline)) {
+    // filters past C_out' are computed and not stored.
+    auto finish_cmp = [&](auto nc, auto psc) __attribute__((always_inline)) {
         constexpr int N = decltype(nc)::value;
         constexpr int j = N / 16, v = N % 16;
+        using JC = std::integral_constant<int, j>;
         if constexpr (OUT == OUT_BITS) {
             // the bit of a value (dot - bound) is its sign.  The values are
             // taken last to first (value vv = 15 - v at step v), each sign
@@ -1155,7 +1257,7 @@ __global__ __launch_bounds__(kMfmaThreads) void bconv2d_mfma_fs_kernel(MfmaParam
             // stores block 0's word of pixel lane, lane >= 32 block 1's
             // (S = 1); with S > 1 lanes < 32 store the wave's block.
             constexpr int vv = 15 - v;
-            const uint32_t u = __float_as_uint(fin[j][vv]);
+            const uint32_t u = __float_as_uint(value(JC{}, std::integral_constant<int, vv>{}, psc));
             uint32_t w = v == 0 ? u >> 31 : __builtin_amdgcn_alignbit(word[j], u, 31);
             if constexpr (v == 15) {
                 w = (w | (w << 8)) & 0x00FF00FFu;
@@ -1176,7 +1278,8 @@ __global__ __launch_bounds__(kMfmaThreads) void bconv2d_mfma_fs_kernel(MfmaParam
             const bool store = fvalid && blk < fin_nbp;
             const int mw = m0 + (fin_b0 + blk) * 32;
             const int m = mw + (v >> 2) * 8 + half * 4 + (v & 3);
-            const int c = min(max((int)fin[j][v], p.lo), p.hi);
+            const int c = min(max((int)value(JC{}, std::integral_constant<int, v>{}, psc), p.lo),
+                              p.hi);
             if (store && co_ok && m < m_end) {
                 if constexpr (OUT == OUT_FLOAT)
                     reinterpret_cast<float *>(p.out)[(size_t)m * p.cout + co] =
@@ -1186,23 +1289,19 @@ __global__ __launch_bounds__(kMfmaThreads) void bconv2d_mfma_fs_kernel(MfmaParam
             }
         }
     };
-    // (the second part of a value, a K step after the first: nothing is left
-    // for it since the bitpacked output needs no lane writes)
-    auto finish_write = [&](auto nc) __attribute__((always_inline)) { (void)nc; };
-    // values [LO, HI) of the finishing order, either part
-    auto finish_range = [&](auto fn, auto loc, auto hic) __attribute__((always_inline)) {
+    // values [LO, HI) of the finishing order, from set PS
+    auto finish_range = [&](auto psc, auto loc, auto hic) __attribute__((always_inline)) {
         constexpr int LO = decltype(loc)::value, HI = decltype(hic)::value;
         if constexpr (LO < HI)
             for_each_index([&](auto uc) __attribute__((always_inline)) {
-                fn(std::integral_constant<int, LO + decltype(uc)::value>{});
+                finish_cmp(std::integral_constant<int, LO + decltype(uc)::value>{}, psc);
             }, std::make_integer_sequence<int, HI - LO>{});
     };
-    // finish the blocks in the accumulators at once (outside the pipeline)
-    auto finish_all = [&](int nbp) __attribute__((always_inline)) {
+    // finish the blocks in accumulator set PS at once (outside the pipeline)
+    auto finish_all = [&](int nbp, auto psc) __attribute__((always_inline)) {
         collect_prev(nbp);
         collect_partner();
-        finish_range(finish_cmp, std::integral_constant<int, 0>{}, std::integral_constant<int, NV>{});
-        finish_range(finish_write, std::integral_constant<int, 0>{}, std::integral_constant<int, NV>{});
+        finish_range(psc, std::integral_constant<int, 0>{}, std::integral_constant<int, NV>{});
     };
 
     // ---- the pipelined loop over pairs (and a last single block)
@@ -1220,13 +1319,16 @@ __global__ __launch_bounds__(kMfmaThreads) void bconv2d_mfma_fs_kernel(MfmaParam
     uint32_t vmask;
     asm volatile("v_mov_b32 %0, 0x88888888" : "=v"(vmask));
 
-    // NBP (2 or 1) blocks from b0: K step i issues its products with a
-    // piece of the previous pair's finishing after each (the matrix pipe
-    // runs one product while the wave issues the piece), then refills its
-    // ring slot with step i + D (of these blocks, or of the next ones)
-    auto body = [&](auto nbp_c, auto prev_c, int b0) __attribute__((always_inline)) {
+    // NBP (2 or 1) blocks from b0 on accumulator set SET: K step i issues
+    // its products with a piece of the previous pair's finishing (from the
+    // other set, S = 1) after the first (the matrix pipe runs one product
+    // while the wave issues the piece), then refills its ring slot with step
+    // i + D (of these blocks, or of the next ones)
+    auto body = [&](auto nbp_c, auto prev_c, auto set_c, int b0) __attribute__((always_inline)) {
         constexpr int NBP = decltype(nbp_c)::value;
         constexpr bool has_prev = decltype(prev_c)::value;   // a compile-time branch per step
+        constexpr int SET = decltype(set_c)::value;
+        constexpr auto ps_c = std::integral_constant<int, (SET + 1) % NSET>{};
         const int nxt = b0 + 2 < nb ? b0 + 2 : b0;
         int next_base[2] = {base[0], base[1]};
         if constexpr (NBP == 2) {
@@ -1258,30 +1360,24 @@ __global__ __launch_bounds__(kMfmaThreads) void bconv2d_mfma_fs_kernel(MfmaParam
                 else
                     breg[i] = (breg[i] ^ u32x4{neg, neg, neg, neg}) & u32x4{keep, keep, keep, keep};
             }
-            // finishing pieces: the compares of values [lo, hi) after the
-            // first product, the lane writes of the previous step's values
-            // [plo, phi) after the second (the last ones after the loop)
+            // finishing piece: values [lo, hi) after the first product
             constexpr int lo = i >= kFirst ? (i - kFirst) * kPer : NV;
             constexpr int hi = lo + kPer < NV ? lo + kPer : NV;
-            constexpr int plo = i > kFirst ? (i - 1 - kFirst) * kPer : NV;
-            constexpr int phi = plo + kPer < NV ? plo + kPer : NV;
 #pragma unroll
             for (int j = 0; j < NBP; ++j) {
                 if constexpr (OUT == OUT_BITS)
-                    acc[j] = mfma_fp4(breg[i], ring[i % D][j], i == 0 ? tinit[j] : acc[j]);
+                    acc[SET][j] = mfma_fp4(breg[i], ring[i % D][j],
+                                           i == 0 ? tinit[j % NT] : acc[SET][j]);
                 else
-                    acc[j] = mfma_fp4(ring[i % D][j], breg[i], i == 0 ? zero16 : acc[j]);
+                    acc[SET][j] = mfma_fp4(ring[i % D][j], breg[i], i == 0 ? zero16 : acc[SET][j]);
                 // pin the product here (it touches no memory and would move)
-                asm volatile("" : "+a"(acc[j]) : : "memory");
+                asm volatile("" : "+a"(acc[SET][j]) : : "memory");
                 if constexpr (has_prev) {
                     if (j == 0) {
                         if constexpr (S > 1 && i == 1) collect_partner();
-                        finish_range(finish_cmp, std::integral_constant<int, lo>{},
+                        finish_range(ps_c, std::integral_constant<int, lo>{},
                                      std::integral_constant<int, hi>{});
                     }
-                    if (j == NBP - 1)
-                        finish_range(finish_write, std::integral_constant<int, plo>{},
-                                     std::integral_constant<int, phi>{});
                 }
                 // keep each piece here: a compiler memory barrier for the
                 // passes that move loads and stores, a scheduling barrier for
@@ -1291,12 +1387,6 @@ __global__ __launch_bounds__(kMfmaThreads) void bconv2d_mfma_fs_kernel(MfmaParam
             }
         };
         for_each_index(step, std::make_integer_sequence<int, KS>{});
-        if constexpr (has_prev) {                        // the last step's lane writes
-            constexpr int llo = KS - 1 >= kFirst ? (KS - 1 - kFirst) * kPer : NV;
-            constexpr int lhi = llo + kPer < NV ? llo + kPer : NV;
-            finish_range(finish_write, std::integral_constant<int, llo>{},
-                         std::integral_constant<int, lhi>{});
-        }
         base[0] = next_base[0];
         base[1] = next_base[1];
         fin_b0 = b0;
@@ -1305,21 +1395,45 @@ __global__ __launch_bounds__(kMfmaThreads) void bconv2d_mfma_fs_kernel(MfmaParam
     constexpr auto one = std::integral_constant<int, 1>{};
     constexpr auto yes = std::integral_constant<bool, true>{};
     constexpr auto no = std::integral_constant<bool, false>{};
+    constexpr auto set0 = std::integral_constant<int, 0>{};
+    constexpr auto set1 = std::integral_constant<int, NSET - 1>{};
+    // the last single block (nb odd) on the set after `last`, then the
+    // finishing of whatever is left
+    auto tail = [&](auto last_c) __attribute__((always_inline)) {
+        constexpr auto nxt_c = std::integral_constant<int, (decltype(last_c)::value + 1) % NSET>{};
+        if (nb & 1) {
+            body(one, yes, nxt_c, nb - 1);
+            finish_all(1, nxt_c);
+        } else {
+            finish_all(2, last_c);
+        }
+    };
     // (the bodies after the first are reached only through it, so that the
     // compiler's counter waits find every filter load retired there, and
     // wait for nothing, stores included, inside them)
     if (npairs > 0) {
-        body(two, no, 0);
-        for (int pidx = 1; pidx < npairs; ++pidx) body(two, yes, 2 * pidx);
-        if (nb & 1) {
-            body(one, yes, nb - 1);
-            finish_all(1);
+        body(two, no, set0, 0);
+        if constexpr (NSET == 1) {
+            for (int pidx = 1; pidx < npairs; ++pidx) body(two, yes, set0, 2 * pidx);
+            tail(set0);
         } else {
-            finish_all(2);
+            // pairs alternate between the sets: unrolled by two so that
+            // every set index is a constant
+            int pidx = 1;
+            for (; pidx + 1 < npairs; pidx += 2) {
+                body(two, yes, set1, 2 * pidx);
+                body(two, yes, set0, 2 * pidx + 2);
+            }
+            if (pidx < npairs) {
+                body(two, yes, set1, 2 * pidx);
+                tail(set1);
+            } else {
+                tail(set0);
+            }
         }
     } else if (nb & 1) {
-        body(one, no, nb - 1);
-        finish_all(1);
+        body(one, no, set0, nb - 1);
+        finish_all(1, set0);
     }
 }
 

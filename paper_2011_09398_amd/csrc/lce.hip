@@ -1023,6 +1023,18 @@ lce_status lce_bconv2d_mfma(const lce_bconv2d_desc *desc, const int32_t *x_packe
     p.div_cwh = lce::make_fastdiv((uint32_t)(p.cwe / 2));
     p.div_kw = lce::make_fastdiv((uint32_t)p.kw);
     p.div_groups = lce::make_fastdiv((uint32_t)(p.region_vec == 4 ? p.cw / 4 : p.cwe));
+    // the filter-stationary and K-split kernels read the input and the
+    // filters as buffers, with 32-bit byte offsets and offsets at or past
+    // 2^31 standing for padding: each must stay below 2 GiB
+    {
+        const int64_t x_bytes = (int64_t)d.n * d.h * d.w * p.cw * 4;
+        const int64_t w_bytes = (int64_t)d.kh * d.kw * cwe * p.coutp * 16;
+        if (x_bytes >= (int64_t(1) << 31) || w_bytes >= (int64_t(1) << 31))
+            return fail(LCE_EUNSUPPORTED,
+                        "the matrix-core path takes inputs and widened filters below 2 GiB "
+                        "(input %lld bytes, widened filters %lld bytes)",
+                        (long long)x_bytes, (long long)w_bytes);
+    }
     const int64_t cus = device_simds() / 4;
     const int blocks32 = p.coutp / 32;
     const int nmax = blocks32 >= 4 ? 4 : blocks32 >= 2 ? 2 : 1;

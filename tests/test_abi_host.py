@@ -127,6 +127,33 @@ def test_bconv2d_validation_errors():
     assert call_bconv(desc(c_out=(1 << 20) + 1, c_in=32, h=1, w=1)) == lce.LCE_EINVAL
 
 
+def call_mfma(d, x=P, w=P, m=None, b=None, t=P, flip=None, out=P):
+    return lce.lib().lce_bconv2d_mfma(ctypes.byref(d), x, w, m, b, t, flip, out, None)
+
+
+def test_bconv2d_mfma_validation_errors():
+    """Every refusal comes back before any device call (none is made here)."""
+    assert call_mfma(desc(clamp=(5, 4))) == lce.LCE_EINVAL
+    assert call_mfma(desc(), x=None) == lce.LCE_EINVAL
+    assert call_mfma(desc(), w=None) == lce.LCE_EINVAL
+    assert call_mfma(desc(), out=None) == lce.LCE_EINVAL
+    assert call_mfma(desc(out_type="bitpacked"), t=None) == lce.LCE_EINVAL
+    assert call_mfma(desc(), x=P + 2) == lce.LCE_EALIGN
+    assert call_mfma(desc(), w=P + 4) == lce.LCE_EALIGN        # widened filters: 16 bytes
+    assert call_mfma(desc(out_type="bitpacked"), flip=P + 1) == lce.LCE_EALIGN
+    # exact fp32 dots need K < 2^24
+    assert call_mfma(desc(c_in=2 ** 21, c_out=1, h=1, w=1)) == lce.LCE_EUNSUPPORTED
+    assert "2^24" in lce.last_error()
+    # the input (2^29 words = 2 GiB) and the widened filters are read as
+    # buffers with 31-bit byte offsets
+    assert call_mfma(desc(n=1, h=2 ** 14, w=2 ** 14, c_in=64, c_out=32,
+                          out_type="bitpacked")) == lce.LCE_EUNSUPPORTED
+    assert "2 GiB" in lce.last_error()
+    assert call_mfma(desc(h=1, w=1, c_in=2 ** 18, c_out=2 ** 14, kh=1, kw=1,
+                          out_type="bitpacked")) == lce.LCE_EUNSUPPORTED
+    assert "2 GiB" in lce.last_error()
+
+
 def call_quant(d, x=P, w=P, m=None, b=None, t=P, flip=None, out=P):
     return lce.lib().lce_quantize_bconv2d(ctypes.byref(d), x, w, m, b, t, flip, out, None)
 

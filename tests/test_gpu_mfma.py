@@ -242,6 +242,31 @@ def test_mfma_fs_every_instance(schedule, ks, s, packed):
         assert_match(layer, got, ref, f"{layer.name} {kh}x{kw} cw={cw} {pv}")
 
 
+@pytest.mark.parametrize("ks,s", FS_INSTANCES, ids=lambda v: str(v))
+def test_mfma_fs_repeated_launches(schedule, ks, s):
+    """Four launches of the same layer, each into a fresh poisoned output,
+    all equal to the oracle: layers whose workgroups hold a single pixel
+    block, where the waves without a block of their own compute values they
+    never store (a kernel once read unassigned registers there and returned
+    wrong bits from the second launch on), every output type."""
+    import paper_2011_09398_amd as lce
+    if schedule != "fs":
+        pytest.skip("filter-stationary instances")
+    lce.set_tuning(mfma_fs_ks=ks, mfma_fs_s=s)
+    shapes = fs_layers(ks, s)
+    for j, out in enumerate(["bitpacked", "float", "int32"]):
+        kh, kw, cw = shapes[(j * 7) % len(shapes)]
+        k = kh * kw * 32 * cwe_of(cw)
+        layer = Layer(f"rep{ks}x{s}_{j}", 3, 12, 14, 32 * cwe_of(cw), 200, kh=kh, kw=kw,
+                      padding="valid", out=out, clamp=(-k // 3, k // 2), input_kind="bits")
+        inp = make_layer_inputs(layer, 8, 94, ks * 10 + s + j)
+        ref = oracle_run(layer, inp, oracle_signs(inp))
+        x, w = gpu_input(inp), gpu_pack_weights(inp)
+        for r in range(4):
+            got = sync_np(mfma_run(layer, inp, x_packed=x, w_packed=w))
+            assert_match(layer, got, ref, f"{layer.name} launch {r}")
+
+
 @pytest.mark.parametrize("wpc", ["1", "2"])
 @pytest.mark.parametrize("ks,s", [(9, 1), (18, 1), (9, 2)], ids=lambda v: str(v))
 def test_mfma_fs_workgroups_per_cu(schedule, ks, s, wpc):
