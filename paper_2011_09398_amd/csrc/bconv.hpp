@@ -540,11 +540,28 @@ __host__ inline int table_lds_words(int rows, int fwg) { return (rows * fwg + 63
 // fields at their maxima, i.e. not waited on.)
 __device__ __forceinline__ void wait_table() { __builtin_amdgcn_s_waitcnt(0x0F70); }
 
+// VEC words of a raw buffer (gfx9 buffer resource: base, byte size, no
+// stride) at byte offset `off`; an offset at or past the size reads zeros.
+template <int VEC>
+__device__ __forceinline__ typename VecOf<VEC>::type buffer_vec(__amdgpu_buffer_rsrc_t r, int off) {
+    if constexpr (VEC == 4) {
+        const auto v = __builtin_amdgcn_raw_buffer_load_b128(r, off, 0, 0);
+        return uint4{v[0], v[1], v[2], v[3]};
+    } else if constexpr (VEC == 2) {
+        const auto v = __builtin_amdgcn_raw_buffer_load_b64(r, off, 0, 0);
+        return uint2{v[0], v[1]};
+    } else {
+        return __builtin_amdgcn_raw_buffer_load_b32(r, off, 0, 0);
+    }
+}
+
 // One lane's share of its im2col row (shape known at compile time): wave w
 // holds taps w, w+4, ... of its pixel, CW words each, read as VEC-word
-// vectors (the tensor aligned to 4*VEC bytes).  load() issues every global
-// load; a padded tap loads the image's first pixel (always in bounds) and
-// store() writes it as 0 words (one padding).
+// vectors (the tensor aligned to 4*VEC bytes).  load() issues every load,
+// as buffer loads of the input (the host keeps it below 2^31 bytes): a
+// padded tap (or a lane past the last pixel) takes an offset past the
+// input and reads 0 words, one padding, so nothing is predicated and
+// store() writes every tap as loaded.
 template <int CW, int KH, int KW, int VEC>
 struct TapStage {
     static constexpr int kTaps = KH * KW;
@@ -552,21 +569,23 @@ struct TapStage {
     static constexpr int kVecs = CW / VEC;
     using Vec = typename VecOf<VEC>::type;
     Vec v[kIters][kVecs];
-    bool in[kIters];
 
-    // ximg: the pixel's image; (iy0, ix0): its window origin
-    __device__ __forceinline__ void load(const BconvParams &p, const uint32_t *ximg, int wave,
+    // img_off: word offset of the pixel's image; (iy0, ix0): its window origin
+    __device__ __forceinline__ void load(const BconvParams &p, uint32_t img_off, int wave,
                                          bool px_ok, int iy0, int ix0) {
+        const __amdgpu_buffer_rsrc_t xb = __builtin_amdgcn_make_buffer_rsrc(
+            const_cast<uint32_t *>(p.x), (short)0,
+            (int)((uint32_t)p.n * p.h * p.wd * CW * 4u), 0x00020000);
 #pragma unroll
         for (int i = 0; i < kIters; ++i) {
             const int t = min(wave + i * kWaves, kTaps - 1);
             const int ky = t / KW, kx = t - (t / KW) * KW;
             const int iy = iy0 + ky, ix = ix0 + kx;
-            in[i] = px_ok && (unsigned)iy < (unsigned)p.h && (unsigned)ix < (unsigned)p.wd;
-            const uint32_t off = in[i] ? ((uint32_t)iy * (uint32_t)p.wd + (uint32_t)ix) * CW : 0u;
-            const Vec *src = reinterpret_cast<const Vec *>(ximg + off);
+            const bool in = px_ok && (unsigned)iy < (unsigned)p.h && (unsigned)ix < (unsigned)p.wd;
+            const int off = in ? (int)((img_off + ((uint32_t)iy * (uint32_t)p.wd + (uint32_t)ix) * CW) * 4u)
+                               : (int)0x80000000u;
 #pragma unroll
-            for (int c = 0; c < kVecs; ++c) v[i][c] = src[c];
+            for (int c = 0; c < kVecs; ++c) v[i][c] = buffer_vec<VEC>(xb, off + c * VEC * 4);
         }
     }
 
@@ -578,7 +597,7 @@ struct TapStage {
             if (t < kTaps) {
                 Vec *dst = reinterpret_cast<Vec *>(row + t * CW);
 #pragma unroll
-                for (int c = 0; c < kVecs; ++c) dst[c] = in[i] ? v[i][c] : VecOf<VEC>::zero();
+                for (int c = 0; c < kVecs; ++c) dst[c] = v[i][c];
             }
         }
     }
@@ -615,7 +634,7 @@ __global__ __launch_bounds__(kThreads) void bconv2d_static_kernel(BconvParams p)
     // fetched while those loads are in flight.
     {
         TapStage<CW, KH, KW, VEC> taps;
-        taps.load(p, p.x + img_off, wave, px_ok, iy0, ix0);
+        taps.load(p, img_off, wave, px_ok, iy0, ix0);
         if constexpr (PADZ) stage_table<kTableRows>(p, co_wg, wave, lane, sat);
         load_bounds<OUT, PADZ>(p, co_wg, p.fwg, bound);
         taps.store(lds + lane * kRS, wave);

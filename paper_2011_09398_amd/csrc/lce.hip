@@ -306,8 +306,18 @@ bool has_static(int cw, int kh, int kw) {
     return false;
 }
 
+// The shape-specialized kernels stage the input through buffer loads (byte
+// offsets below 2^31); a larger input runs the generic kernel.
+bool input_fits_buffer(const BconvParams &p) {
+    return (int64_t)p.n * p.h * p.wd * p.cw * 4 < (int64_t(1) << 31);
+}
+
 template <int OUT, bool PADZ>
 void dispatch(const BconvParams &p, dim3 grid, hipStream_t s, int vec) {
+    if (!input_fits_buffer(p)) {
+        launch_generic<OUT, PADZ>(p, grid, s);
+        return;
+    }
     if (p.kh == 3 && p.kw == 3) {
         switch (p.cw) {
             case 1: launch_static<1, 3, 3, OUT, PADZ>(p, grid, s, vec); return;
@@ -686,7 +696,7 @@ lce_status lce_bconv2d(const lce_bconv2d_desc *desc, const int32_t *x_packed,
     p.rs = lce::row_stride(p.slab);
 
     const int filters = d.out_type == LCE_OUT_BITPACKED ? p.cwo * 32 : p.cout;
-    if (has_static(p.cw, p.kh, p.kw)) {
+    if (has_static(p.cw, p.kh, p.kw) && input_fits_buffer(p)) {
         choose_schedule(p, filters);
     } else {
         p.nb = 1; p.ks = 1; p.fwg = lce::kWaves * lce::kRN; p.ksplit = p.kwords;
