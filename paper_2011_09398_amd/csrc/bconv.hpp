@@ -108,11 +108,17 @@ struct BconvParams {
     int32_t fwg;            // filters per workgroup = (4 / ks) * nb * RN
     int32_t ksplit;         // K words per split (multiple of 4), ks > 1
     int32_t out_vec4;       // out is 16-byte aligned (float output may use float4 stores)
-    int32_t slab;           // generic kernel: words staged per pass
-    int32_t rs;             // generic kernel: LDS row stride (words)
+    int32_t tiles;          // static kernel: grid size when the tiles are renumbered
+                            // filter-major per XCD, 0 = launch order
+    FastDiv div_tile;       // static kernel, filter-major: tile index -> filter group (by grid x)
     const uint32_t *flip;   // [Cwo] or null: output bits to invert (bitpacked output)
+    // (the fields above fill the first three 64-byte lines, which the static
+    // kernel fetches at once; those below serve zero padding, the generic and
+    // the quantize-fused kernels)
     const int32_t *padc;    // zero padding: table T [(KH+1)*KW*(KW+1)/2][Cout]
     FastDiv div_fwg;        // static kernel, zero padding: flat table index -> row
+    int32_t slab;           // generic kernel: words staged per pass
+    int32_t rs;             // generic kernel: LDS row stride (words)
     const float *xf;        // quantize-fused kernel: float32 input [N][H][W][32*Cw]
     int32_t band_rows;      // quantize-fused kernel: rows of the tallest input band
     int32_t band_pack;      // quantize-fused kernel: LDS word offset of the packed band
@@ -603,6 +609,42 @@ struct TapStage {
     }
 };
 
+// Workgroup tile (pixel block bx, filter group by) of this launch index.
+// The 8 XCDs take the workgroups round-robin in launch order (index L to
+// XCD L % 8), each with its own L2, so in launch order every XCD's blocks
+// span all filter groups and every L2 fetches every filter.  Where the
+// filters outweigh the input, the tiles are renumbered filter-major (the
+// tiles of one filter group consecutive) and XCD x runs the contiguous
+// range [x*q + min(x, r), ...) of the T = 8q + r tiles: each L2 then
+// fetches an eighth of the filters.  (Pixel-major ranges cut the input's
+// re-reads likewise where the input is larger, but measured no faster than
+// the launch order.)
+constexpr uint32_t kXcdCount = 8;
+
+// The first three 64-byte lines of the kernel arguments (one field of
+// each: every field the static kernel reads outside zero padding), fetched
+// in one round trip at the top of the kernel: the compiler would otherwise
+// load them in dependent batches (behind the tile-order branch and the
+// pixel test), each first touch of a line a full memory latency.
+__device__ __forceinline__ void fetch_arg_lines(const BconvParams &p) {
+    asm volatile("" ::"s"(p.x), "s"(p.oh), "s"(p.div_ow.magic));
+}
+
+__device__ __forceinline__ void static_tile(const BconvParams &p, int &bx, int &by) {
+    if (!p.tiles) {
+        bx = blockIdx.x;
+        by = blockIdx.y;
+        return;
+    }
+    const uint32_t gx = p.div_tile.d, T = (uint32_t)p.tiles;
+    const uint32_t L = blockIdx.y * gx + blockIdx.x;
+    const uint32_t q = T / kXcdCount, r = T % kXcdCount, x = L % kXcdCount;
+    const uint32_t t = x * q + min(x, r) + L / kXcdCount;
+    const uint32_t fg = fast_div(t, p.div_tile);
+    bx = (int)(t - fg * gx);
+    by = (int)fg;
+}
+
 // Shape-specialized kernel: Cw, KH, KW known at compile time, so the whole
 // im2col row fits one LDS slab and the filter-row offsets are immediates.
 // VEC = words per global load when staging (needs x aligned to 4*VEC bytes).
@@ -619,11 +661,14 @@ __global__ __launch_bounds__(kThreads) void bconv2d_static_kernel(BconvParams p)
     __shared__ __attribute__((aligned(16))) uint32_t bound[kMaxFiltersWG];
     extern __shared__ __attribute__((aligned(16))) int32_t sat[];   // PADZ: kTableRows rows
 
+    fetch_arg_lines(p);
     const int lane = threadIdx.x & 63;
     const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
-    const int m = blockIdx.x * kPix + lane;
+    int bx, by;
+    static_tile(p, bx, by);
+    const int m = bx * kPix + lane;
     const bool px_ok = m < p.m;
-    const int co_wg = blockIdx.y * p.fwg;
+    const int co_wg = by * p.fwg;
     uint32_t img_off = 0;
     int iy0 = 0, ix0 = 0;
     if (px_ok) pixel_origin(p, m, img_off, iy0, ix0, CW);

@@ -269,12 +269,19 @@ const char *quant_unsupported(const lce_bconv2d_desc &d, const Geometry &g) {
 }
 
 template <int CW, int KH, int KW, int OUT, bool PADZ>
-void launch_static(const BconvParams &p, dim3 grid, hipStream_t s, int vec) {
+void launch_static(const BconvParams &p0, dim3 grid, hipStream_t s, int vec) {
     // zero padding: the correction table's rows in dynamic LDS
     const size_t lds =
-        PADZ ? (size_t)lce::table_lds_words((KH + 1) * lce::interval_count(KW), p.fwg) *
+        PADZ ? (size_t)lce::table_lds_words((KH + 1) * lce::interval_count(KW), p0.fwg) *
                    sizeof(int32_t)
              : 0;
+    // tiles renumbered filter-major per XCD where the filters outweigh the
+    // input
+    BconvParams p = p0;
+    const double filter_bytes = 4.0 * p.cout * p.kwords;
+    const double input_bytes = 4.0 * p.n * p.h * p.wd * p.cw;
+    p.tiles = filter_bytes > input_bytes ? (int)(grid.x * grid.y) : 0;
+    p.div_tile = lce::make_fastdiv(grid.x);
     if (vec == 4 && CW % 4 == 0)
         hipLaunchKernelGGL(
             (lce::bconv2d_static_kernel<CW, KH, KW, (CW % 4 == 0 ? 4 : 1), OUT, PADZ>), grid,
