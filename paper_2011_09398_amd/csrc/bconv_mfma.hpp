@@ -715,6 +715,31 @@ __device__ __forceinline__ void region_finish(const MfmaParams &p, u32x4 *atile,
     }
 }
 
+// Bitpacked output of one transposed 32x32 accumulator block (filters as
+// the row operand: lane = pixel lane % 32, value v = filter (v/4)*8 +
+// half*4 + v%4), given the dot bounds t[q] of filters 8q + half*4 + 0..3.
+// Bit f of the returned word (the same in lanes l and l + 32) is filter f's
+// "dot < T", the sign of dot - T (an integer dot below 2^24 minus an
+// integer or infinite bound: exact in sign).  The signs are shifted into a
+// word last value first (one v_alignbit_b32 each), so that bit v is value
+// v's; nibble q then moves to nibble 2q + half and the lane halves merge.
+__device__ __forceinline__ uint32_t transposed_block_bits(const mfma_v16f &val,
+                                                          const float4 (&t)[4], int half) {
+    uint32_t w = 0;
+#pragma unroll
+    for (int k = 0; k < 16; ++k) {
+        const int v = 15 - k;
+        const float4 tq = t[v >> 2];
+        const float tv = (v & 3) == 0 ? tq.x : (v & 3) == 1 ? tq.y : (v & 3) == 2 ? tq.z : tq.w;
+        const uint32_t u = __float_as_uint(val[v] - tv);
+        w = k == 0 ? u >> 31 : __builtin_amdgcn_alignbit(w, u, 31);
+    }
+    w = (w | (w << 8)) & 0x00FF00FFu;
+    w = ((w | (w << 4)) & 0x0F0F0F0Fu) << (4 * half);
+    const auto sw = __builtin_amdgcn_permlane32_swap(w, w, false, false);
+    return sw[0] | sw[1];
+}
+
 // K-split schedule, for layers whose output tile per workgroup is small
 // next to K (few pixels, many channels).  The four waves of a workgroup
 // compute the same 32*MBW pixels x 32*NBLK filters, each over a quarter of
@@ -787,8 +812,10 @@ __global__ __launch_bounds__(kMfmaThreads) void bconv2d_mfma_ks_kernel(MfmaParam
     // after the region's, so that its widening does not wait for them; an
     // absent array reads zeros, replaced by the default)
     float ep_a[NBLK], ep_b[NBLK];
+    uint32_t flip_w[NBLK];                               // bitpacked output: flip words
     {
         const uint32_t cb = (uint32_t)p.cout * 4u;
+        const __amdgpu_buffer_rsrc_t fb = buffer_of(p.flip, p.flip ? (uint32_t)p.cwo * 4u : 0u);
         const __amdgpu_buffer_rsrc_t ab = buffer_of(OUT == OUT_BITS ? p.thr : p.mult,
                                                     OUT == OUT_BITS || p.mult ? cb : 0u);
         const __amdgpu_buffer_rsrc_t bb = buffer_of(p.bias, p.bias ? cb : 0u);
@@ -796,6 +823,10 @@ __global__ __launch_bounds__(kMfmaThreads) void bconv2d_mfma_ks_kernel(MfmaParam
         for (int i = 0; i < NBLK; ++i) {
             const int co4 = min(n_base + 32 * i + l32, p.cout - 1) * 4;
             ep_a[i] = ep_b[i] = 0.0f;
+            flip_w[i] = 0u;
+            if constexpr (OUT == OUT_BITS)
+                flip_w[i] = __builtin_amdgcn_raw_buffer_load_b32(
+                    fb, min((n_base >> 5) + i, p.cwo - 1) * 4, 0, 0);
             if constexpr (OUT == OUT_BITS) {
                 ep_a[i] = __uint_as_float(__builtin_amdgcn_raw_buffer_load_b32(ab, co4, 0, 0));
             } else if constexpr (OUT == OUT_FLOAT) {
@@ -834,6 +865,20 @@ __global__ __launch_bounds__(kMfmaThreads) void bconv2d_mfma_ks_kernel(MfmaParam
     // words arrive, while the filter ring is still arriving
     region_widen<kMfmaThreads>(g, rch, atile, plane, tid, 0);
     region_finish<kMfmaThreads>(g, atile, row0, plane, tid);
+    // bitpacked output: the dot bound of each of the workgroup's filters, in
+    // LDS past the A planes and the reduction buffer (tb[32*ib + f] for
+    // filter n_base + 32*ib + f; filters past C_out get -inf, bit 0)
+    float *tb = reinterpret_cast<float *>(
+        reinterpret_cast<char *>(smem) + max(p.cwe * plane * 16, kBlocks * 3 * 16 * 64 * 4));
+    if constexpr (OUT == OUT_BITS) {
+        if (wave == 0 && half == 0) {
+#pragma unroll
+            for (int ib = 0; ib < NBLK; ++ib)
+                tb[32 * ib + l32] = n_base + 32 * ib + l32 < p.cout
+                                        ? thr_to_dot_bound_f(ep_a[ib], p.lo, p.hi)
+                                        : -INFINITY;
+        }
+    }
     int z = lds_barrier();                               // the A planes are complete
 
     mfma_v16f acc[MBW][NBLK];
@@ -868,7 +913,12 @@ __global__ __launch_bounds__(kMfmaThreads) void bconv2d_mfma_ks_kernel(MfmaParam
 #pragma unroll
         for (int ib = 0; ib < NBLK; ++ib)
 #pragma unroll
-            for (int b = 0; b < MBW; ++b) acc[b][ib] = mfma_fp4(acur[b], cur[ib], acc[b][ib]);
+            for (int b = 0; b < MBW; ++b) {
+                if constexpr (OUT == OUT_BITS)      // transposed: lane = pixel
+                    acc[b][ib] = mfma_fp4(cur[ib], acur[b], acc[b][ib]);
+                else
+                    acc[b][ib] = mfma_fp4(acur[b], cur[ib], acc[b][ib]);
+            }
 #pragma unroll
         for (int b = 0; b < MBW; ++b)
 #pragma unroll
@@ -922,7 +972,8 @@ __global__ __launch_bounds__(kMfmaThreads) void bconv2d_mfma_ks_kernel(MfmaParam
 
     // ---- epilogue on this wave's blocks.  Value v of block (b, ib) is
     // pixel (v/4)*8 + half*4 + v%4 of pixel block b and filter
-    // n_base + 32*ib + l32.
+    // n_base + 32*ib + l32; bitpacked output (transposed products): pixel
+    // l32 of block b and filter n_base + 32*ib + (v/4)*8 + half*4 + v%4.
     const int nblk = min(NBLK, (p.coutp - n_base) >> 5);
 #pragma unroll
     for (int j = 0; j < kBlocks; ++j) {
@@ -934,13 +985,18 @@ __global__ __launch_bounds__(kMfmaThreads) void bconv2d_mfma_ks_kernel(MfmaParam
         const bool co_ok = co < p.cout;
         const int mw = m0 + b * 32;
         if constexpr (OUT == OUT_BITS) {
-            const float T = co_ok ? thr_to_dot_bound_f(ep_a[ib], p.lo, p.hi) : -INFINITY;
-            const uint32_t word =
-                p.flip ? block_bits(val, T, block_flip(p.flip, (n_base >> 5) + ib, co_ok))
-                       : block_bits(val, T, 0);
-            const int m = mw + lane;
+            float4 t[4];
+#pragma unroll
+            for (int q = 0; q < 4; ++q)
+                t[q] = reinterpret_cast<const float4 *>(tb + 32 * ib + 8 * q + 4 * half)[z];
+            uint32_t word = transposed_block_bits(val, t, half);
+            // the flip word of the block (0 without a flip mask), restricted
+            // to the filters below C_out
+            const int nv = p.cout - (n_base + 32 * ib);
+            word ^= flip_w[ib] & (nv >= 32 ? ~0u : (1u << nv) - 1u);
+            const int m = mw + l32;
             if (lane < 32 && m < p.m)
-                reinterpret_cast<uint32_t *>(p.out)[(size_t)m * p.cwo + (co >> 5)] = word;
+                reinterpret_cast<uint32_t *>(p.out)[(size_t)m * p.cwo + (n_base >> 5) + ib] = word;
         } else {
 #pragma unroll
             for (int v = 0; v < 16; ++v) {

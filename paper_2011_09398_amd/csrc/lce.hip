@@ -616,15 +616,13 @@ FsPlan plan_mfma_fs(const lce::MfmaParams &p, int64_t cus, int blocks32, int kst
     return best;
 }
 
-// LDS of the K-split kernel: every widened word of the region followed by
-// the packed region it is widened from (with the 256-word slack of its last
-// DMA instruction), or the reduction buffer (three partial copies of every
-// 32x32 block), which reuses them.
+// LDS of the K-split kernel: every widened word of the region, or the
+// reduction buffer (three partial copies of every 32x32 block), which
+// reuses it; then the dot bounds of the workgroup's filters.
 size_t mfma_ks_lds(const lce::MfmaParams &p, int mbw, int nblk, int tile_rows) {
     const size_t a = (size_t)p.cwe * tile_rows * p.pw * 16;
-    const size_t bits = ((size_t)tile_rows * p.pw * p.cw + 256) * 4;
     const size_t red = (size_t)mbw * nblk * 3 * 16 * 64 * 4;
-    return std::max(a + bits, red);
+    return std::max(a, red) + (size_t)nblk * 32 * 4;
 }
 
 }  // namespace
