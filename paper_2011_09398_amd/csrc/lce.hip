@@ -531,25 +531,20 @@ struct FsShape {
 };
 constexpr FsShape kFsShapes[] = {{9, 1}, {18, 1}, {5, 2}, {9, 2}, {18, 2}, {18, 4}};
 
-// LDS of the filter-stationary kernel: every widened word of the region,
-// then the larger of the packed region (staged before the loop, with the
-// 256-word slack of its last DMA instruction) and (S > 1) the partial-sum
-// exchange: two buffers x F filter blocks x two pixel blocks x (S-1)
-// partials, 4 KB each; then the bounds of the F filter blocks (bitpacked
-// output) and the A-tile offset of each pixel's window origin (one int per
-// pixel of the workgroup's whole blocks).
-// Bytes from the end of the A tile to the bounds of a bitpacked output
-// (after the larger of the packed region and the exchange, 16-byte aligned).
-size_t mfma_fs_thr_offset(const lce::MfmaParams &p, FsShape sh, int tile_rows) {
-    const size_t bits = ((size_t)tile_rows * p.pw * p.cw + 256) * 4;
-    const size_t red = sh.s > 1 ? (size_t)2 * (4 / sh.s) * 2 * (sh.s - 1) * 4096 : 0;
-    return (std::max(bits, red) + 15) / 16 * 16;
+// LDS of the filter-stationary kernel: every widened word of the region
+// (staged through registers), then (S > 1) the partial-sum exchange: two
+// buffers x F filter blocks x two pixel blocks x (S-1) partials, 4 KB each;
+// then the bounds of the F filter blocks (bitpacked output) and the A-tile
+// offset of each pixel's window origin (one int per pixel of the
+// workgroup's whole blocks).
+// Bytes from the end of the A tile to the bounds (after the exchange).
+size_t mfma_fs_thr_offset(FsShape sh) {
+    return sh.s > 1 ? (size_t)2 * (4 / sh.s) * 2 * (sh.s - 1) * 4096 : 0;
 }
 
 size_t mfma_fs_lds(const lce::MfmaParams &p, FsShape sh, int tile_rows, int pixels) {
     const size_t a = (size_t)p.cwe * tile_rows * p.pw * 16;
-    return a + mfma_fs_thr_offset(p, sh, tile_rows) + (4 / sh.s) * 32 * 4 +
-           (size_t)(pixels + 31) / 32 * 32 * 4;
+    return a + mfma_fs_thr_offset(sh) + (4 / sh.s) * 32 * 4 + (size_t)(pixels + 31) / 32 * 32 * 4;
 }
 
 struct FsPlan {
@@ -1081,7 +1076,7 @@ lce_status lce_bconv2d_mfma(const lce_bconv2d_desc *desc, const int32_t *x_packe
         if (fp.shape.ks) {
             p.tile_rows = fp.tile_rows;
             p.fs_pixels = fp.pixels;
-            p.fs_thr_off = (int32_t)(mfma_fs_thr_offset(p, fp.shape, fp.tile_rows) / 4);
+            p.fs_thr_off = (int32_t)(mfma_fs_thr_offset(fp.shape) / 4);
             p.div_plane = lce::make_fastdiv((uint32_t)(fp.tile_rows * p.pw));
             fill_step_table(p, d, fp.tile_rows * p.pw, (int)ksteps);
             size_t lds = fp.lds;
