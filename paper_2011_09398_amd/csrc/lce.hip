@@ -276,11 +276,12 @@ void launch_static(const BconvParams &p0, dim3 grid, hipStream_t s, int vec) {
                    sizeof(int32_t)
              : 0;
     // tiles renumbered filter-major per XCD where the filters outweigh the
-    // input
+    // input (and the tile count fits the kernel's 32-bit tile arithmetic)
     BconvParams p = p0;
     const double filter_bytes = 4.0 * p.cout * p.kwords;
     const double input_bytes = 4.0 * p.n * p.h * p.wd * p.cw;
-    p.tiles = filter_bytes > input_bytes ? (int)(grid.x * grid.y) : 0;
+    const int64_t tiles = (int64_t)grid.x * grid.y;
+    p.tiles = filter_bytes > input_bytes && tiles <= INT32_MAX ? (int)tiles : 0;
     p.div_tile = lce::make_fastdiv(grid.x);
     if (vec == 4 && CW % 4 == 0)
         hipLaunchKernelGGL(
