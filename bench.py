@@ -253,7 +253,7 @@ def time_graph_steps(step: Step, steps: int) -> float:
 def time_repeated(fn, reps: int, graph: bool) -> float:
     """Average duration (ms) of `fn` launched `reps` times back to back."""
     import torch
-    for _ in range(5):
+    for _ in range(10):
         fn()
     torch.cuda.synchronize()
     e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
@@ -278,6 +278,36 @@ def time_repeated(fn, reps: int, graph: bool) -> float:
         e1.record()
     torch.cuda.synchronize()
     return e0.elapsed_time(e1) / reps
+
+
+TRIALS = 7
+
+
+def time_trials(fn, reps: int, graph: bool, trials: int = TRIALS):
+    """`trials` timings of time_repeated (ms each): the per-layer figures
+    are their median, with p10 and p90 beside it."""
+    return [time_repeated(fn, reps, graph) for _ in range(trials)]
+
+
+def trial_fields(ts):
+    """median (ms) and the record's spread fields of a list of trials."""
+    import numpy as np
+    a = np.asarray(ts) * 1e3
+    return float(np.median(a)) / 1e3, {
+        "trials": len(ts), "us_p10": round(float(np.percentile(a, 10)), 3),
+        "us_p90": round(float(np.percentile(a, 90)), 3)}
+
+
+def inputs_digest(inp):
+    """The first 16 hex digits of the SHA-256 of each generated tensor of a
+    layer (the same buffers the oracle and the GPU consume)."""
+    from workloads import sha256
+    out = {}
+    for name in ("x_float", "x_words", "w_float", "mult", "bias", "thr"):
+        a = getattr(inp, name, None)
+        if a is not None:
+            out[name] = sha256(a)[:16]
+    return out
 
 
 def layer_record(layer, ms, probe_tops=None, kind="xor", times=None):
@@ -586,7 +616,19 @@ def cpu_baseline(cfg_idx: int, target_s: float):
             "kind": "oracle",
             "sample": f"the whole step on {images} of {n} images, {reps} pass(es) "
                       f"({ops / 1e9:.2f} G binary ops, {dt:.2f} s wall)",
-            "cpu": platform.processor() or platform.machine()}
+            "cpu": cpu_model()}
+
+
+def cpu_model() -> str:
+    """The host CPU's model name (/proc/cpuinfo), else the platform's."""
+    try:
+        with open("/proc/cpuinfo") as f:
+            for line in f:
+                if line.startswith("model name"):
+                    return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    return platform.processor() or platform.machine()
 
 
 def measured_traffic(layer_name, kind):
@@ -665,14 +707,17 @@ def main():
         log("VALU xor+popcount probe")
         probe = valu_probe()
 
-    log(f"per-launch timing, {args.reps} launches each")
+    log(f"per-launch timing, {TRIALS} trials of {args.reps} launches each")
     layers = []
-    for pack, call, layer, kind, times in zip(step.packs, step.calls, step.layers, step.kinds,
-                                              step.times):
+    for pack, call, layer, kind, times, inp in zip(step.packs, step.calls, step.layers,
+                                                   step.kinds, step.times, step.inputs):
         if pack is not None:   # the layer's line below covers bitpack + conv
             layers.append(bitpack_record(layer, time_repeated(pack, args.reps, graph=False)))
-        layers.append(layer_record(layer, time_repeated(call, args.reps, graph=False), probe,
-                                   kind, times))
+        ms, spread = trial_fields(time_trials(call, args.reps, graph=False))
+        r = layer_record(layer, ms, probe, kind, times)
+        r.update(spread)
+        r["inputs_sha256"] = inputs_digest(inp)
+        layers.append(r)
     conv = [r for r in layers if "binary_ops" in r]
     dom = max(conv, key=lambda r: r["us"])
     roofline = roofline_record(dom, dom["kernel"], cfg_idx, probe)
@@ -680,8 +725,10 @@ def main():
     # against the VALU peak, whichever implementation the step uses.
     xor_layers = []
     for call, layer in zip(step.xor_calls, step.layers):
-        xor_layers.append(layer_record(layer, time_repeated(call, args.reps, graph=False),
-                                       probe, "xor"))
+        ms, spread = trial_fields(time_trials(call, args.reps, graph=False))
+        r = layer_record(layer, ms, probe, "xor")
+        r.update(spread)
+        xor_layers.append(r)
     roofline_valu = roofline_record(max(xor_layers, key=lambda r: r["us"]), "xor", cfg_idx,
                                     probe)
     roofline_valu["layers_valu_frac"] = {r["layer"]: r["valu_frac"] for r in xor_layers}
