@@ -179,8 +179,9 @@ __device__ __forceinline__ void write_value_bits(uint64_t m, uint32_t &word) {
         : "s"((uint32_t)m), "s"((uint32_t)(m >> 32)), "i"(r0), "i"(r0 + 4));
 }
 
-// Bitpacked output of one 32x32 accumulator block.  Value v of the block is
-// pixel (v/4)*8 + half*4 + v%4 and filter lane % 32, so one ballot of
+// Bitpacked output of one 32x32 accumulator block (pixel-split schedule).
+// Value v of the block is pixel (v/4)*8 + half*4 + v%4 and filter
+// lane % 32, so one ballot of
 // "value < T" over the wave gives the 32 filter bits of two pixels (lanes
 // 0-31 and 32-63); v_writelane drops each 32-bit half into the lane of its
 // pixel.  fmask (wave-uniform) flips chosen filters.  Lane l < 32 returns
@@ -755,6 +756,10 @@ __device__ __forceinline__ uint32_t transposed_block_bits(const mfma_v16f &val,
 //     wave owns to that wave through LDS in one exchange (block j belongs to
 //     wave j % 4); the owner adds them (fp32 adds of integers below 2^24 are
 //     exact in any order) and applies the output transform.
+//   * Bitpacked output: the products are transposed (filters as the row
+//     operand, lane = pixel), so that each lane packs its own pixel's filter
+//     bits from the signs of dot - bound (transposed_block_bits), with the
+//     bounds of the workgroup's filters in LDS.
 //   (Loading the packed filter copy and widening it at use, as the
 //   filter-stationary schedule does, measured 10% slower here.)
 //   * Tiles are renumbered so that each of the 8 XCDs (which take the
