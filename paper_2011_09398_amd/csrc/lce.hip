@@ -396,8 +396,8 @@ int device_simds() { return 4 * device_attribute<hipDeviceAttributeMultiprocesso
 // and set-up, ~35 per extra block and ~20 for a K-split reduction (counts
 // from the measured instruction mix).  Schedules with fewer than 2 waves per
 // SIMD are only used when nothing else is possible: a lone wave cannot hide
-// its own memory latency.  LCE_BCONV_NB / LCE_BCONV_KS override the choice
-// (tuning only).
+// its own memory latency.  The xor_nb / xor_ks tuning keys override the
+// choice.
 void choose_schedule(BconvParams &p, int filters) {
     const long pix_blocks = (p.m + lce::kPix - 1) / lce::kPix;
     const long units = pix_blocks * ((filters + lce::kRN - 1) / lce::kRN);
@@ -562,7 +562,8 @@ struct FsPlan {
 // steps).  With KS = 18 the second workgroup's filter loads and widening
 // cost more than the overlap gains (measured slower on 28x28x128).  Every
 // instance with S = 1 and KS <= 9 keeps its registers within the 256 per
-// lane that two waves per SIMD leave.  LCE_MFMA_FS_WPC = 1 / 2 forces it.
+// lane that two waves per SIMD leave.  The mfma_fs_wpc tuning key (1 or 2)
+// forces it.
 int fs_wgs_per_cu(FsShape sh) {
     const int e = tuning(LCE_TUNE_MFMA_FS_WPC);
     if (e == 1 || e == 2) return e;
@@ -1052,12 +1053,15 @@ lce_status lce_bconv2d_mfma(const lce_bconv2d_desc *desc, const int32_t *x_packe
 
     // K-split schedule (all four waves on one tile, K divided among them),
     // for long K: it widens the whole input region up front and ends with a
-    // reduction, which pay off from about 12 K steps per wave on (measured
-    // on 3x3 layers: 72 K steps 1.6x faster than the pixel split, 36 or
-    // fewer slower).  The tile is 32*MBW pixels x 32*NBLK filters: the
-    // largest (at most eight 32x32 blocks) whose grid still gives every CU
-    // 1.5 workgroups, among those whose LDS fits.  LCE_MFMA_KS=1 / 0 force
-    // either schedule (the K-split one where its LDS fits).
+    // reduction, which pay off from about 5 K steps per wave on (measured
+    // on the batch-1 sweep layers with 25 and 27 K steps, which no
+    // filter-stationary instance covers within 1/8 padding: 3.7-5.7 us
+    // against 7.4-10.2 us on the pixel split, whose K stages run one after
+    // another behind barriers).  The tile is 32*MBW pixels x 32*NBLK
+    // filters: the largest (at most eight 32x32 blocks) whose grid still
+    // gives every CU 1.5 workgroups, among those whose LDS fits.  The
+    // mfma_schedule tuning key forces either schedule (the K-split one where
+    // its LDS fits).
     const int64_t ksteps = (int64_t)d.kh * d.kw * (p.cwe / 2);
     // 0 auto, 1 filter-stationary, 2 K split, 3 pixel split
     const int sched = tuning(LCE_TUNE_MFMA_SCHEDULE);
@@ -1065,11 +1069,11 @@ lce_status lce_bconv2d_mfma(const lce_bconv2d_desc *desc, const int32_t *x_packe
 
     // Filter-stationary schedule: the default wherever an instance fits, up
     // to 36 K steps.  Longer K runs on the K-split schedule below unless an
-    // instance is forced (LCE_MFMA_FS_KS / _S): with S = 4 waves per filter
-    // block every filter group re-widens the same input region and the
-    // partial sums add LDS traffic, measured slower than the K split on the
-    // 7x7x512 layer.  LCE_MFMA_FS=0 turns it off, LCE_MFMA_KS forces one of
-    // the others.
+    // instance is forced (tuning keys mfma_fs_ks and mfma_fs_s): with S = 4
+    // waves per filter block every filter group re-widens the same input
+    // region and the partial sums add LDS traffic, measured slower than the
+    // K split on the 7x7x512 layer.  The mfma_schedule key forces one of the
+    // others.
     const bool fs_forced = tuning(LCE_TUNE_MFMA_FS_KS) && tuning(LCE_TUNE_MFMA_FS_S);
     if (ks_env < 0 &&
         (ksteps <= 36 || (fs_forced && ksteps <= 72))) {
@@ -1083,7 +1087,7 @@ lce_status lce_bconv2d_mfma(const lce_bconv2d_desc *desc, const int32_t *x_packe
             size_t lds = fp.lds;
             // claim more than 1/(wpc+1) of a CU's LDS when the grid fits the
             // CUs, so that no CU holds more than wpc workgroups while another
-            // holds fewer (LCE_MFMA_FS_PAD=0 turns this off)
+            // holds fewer (tuning key mfma_fs_pad = -1 turns this off)
             const int64_t wgs = fp.groups * ((blocks32 + 4 / fp.shape.s - 1) / (4 / fp.shape.s));
             const int wpc = fs_wgs_per_cu(fp.shape);
             if (tuning(LCE_TUNE_MFMA_FS_PAD) >= 0 && wgs <= cus * wpc &&
@@ -1097,7 +1101,7 @@ lce_status lce_bconv2d_mfma(const lce_bconv2d_desc *desc, const int32_t *x_packe
         }
     }
 
-    if (ks_env == 1 || (ks_env != 0 && ksteps >= 48)) {
+    if (ks_env == 1 || (ks_env != 0 && ksteps >= 20)) {
         static const int kTiles[][2] = {{4, 2}, {2, 4}, {2, 2}, {4, 1}, {1, 4},
                                         {2, 1}, {1, 2}, {1, 1}};
         int mbw = 0, knb = 0, rows = 0;
