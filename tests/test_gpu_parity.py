@@ -297,6 +297,10 @@ def test_every_static_instance(k, cw, out, stride):
     (1, 6, 6, 32, 100, 1, "float"),
     (2, 7, 9, 160, 70, 1, "bitpacked", 5),
     (1, 8, 8, 96, 64, 1, "float", 5),
+    # filters outweigh the input with several pixel blocks: the tiles are
+    # renumbered filter-major per XCD (tile counts not a multiple of 8)
+    (3, 9, 9, 256, 200, 1, "bitpacked"),
+    (5, 7, 7, 512, 72, 2, "float"),
 ])
 def test_every_schedule_matches_oracle(nb, ks, shape):
     """Every work split of the shape-specialized kernel (filter blocks per
