@@ -36,7 +36,8 @@ EXPORTS = ("lce_packed_words", "lce_bconv2d_out_shape", "lce_bitpack", "lce_bcon
            "lce_bconv2d_pad_correction_size", "lce_bconv2d_pad_correction",
            "lce_fold_thresholds", "lce_bmaxpool2d_out_shape", "lce_bmaxpool2d",
            "lce_dequantize", "lce_bconv2d_mfma_weights_size", "lce_bconv2d_mfma_weights",
-           "lce_bconv2d_mfma", "lce_quantize_bconv2d", "lce_set_tuning", "lce_get_tuning",
+           "lce_bconv2d_mfma", "lce_quantize_bconv2d", "lce_quantize_bconv2d_mfma",
+           "lce_set_tuning", "lce_get_tuning",
            "lce_last_error")
 
 # lce_tuning_key values, by the names tuning() takes.
@@ -107,6 +108,9 @@ def lib() -> ctypes.CDLL:
         L.lce_bconv2d_mfma.restype = ctypes.c_int
         L.lce_quantize_bconv2d.argtypes = [ctypes.POINTER(Desc), vp, vp, vp, vp, vp, vp, vp, vp]
         L.lce_quantize_bconv2d.restype = ctypes.c_int
+        L.lce_quantize_bconv2d_mfma.argtypes = [ctypes.POINTER(Desc), vp, vp, vp, vp, vp, vp,
+                                                vp, vp]
+        L.lce_quantize_bconv2d_mfma.restype = ctypes.c_int
         L.lce_set_tuning.argtypes = [i32, i32]
         L.lce_set_tuning.restype = ctypes.c_int
         L.lce_get_tuning.argtypes = [i32]
@@ -441,21 +445,25 @@ def mfma_weights(w_packed, c_in: int, out=None):
     return out
 
 
-def bconv2d_mfma(x_packed, w_fp4, c_in: int, c_out: int, kernel, *, stride=1,
-                 padding: str = "same", pad_value: str = "one",
-                 clamp: Optional[Tuple[int, int]] = None, out_type: str = "float",
-                 multiplier=None, bias=None, thresholds=None, flip=None, out=None):
-    """LceBConv2d on the matrix cores: x_packed int32 [N,H,W,Cw], w_fp4 from
-    mfma_weights(); kernel = (KH, KW) or an int.  Output as bconv2d."""
+def _mfma_conv(fn, x, x_float: bool, w_fp4, c_in: int, c_out: int, kernel, stride, padding,
+               pad_value, clamp, out_type, multiplier, bias, thresholds, flip, out):
+    """Shared marshalling of the two matrix-core entry points (packed or
+    float input); returns the output tensor."""
     import torch
-    _require(x_packed, torch.int32, "x_packed")
+    if x_float:
+        _require(x, torch.float32, "x")
+        n, h, w, c = x.shape
+        if c != c_in:
+            raise ValueError(f"x has {c} channels, c_in={c_in}")
+    else:
+        _require(x, torch.int32, "x_packed")
+        n, h, w, cw = x.shape
+        if cw != packed_words(c_in):
+            raise ValueError(f"packed channel words {cw} do not match c_in={c_in}")
     if not isinstance(w_fp4, torch.Tensor) or w_fp4.device.type != "cuda":
         raise TypeError("w_fp4 must be a device tensor")
     if not w_fp4.is_contiguous():
         raise ValueError("w_fp4 must be contiguous")
-    n, h, w, cw = x_packed.shape
-    if cw != packed_words(c_in):
-        raise ValueError(f"packed channel words {cw} do not match c_in={c_in}")
     kh, kw = (kernel, kernel) if isinstance(kernel, int) else tuple(kernel)
     desc = make_desc(n, h, w, c_in, c_out, kh, kw, stride, padding, pad_value, clamp, out_type)
     oh, ow = out_shape(desc)
@@ -479,14 +487,39 @@ def bconv2d_mfma(x_packed, w_fp4, c_in: int, c_out: int, kernel, *, stride=1,
     oc = packed_words(c_out) if out_type == "bitpacked" else c_out
     dt = torch.float32 if out_type == "float" else torch.int32
     if out is None:
-        out = torch.empty((n, oh, ow, oc), dtype=dt, device=x_packed.device)
+        out = torch.empty((n, oh, ow, oc), dtype=dt, device=x.device)
     else:
         _require(out, dt, "out")
         if out.numel() != n * oh * ow * oc:
             raise ValueError(f"out must hold {n}x{oh}x{ow}x{oc} elements")
-    _check(lib().lce_bconv2d_mfma(ctypes.byref(desc), x_packed.data_ptr(), w_fp4.data_ptr(),
-                                  *ptrs, out.data_ptr(), _stream_handle(x_packed)))
+    _check(fn(ctypes.byref(desc), x.data_ptr(), w_fp4.data_ptr(), *ptrs, out.data_ptr(),
+              _stream_handle(x)))
     return out
+
+
+def bconv2d_mfma(x_packed, w_fp4, c_in: int, c_out: int, kernel, *, stride=1,
+                 padding: str = "same", pad_value: str = "one",
+                 clamp: Optional[Tuple[int, int]] = None, out_type: str = "float",
+                 multiplier=None, bias=None, thresholds=None, flip=None, out=None):
+    """LceBConv2d on the matrix cores: x_packed int32 [N,H,W,Cw], w_fp4 from
+    mfma_weights(); kernel = (KH, KW) or an int.  Output as bconv2d."""
+    return _mfma_conv(lib().lce_bconv2d_mfma, x_packed, False, w_fp4, c_in, c_out, kernel,
+                      stride, padding, pad_value, clamp, out_type, multiplier, bias,
+                      thresholds, flip, out)
+
+
+def quantize_bconv2d_mfma(x, w_fp4, c_out: int, kernel, *, stride=1, padding: str = "same",
+                          pad_value: str = "one", clamp: Optional[Tuple[int, int]] = None,
+                          out_type: str = "float", multiplier=None, bias=None,
+                          thresholds=None, flip=None, out=None):
+    """LceQuantize + LceBConv2d on the matrix cores in one launch: x float32
+    [N,H,W,C_in] (C_in a multiple of 32, 16-byte aligned), w_fp4 from
+    mfma_weights().  The result equals bconv2d_mfma(bitpack(x), ...).  Shapes
+    the filter-stationary schedule does not take raise LceError with status
+    LCE_EUNSUPPORTED (nothing is launched); run bitpack and bconv2d_mfma."""
+    return _mfma_conv(lib().lce_quantize_bconv2d_mfma, x, True, w_fp4, x.shape[-1], c_out,
+                      kernel, stride, padding, pad_value, clamp, out_type, multiplier, bias,
+                      thresholds, flip, out)
 
 
 class PreparedBConv2dMfma:
@@ -546,6 +579,33 @@ class PreparedBConv2d:
                      ptr(thresholds), ptr(flip), ptr(pad_correction), out.data_ptr())
         self.keep = (x_packed, w_packed, multiplier, bias, thresholds, flip, pad_correction, out)
         self._fn = lib().lce_bconv2d
+
+    def __call__(self, stream=None):
+        st = self._fn(self._desc_ref, *self.args, _current_stream() if stream is None else stream)
+        if st != LCE_OK:
+            raise LceError(st, last_error())
+
+
+class PreparedQuantBConv2dMfma:
+    """A quantize_bconv2d_mfma call marshalled once (see PreparedBConv2d)."""
+
+    def __init__(self, x, w_fp4, c_out, kernel, out, *, stride=1, padding="same",
+                 pad_value="one", clamp=None, out_type="float", multiplier=None, bias=None,
+                 thresholds=None, flip=None):
+        quantize_bconv2d_mfma(x, w_fp4, c_out, kernel, stride=stride, padding=padding,
+                              pad_value=pad_value, clamp=clamp, out_type=out_type,
+                              multiplier=multiplier, bias=bias, thresholds=thresholds,
+                              flip=flip, out=out)
+        n, h, w, c_in = x.shape
+        kh, kw = (kernel, kernel) if isinstance(kernel, int) else tuple(kernel)
+        self.desc = make_desc(n, h, w, c_in, c_out, kh, kw, stride, padding, pad_value, clamp,
+                              out_type)
+        self._desc_ref = ctypes.byref(self.desc)
+        ptr = lambda t: None if t is None else t.data_ptr()
+        self.args = (x.data_ptr(), w_fp4.data_ptr(), ptr(multiplier), ptr(bias),
+                     ptr(thresholds), ptr(flip), out.data_ptr())
+        self.keep = (x, w_fp4, multiplier, bias, thresholds, flip, out)
+        self._fn = lib().lce_quantize_bconv2d_mfma
 
     def __call__(self, stream=None):
         st = self._fn(self._desc_ref, *self.args, _current_stream() if stream is None else stream)

@@ -716,6 +716,97 @@ __device__ __forceinline__ void region_finish(const MfmaParams &p, u32x4 *atile,
     }
 }
 
+// LceQuantize fused into the region staging (arXiv 2011.09398 Section 3.2:
+// a float activation is sign-binarized, then convolved).  The input is
+// float32 NHWC with C_in a multiple of 32, and p.x points at it.  An element
+// is word j of region location rc, i.e. channels 32j .. 32j+31 of that
+// location: 128 bytes, eight 16-byte buffer loads.  Its bit c is x < 0 (the
+// sign test of the bitpack kernel: -0.0 and NaN give +1), and it is then
+// widened like a packed word.  A location outside the image reads zeros past
+// the buffer, which binarize to +1.0 (one padding); zero padding takes the
+// outside flag, as for packed input.  The host keeps the float input below
+// 2 GiB.
+typedef float f32x4_t __attribute__((ext_vector_type(4)));
+constexpr int kRegUF = 2;
+
+struct RegionChunkF {
+    f32x4_t v[kRegUF][8];
+    uint32_t out;                        // bit u: element u lies outside the image
+};
+
+template <int NT>
+__device__ __forceinline__ void region_load_f(const MfmaParams &p, int row0, int plane, int tid,
+                                              int e0, RegionChunkF &ch) {
+    const int total = plane * p.cw;
+    const __amdgpu_buffer_rsrc_t xb =
+        buffer_of(p.x, (uint32_t)p.n * p.h * p.w * p.cw * 128u);
+    ch.out = 0;
+    const int wave_e0 = e0 + (tid & ~63);
+#pragma unroll
+    for (int u = 0; u < kRegUF; ++u) {
+        if (wave_e0 + u * NT >= total) {
+#pragma unroll
+            for (int i = 0; i < 8; ++i) ch.v[u][i] = f32x4_t{0.0f, 0.0f, 0.0f, 0.0f};
+            continue;
+        }
+        const int e = min(e0 + u * NT + tid, total - 1);
+        const int j = (int)fast_div((uint32_t)e, p.div_plane);
+        bool in;
+        // byte offset of packed word j of the location, times 32: its floats
+        const int off = region_offset(p, row0, e - j * plane, j, in);
+        const int offf = in ? off * 32 : kBufOutside;
+#pragma unroll
+        for (int i = 0; i < 8; ++i) {
+            const auto w = __builtin_amdgcn_raw_buffer_load_b128(xb, offf + 16 * i, 0, 0);
+            ch.v[u][i] = f32x4_t{__uint_as_float(w[0]), __uint_as_float(w[1]),
+                                 __uint_as_float(w[2]), __uint_as_float(w[3])};
+        }
+        ch.out |= in ? 0u : 1u << u;
+    }
+}
+
+template <int NT>
+__device__ __forceinline__ void region_widen_f(const MfmaParams &p, const RegionChunkF &ch,
+                                               u32x4 *atile, int plane, int tid, int e0) {
+    const int total = plane * p.cw;
+#pragma unroll
+    for (int u = 0; u < kRegUF; ++u) {
+        const int e = e0 + u * NT + tid;
+        if (e >= total) break;
+        uint32_t bits = 0;
+#pragma unroll
+        for (int i = 0; i < 8; ++i) {
+            const f32x4_t f = ch.v[u][i];
+            const uint32_t nib = (uint32_t)(f.x < 0.0f) | ((uint32_t)(f.y < 0.0f) << 1) |
+                                 ((uint32_t)(f.z < 0.0f) << 2) | ((uint32_t)(f.w < 0.0f) << 3);
+            bits |= nib << (4 * i);
+        }
+        const uint32_t fill = p.pad_zero && ((ch.out >> u) & 1u) ? 0u : kFp4PlusOne;
+        atile[e] = widen_word(bits, fill);
+    }
+}
+
+// The rest of the float region after the first chunk, then the words past
+// Cw (as region_finish).
+template <int NT>
+__device__ __forceinline__ void region_finish_f(const MfmaParams &p, u32x4 *atile, int row0,
+                                                int plane, int tid) {
+    const int total = plane * p.cw;
+    for (int e0 = kRegUF * NT; e0 < total; e0 += kRegUF * NT) {
+        RegionChunkF ch;
+        region_load_f<NT>(p, row0, plane, tid, e0, ch);
+        region_widen_f<NT>(p, ch, atile, plane, tid, e0);
+    }
+    for (int e = plane * p.cw + tid; e < plane * p.cwe; e += NT) {
+        uint32_t fill = kFp4PlusOne;
+        if (p.pad_zero) {
+            const int j = (int)fast_div((uint32_t)e, p.div_plane);
+            if (!region_inside(p, row0, e - j * plane)) fill = 0u;
+        }
+        atile[e] = widen_word(0u, fill);
+    }
+}
+
 // Bitpacked output of one transposed 32x32 accumulator block (filters as
 // the row operand: lane = pixel lane % 32, value v = filter (v/4)*8 +
 // half*4 + v%4), given the dot bounds t[q] of filters 8q + half*4 + 0..3.
@@ -1057,7 +1148,9 @@ __device__ __forceinline__ void for_each_index(Fn &&f, std::integer_sequence<int
 }
 
 
-template <int KS, int S, int OUT, bool PK>
+// QF: the input is float32 and binarized while its region is staged
+// (region_load_f), LceQuantize fused into the convolution.
+template <int KS, int S, int OUT, bool PK, bool QF = false>
 __global__ __launch_bounds__(kMfmaThreads) void bconv2d_mfma_fs_kernel(MfmaParams p) {
     static_assert(S == 1 || S == 2 || S == 4, "1, 2 or 4 waves per filter block");
     // every argument line this kernel reads in one round trip, the tap
@@ -1104,8 +1197,11 @@ __global__ __launch_bounds__(kMfmaThreads) void bconv2d_mfma_fs_kernel(MfmaParam
     mfma_pixel(g, m0, row0, col0);
     // the region's first chunk (its loads before the filters': the widening
     // needs it first)
-    RegionChunk rch;
-    region_load<kMfmaThreads>(g, row0, plane, tid, 0, rch);
+    std::conditional_t<QF, RegionChunkF, RegionChunk> rch;
+    if constexpr (QF)
+        region_load_f<kMfmaThreads>(g, row0, plane, tid, 0, rch);
+    else
+        region_load<kMfmaThreads>(g, row0, plane, tid, 0, rch);
 
     // ---- per-lane output-transform parameters of filter co, as buffer
     // loads issued between the region's and the filters' (so that waiting
@@ -1183,8 +1279,13 @@ __global__ __launch_bounds__(kMfmaThreads) void bconv2d_mfma_fs_kernel(MfmaParam
     // The region, widened as its words arrive (the compiler waits for them
     // here, with the filter loads still outstanding), the rest of it if any,
     // and the words past Cw.
-    region_widen<kMfmaThreads>(g, rch, atile, plane, tid, 0);
-    region_finish<kMfmaThreads>(g, atile, row0, plane, tid);
+    if constexpr (QF) {
+        region_widen_f<kMfmaThreads>(g, rch, atile, plane, tid, 0);
+        region_finish_f<kMfmaThreads>(g, atile, row0, plane, tid);
+    } else {
+        region_widen<kMfmaThreads>(g, rch, atile, plane, tid, 0);
+        region_finish<kMfmaThreads>(g, atile, row0, plane, tid);
+    }
     int z;
     const bool flipped = OUT == OUT_BITS && fvalid && co_ok && ((flip_word >> l32) & 1u);
     // sign bits of a flipped filter (in the widened or the packed form),

@@ -19,9 +19,9 @@ void launch_mfma_pixel(const MfmaParams &p, int out_type, int cc, int nblk, int 
 void launch_mfma_ksplit(const MfmaParams &p, int out_type, int nblk, int mbw, dim3 grid,
                         size_t lds, hipStream_t stream);
 // filter-stationary schedule: instance (KS, S);
-// pk: load the packed filter copy
-void launch_mfma_fs(const MfmaParams &p, int ks, int s, bool pk, int out_type, dim3 grid,
-                     size_t lds, hipStream_t stream);
+// pk: load the packed filter copy; qf: float32 input, binarized while staged
+void launch_mfma_fs(const MfmaParams &p, int ks, int s, bool pk, bool qf, int out_type,
+                    dim3 grid, size_t lds, hipStream_t stream);
 
 // quantize-fused XOR/POPCOUNT convolution (float input, Cw = C_in/32 words
 // per pixel): whether an instance exists, and its launch

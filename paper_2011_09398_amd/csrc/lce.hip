@@ -622,6 +622,89 @@ size_t mfma_ks_lds(const lce::MfmaParams &p, int mbw, int nblk, int tile_rows) {
     return std::max(a, red) + (size_t)nblk * 32 * 4;
 }
 
+// The matrix-core launch parameters of a validated descriptor, all but the
+// schedule's: x is the packed input, or (qf) the float32 input, 32 floats
+// per packed word.  Fails with EUNSUPPORTED past the 2 GiB reach of the
+// buffer loads; launches nothing.
+lce_status mfma_params(const lce_bconv2d_desc &d, const Geometry &g, const void *x, bool qf,
+                       const void *w_fp4, const float *multiplier, const float *bias,
+                       const float *thresholds, const int32_t *flip, void *out,
+                       lce::MfmaParams *pp) {
+    lce::MfmaParams &p = *pp;
+    p = lce::MfmaParams{};
+    p.x = reinterpret_cast<const uint32_t *>(x);
+    p.wexp = reinterpret_cast<const lce::u32x4 *>(w_fp4);
+    p.mult = d.out_type == LCE_OUT_FLOAT32 ? multiplier : nullptr;
+    p.bias = d.out_type == LCE_OUT_FLOAT32 ? bias : nullptr;
+    p.thr = thresholds;
+    p.flip = d.out_type == LCE_OUT_BITPACKED ? reinterpret_cast<const uint32_t *>(flip) : nullptr;
+    p.out = out;
+    int cc, cwe;
+    p.n = d.n; p.h = d.h; p.w = d.w; p.cw = packed_words(d.c_in);
+    mfma_chunk(p.cw, &cc, &cwe);
+    p.cwe = cwe;
+    p.oh = g.oh; p.ow = g.ow; p.cout = d.c_out; p.coutp = (d.c_out + 31) / 32 * 32;
+    // the packed copy follows the widened filters in the same buffer
+    p.wpk = reinterpret_cast<const uint32_t *>(p.wexp + (int64_t)d.kh * d.kw * cwe * p.coutp);
+    p.cwo = packed_words(d.c_out);
+    p.kh = d.kh; p.kw = d.kw; p.sh = d.stride_h; p.sw = d.stride_w; p.pt = g.pt; p.pl = g.pl;
+    p.ph = (g.oh - 1) * d.stride_h + d.kh;
+    p.pw = (g.ow - 1) * d.stride_w + d.kw;
+    p.lo = d.clamp_min; p.hi = d.clamp_max;
+    p.m = d.n * g.oh * g.ow;
+    p.pad_zero = d.pad_value == LCE_PAD_ZERO ? 1 : 0;
+    p.region_vec = !qf && p.cw % 4 == 0 && aligned(x, 16) ? 4 : 1;
+    p.div_ohw = lce::make_fastdiv((uint32_t)(g.oh * g.ow));
+    p.div_ow = lce::make_fastdiv((uint32_t)g.ow);
+    p.div_ph = lce::make_fastdiv((uint32_t)p.ph);
+    p.div_pw = lce::make_fastdiv((uint32_t)p.pw);
+
+    p.div_cwh = lce::make_fastdiv((uint32_t)(p.cwe / 2));
+    p.div_kw = lce::make_fastdiv((uint32_t)p.kw);
+    p.div_groups = lce::make_fastdiv((uint32_t)(p.region_vec == 4 ? p.cw / 4 : p.cwe));
+    // the filter-stationary and K-split kernels read the input and the
+    // filters as buffers, with 32-bit byte offsets and offsets at or past
+    // 2^31 standing for padding: each must stay below 2 GiB
+    {
+        const int64_t x_bytes = (int64_t)d.n * d.h * d.w * p.cw * (qf ? 128 : 4);
+        const int64_t w_bytes = (int64_t)d.kh * d.kw * cwe * p.coutp * 16;
+        if (x_bytes >= (int64_t(1) << 31) || w_bytes >= (int64_t(1) << 31))
+            return fail(LCE_EUNSUPPORTED,
+                        "the matrix-core path takes inputs and widened filters below 2 GiB "
+                        "(input %lld bytes, widened filters %lld bytes)",
+                        (long long)x_bytes, (long long)w_bytes);
+    }
+    return ok();
+}
+
+// Plans the filter-stationary schedule of a layer and launches it (qf: the
+// input is float32, binarized while staged); false, with nothing launched,
+// when no instance fits.
+bool launch_fs_plan(lce::MfmaParams &p, const lce_bconv2d_desc &d, int64_t cus, int blocks32,
+                    int64_t ksteps, bool qf, hipStream_t stream) {
+    const FsPlan fp = plan_mfma_fs(p, cus, blocks32, (int)ksteps);
+    if (!fp.shape.ks) return false;
+    p.tile_rows = fp.tile_rows;
+    p.fs_pixels = fp.pixels;
+    p.fs_thr_off = (int32_t)(mfma_fs_thr_offset(fp.shape) / 4);
+    p.div_plane = lce::make_fastdiv((uint32_t)(fp.tile_rows * p.pw));
+    fill_step_table(p, d, fp.tile_rows * p.pw, (int)ksteps);
+    size_t lds = fp.lds;
+    // claim more than 1/(wpc+1) of a CU's LDS when the grid fits the
+    // CUs, so that no CU holds more than wpc workgroups while another
+    // holds fewer (tuning key mfma_fs_pad = -1 turns this off)
+    const int64_t wgs = fp.groups * ((blocks32 + 4 / fp.shape.s - 1) / (4 / fp.shape.s));
+    const int wpc = fs_wgs_per_cu(fp.shape);
+    if (tuning(LCE_TUNE_MFMA_FS_PAD) >= 0 && wgs <= cus * wpc &&
+        lds * (wpc + 1) <= (size_t)device_max_lds())
+        lds = std::max(lds, (size_t)device_max_lds() / (wpc + 1) + 1024);
+    const dim3 grid((unsigned)fp.groups,
+                    (unsigned)((blocks32 + 4 / fp.shape.s - 1) / (4 / fp.shape.s)));
+    const bool pk = d.c_in == 32 * p.cwe && tuning(LCE_TUNE_MFMA_PACKED) >= 0;
+    lce::launch_mfma_fs(p, fp.shape.ks, fp.shape.s, pk, qf, d.out_type, grid, lds, stream);
+    return true;
+}
+
 }  // namespace
 
 extern "C" {
@@ -1004,49 +1087,11 @@ lce_status lce_bconv2d_mfma(const lce_bconv2d_desc *desc, const int32_t *x_packe
                     "K = %lld: the matrix-core path keeps dots exact in fp32 only below 2^24",
                     (long long)k);
 
-    lce::MfmaParams p{};
-    p.x = reinterpret_cast<const uint32_t *>(x_packed);
-    p.wexp = reinterpret_cast<const lce::u32x4 *>(w_fp4);
-    p.mult = d.out_type == LCE_OUT_FLOAT32 ? multiplier : nullptr;
-    p.bias = d.out_type == LCE_OUT_FLOAT32 ? bias : nullptr;
-    p.thr = thresholds;
-    p.flip = d.out_type == LCE_OUT_BITPACKED ? reinterpret_cast<const uint32_t *>(flip) : nullptr;
-    p.out = out;
+    lce::MfmaParams p;
+    st = mfma_params(d, g, x_packed, false, w_fp4, multiplier, bias, thresholds, flip, out, &p);
+    if (st != LCE_OK) return st;
     int cc, cwe;
-    p.n = d.n; p.h = d.h; p.w = d.w; p.cw = packed_words(d.c_in);
     mfma_chunk(p.cw, &cc, &cwe);
-    p.cwe = cwe;
-    p.oh = g.oh; p.ow = g.ow; p.cout = d.c_out; p.coutp = (d.c_out + 31) / 32 * 32;
-    // the packed copy follows the widened filters in the same buffer
-    p.wpk = reinterpret_cast<const uint32_t *>(p.wexp + (int64_t)d.kh * d.kw * cwe * p.coutp);
-    p.cwo = packed_words(d.c_out);
-    p.kh = d.kh; p.kw = d.kw; p.sh = d.stride_h; p.sw = d.stride_w; p.pt = g.pt; p.pl = g.pl;
-    p.ph = (g.oh - 1) * d.stride_h + d.kh;
-    p.pw = (g.ow - 1) * d.stride_w + d.kw;
-    p.lo = d.clamp_min; p.hi = d.clamp_max;
-    p.m = d.n * g.oh * g.ow;
-    p.pad_zero = d.pad_value == LCE_PAD_ZERO ? 1 : 0;
-    p.region_vec = (p.cw % 4 == 0 && aligned(x_packed, 16)) ? 4 : 1;
-    p.div_ohw = lce::make_fastdiv((uint32_t)(g.oh * g.ow));
-    p.div_ow = lce::make_fastdiv((uint32_t)g.ow);
-    p.div_ph = lce::make_fastdiv((uint32_t)p.ph);
-    p.div_pw = lce::make_fastdiv((uint32_t)p.pw);
-
-    p.div_cwh = lce::make_fastdiv((uint32_t)(p.cwe / 2));
-    p.div_kw = lce::make_fastdiv((uint32_t)p.kw);
-    p.div_groups = lce::make_fastdiv((uint32_t)(p.region_vec == 4 ? p.cw / 4 : p.cwe));
-    // the filter-stationary and K-split kernels read the input and the
-    // filters as buffers, with 32-bit byte offsets and offsets at or past
-    // 2^31 standing for padding: each must stay below 2 GiB
-    {
-        const int64_t x_bytes = (int64_t)d.n * d.h * d.w * p.cw * 4;
-        const int64_t w_bytes = (int64_t)d.kh * d.kw * cwe * p.coutp * 16;
-        if (x_bytes >= (int64_t(1) << 31) || w_bytes >= (int64_t(1) << 31))
-            return fail(LCE_EUNSUPPORTED,
-                        "the matrix-core path takes inputs and widened filters below 2 GiB "
-                        "(input %lld bytes, widened filters %lld bytes)",
-                        (long long)x_bytes, (long long)w_bytes);
-    }
     const int64_t cus = device_simds() / 4;
     const int blocks32 = p.coutp / 32;
     const int nmax = blocks32 >= 4 ? 4 : blocks32 >= 2 ? 2 : 1;
@@ -1077,28 +1122,8 @@ lce_status lce_bconv2d_mfma(const lce_bconv2d_desc *desc, const int32_t *x_packe
     const bool fs_forced = tuning(LCE_TUNE_MFMA_FS_KS) && tuning(LCE_TUNE_MFMA_FS_S);
     if (ks_env < 0 &&
         (ksteps <= 36 || (fs_forced && ksteps <= 72))) {
-        const FsPlan fp = plan_mfma_fs(p, cus, blocks32, (int)ksteps);
-        if (fp.shape.ks) {
-            p.tile_rows = fp.tile_rows;
-            p.fs_pixels = fp.pixels;
-            p.fs_thr_off = (int32_t)(mfma_fs_thr_offset(fp.shape) / 4);
-            p.div_plane = lce::make_fastdiv((uint32_t)(fp.tile_rows * p.pw));
-            fill_step_table(p, d, fp.tile_rows * p.pw, (int)ksteps);
-            size_t lds = fp.lds;
-            // claim more than 1/(wpc+1) of a CU's LDS when the grid fits the
-            // CUs, so that no CU holds more than wpc workgroups while another
-            // holds fewer (tuning key mfma_fs_pad = -1 turns this off)
-            const int64_t wgs = fp.groups * ((blocks32 + 4 / fp.shape.s - 1) / (4 / fp.shape.s));
-            const int wpc = fs_wgs_per_cu(fp.shape);
-            if (tuning(LCE_TUNE_MFMA_FS_PAD) >= 0 && wgs <= cus * wpc &&
-                lds * (wpc + 1) <= (size_t)device_max_lds())
-                lds = std::max(lds, (size_t)device_max_lds() / (wpc + 1) + 1024);
-            const dim3 grid((unsigned)fp.groups,
-                            (unsigned)((blocks32 + 4 / fp.shape.s - 1) / (4 / fp.shape.s)));
-            const bool pk = d.c_in == 32 * p.cwe && tuning(LCE_TUNE_MFMA_PACKED) >= 0;
-            lce::launch_mfma_fs(p, fp.shape.ks, fp.shape.s, pk, d.out_type, grid, lds, stream);
+        if (launch_fs_plan(p, d, cus, blocks32, ksteps, false, stream))
             return check_launch("lce_bconv2d_mfma launch");
-        }
     }
 
     if (ks_env == 1 || (ks_env != 0 && ksteps >= 20)) {
@@ -1170,6 +1195,51 @@ lce_status lce_bconv2d_mfma(const lce_bconv2d_desc *desc, const int32_t *x_packe
     const dim3 grid((unsigned)pix_groups, (unsigned)((blocks32 + nblk - 1) / nblk));
     lce::launch_mfma_pixel(p, d.out_type, cc, nblk, mb, grid, lds, stream);
     return check_launch("lce_bconv2d_mfma launch");
+}
+
+lce_status lce_quantize_bconv2d_mfma(const lce_bconv2d_desc *desc, const float *x,
+                                     const void *w_fp4, const float *multiplier,
+                                     const float *bias, const float *thresholds,
+                                     const int32_t *flip, void *out, hipStream_t stream) {
+    Geometry g;
+    lce_status st = validate_desc(desc, &g);
+    if (st != LCE_OK) return st;
+    const lce_bconv2d_desc &d = *desc;
+    if (!x || !w_fp4 || !out) return fail(LCE_EINVAL, "x/w_fp4/out is NULL");
+    if (d.out_type == LCE_OUT_BITPACKED && !thresholds)
+        return fail(LCE_EINVAL, "bitpacked output needs thresholds");
+    if (!aligned(x, 16) || !aligned(w_fp4, 16))
+        return fail(LCE_EALIGN, "x and w_fp4 must be 16-byte aligned (16-byte loads)");
+    if (!aligned(out, 4) || (multiplier && !aligned(multiplier, 4)) ||
+        (bias && !aligned(bias, 4)) || (thresholds && !aligned(thresholds, 4)) ||
+        (flip && !aligned(flip, 4)))
+        return fail(LCE_EALIGN, "out and the per-channel arrays must be 4-byte aligned");
+    if (d.c_in % 32 != 0)
+        return fail(LCE_EUNSUPPORTED,
+                    "c_in %d is not a multiple of 32; run lce_bitpack, then lce_bconv2d_mfma",
+                    d.c_in);
+    if ((int64_t)d.n * g.oh * g.ow > INT32_MAX - lce::kMfmaPixMax)
+        return fail(LCE_EINVAL, "too many output pixels for the matrix-core path");
+    const int64_t k = (int64_t)d.kh * d.kw * d.c_in;
+    if (k >= (1 << 24))
+        return fail(LCE_EUNSUPPORTED,
+                    "K = %lld: the matrix-core path keeps dots exact in fp32 only below 2^24",
+                    (long long)k);
+    lce::MfmaParams p;
+    st = mfma_params(d, g, x, true, w_fp4, multiplier, bias, thresholds, flip, out, &p);
+    if (st != LCE_OK) return st;
+    // the filter-stationary schedule only (the others stage the region by
+    // LDS DMA or over several passes): the shapes it takes, by the same plan
+    // as lce_bconv2d_mfma's
+    const int64_t ksteps = (int64_t)d.kh * d.kw * (p.cwe / 2);
+    const bool fs_forced = tuning(LCE_TUNE_MFMA_FS_KS) && tuning(LCE_TUNE_MFMA_FS_S);
+    const bool fits_k = ksteps <= 36 || (fs_forced && ksteps <= 72);
+    if (!fits_k ||
+        !launch_fs_plan(p, d, device_simds() / 4, p.coutp / 32, ksteps, true, stream))
+        return fail(LCE_EUNSUPPORTED,
+                    "no filter-stationary instance takes this shape (%lld K steps); run "
+                    "lce_bitpack, then lce_bconv2d_mfma", (long long)ksteps);
+    return check_launch("lce_quantize_bconv2d_mfma launch");
 }
 
 lce_status lce_set_tuning(int32_t key, int32_t value) {

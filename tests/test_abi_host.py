@@ -154,6 +154,38 @@ def test_bconv2d_mfma_validation_errors():
     assert "2 GiB" in lce.last_error()
 
 
+def call_quant_mfma(d, x=P, w=P, m=None, b=None, t=P, flip=None, out=P):
+    return lce.lib().lce_quantize_bconv2d_mfma(ctypes.byref(d), x, w, m, b, t, flip, out, None)
+
+
+def test_quantize_bconv2d_mfma_validation_errors():
+    """The float-input matrix-core entry refuses before any device call:
+    bad arguments, alignment (x and w_fp4 16 bytes), C_in not a multiple of
+    32, K >= 2^24, a float input of 2 GiB or more, and K steps beyond the
+    filter-stationary schedule's 36."""
+    L = lce.lib()
+    assert L.lce_quantize_bconv2d_mfma(None, P, P, None, None, P, None, P, None) == lce.LCE_EINVAL
+    assert call_quant_mfma(desc(clamp=(5, 4))) == lce.LCE_EINVAL
+    assert call_quant_mfma(desc(), x=None) == lce.LCE_EINVAL
+    assert call_quant_mfma(desc(), w=None) == lce.LCE_EINVAL
+    assert call_quant_mfma(desc(), out=None) == lce.LCE_EINVAL
+    assert call_quant_mfma(desc(out_type="bitpacked"), t=None) == lce.LCE_EINVAL
+    assert call_quant_mfma(desc(), x=P + 4) == lce.LCE_EALIGN      # float input: 16 bytes
+    assert call_quant_mfma(desc(), w=P + 4) == lce.LCE_EALIGN
+    assert call_quant_mfma(desc(out_type="bitpacked"), flip=P + 1) == lce.LCE_EALIGN
+    assert call_quant_mfma(desc(c_in=48)) == lce.LCE_EUNSUPPORTED
+    assert "multiple of 32" in lce.last_error()
+    assert call_quant_mfma(desc(c_in=2 ** 21, c_out=1, h=1, w=1)) == lce.LCE_EUNSUPPORTED
+    assert "2^24" in lce.last_error()
+    # 2^24 pixels x 32 channels of float32 = 2 GiB
+    assert call_quant_mfma(desc(n=1, h=2 ** 12, w=2 ** 12, c_in=32, c_out=32,
+                                out_type="bitpacked")) == lce.LCE_EUNSUPPORTED
+    assert "2 GiB" in lce.last_error()
+    # 3x3 over 512 channels: 72 K steps, beyond the filter-stationary default
+    assert call_quant_mfma(desc(c_in=512, c_out=32)) == lce.LCE_EUNSUPPORTED
+    assert "filter-stationary" in lce.last_error()
+
+
 def call_quant(d, x=P, w=P, m=None, b=None, t=P, flip=None, out=P):
     return lce.lib().lce_quantize_bconv2d(ctypes.byref(d), x, w, m, b, t, flip, out, None)
 
