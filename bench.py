@@ -68,7 +68,8 @@ PEAK_FP4_TFLOPS = 10100.0
 # The arithmetic each implementation computes in (the bench line's dtype).
 DTYPES = {"xor": "u32 xor+popcount (VALU), int32 accumulate",
           "mfma": "fp4 e2m1 MFMA, fp32 accumulate (integer-exact dot)",
-          "fused": "fp32 sign test + u32 xor+popcount (VALU), int32 accumulate"}
+          "fused": "fp32 sign test + u32 xor+popcount (VALU), int32 accumulate",
+          "fused_mfma": "fp32 sign test + fp4 e2m1 MFMA, fp32 accumulate (integer-exact dot)"}
 HBM_PEAK_GBS = 8000.0
 
 
@@ -121,6 +122,7 @@ class Step:
         self.inputs = [make_layer_inputs(l, 0, cfg_idx, i) for i, l in enumerate(self.layers)]
         dev = lambda a: torch.from_numpy(np.ascontiguousarray(a)).cuda()
         self.xor_calls, self.mfma_calls, self.fused_calls = [], [], []
+        self.fused_mfma_calls = []
         self.packs, self.outs, self.keep = [], [], []
         for i, (layer, inp) in enumerate(zip(self.layers, self.inputs)):
             w_packed = lce.bitpack(dev(inp.w_float))          # 1-bit weight storage
@@ -163,6 +165,17 @@ class Step:
                     if e.status != lce.LCE_EUNSUPPORTED:
                         raise
             self.fused_calls.append(fused)
+            fused_mfma = None
+            if pack is not None:      # float input: the quantize-fused matrix-core launch
+                try:
+                    fused_mfma = lce.PreparedQuantBConv2dMfma(
+                        xf, w_fp4, layer.c_out, (layer.kh, layer.kw), out,
+                        stride=layer.strides, padding=layer.padding, clamp=layer.clamp,
+                        out_type=layer.out, **kw)
+                except lce.LceError as e:
+                    if e.status != lce.LCE_EUNSUPPORTED:
+                        raise
+            self.fused_mfma_calls.append(fused_mfma)
             self.packs.append(pack)
             self.outs.append(out)
             self.keep.append((w_packed, x_packed, kw))
@@ -170,11 +183,20 @@ class Step:
         self.kinds = ["xor"] * len(self.calls)
         self.times = [None] * len(self.calls)
 
+    def kinds_of(self, i):
+        """The whole-layer forms layer i has: bitpack (float input) + the XOR
+        or the matrix-core convolution, and the quantize-fused launches of
+        either kernel where they cover the shape."""
+        return (["xor", "mfma"] + (["fused"] if self.fused_calls[i] is not None else [])
+                + (["fused_mfma"] if self.fused_mfma_calls[i] is not None else []))
+
     def layer_call(self, i, kind):
         """Layer i as one callable: bitpack (float input) then the named
-        convolution, or the quantize-fused launch."""
+        convolution, or a quantize-fused launch."""
         if kind == "fused":
             return self.fused_calls[i]
+        if kind == "fused_mfma":
+            return self.fused_mfma_calls[i]
         conv = self.mfma_calls[i] if kind == "mfma" else self.xor_calls[i]
         pack = self.packs[i]
         if pack is None:
@@ -190,14 +212,14 @@ class Step:
         or the named one for the step: bitpack (float input) + XOR/POPCOUNT
         conv, bitpack + matrix-core conv, or the quantize-fused launch.
         graph: time from captured graphs (layers shorter than an eager
-        launch).  times[i] = (xor, mfma[, fused]) whole-layer ms."""
+        launch).  times[i] = {form: whole-layer ms}."""
         self.times = []
         for i in range(len(self.layers)):
-            kinds = ["xor", "mfma"] + (["fused"] if self.fused_calls[i] is not None else [])
-            t = [time_repeated(self.layer_call(i, k), reps, graph=graph) for k in kinds]
-            self.times.append(tuple(t))
-            kind = mode if mode != "auto" else kinds[min(range(len(t)), key=t.__getitem__)]
-            if kind == "fused" and self.fused_calls[i] is None:
+            kinds = self.kinds_of(i)
+            t = {k: time_repeated(self.layer_call(i, k), reps, graph=graph) for k in kinds}
+            self.times.append(t)
+            kind = mode if mode != "auto" else min(kinds, key=t.__getitem__)
+            if kind not in kinds:
                 kind = "xor"
             self.kinds[i] = kind
             self.calls[i] = self.layer_call(i, kind)
@@ -312,10 +334,11 @@ def inputs_digest(inp):
 
 def layer_record(layer, ms, probe_tops=None, kind="xor", times=None):
     """One layer's launch(es): binary GOPS against the roofline of the unit
-    that ran it (VALU xor+popcount, or dense fp4 MFMA; "fused" is the
-    XOR+POPCOUNT kernel binarizing its float input itself).  For a float
-    input, `us` covers the whole layer: bitpack + conv, or the fused launch.
-    times: the (xor, mfma[, fused]) timings the choice was made from."""
+    that ran it (VALU xor+popcount, or dense fp4 MFMA; "fused" and
+    "fused_mfma" are the XOR+POPCOUNT and the matrix-core kernels binarizing
+    their float input themselves).  For a float input, `us` covers the whole
+    layer: bitpack + conv, or the fused launch.
+    times: {form: ms} of the whole-layer forms the choice was made from."""
     ops = layer.binary_ops
     tops = ops / (ms * 1e-3) / 1e12
     r = {"layer": layer.name, "batch": layer.n, "kernel": kind, "us": round(ms * 1e3, 3),
@@ -329,9 +352,8 @@ def layer_record(layer, ms, probe_tops=None, kind="xor", times=None):
     else:
         r["mfma_fp4_frac"] = round(tops / PEAK_FP4_TFLOPS, 4)
     if times is not None:
-        r["us_xor"], r["us_mfma"] = round(times[0] * 1e3, 3), round(times[1] * 1e3, 3)
-        if len(times) > 2:
-            r["us_fused"] = round(times[2] * 1e3, 3)
+        for k, t in times.items():
+            r[f"us_{k}"] = round(t * 1e3, 3)
     return r
 
 
@@ -446,7 +468,8 @@ def sweep_lines(args, probe=None):
         tx = time_repeated(x, args.reps, graph=True)
         tm = time_repeated(m, args.reps, graph=True)
         kind = args.kernel if args.kernel != "auto" else ("mfma" if tm < tx else "xor")
-        r = layer_record(layer, tm if kind == "mfma" else tx, probe, kind, (tx, tm))
+        r = layer_record(layer, tm if kind == "mfma" else tx, probe, kind,
+                         {"xor": tx, "mfma": tm})
         r["macs"] = layer.macs
         out.append(r)
     return out
@@ -466,11 +489,10 @@ def batch1_lines(args, probe=None):
             r = bitpack_record(layer, time_repeated(pack, args.reps, graph=True))
             r["config"] = cfg
             out.append(r)
-            kinds = ["xor", "mfma"] + (["fused"] if s.fused_calls[i] is not None else [])
-            whole = [time_repeated(s.layer_call(i, k), args.reps, graph=True) for k in kinds]
-            best = min(range(len(kinds)), key=whole.__getitem__)
-            kind = args.kernel if args.kernel != "auto" else kinds[best]
-            r = layer_record(layer, whole[kinds.index(kind)], probe, kind, tuple(whole))
+            kinds = s.kinds_of(i)
+            whole = {k: time_repeated(s.layer_call(i, k), args.reps, graph=True) for k in kinds}
+            kind = args.kernel if args.kernel != "auto" else min(kinds, key=whole.__getitem__)
+            r = layer_record(layer, whole[kind], probe, kind, whole)
             r["us_conv_xor"] = round(time_repeated(x, args.reps, graph=True) * 1e3, 3)
             r["us_conv_mfma"] = round(time_repeated(m, args.reps, graph=True) * 1e3, 3)
             r["config"] = cfg
@@ -801,7 +823,8 @@ def roofline_record(rec, kind, cfg_idx, probe):
         r = {"bound": "mfma", "achieved": round(rec["binary_gops"] / 1e3, 2),
              "peak": PEAK_FP4_TFLOPS, "unit": "TFLOP/s", "frac": rec["mfma_fp4_frac"],
              "traffic": measured_traffic(rec["layer"], "mfma") if cfg_idx == 4 else None,
-             "kernel": f"bconv2d_mfma (fp4 e2m1 MFMA) {rec['layer']} (batch {rec['batch']})"}
+             "kernel": f"bconv2d_mfma{' (quantize-fused)' if kind == 'fused_mfma' else ''} "
+                       f"(fp4 e2m1 MFMA) {rec['layer']} (batch {rec['batch']})"}
     r.update({"per_launch_binary_ops": rec["binary_ops"], "avg_launch_us": rec["us"]})
     return r
 
