@@ -265,18 +265,19 @@ lce_status lce_bconv2d_mfma(const lce_bconv2d_desc *desc, const int32_t *x_packe
  * and bitpacked, then convolved).  The result equals lce_bitpack of x
  * followed by lce_bconv2d_mfma (and so lce_bconv2d) on the packed tensor,
  * bit for bit, with no packed copy written to memory: each workgroup of the
- * filter-stationary schedule binarizes the input region its windows read
- * while staging it.
+ * filter-stationary or the K-split schedule binarizes the input region its
+ * windows read while staging it.
  *   x          float32 [N][H][W][C_in]  (device, 16-byte aligned); the sign
  *              test is lce_bitpack's (x < 0.0f is a 1 bit = -1.0, so -0.0
  *              and NaN give +1.0)
  *   w_fp4, multiplier, bias, thresholds, flip, out: as lce_bconv2d_mfma
  * Covered: C_in a multiple of 32, input below 2 GiB, and the shapes the
  * filter-stationary schedule takes (by default up to 36 K steps of 64
- * channels, e.g. 3x3 filters over up to 256 channels, with an input region
- * per workgroup that fits its LDS).  Other requests return LCE_EUNSUPPORTED
- * before anything is launched, and the caller runs lce_bitpack and
- * lce_bconv2d_mfma instead.
+ * channels that one of its instances covers with at most 1/8 padding) or,
+ * from 20 K steps, the K-split one (every 3x3 and 5x5 filter), with an
+ * input region per workgroup that fits its LDS.  Other requests (e.g. 1x1
+ * filters over few channels) return LCE_EUNSUPPORTED before anything is
+ * launched, and the caller runs lce_bitpack and lce_bconv2d_mfma instead.
  * Errors: as lce_bconv2d_mfma, plus LCE_EUNSUPPORTED (above) and LCE_EALIGN
  *         for an x that is not 16-byte aligned. */
 lce_status lce_quantize_bconv2d_mfma(const lce_bconv2d_desc *desc, const float *x,

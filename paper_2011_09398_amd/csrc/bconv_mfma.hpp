@@ -860,7 +860,9 @@ __device__ __forceinline__ uint32_t transposed_block_bits(const mfma_v16f &val,
 constexpr int kRing = 4;
 constexpr unsigned kXcds = 8;
 
-template <int OUT, int NBLK, int MBW>
+// QF: the input is float32 and binarized while its region is staged
+// (region_load_f), LceQuantize fused into the convolution.
+template <int OUT, int NBLK, int MBW, bool QF = false>
 __global__ __launch_bounds__(kMfmaThreads) void bconv2d_mfma_ks_kernel(MfmaParams p) {
     constexpr int BN = 32 * NBLK;
     constexpr int BM = 32 * MBW;
@@ -901,8 +903,11 @@ __global__ __launch_bounds__(kMfmaThreads) void bconv2d_mfma_ks_kernel(MfmaParam
 
     // the region's first chunk (its loads before the filters': the widening
     // needs it first)
-    RegionChunk rch;
-    region_load<kMfmaThreads>(g, row0, plane, tid, 0, rch);
+    std::conditional_t<QF, RegionChunkF, RegionChunk> rch;
+    if constexpr (QF)
+        region_load_f<kMfmaThreads>(g, row0, plane, tid, 0, rch);
+    else
+        region_load<kMfmaThreads>(g, row0, plane, tid, 0, rch);
 
     // output-transform parameters of the NBLK filter blocks (buffer loads
     // after the region's, so that its widening does not wait for them; an
@@ -959,8 +964,13 @@ __global__ __launch_bounds__(kMfmaThreads) void bconv2d_mfma_ks_kernel(MfmaParam
 
     // ---- widen the whole region (every word of every location) as its
     // words arrive, while the filter ring is still arriving
-    region_widen<kMfmaThreads>(g, rch, atile, plane, tid, 0);
-    region_finish<kMfmaThreads>(g, atile, row0, plane, tid);
+    if constexpr (QF) {
+        region_widen_f<kMfmaThreads>(g, rch, atile, plane, tid, 0);
+        region_finish_f<kMfmaThreads>(g, atile, row0, plane, tid);
+    } else {
+        region_widen<kMfmaThreads>(g, rch, atile, plane, tid, 0);
+        region_finish<kMfmaThreads>(g, atile, row0, plane, tid);
+    }
     // bitpacked output: the dot bound of each of the workgroup's filters, in
     // LDS past the A planes and the reduction buffer (tb[32*ib + f] for
     // filter n_base + 32*ib + f; filters past C_out get -inf, bit 0)

@@ -15,9 +15,10 @@ namespace lce {
 // pixel blocks per wave
 void launch_mfma_pixel(const MfmaParams &p, int out_type, int cc, int nblk, int mb, dim3 grid,
                        size_t lds, hipStream_t stream);
-// K-split schedule: tile of 32*MBW pixels x 32*NBLK filters
-void launch_mfma_ksplit(const MfmaParams &p, int out_type, int nblk, int mbw, dim3 grid,
-                        size_t lds, hipStream_t stream);
+// K-split schedule: tile of 32*MBW pixels x 32*NBLK filters; qf: float32
+// input, binarized while staged
+void launch_mfma_ksplit(const MfmaParams &p, int out_type, int nblk, int mbw, bool qf,
+                        dim3 grid, size_t lds, hipStream_t stream);
 // filter-stationary schedule: instance (KS, S);
 // pk: load the packed filter copy; qf: float32 input, binarized while staged
 void launch_mfma_fs(const MfmaParams &p, int ks, int s, bool pk, bool qf, int out_type,

@@ -570,6 +570,25 @@ int fs_wgs_per_cu(FsShape sh) {
     return sh.s == 1 && sh.ks <= 9 ? 2 : 1;
 }
 
+// Whether filter-stationary instance sh takes a layer of `ksteps` K steps:
+// its waves cover them with every wave busy and (unless an instance is
+// forced through the tuning keys) at most 1/8 of them padding; a forced
+// instance or S excludes the others.
+bool fs_shape_takes(FsShape sh, int64_t ksteps) {
+    const int env_ks = tuning(LCE_TUNE_MFMA_FS_KS), env_s = tuning(LCE_TUNE_MFMA_FS_S);
+    if (env_ks && sh.ks != env_ks) return false;
+    if (env_s && sh.s != env_s) return false;
+    const int cover = sh.ks * sh.s;
+    if (cover < ksteps || cover - sh.ks >= ksteps) return false;   // every wave has work
+    return (env_ks && env_s) || (cover - ksteps) * 8 <= ksteps;
+}
+
+bool fs_any_takes(int64_t ksteps) {
+    for (const FsShape &sh : kFsShapes)
+        if (fs_shape_takes(sh, ksteps)) return true;
+    return false;
+}
+
 // The filter-stationary plan of a layer: among the instances whose K steps
 // cover the layer's with at most 1/8 padding (any, when forced), the one
 // with the fewest matrix products per SIMD (pixel blocks per workgroup x
@@ -580,13 +599,8 @@ int fs_wgs_per_cu(FsShape sh) {
 FsPlan plan_mfma_fs(const lce::MfmaParams &p, int64_t cus, int blocks32, int ksteps) {
     FsPlan best;
     int64_t best_cost = -1;
-    const int env_ks = tuning(LCE_TUNE_MFMA_FS_KS), env_s = tuning(LCE_TUNE_MFMA_FS_S);
     for (const FsShape &sh : kFsShapes) {
-        if (env_ks && sh.ks != env_ks) continue;
-        if (env_s && sh.s != env_s) continue;
-        const int cover = sh.ks * sh.s;
-        if (cover < ksteps || cover - sh.ks >= ksteps) continue;   // every wave has work
-        if (!(env_ks && env_s) && (cover - ksteps) * 8 > ksteps) continue;
+        if (!fs_shape_takes(sh, ksteps)) continue;
         const int f = 4 / sh.s;
         const int64_t fgroups = (blocks32 + f - 1) / f;
         const int wpc = fs_wgs_per_cu(sh);
@@ -703,6 +717,43 @@ bool launch_fs_plan(lce::MfmaParams &p, const lce_bconv2d_desc &d, int64_t cus, 
     const bool pk = d.c_in == 32 * p.cwe && tuning(LCE_TUNE_MFMA_PACKED) >= 0;
     lce::launch_mfma_fs(p, fp.shape.ks, fp.shape.s, pk, qf, d.out_type, grid, lds, stream);
     return true;
+}
+
+// Plans the K-split schedule of a layer and launches it (qf: the input is
+// float32, binarized while staged): the tile of 32*MBW pixels x 32*NBLK
+// filters is the largest (at most eight 32x32 blocks) whose grid still gives
+// every CU 1.5 workgroups, among those whose LDS fits; false, with nothing
+// launched, when none fits.
+bool launch_ks_plan(lce::MfmaParams &p, const lce_bconv2d_desc &d, int64_t cus, int blocks32,
+                    bool qf, hipStream_t stream) {
+    const int nmax = blocks32 >= 4 ? 4 : blocks32 >= 2 ? 2 : 1;
+    static const int kTiles[][2] = {{4, 2}, {2, 4}, {2, 2}, {4, 1}, {1, 4},
+                                    {2, 1}, {1, 2}, {1, 1}};
+    int mbw = 0, knb = 0, rows = 0;
+    int64_t best_wgs = -1;
+    const int env_mb = tuning(LCE_TUNE_MFMA_TILE_M), env_nb = tuning(LCE_TUNE_MFMA_TILE_N);
+    for (const auto &o : kTiles) {
+        if (o[1] > nmax) continue;
+        if (env_mb && o[0] != env_mb) continue;
+        if (env_nb && o[1] != env_nb) continue;
+        const int tr = mfma_tile_rows(p, 32 * o[0]);
+        if (mfma_ks_lds(p, o[0], o[1], tr) > (size_t)device_max_lds()) continue;
+        const int64_t wgs = ((int64_t)p.m + 32 * o[0] - 1) / (32 * o[0]) *
+                            ((blocks32 + o[1] - 1) / o[1]);
+        if (2 * wgs >= 3 * cus) { mbw = o[0]; knb = o[1]; rows = tr; break; }
+        if (wgs > best_wgs) { best_wgs = wgs; mbw = o[0]; knb = o[1]; rows = tr; }
+    }
+    if (mbw) {
+        p.tile_rows = rows;
+        p.div_plane = lce::make_fastdiv((uint32_t)(rows * p.pw));
+        const size_t lds = mfma_ks_lds(p, mbw, knb, rows);
+        const dim3 grid((unsigned)(((int64_t)p.m + 32 * mbw - 1) / (32 * mbw)),
+                        (unsigned)((blocks32 + knb - 1) / knb));
+        p.div_ks_gx = lce::make_fastdiv(grid.x);
+        lce::launch_mfma_ksplit(p, d.out_type, knb, mbw, qf, grid, lds, stream);
+        return true;
+    }
+    return false;
 }
 
 }  // namespace
@@ -1127,32 +1178,8 @@ lce_status lce_bconv2d_mfma(const lce_bconv2d_desc *desc, const int32_t *x_packe
     }
 
     if (ks_env == 1 || (ks_env != 0 && ksteps >= 20)) {
-        static const int kTiles[][2] = {{4, 2}, {2, 4}, {2, 2}, {4, 1}, {1, 4},
-                                        {2, 1}, {1, 2}, {1, 1}};
-        int mbw = 0, knb = 0, rows = 0;
-        int64_t best_wgs = -1;
-        const int env_mb = tuning(LCE_TUNE_MFMA_TILE_M), env_nb = tuning(LCE_TUNE_MFMA_TILE_N);
-        for (const auto &o : kTiles) {
-            if (o[1] > nmax) continue;
-            if (env_mb && o[0] != env_mb) continue;
-            if (env_nb && o[1] != env_nb) continue;
-            const int tr = mfma_tile_rows(p, 32 * o[0]);
-            if (mfma_ks_lds(p, o[0], o[1], tr) > (size_t)device_max_lds()) continue;
-            const int64_t wgs = ((int64_t)p.m + 32 * o[0] - 1) / (32 * o[0]) *
-                                ((blocks32 + o[1] - 1) / o[1]);
-            if (2 * wgs >= 3 * cus) { mbw = o[0]; knb = o[1]; rows = tr; break; }
-            if (wgs > best_wgs) { best_wgs = wgs; mbw = o[0]; knb = o[1]; rows = tr; }
-        }
-        if (mbw) {
-            p.tile_rows = rows;
-            p.div_plane = lce::make_fastdiv((uint32_t)(rows * p.pw));
-            const size_t lds = mfma_ks_lds(p, mbw, knb, rows);
-            const dim3 grid((unsigned)(((int64_t)p.m + 32 * mbw - 1) / (32 * mbw)),
-                            (unsigned)((blocks32 + knb - 1) / knb));
-            p.div_ks_gx = lce::make_fastdiv(grid.x);
-            lce::launch_mfma_ksplit(p, d.out_type, knb, mbw, grid, lds, stream);
+        if (launch_ks_plan(p, d, cus, blocks32, false, stream))
             return check_launch("lce_bconv2d_mfma launch");
-        }
     }
 
     // Pixel-split schedule: MB pixel blocks of 32 per wave (128*MB pixels
@@ -1228,18 +1255,24 @@ lce_status lce_quantize_bconv2d_mfma(const lce_bconv2d_desc *desc, const float *
     lce::MfmaParams p;
     st = mfma_params(d, g, x, true, w_fp4, multiplier, bias, thresholds, flip, out, &p);
     if (st != LCE_OK) return st;
-    // the filter-stationary schedule only (the others stage the region by
-    // LDS DMA or over several passes): the shapes it takes, by the same plan
-    // as lce_bconv2d_mfma's
+    // the schedules that stage the region through registers, by the same
+    // plans as lce_bconv2d_mfma's: filter-stationary where one of its
+    // instances takes the shape, else the K split from 20 K steps (the pixel
+    // split stages by LDS DMA and is not fused)
     const int64_t ksteps = (int64_t)d.kh * d.kw * (p.cwe / 2);
     const bool fs_forced = tuning(LCE_TUNE_MFMA_FS_KS) && tuning(LCE_TUNE_MFMA_FS_S);
-    const bool fits_k = ksteps <= 36 || (fs_forced && ksteps <= 72);
-    if (!fits_k ||
-        !launch_fs_plan(p, d, device_simds() / 4, p.coutp / 32, ksteps, true, stream))
-        return fail(LCE_EUNSUPPORTED,
-                    "no filter-stationary instance takes this shape (%lld K steps); run "
-                    "lce_bitpack, then lce_bconv2d_mfma", (long long)ksteps);
-    return check_launch("lce_quantize_bconv2d_mfma launch");
+    const bool fs_k = (ksteps <= 36 || (fs_forced && ksteps <= 72)) && fs_any_takes(ksteps);
+    const bool ks_k = ksteps >= 20;
+    if (fs_k || ks_k) {
+        const int64_t cus = device_simds() / 4;
+        const int blocks32 = p.coutp / 32;
+        if ((fs_k && launch_fs_plan(p, d, cus, blocks32, ksteps, true, stream)) ||
+            (ks_k && launch_ks_plan(p, d, cus, blocks32, true, stream)))
+            return check_launch("lce_quantize_bconv2d_mfma launch");
+    }
+    return fail(LCE_EUNSUPPORTED,
+                "neither the filter-stationary nor the K-split schedule takes this shape "
+                "(%lld K steps); run lce_bitpack, then lce_bconv2d_mfma", (long long)ksteps);
 }
 
 lce_status lce_set_tuning(int32_t key, int32_t value) {

@@ -161,8 +161,8 @@ def call_quant_mfma(d, x=P, w=P, m=None, b=None, t=P, flip=None, out=P):
 def test_quantize_bconv2d_mfma_validation_errors():
     """The float-input matrix-core entry refuses before any device call:
     bad arguments, alignment (x and w_fp4 16 bytes), C_in not a multiple of
-    32, K >= 2^24, a float input of 2 GiB or more, and K steps beyond the
-    filter-stationary schedule's 36."""
+    32, K >= 2^24, a float input of 2 GiB or more, and a shape neither the
+    filter-stationary nor the K-split schedule takes."""
     L = lce.lib()
     assert L.lce_quantize_bconv2d_mfma(None, P, P, None, None, P, None, P, None) == lce.LCE_EINVAL
     assert call_quant_mfma(desc(clamp=(5, 4))) == lce.LCE_EINVAL
@@ -181,9 +181,10 @@ def test_quantize_bconv2d_mfma_validation_errors():
     assert call_quant_mfma(desc(n=1, h=2 ** 12, w=2 ** 12, c_in=32, c_out=32,
                                 out_type="bitpacked")) == lce.LCE_EUNSUPPORTED
     assert "2 GiB" in lce.last_error()
-    # 3x3 over 512 channels: 72 K steps, beyond the filter-stationary default
-    assert call_quant_mfma(desc(c_in=512, c_out=32)) == lce.LCE_EUNSUPPORTED
-    assert "filter-stationary" in lce.last_error()
+    # 1x1 over 128 channels: 2 K steps, no filter-stationary instance within
+    # 1/8 padding and too few for the K split
+    assert call_quant_mfma(desc(c_in=128, c_out=32, kh=1, kw=1)) == lce.LCE_EUNSUPPORTED
+    assert "filter-stationary" in lce.last_error() and "K-split" in lce.last_error()
 
 
 def call_quant(d, x=P, w=P, m=None, b=None, t=P, flip=None, out=P):

@@ -1,13 +1,12 @@
 """GPU parity of the quantize-fused matrix-core convolution
 (lce_quantize_bconv2d_mfma).
 
-The float input is binarized while the filter-stationary kernel stages its
-region.  The output must equal the oracle's binarize + bconv2d (bit for bit
+The float input is binarized while the filter-stationary or the K-split
+kernel stages its region.  The output must equal the oracle's binarize + bconv2d (bit for bit
 for bitpacked and int32 outputs, within the float tolerance for float
 outputs; the dot is the exact integer either way), and equal lce_bitpack +
-lce_bconv2d_mfma on the same device buffers bit for bit.  Shapes the
-filter-stationary schedule does not take must be refused before anything is
-launched.  Output buffers are poisoned first.
+lce_bconv2d_mfma on the same device buffers bit for bit.  Shapes neither
+schedule takes must be refused before anything is launched.  Output buffers are poisoned first.
 """
 import numpy as np
 import pytest
@@ -81,6 +80,12 @@ def k_steps(layer):
     return layer.kh * layer.kw * ((layer.cw + 1) // 2)
 
 
+def taken(layer):
+    """Filter-stationary where one of its instances takes the layer, else the
+    K split from 20 K steps."""
+    return fs_takes(layer) or k_steps(layer) >= 20
+
+
 def fs_takes(layer):
     """Whether a filter-stationary instance (KS K steps per wave, S waves per
     filter block) covers the layer's K steps with every wave busy and at
@@ -118,10 +123,9 @@ def check(layer, inp, what, pad_value="one", x_float=None):
 def test_batch1_configs(cfg, idx):
     layer = config(cfg)[idx]
     assert layer.input_kind == "float"
-    taken = check(layer, make_layer_inputs(layer, 0, cfg, idx), f"config {cfg} layer {idx}")
-    # every one of them but the 72-K-step 7x7x512 layer is taken
-    assert taken == fs_takes(layer), (layer.name, k_steps(layer))
-    assert taken == (k_steps(layer) <= 36)
+    # every one of them is taken (the 72-K-step 7x7x512 one by the K split)
+    assert check(layer, make_layer_inputs(layer, 0, cfg, idx), f"config {cfg} layer {idx}")
+    assert taken(layer)
 
 
 def test_stack_first_layer_full_batch():
@@ -145,9 +149,10 @@ SHAPES = [
     (2, 7, 9, 512, 100, 1, 1, 1, "same", "int32"),        # 8 K steps
     (2, 10, 8, 192, 64, 3, 1, 2, "same", "bitpacked"),    # 9 K steps
     (1, 12, 12, 128, 40, 1, 5, 1, "same", "float"),       # 10 K steps
-    (3, 9, 6, 32, 72, 5, 5, 2, "same", "bitpacked"),      # 25 K steps: refused
+    (3, 9, 6, 32, 72, 5, 5, 2, "same", "bitpacked"),      # 25 K steps: K split
+    (2, 9, 7, 160, 90, 3, 3, 1, "same", "float"),         # 27 K steps: K split
+    (1, 8, 8, 512, 64, 3, 3, 1, "same", "bitpacked"),     # 72 K steps: K split
     (3, 12, 10, 128, 200, 1, 1, 1, "valid", "int32"),     # 2 K steps: refused
-    (1, 8, 8, 512, 64, 3, 3, 1, "same", "bitpacked"),     # 72 K steps: refused
 ]
 
 
@@ -160,8 +165,8 @@ def test_shapes(shape, pad_value):
     clamp = (-k // 3, k // 2) if out != "bitpacked" else None
     layer = Layer("qfm", n, h, w, ci, co, kh=kh, kw=kw, stride=s, padding=pad, out=out,
                   clamp=clamp, input_kind="float")
-    taken = check(layer, make_layer_inputs(layer, 1, 0, 11), layer.name, pad_value)
-    assert taken == fs_takes(layer), (layer.name, k_steps(layer))
+    was_taken = check(layer, make_layer_inputs(layer, 1, 0, 11), layer.name, pad_value)
+    assert was_taken == taken(layer), (layer.name, k_steps(layer))
 
 
 # ------------------------------------------------ every filter-stationary instance
@@ -201,6 +206,24 @@ def test_every_instance(ks, s, packed):
                       input_kind="float")
         assert check(layer, make_layer_inputs(layer, 2, 0, ks * 10 + s + j),
                      f"{layer.name} {kh}x{kw} c_in={ci}", ["one", "zero"][j % 2])
+
+
+@pytest.mark.parametrize("mbw,nblk", [(4, 2), (2, 4), (2, 2), (4, 1), (1, 4), (2, 1), (1, 2),
+                                      (1, 1)])
+def test_ksplit_every_tile(mbw, nblk):
+    """Each K-split tile forced (tuning keys): configuration 3's 7x7x512
+    layer and ragged layers with zero padding and a stride."""
+    import paper_2011_09398_amd as lce
+    lce.set_tuning(mfma_tile_m=mbw, mfma_tile_n=nblk)
+    idx, layer = next((i, l) for i, l in enumerate(config(3)) if l.c_in == 512)
+    assert k_steps(layer) == 72
+    assert check(layer, make_layer_inputs(layer, 0, 3, idx), f"7x7x512 mb={mbw} nblk={nblk}")
+    for j, (lay, pv) in enumerate(((Layer("rk", 3, 11, 9, 160, 200, out="float",
+                                          clamp=(-60, 90), input_kind="float"), "one"),
+                                   (Layer("s2z", 2, 13, 10, 96, 136, kh=5, kw=5, stride=2,
+                                          out="bitpacked", input_kind="float"), "zero"))):
+        assert check(lay, make_layer_inputs(lay, 5, 0, 40 + 10 * nblk + mbw + j),
+                     f"{lay.name} mb={mbw} nblk={nblk}", pv)
 
 
 @pytest.mark.parametrize("wpc", [1, 2])
