@@ -272,12 +272,15 @@ lce_status lce_bconv2d_mfma(const lce_bconv2d_desc *desc, const int32_t *x_packe
  *              and NaN give +1.0)
  *   w_fp4, multiplier, bias, thresholds, flip, out: as lce_bconv2d_mfma
  * Covered: C_in a multiple of 32, input below 2 GiB, and the shapes the
- * filter-stationary schedule takes (by default up to 36 K steps of 64
- * channels that one of its instances covers with at most 1/8 padding) or,
- * from 20 K steps, the K-split one (every 3x3 and 5x5 filter), with an
+ * filter-stationary schedule takes (up to 72 K steps of 64 channels that
+ * one of its instances covers with at most 1/8 padding; tried first up to
+ * 36 K steps, and beyond where the K split's grid would not fill the CUs)
+ * or, from 20 K steps, the K-split one (every 3x3 and 5x5 filter), with an
  * input region per workgroup that fits its LDS.  Other requests (e.g. 1x1
  * filters over few channels) return LCE_EUNSUPPORTED before anything is
  * launched, and the caller runs lce_bitpack and lce_bconv2d_mfma instead.
+ * LCE_TUNE_MFMA_SCHEDULE 1 or 2 restricts the choice to that schedule (2
+ * then takes any K); 3, the pixel split, has no fused form and is refused.
  * Errors: as lce_bconv2d_mfma, plus LCE_EUNSUPPORTED (above) and LCE_EALIGN
  *         for an x that is not 16-byte aligned. */
 lce_status lce_quantize_bconv2d_mfma(const lce_bconv2d_desc *desc, const float *x,
@@ -336,8 +339,9 @@ lce_status lce_dequantize(const int32_t *x_packed, float *out, int64_t rows, int
 typedef enum {
     LCE_TUNE_XOR_NB = 0,          /* lce_bconv2d: blocks of 8 filters per wave, 1..4    */
     LCE_TUNE_XOR_KS = 1,          /* lce_bconv2d: waves sharing a block's K range 1/2/4 */
-    LCE_TUNE_MFMA_SCHEDULE = 2,   /* lce_bconv2d_mfma: 1 filter-stationary (where an
-                                     instance fits), 2 K split, 3 pixel split            */
+    LCE_TUNE_MFMA_SCHEDULE = 2,   /* lce_bconv2d_mfma and lce_quantize_bconv2d_mfma:
+                                     1 filter-stationary (where an instance fits),
+                                     2 K split, 3 pixel split (not fused)               */
     LCE_TUNE_MFMA_FS_KS = 3,      /* filter-stationary instance: K steps per wave       */
     LCE_TUNE_MFMA_FS_S = 4,       /* filter-stationary instance: waves per filter block */
     LCE_TUNE_MFMA_FS_WPC = 5,     /* filter-stationary grid: 1 or 2 workgroups per CU   */

@@ -550,7 +550,7 @@ size_t mfma_fs_lds(const lce::MfmaParams &p, FsShape sh, int tile_rows, int pixe
 
 struct FsPlan {
     FsShape shape{0, 0};
-    int pixels = 0, tile_rows = 0;
+    int pixels = 0, tile_rows = 0, wpc = 1;
     int64_t groups = 0;
     size_t lds = 0;
 };
@@ -558,17 +558,29 @@ struct FsPlan {
 // Workgroups per CU the filter-stationary grid is sized for.  Two (two
 // waves per SIMD, each hiding the other's finishing work and LDS waits
 // behind its matrix products) where a wave's filters are few, KS <= 9 and
-// S = 1: measured about 1.1x faster on the 56x56x64->128/s2 layer (9 K
-// steps).  With KS = 18 the second workgroup's filter loads and widening
-// cost more than the overlap gains (measured slower on 28x28x128).  Every
-// instance with S = 1 and KS <= 9 keeps its registers within the 256 per
-// lane that two waves per SIMD leave.  The mfma_fs_wpc tuning key (1 or 2)
-// forces it.
-int fs_wgs_per_cu(FsShape sh) {
+// S = 1, and one workgroup per CU would still hold more than one pixel
+// block (`px1`: its pixels): measured about 1.1x faster on the batch-64
+// 56x56x64->128/s2 layer (9 K steps), while where one block per workgroup
+// is all there is (batch-1 layers) the second workgroup only adds its
+// set-up (56x56x64->64: 3.92 vs 3.53 us).  With KS = 18 the second
+// workgroup's filter loads and widening cost more than the overlap gains
+// (measured slower on 28x28x128).  Every instance with S = 1 and KS <= 9
+// keeps its registers within the 256 per lane that two waves per SIMD
+// leave.  The mfma_fs_wpc tuning key (1 or 2) forces it.
+int fs_wgs_per_cu(FsShape sh, int64_t px1) {
     const int e = tuning(LCE_TUNE_MFMA_FS_WPC);
     if (e == 1 || e == 2) return e;
-    return sh.s == 1 && sh.ks <= 9 ? 2 : 1;
+    return sh.s == 1 && sh.ks <= 9 && px1 > 32 ? 2 : 1;
 }
+
+// Price of the partial-sum exchange of an instance with S > 1, in matrix
+// products per workgroup: a fixed part (two barriers, the sums written and
+// read back through LDS) plus one product per pixel block.  Calibrated on
+// the batch-1 layers of one block per workgroup: (9, 1) beats (5, 2) on
+// 56x56x64->64 (3.53 vs 3.68 us) and 56x56x64->128/s2 (3.32 vs 3.42), and
+// (9, 2) beats (18, 1) on 28x28x128->128 (3.53 vs 3.74), so the fixed part
+// lies between 3 and 8 products.
+constexpr int64_t kFsExchangeFixed = 4;
 
 // Whether filter-stationary instance sh takes a layer of `ksteps` K steps:
 // its waves cover them with every wave busy and (unless an instance is
@@ -592,10 +604,9 @@ bool fs_any_takes(int64_t ksteps) {
 // The filter-stationary plan of a layer: among the instances whose K steps
 // cover the layer's with at most 1/8 padding (any, when forced), the one
 // with the fewest matrix products per SIMD (pixel blocks per workgroup x
-// KS, plus one per block for the exchange, x workgroups per CU), with
-// about wpc workgroups per CU: each filter group gets wpc x CUs / filter
-// groups workgroups, each an equal share of the pixels.  shape.ks == 0:
-// none fits.
+// KS, plus the exchange, x workgroups per CU), with about wpc workgroups
+// per CU: each filter group gets wpc x CUs / filter groups workgroups,
+// each an equal share of the pixels.  shape.ks == 0: none fits.
 FsPlan plan_mfma_fs(const lce::MfmaParams &p, int64_t cus, int blocks32, int ksteps) {
     FsPlan best;
     int64_t best_cost = -1;
@@ -603,7 +614,8 @@ FsPlan plan_mfma_fs(const lce::MfmaParams &p, int64_t cus, int blocks32, int kst
         if (!fs_shape_takes(sh, ksteps)) continue;
         const int f = 4 / sh.s;
         const int64_t fgroups = (blocks32 + f - 1) / f;
-        const int wpc = fs_wgs_per_cu(sh);
+        const int64_t pg1 = std::max<int64_t>(1, cus / fgroups);
+        const int wpc = fs_wgs_per_cu(sh, ((int64_t)p.m + pg1 - 1) / pg1);
         const int64_t pg = std::max<int64_t>(1, cus * wpc / fgroups);
         // (not rounded to whole blocks: the block count is the same, and an
         // exact share often covers whole images or rows, with fewer rows)
@@ -614,12 +626,13 @@ FsPlan plan_mfma_fs(const lce::MfmaParams &p, int64_t cus, int blocks32, int kst
         if (lds > (size_t)device_max_lds()) continue;
         if ((int64_t)tr * p.pw * p.cwe > INT32_MAX / 2) continue;
         const int64_t nb = (px + 31) / 32;
-        const int64_t cost = (nb * sh.ks + (sh.s > 1 ? nb : 0)) * wpc;   // per CU
+        const int64_t cost = (nb * sh.ks + (sh.s > 1 ? nb + kFsExchangeFixed : 0)) * wpc;
         if (best_cost < 0 || cost < best_cost) {
             best_cost = cost;
             best.shape = sh;
             best.pixels = (int)px;
             best.tile_rows = tr;
+            best.wpc = wpc;
             best.groups = ((int64_t)p.m + px - 1) / px;
             best.lds = lds;
         }
@@ -708,7 +721,7 @@ bool launch_fs_plan(lce::MfmaParams &p, const lce_bconv2d_desc &d, int64_t cus, 
     // CUs, so that no CU holds more than wpc workgroups while another
     // holds fewer (tuning key mfma_fs_pad = -1 turns this off)
     const int64_t wgs = fp.groups * ((blocks32 + 4 / fp.shape.s - 1) / (4 / fp.shape.s));
-    const int wpc = fs_wgs_per_cu(fp.shape);
+    const int wpc = fp.wpc;
     if (tuning(LCE_TUNE_MFMA_FS_PAD) >= 0 && wgs <= cus * wpc &&
         lds * (wpc + 1) <= (size_t)device_max_lds())
         lds = std::max(lds, (size_t)device_max_lds() / (wpc + 1) + 1024);
@@ -719,18 +732,20 @@ bool launch_fs_plan(lce::MfmaParams &p, const lce_bconv2d_desc &d, int64_t cus, 
     return true;
 }
 
-// Plans the K-split schedule of a layer and launches it (qf: the input is
-// float32, binarized while staged): the tile of 32*MBW pixels x 32*NBLK
-// filters is the largest (at most eight 32x32 blocks) whose grid still gives
-// every CU 1.5 workgroups, among those whose LDS fits; false, with nothing
-// launched, when none fits.
-bool launch_ks_plan(lce::MfmaParams &p, const lce_bconv2d_desc &d, int64_t cus, int blocks32,
-                    bool qf, hipStream_t stream) {
+// The K-split plan of a layer: the tile of 32*MBW pixels x 32*NBLK filters
+// is the largest (at most eight 32x32 blocks) whose grid still gives every
+// CU 1.5 workgroups, among those whose LDS fits, else the one with the most
+// workgroups; mbw == 0: none fits.
+struct KsPlan {
+    int mbw = 0, nblk = 0, tile_rows = 0;
+    int64_t wgs = 0;
+};
+
+KsPlan plan_mfma_ks(const lce::MfmaParams &p, int64_t cus, int blocks32) {
     const int nmax = blocks32 >= 4 ? 4 : blocks32 >= 2 ? 2 : 1;
     static const int kTiles[][2] = {{4, 2}, {2, 4}, {2, 2}, {4, 1}, {1, 4},
                                     {2, 1}, {1, 2}, {1, 1}};
-    int mbw = 0, knb = 0, rows = 0;
-    int64_t best_wgs = -1;
+    KsPlan best;
     const int env_mb = tuning(LCE_TUNE_MFMA_TILE_M), env_nb = tuning(LCE_TUNE_MFMA_TILE_N);
     for (const auto &o : kTiles) {
         if (o[1] > nmax) continue;
@@ -740,20 +755,25 @@ bool launch_ks_plan(lce::MfmaParams &p, const lce_bconv2d_desc &d, int64_t cus, 
         if (mfma_ks_lds(p, o[0], o[1], tr) > (size_t)device_max_lds()) continue;
         const int64_t wgs = ((int64_t)p.m + 32 * o[0] - 1) / (32 * o[0]) *
                             ((blocks32 + o[1] - 1) / o[1]);
-        if (2 * wgs >= 3 * cus) { mbw = o[0]; knb = o[1]; rows = tr; break; }
-        if (wgs > best_wgs) { best_wgs = wgs; mbw = o[0]; knb = o[1]; rows = tr; }
+        if (2 * wgs >= 3 * cus) return KsPlan{o[0], o[1], tr, wgs};
+        if (wgs > best.wgs) best = KsPlan{o[0], o[1], tr, wgs};
     }
-    if (mbw) {
-        p.tile_rows = rows;
-        p.div_plane = lce::make_fastdiv((uint32_t)(rows * p.pw));
-        const size_t lds = mfma_ks_lds(p, mbw, knb, rows);
-        const dim3 grid((unsigned)(((int64_t)p.m + 32 * mbw - 1) / (32 * mbw)),
-                        (unsigned)((blocks32 + knb - 1) / knb));
-        p.div_ks_gx = lce::make_fastdiv(grid.x);
-        lce::launch_mfma_ksplit(p, d.out_type, knb, mbw, qf, grid, lds, stream);
-        return true;
-    }
-    return false;
+    return best;
+}
+
+// Launches the K-split plan `kp` (qf: the input is float32, binarized while
+// staged); false, with nothing launched, when no tile fits.
+bool launch_ks_plan(lce::MfmaParams &p, const lce_bconv2d_desc &d, const KsPlan &kp, int blocks32,
+                    bool qf, hipStream_t stream) {
+    if (!kp.mbw) return false;
+    p.tile_rows = kp.tile_rows;
+    p.div_plane = lce::make_fastdiv((uint32_t)(kp.tile_rows * p.pw));
+    const size_t lds = mfma_ks_lds(p, kp.mbw, kp.nblk, kp.tile_rows);
+    const dim3 grid((unsigned)(((int64_t)p.m + 32 * kp.mbw - 1) / (32 * kp.mbw)),
+                    (unsigned)((blocks32 + kp.nblk - 1) / kp.nblk));
+    p.div_ks_gx = lce::make_fastdiv(grid.x);
+    lce::launch_mfma_ksplit(p, d.out_type, kp.nblk, kp.mbw, qf, grid, lds, stream);
+    return true;
 }
 
 }  // namespace
@@ -1178,7 +1198,7 @@ lce_status lce_bconv2d_mfma(const lce_bconv2d_desc *desc, const int32_t *x_packe
     }
 
     if (ks_env == 1 || (ks_env != 0 && ksteps >= 20)) {
-        if (launch_ks_plan(p, d, cus, blocks32, false, stream))
+        if (launch_ks_plan(p, d, plan_mfma_ks(p, cus, blocks32), blocks32, false, stream))
             return check_launch("lce_bconv2d_mfma launch");
     }
 
@@ -1258,21 +1278,32 @@ lce_status lce_quantize_bconv2d_mfma(const lce_bconv2d_desc *desc, const float *
     // the schedules that stage the region through registers, by the same
     // plans as lce_bconv2d_mfma's: filter-stationary where one of its
     // instances takes the shape, else the K split from 20 K steps (the pixel
-    // split stages by LDS DMA and is not fused)
+    // split stages by LDS DMA and is not fused).  From 37 to 72 K steps the
+    // filter-stationary schedule also comes first where the K split's grid
+    // has fewer workgroups than CUs: each of those few workgroups stages a
+    // large region, and a float region costs 32 times the packed bytes
+    // (batch-1 7x7x512: 32 workgroups, 6.96 us, against 6.31 us on the
+    // (18, 4) instance; at batch 64, 392 workgroups, the K split is faster,
+    // 20.6 vs 22.2 us).  The mfma_schedule key restricts the choice to one
+    // schedule (the filter-stationary one then up to 72 K steps).
     const int64_t ksteps = (int64_t)d.kh * d.kw * (p.cwe / 2);
-    const bool fs_forced = tuning(LCE_TUNE_MFMA_FS_KS) && tuning(LCE_TUNE_MFMA_FS_S);
-    const bool fs_k = (ksteps <= 36 || (fs_forced && ksteps <= 72)) && fs_any_takes(ksteps);
-    const bool ks_k = ksteps >= 20;
+    const int sched = tuning(LCE_TUNE_MFMA_SCHEDULE);   // 0 auto, 1 FS, 2 K split, 3 pixel
+    const bool fs_k = (sched == 0 || sched == 1) && ksteps <= 72 && fs_any_takes(ksteps);
+    const bool ks_k = (sched == 0 && ksteps >= 20) || sched == 2;
     if (fs_k || ks_k) {
         const int64_t cus = device_simds() / 4;
         const int blocks32 = p.coutp / 32;
-        if ((fs_k && launch_fs_plan(p, d, cus, blocks32, ksteps, true, stream)) ||
-            (ks_k && launch_ks_plan(p, d, cus, blocks32, true, stream)))
+        const KsPlan kp = ks_k ? plan_mfma_ks(p, cus, blocks32) : KsPlan{};
+        const bool fs_first =
+            fs_k && (ksteps <= 36 || sched == 1 || !kp.mbw || kp.wgs < cus);
+        if ((fs_first && launch_fs_plan(p, d, cus, blocks32, ksteps, true, stream)) ||
+            (ks_k && launch_ks_plan(p, d, kp, blocks32, true, stream)))
             return check_launch("lce_quantize_bconv2d_mfma launch");
     }
     return fail(LCE_EUNSUPPORTED,
                 "neither the filter-stationary nor the K-split schedule takes this shape "
-                "(%lld K steps); run lce_bitpack, then lce_bconv2d_mfma", (long long)ksteps);
+                "(%lld K steps%s); run lce_bitpack, then lce_bconv2d_mfma", (long long)ksteps,
+                sched ? ", schedule restricted by the mfma_schedule tuning key" : "");
 }
 
 lce_status lce_set_tuning(int32_t key, int32_t value) {

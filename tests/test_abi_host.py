@@ -187,6 +187,22 @@ def test_quantize_bconv2d_mfma_validation_errors():
     assert "filter-stationary" in lce.last_error() and "K-split" in lce.last_error()
 
 
+def test_quantize_bconv2d_mfma_schedule_key_refusals():
+    """The mfma_schedule tuning key restricts the fused entry's choice: the
+    pixel split has no fused form, and a filter-stationary restriction
+    refuses a shape none of its instances takes (27 K steps) -- both before
+    any device call."""
+    try:
+        lce.set_tuning(mfma_schedule="pixel")
+        assert call_quant_mfma(desc()) == lce.LCE_EUNSUPPORTED
+        assert "mfma_schedule" in lce.last_error()
+        lce.set_tuning(mfma_schedule="fs")
+        assert call_quant_mfma(desc(c_in=160, c_out=32)) == lce.LCE_EUNSUPPORTED
+        assert "27 K steps" in lce.last_error()
+    finally:
+        lce.set_tuning(mfma_schedule=0)
+
+
 def call_quant(d, x=P, w=P, m=None, b=None, t=P, flip=None, out=P):
     return lce.lib().lce_quantize_bconv2d(ctypes.byref(d), x, w, m, b, t, flip, out, None)
 

@@ -89,9 +89,9 @@ def taken(layer):
 def fs_takes(layer):
     """Whether a filter-stationary instance (KS K steps per wave, S waves per
     filter block) covers the layer's K steps with every wave busy and at
-    most 1/8 of them padding, within the default plan's 36 K steps."""
+    most 1/8 of them padding, within the fused plan's 72 K steps."""
     steps = k_steps(layer)
-    return steps <= 36 and any(ks * s >= steps > ks * (s - 1) and (ks * s - steps) * 8 <= steps
+    return steps <= 72 and any(ks * s >= steps > ks * (s - 1) and (ks * s - steps) * 8 <= steps
                                for ks, s in FS_INSTANCES)
 
 
@@ -123,7 +123,8 @@ def check(layer, inp, what, pad_value="one", x_float=None):
 def test_batch1_configs(cfg, idx):
     layer = config(cfg)[idx]
     assert layer.input_kind == "float"
-    # every one of them is taken (the 72-K-step 7x7x512 one by the K split)
+    # every one of them is taken (the 72-K-step 7x7x512 one by the (18, 4)
+    # filter-stationary instance)
     assert check(layer, make_layer_inputs(layer, 0, cfg, idx), f"config {cfg} layer {idx}")
     assert taken(layer)
 
@@ -214,7 +215,7 @@ def test_ksplit_every_tile(mbw, nblk):
     """Each K-split tile forced (tuning keys): configuration 3's 7x7x512
     layer and ragged layers with zero padding and a stride."""
     import paper_2011_09398_amd as lce
-    lce.set_tuning(mfma_tile_m=mbw, mfma_tile_n=nblk)
+    lce.set_tuning(mfma_schedule="ksplit", mfma_tile_m=mbw, mfma_tile_n=nblk)
     idx, layer = next((i, l) for i, l in enumerate(config(3)) if l.c_in == 512)
     assert k_steps(layer) == 72
     assert check(layer, make_layer_inputs(layer, 0, 3, idx), f"7x7x512 mb={mbw} nblk={nblk}")
@@ -224,6 +225,31 @@ def test_ksplit_every_tile(mbw, nblk):
                                           out="bitpacked", input_kind="float"), "zero"))):
         assert check(lay, make_layer_inputs(lay, 5, 0, 40 + 10 * nblk + mbw + j),
                      f"{lay.name} mb={mbw} nblk={nblk}", pv)
+
+
+@pytest.mark.parametrize("sched", ["ksplit", "fs"])
+def test_schedule_key(sched):
+    """The mfma_schedule key restricts the fused entry to one schedule: the K
+    split on layers of 9 and 18 K steps (which the default plan gives to the
+    filter-stationary schedule), the filter-stationary one on configuration
+    3's 7x7x512 layer (72 K steps) and on a 5x5 layer of 50 K steps that no
+    instance takes (refused)."""
+    import paper_2011_09398_amd as lce
+    lce.set_tuning(mfma_schedule=sched)
+    if sched == "ksplit":
+        for j, layer in enumerate((Layer("k9", 2, 15, 13, 64, 72, out="bitpacked",
+                                         input_kind="float"),
+                                   Layer("k18", 1, 11, 12, 128, 100, stride=2, out="float",
+                                         clamp=(-300, 500), input_kind="float"))):
+            assert k_steps(layer) in (9, 18)
+            assert check(layer, make_layer_inputs(layer, 6, 0, 50 + j), f"{layer.name} ksplit",
+                         ["one", "zero"][j])
+    else:
+        idx, layer = next((i, l) for i, l in enumerate(config(3)) if l.c_in == 512)
+        assert check(layer, make_layer_inputs(layer, 0, 3, idx), "7x7x512 fs")
+        lay = Layer("k50", 1, 9, 9, 128, 64, kh=5, kw=5, out="float", input_kind="float")
+        assert k_steps(lay) == 50
+        assert not check(lay, make_layer_inputs(lay, 6, 0, 60), "k50 fs refused")
 
 
 @pytest.mark.parametrize("wpc", [1, 2])
