@@ -349,7 +349,9 @@ typedef enum {
     LCE_TUNE_MFMA_PACKED = 7,     /* -1: load widened filters where packed ones would do */
     LCE_TUNE_MFMA_TILE_M = 8,     /* K-split / pixel-split tile: 32-pixel blocks        */
     LCE_TUNE_MFMA_TILE_N = 9,     /* K-split / pixel-split tile: 32-filter blocks       */
-    LCE_TUNE_COUNT = 10
+    LCE_TUNE_MFMA_FS_WINDOW = 10, /* -1: filter-stationary workgroups stage whole padded
+                                     rows, also where a share's window of columns would do */
+    LCE_TUNE_COUNT = 11
 } lce_tuning_key;
 
 /* Set override `key` to `value` (0 = automatic).

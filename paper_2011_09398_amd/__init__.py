@@ -43,7 +43,7 @@ EXPORTS = ("lce_packed_words", "lce_bconv2d_out_shape", "lce_bitpack", "lce_bcon
 # lce_tuning_key values, by the names tuning() takes.
 TUNING_KEYS = {"xor_nb": 0, "xor_ks": 1, "mfma_schedule": 2, "mfma_fs_ks": 3, "mfma_fs_s": 4,
                "mfma_fs_wpc": 5, "mfma_fs_pad": 6, "mfma_packed": 7, "mfma_tile_m": 8,
-               "mfma_tile_n": 9}
+               "mfma_tile_n": 9, "mfma_fs_window": 10}
 MFMA_SCHEDULES = {"auto": 0, "fs": 1, "ksplit": 2, "pixel": 3}
 
 

@@ -13,13 +13,13 @@ INCLUDE = os.path.join(ROOT, "include")
 LIB = os.path.join(PKG, "liblce.so")
 # One translation unit per kernel family, compiled in parallel, then linked.
 SOURCES = [os.path.join(CSRC, f) for f in ("lce.hip", "mfma_tiles.hip", "mfma_fs.hip",
-                                                  "quant_conv.hip")]
+                                                  "mfma_fs_win.hip", "quant_conv.hip")]
 BUILD_DIR = os.path.join(PKG, "_build")
 # Measurement-only probe of the xor/popcount VALU rate (not part of the C ABI).
 PROBE_LIB = os.path.join(PKG, "libprobe.so")
 PROBE_SOURCES = [os.path.join(CSRC, "valu_probe.hip")]
 HEADERS = [os.path.join(CSRC, f) for f in ("bitpack.hpp", "bconv.hpp", "pool.hpp",
-                                                 "bconv_mfma.hpp", "launch.hpp", "dpp.hpp",
+                                                 "bconv_mfma.hpp", "launch.hpp", "mfma_fs_launch.hpp", "dpp.hpp",
                                                  "bconv_quant.hpp")] + \
           [os.path.join(INCLUDE, "lce.h")]
 

@@ -543,10 +543,13 @@ __global__ __launch_bounds__(kMfmaThreads) void bconv2d_mfma_kernel(MfmaParams p
     }
 }
 
-// Whether region location rc lies inside the image.
-__device__ __forceinline__ bool region_inside(const MfmaParams &p, int row0, int rc) {
+// Whether region location rc lies inside the image.  The region is
+// tile_rows x pw locations from padded row row0 and padded column c0 (c0 = 0
+// unless a filter-stationary workgroup stages only its share's window of
+// columns, pw then being the window's width).
+__device__ __forceinline__ bool region_inside(const MfmaParams &p, int row0, int c0, int rc) {
     const int r = (int)fast_div((uint32_t)rc, p.div_pw);
-    const int c = rc - r * p.pw;
+    const int c = c0 + rc - r * p.pw;
     const int R = row0 + r;
     const int img = (int)fast_div((uint32_t)R, p.div_ph);
     const int yy = R - img * p.ph - p.pt, xx = c - p.pl;
@@ -613,11 +616,12 @@ struct RegionChunk {
 };
 
 // byte offset in the input of word `word` of region location rc
-// (kBufOutside when the location is outside the image)
-__device__ __forceinline__ int region_offset(const MfmaParams &p, int row0, int rc, int word,
-                                             bool &inside) {
+// (kBufOutside when the location is outside the image; region origin as in
+// region_inside)
+__device__ __forceinline__ int region_offset(const MfmaParams &p, int row0, int c0, int rc,
+                                             int word, bool &inside) {
     const int r = (int)fast_div((uint32_t)rc, p.div_pw);
-    const int c = rc - r * p.pw;
+    const int c = c0 + rc - r * p.pw;
     const int R = row0 + r;
     const int img = (int)fast_div((uint32_t)R, p.div_ph);
     const int yy = R - img * p.ph - p.pt, xx = c - p.pl;
@@ -633,8 +637,8 @@ __device__ __forceinline__ int region_elements(const MfmaParams &p, int plane) {
 }
 
 template <int NT>
-__device__ __forceinline__ void region_load(const MfmaParams &p, int row0, int plane, int tid,
-                                            int e0, RegionChunk &ch) {
+__device__ __forceinline__ void region_load(const MfmaParams &p, int row0, int c0, int plane,
+                                            int tid, int e0, RegionChunk &ch) {
     const int total = region_elements(p, plane);
     const __amdgpu_buffer_rsrc_t xb = input_buffer(p);
     ch.out = 0;
@@ -651,7 +655,7 @@ __device__ __forceinline__ void region_load(const MfmaParams &p, int row0, int p
             const int e = min(e0 + u * NT + tid, total - 1);
             const int g = (int)fast_div((uint32_t)e, p.div_plane);
             bool in;
-            const int off = region_offset(p, row0, e - g * plane, 4 * g, in);
+            const int off = region_offset(p, row0, c0, e - g * plane, 4 * g, in);
             ch.w[u] = __builtin_amdgcn_raw_buffer_load_b128(xb, off, 0, 0);
             ch.out |= in ? 0u : 1u << u;
         }
@@ -665,7 +669,7 @@ __device__ __forceinline__ void region_load(const MfmaParams &p, int row0, int p
             const int e = min(e0 + u * NT + tid, total - 1);
             const int j = (int)fast_div((uint32_t)e, p.div_plane);
             bool in;
-            const int off = region_offset(p, row0, e - j * plane, j, in);
+            const int off = region_offset(p, row0, c0, e - j * plane, j, in);
             ch.w[u].x = __builtin_amdgcn_raw_buffer_load_b32(xb, off, 0, 0);
             ch.out |= in ? 0u : 1u << u;
         }
@@ -699,18 +703,18 @@ __device__ __forceinline__ void region_widen(const MfmaParams &p, const RegionCh
 // 0.0 outside the image under zero padding.
 template <int NT>
 __device__ __forceinline__ void region_finish(const MfmaParams &p, u32x4 *atile, int row0,
-                                              int plane, int tid) {
+                                              int c0, int plane, int tid) {
     const int total = region_elements(p, plane);
     for (int e0 = kRegU * NT; e0 < total; e0 += kRegU * NT) {
         RegionChunk ch;
-        region_load<NT>(p, row0, plane, tid, e0, ch);
+        region_load<NT>(p, row0, c0, plane, tid, e0, ch);
         region_widen<NT>(p, ch, atile, plane, tid, e0);
     }
     for (int e = plane * p.cw + tid; e < plane * p.cwe; e += NT) {
         uint32_t fill = kFp4PlusOne;
         if (p.pad_zero) {
             const int j = (int)fast_div((uint32_t)e, p.div_plane);
-            if (!region_inside(p, row0, e - j * plane)) fill = 0u;
+            if (!region_inside(p, row0, c0, e - j * plane)) fill = 0u;
         }
         atile[e] = widen_word(0u, fill);
     }
@@ -735,8 +739,8 @@ struct RegionChunkF {
 };
 
 template <int NT>
-__device__ __forceinline__ void region_load_f(const MfmaParams &p, int row0, int plane, int tid,
-                                              int e0, RegionChunkF &ch) {
+__device__ __forceinline__ void region_load_f(const MfmaParams &p, int row0, int c0, int plane,
+                                              int tid, int e0, RegionChunkF &ch) {
     const int total = plane * p.cw;
     const __amdgpu_buffer_rsrc_t xb =
         buffer_of(p.x, (uint32_t)p.n * p.h * p.w * p.cw * 128u);
@@ -753,7 +757,7 @@ __device__ __forceinline__ void region_load_f(const MfmaParams &p, int row0, int
         const int j = (int)fast_div((uint32_t)e, p.div_plane);
         bool in;
         // byte offset of packed word j of the location, times 32: its floats
-        const int off = region_offset(p, row0, e - j * plane, j, in);
+        const int off = region_offset(p, row0, c0, e - j * plane, j, in);
         const int offf = in ? off * 32 : kBufOutside;
 #pragma unroll
         for (int i = 0; i < 8; ++i) {
@@ -790,18 +794,18 @@ __device__ __forceinline__ void region_widen_f(const MfmaParams &p, const Region
 // Cw (as region_finish).
 template <int NT>
 __device__ __forceinline__ void region_finish_f(const MfmaParams &p, u32x4 *atile, int row0,
-                                                int plane, int tid) {
+                                                int c0, int plane, int tid) {
     const int total = plane * p.cw;
     for (int e0 = kRegUF * NT; e0 < total; e0 += kRegUF * NT) {
         RegionChunkF ch;
-        region_load_f<NT>(p, row0, plane, tid, e0, ch);
+        region_load_f<NT>(p, row0, c0, plane, tid, e0, ch);
         region_widen_f<NT>(p, ch, atile, plane, tid, e0);
     }
     for (int e = plane * p.cw + tid; e < plane * p.cwe; e += NT) {
         uint32_t fill = kFp4PlusOne;
         if (p.pad_zero) {
             const int j = (int)fast_div((uint32_t)e, p.div_plane);
-            if (!region_inside(p, row0, e - j * plane)) fill = 0u;
+            if (!region_inside(p, row0, c0, e - j * plane)) fill = 0u;
         }
         atile[e] = widen_word(0u, fill);
     }
@@ -905,9 +909,9 @@ __global__ __launch_bounds__(kMfmaThreads) void bconv2d_mfma_ks_kernel(MfmaParam
     // needs it first)
     std::conditional_t<QF, RegionChunkF, RegionChunk> rch;
     if constexpr (QF)
-        region_load_f<kMfmaThreads>(g, row0, plane, tid, 0, rch);
+        region_load_f<kMfmaThreads>(g, row0, 0, plane, tid, 0, rch);
     else
-        region_load<kMfmaThreads>(g, row0, plane, tid, 0, rch);
+        region_load<kMfmaThreads>(g, row0, 0, plane, tid, 0, rch);
 
     // output-transform parameters of the NBLK filter blocks (buffer loads
     // after the region's, so that its widening does not wait for them; an
@@ -966,10 +970,10 @@ __global__ __launch_bounds__(kMfmaThreads) void bconv2d_mfma_ks_kernel(MfmaParam
     // words arrive, while the filter ring is still arriving
     if constexpr (QF) {
         region_widen_f<kMfmaThreads>(g, rch, atile, plane, tid, 0);
-        region_finish_f<kMfmaThreads>(g, atile, row0, plane, tid);
+        region_finish_f<kMfmaThreads>(g, atile, row0, 0, plane, tid);
     } else {
         region_widen<kMfmaThreads>(g, rch, atile, plane, tid, 0);
-        region_finish<kMfmaThreads>(g, atile, row0, plane, tid);
+        region_finish<kMfmaThreads>(g, atile, row0, 0, plane, tid);
     }
     // bitpacked output: the dot bound of each of the workgroup's filters, in
     // LDS past the A planes and the reduction buffer (tb[32*ib + f] for
@@ -1159,8 +1163,11 @@ __device__ __forceinline__ void for_each_index(Fn &&f, std::integer_sequence<int
 
 
 // QF: the input is float32 and binarized while its region is staged
-// (region_load_f), LceQuantize fused into the convolution.
-template <int KS, int S, int OUT, bool PK, bool QF = false>
+// (region_load_f), LceQuantize fused into the convolution.  WIN: every
+// share lies within one output row and the workgroup stages only the padded
+// columns its windows read (pw is then their count, from the share's first
+// pixel's window origin); otherwise whole padded rows.
+template <int KS, int S, int OUT, bool PK, bool QF = false, bool WIN = false>
 __global__ __launch_bounds__(kMfmaThreads) void bconv2d_mfma_fs_kernel(MfmaParams p) {
     static_assert(S == 1 || S == 2 || S == 4, "1, 2 or 4 waves per filter block");
     // every argument line this kernel reads in one round trip, the tap
@@ -1205,13 +1212,15 @@ __global__ __launch_bounds__(kMfmaThreads) void bconv2d_mfma_fs_kernel(MfmaParam
     const MfmaParams g = pinned_geometry(p);     // (geometry in scalar registers)
     int row0, col0;
     mfma_pixel(g, m0, row0, col0);
+    // the region's first padded column
+    const int wc0 = WIN ? col0 : 0;
     // the region's first chunk (its loads before the filters': the widening
     // needs it first)
     std::conditional_t<QF, RegionChunkF, RegionChunk> rch;
     if constexpr (QF)
-        region_load_f<kMfmaThreads>(g, row0, plane, tid, 0, rch);
+        region_load_f<kMfmaThreads>(g, row0, wc0, plane, tid, 0, rch);
     else
-        region_load<kMfmaThreads>(g, row0, plane, tid, 0, rch);
+        region_load<kMfmaThreads>(g, row0, wc0, plane, tid, 0, rch);
 
     // ---- per-lane output-transform parameters of filter co, as buffer
     // loads issued between the region's and the filters' (so that waiting
@@ -1283,7 +1292,7 @@ __global__ __launch_bounds__(kMfmaThreads) void bconv2d_mfma_fs_kernel(MfmaParam
     for (int t = tid; t < nb * 32; t += kMfmaThreads) {
         int prow, pcol;
         mfma_pixel(g, min(m0 + t, m_end - 1), prow, pcol);
-        btab[t] = (prow - row0) * PW + pcol;
+        btab[t] = (prow - row0) * PW + (pcol - wc0);
     }
 
     // The region, widened as its words arrive (the compiler waits for them
@@ -1291,10 +1300,10 @@ __global__ __launch_bounds__(kMfmaThreads) void bconv2d_mfma_fs_kernel(MfmaParam
     // and the words past Cw.
     if constexpr (QF) {
         region_widen_f<kMfmaThreads>(g, rch, atile, plane, tid, 0);
-        region_finish_f<kMfmaThreads>(g, atile, row0, plane, tid);
+        region_finish_f<kMfmaThreads>(g, atile, row0, wc0, plane, tid);
     } else {
         region_widen<kMfmaThreads>(g, rch, atile, plane, tid, 0);
-        region_finish<kMfmaThreads>(g, atile, row0, plane, tid);
+        region_finish<kMfmaThreads>(g, atile, row0, wc0, plane, tid);
     }
     int z;
     const bool flipped = OUT == OUT_BITS && fvalid && co_ok && ((flip_word >> l32) & 1u);

@@ -23,6 +23,10 @@ void launch_mfma_ksplit(const MfmaParams &p, int out_type, int nblk, int mbw, bo
 // pk: load the packed filter copy; qf: float32 input, binarized while staged
 void launch_mfma_fs(const MfmaParams &p, int ks, int s, bool pk, bool qf, int out_type,
                     dim3 grid, size_t lds, hipStream_t stream);
+// the same, each workgroup staging only its share's window of padded columns
+// (p.pw = the window's width; every share within one output row)
+void launch_mfma_fs_window(const MfmaParams &p, int ks, int s, bool pk, bool qf, int out_type,
+                           dim3 grid, size_t lds, hipStream_t stream);
 
 // quantize-fused XOR/POPCOUNT convolution (float input, Cw = C_in/32 words
 // per pixel): whether an instance exists, and its launch

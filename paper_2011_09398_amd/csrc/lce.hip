@@ -543,14 +543,16 @@ size_t mfma_fs_thr_offset(FsShape sh) {
     return sh.s > 1 ? (size_t)2 * (4 / sh.s) * 2 * (sh.s - 1) * 4096 : 0;
 }
 
-size_t mfma_fs_lds(const lce::MfmaParams &p, FsShape sh, int tile_rows, int pixels) {
-    const size_t a = (size_t)p.cwe * tile_rows * p.pw * 16;
+size_t mfma_fs_lds(const lce::MfmaParams &p, FsShape sh, int tile_rows, int width, int pixels) {
+    const size_t a = (size_t)p.cwe * tile_rows * width * 16;
     return a + mfma_fs_thr_offset(sh) + (4 / sh.s) * 32 * 4 + (size_t)(pixels + 31) / 32 * 32 * 4;
 }
 
 struct FsPlan {
     FsShape shape{0, 0};
     int pixels = 0, tile_rows = 0, wpc = 1;
+    int width = 0;          // padded columns each workgroup stages
+    bool window = false;    // width < pw: each share's own window of columns
     int64_t groups = 0;
     size_t lds = 0;
 };
@@ -606,7 +608,12 @@ bool fs_any_takes(int64_t ksteps) {
 // with the fewest matrix products per SIMD (pixel blocks per workgroup x
 // KS, plus the exchange, x workgroups per CU), with about wpc workgroups
 // per CU: each filter group gets wpc x CUs / filter groups workgroups,
-// each an equal share of the pixels.  shape.ks == 0: none fits.
+// each an equal share of the pixels.  A share shorter than an output row
+// is rounded up to a divisor of OW where that keeps its pixel block count,
+// so that every share lies within one output row; each workgroup then
+// stages only the (px - 1)*sw + KW padded columns its windows read, not
+// whole rows (batch 1: the 56x56x64->128/s2 layer's 4-pixel shares read 9
+// of 57 columns).  shape.ks == 0: none fits.
 FsPlan plan_mfma_fs(const lce::MfmaParams &p, int64_t cus, int blocks32, int ksteps) {
     FsPlan best;
     int64_t best_cost = -1;
@@ -619,12 +626,22 @@ FsPlan plan_mfma_fs(const lce::MfmaParams &p, int64_t cus, int blocks32, int kst
         const int64_t pg = std::max<int64_t>(1, cus * wpc / fgroups);
         // (not rounded to whole blocks: the block count is the same, and an
         // exact share often covers whole images or rows, with fewer rows)
-        const int64_t px = ((int64_t)p.m + pg - 1) / pg;
+        int64_t px = ((int64_t)p.m + pg - 1) / pg;
         if (px > (1 << 20)) continue;
+        int width = p.pw;
+        if (px < p.ow && tuning(LCE_TUNE_MFMA_FS_WINDOW) >= 0) {
+            int64_t dv = px;
+            while (p.ow % dv) ++dv;                       // (OW itself at the latest)
+            const int w = (int)((dv - 1) * p.sw + p.kw);
+            if ((dv + 31) / 32 == (px + 31) / 32 && w < p.pw) {
+                px = dv;
+                width = w;
+            }
+        }
         const int tr = mfma_tile_rows(p, (int)px);
-        const size_t lds = mfma_fs_lds(p, sh, tr, (int)px);
+        const size_t lds = mfma_fs_lds(p, sh, tr, width, (int)px);
         if (lds > (size_t)device_max_lds()) continue;
-        if ((int64_t)tr * p.pw * p.cwe > INT32_MAX / 2) continue;
+        if ((int64_t)tr * width * p.cwe > INT32_MAX / 2) continue;
         const int64_t nb = (px + 31) / 32;
         const int64_t cost = (nb * sh.ks + (sh.s > 1 ? nb + kFsExchangeFixed : 0)) * wpc;
         if (best_cost < 0 || cost < best_cost) {
@@ -633,6 +650,8 @@ FsPlan plan_mfma_fs(const lce::MfmaParams &p, int64_t cus, int blocks32, int kst
             best.pixels = (int)px;
             best.tile_rows = tr;
             best.wpc = wpc;
+            best.width = width;
+            best.window = width < p.pw;
             best.groups = ((int64_t)p.m + px - 1) / px;
             best.lds = lds;
         }
@@ -714,6 +733,10 @@ bool launch_fs_plan(lce::MfmaParams &p, const lce_bconv2d_desc &d, int64_t cus, 
     p.tile_rows = fp.tile_rows;
     p.fs_pixels = fp.pixels;
     p.fs_thr_off = (int32_t)(mfma_fs_thr_offset(fp.shape) / 4);
+    if (fp.window) {        // the region: tile_rows x width from each share's first column
+        p.pw = fp.width;
+        p.div_pw = lce::make_fastdiv((uint32_t)fp.width);
+    }
     p.div_plane = lce::make_fastdiv((uint32_t)(fp.tile_rows * p.pw));
     fill_step_table(p, d, fp.tile_rows * p.pw, (int)ksteps);
     size_t lds = fp.lds;
@@ -728,7 +751,11 @@ bool launch_fs_plan(lce::MfmaParams &p, const lce_bconv2d_desc &d, int64_t cus, 
     const dim3 grid((unsigned)fp.groups,
                     (unsigned)((blocks32 + 4 / fp.shape.s - 1) / (4 / fp.shape.s)));
     const bool pk = d.c_in == 32 * p.cwe && tuning(LCE_TUNE_MFMA_PACKED) >= 0;
-    lce::launch_mfma_fs(p, fp.shape.ks, fp.shape.s, pk, qf, d.out_type, grid, lds, stream);
+    if (fp.window)
+        lce::launch_mfma_fs_window(p, fp.shape.ks, fp.shape.s, pk, qf, d.out_type, grid, lds,
+                                   stream);
+    else
+        lce::launch_mfma_fs(p, fp.shape.ks, fp.shape.s, pk, qf, d.out_type, grid, lds, stream);
     return true;
 }
 

@@ -242,6 +242,37 @@ def test_mfma_fs_every_instance(schedule, ks, s, packed):
         assert_match(layer, got, ref, f"{layer.name} {kh}x{kw} cw={cw} {pv}")
 
 
+# Layers whose filter-stationary shares are shorter than an output row, so
+# that each workgroup stages only its share's window of padded columns:
+# stride 1, 2, 3 and (1, 2), one and two filter blocks per workgroup, SAME
+# and VALID padding, several images.
+WINDOW_LAYERS = [
+    Layer("win_s1", 1, 20, 24, 64, 100, out="float", clamp=None),
+    Layer("win_s2", 2, 17, 23, 96, 64, stride=2, out="bitpacked"),
+    Layer("win_s12", 1, 13, 30, 128, 40, stride=1, stride_w=2, out="int32", clamp=(-200, 300)),
+    Layer("win_s3", 1, 11, 40, 64, 200, stride=3, out="bitpacked"),
+    Layer("win_valid", 3, 9, 16, 256, 72, padding="valid", out="float", clamp=(-500, 700)),
+    Layer("win_c1", 1, 30, 32, 32, 32, padding="valid", out="bitpacked"),
+]
+
+
+@pytest.mark.parametrize("pad_value", ["one", "zero"])
+@pytest.mark.parametrize("layer", WINDOW_LAYERS, ids=lambda l: l.name)
+def test_mfma_fs_column_window(schedule, layer, pad_value):
+    """Staging each share's window of columns gives the oracle's output, the
+    same as staging whole padded rows (tuning key mfma_fs_window = -1)."""
+    import paper_2011_09398_amd as lce
+    if schedule != "fs":
+        pytest.skip("filter-stationary windows")
+    inp = make_layer_inputs(layer, 13, 77, WINDOW_LAYERS.index(layer))
+    got = sync_np(mfma_run(layer, inp, pad_value=pad_value))
+    ref = oracle_run(layer, inp, oracle_signs(inp), 0 if pad_value == "zero" else 1)
+    assert_match(layer, got, ref, f"{layer.name} {pad_value}")
+    lce.set_tuning(mfma_fs_window=-1)
+    rows = sync_np(mfma_run(layer, inp, pad_value=pad_value))
+    assert np.array_equal(got.view(np.uint32), rows.view(np.uint32)), layer.name
+
+
 @pytest.mark.parametrize("ks,s", FS_INSTANCES, ids=lambda v: str(v))
 def test_mfma_fs_repeated_launches(schedule, ks, s):
     """Four launches of the same layer, each into a fresh poisoned output,
