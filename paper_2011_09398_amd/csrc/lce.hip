@@ -613,7 +613,9 @@ bool fs_any_takes(int64_t ksteps) {
 // so that every share lies within one output row; each workgroup then
 // stages only the (px - 1)*sw + KW padded columns its windows read, not
 // whole rows (batch 1: the 56x56x64->128/s2 layer's 4-pixel shares read 9
-// of 57 columns).  shape.ks == 0: none fits.
+// of 57 columns), or, where that window is the whole row, KH rows instead
+// of the KH + sh of a share across two output rows.  shape.ks == 0: none
+// fits.
 FsPlan plan_mfma_fs(const lce::MfmaParams &p, int64_t cus, int blocks32, int ksteps) {
     FsPlan best;
     int64_t best_cost = -1;
@@ -629,16 +631,18 @@ FsPlan plan_mfma_fs(const lce::MfmaParams &p, int64_t cus, int blocks32, int kst
         int64_t px = ((int64_t)p.m + pg - 1) / pg;
         if (px > (1 << 20)) continue;
         int width = p.pw;
+        int tr = mfma_tile_rows(p, (int)px);
         if (px < p.ow && tuning(LCE_TUNE_MFMA_FS_WINDOW) >= 0) {
             int64_t dv = px;
             while (p.ow % dv) ++dv;                       // (OW itself at the latest)
             const int w = (int)((dv - 1) * p.sw + p.kw);
-            if ((dv + 31) / 32 == (px + 31) / 32 && w < p.pw) {
+            const int tr_dv = mfma_tile_rows(p, (int)dv);
+            if ((dv + 31) / 32 == (px + 31) / 32 && (w < p.pw || tr_dv < tr)) {
                 px = dv;
                 width = w;
+                tr = tr_dv;
             }
         }
-        const int tr = mfma_tile_rows(p, (int)px);
         const size_t lds = mfma_fs_lds(p, sh, tr, width, (int)px);
         if (lds > (size_t)device_max_lds()) continue;
         if ((int64_t)tr * width * p.cwe > INT32_MAX / 2) continue;
