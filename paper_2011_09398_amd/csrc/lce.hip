@@ -614,8 +614,10 @@ bool fs_any_takes(int64_t ksteps) {
 // stages only the (px - 1)*sw + KW padded columns its windows read, not
 // whole rows (batch 1: the 56x56x64->128/s2 layer's 4-pixel shares read 9
 // of 57 columns), or, where that window is the whole row, KH rows instead
-// of the KH + sh of a share across two output rows.  shape.ks == 0: none
-// fits.
+// of the KH + sh of a share across two output rows.  A longer share is
+// rounded up to whole output rows where that keeps its block count and
+// stages fewer rows (batch 16, 28x28x128: 56 pixels over 4 padded rows
+// instead of 49 over 5).  shape.ks == 0: none fits.
 FsPlan plan_mfma_fs(const lce::MfmaParams &p, int64_t cus, int blocks32, int ksteps) {
     FsPlan best;
     int64_t best_cost = -1;
@@ -640,6 +642,14 @@ FsPlan plan_mfma_fs(const lce::MfmaParams &p, int64_t cus, int blocks32, int kst
             if ((dv + 31) / 32 == (px + 31) / 32 && (w < p.pw || tr_dv < tr)) {
                 px = dv;
                 width = w;
+                tr = tr_dv;
+            }
+        } else if (px % p.ow && tuning(LCE_TUNE_MFMA_FS_WINDOW) >= 0) {
+            // a share of several rows: whole rows where that stages fewer
+            const int64_t dv = (px + p.ow - 1) / p.ow * p.ow;
+            const int tr_dv = mfma_tile_rows(p, (int)dv);
+            if ((dv + 31) / 32 == (px + 31) / 32 && tr_dv < tr) {
+                px = dv;
                 tr = tr_dv;
             }
         }
