@@ -252,6 +252,32 @@ def test_schedule_key(sched):
         assert not check(lay, make_layer_inputs(lay, 6, 0, 60), "k50 fs refused")
 
 
+@pytest.mark.parametrize("layer", [
+    Layer("win_f1", 1, 20, 24, 64, 100, out="float", clamp=None, input_kind="float"),
+    Layer("win_f2", 2, 17, 23, 96, 64, stride=2, out="bitpacked", input_kind="float"),
+    Layer("win_f12", 1, 13, 30, 128, 40, stride=1, stride_w=2, out="int32", clamp=(-200, 300),
+          input_kind="float"),
+    Layer("rows_f", 1, 7, 7, 512, 512, out="bitpacked", input_kind="float"),
+], ids=lambda l: l.name)
+def test_column_windows_and_row_rounding(layer):
+    """Shares within one output row stage only their window of columns (or,
+    where the window is the whole row, fewer rows): the oracle's output, the
+    same as with whole-row shares (tuning key mfma_fs_window = -1), one and
+    zero padding."""
+    import paper_2011_09398_amd as lce
+    for j, pv in enumerate(("one", "zero")):
+        inp = make_layer_inputs(layer, 8, 0, 70 + j)
+        lce.set_tuning(mfma_fs_window=0)
+        assert check(layer, inp, f"{layer.name} {pv}", pv)
+        x = dev(inp.x_float)
+        w_fp4 = lce.mfma_weights(gpu_pack_weights(inp), layer.c_in)
+        win = sync_np(fused(layer, inp, x, w_fp4, pv))
+        lce.set_tuning(mfma_fs_window=-1)
+        rows = sync_np(fused(layer, inp, x, w_fp4, pv))
+        assert np.array_equal(win.view(np.uint32), rows.view(np.uint32)), (layer.name, pv)
+    lce.set_tuning(mfma_fs_window=0)
+
+
 @pytest.mark.parametrize("wpc", [1, 2])
 def test_workgroups_per_cu(wpc):
     import paper_2011_09398_amd as lce
