@@ -616,8 +616,10 @@ bool fs_any_takes(int64_t ksteps) {
 // of 57 columns), or, where that window is the whole row, KH rows instead
 // of the KH + sh of a share across two output rows.  A longer share is
 // rounded up to whole output rows where that keeps its block count and
-// stages fewer rows (batch 16, 28x28x128: 56 pixels over 4 padded rows
-// instead of 49 over 5).  shape.ks == 0: none fits.
+// stages no more rows (batch 16, 28x28x128: 56 pixels over 4 padded rows
+// instead of 49 over 5; batch 64, 56x56x64->128/s2: 112 pixels, 3.5 of its
+// 4 blocks useful instead of 98 pixels' 3.06, over the same 9 rows, with
+// fewer workgroups).  shape.ks == 0: none fits.
 FsPlan plan_mfma_fs(const lce::MfmaParams &p, int64_t cus, int blocks32, int ksteps) {
     FsPlan best;
     int64_t best_cost = -1;
@@ -645,10 +647,10 @@ FsPlan plan_mfma_fs(const lce::MfmaParams &p, int64_t cus, int blocks32, int kst
                 tr = tr_dv;
             }
         } else if (px % p.ow && tuning(LCE_TUNE_MFMA_FS_WINDOW) >= 0) {
-            // a share of several rows: whole rows where that stages fewer
+            // a share of several rows: whole rows where that stages no more
             const int64_t dv = (px + p.ow - 1) / p.ow * p.ow;
             const int tr_dv = mfma_tile_rows(p, (int)dv);
-            if ((dv + 31) / 32 == (px + 31) / 32 && tr_dv < tr) {
+            if ((dv + 31) / 32 == (px + 31) / 32 && tr_dv <= tr) {
                 px = dv;
                 tr = tr_dv;
             }
