@@ -678,7 +678,7 @@ def log(msg):
 def main():
     args = parse()
     if args.gpus != 1:
-        print(f"bench.py runs on one GPU: this build has no multi-GPU path "
+        print(f"bench.py runs on one GPU: the library has no multi-GPU path "
               f"(--gpus {args.gpus} was requested)", file=sys.stderr)
         sys.exit(2)
     import torch

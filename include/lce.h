@@ -47,7 +47,7 @@ extern "C" {
 typedef enum {
     LCE_OK = 0,
     LCE_EINVAL = 1,        /* null pointer, bad size or enum, empty output   */
-    LCE_EUNSUPPORTED = 2,  /* well-formed request this build does not run    */
+    LCE_EUNSUPPORTED = 2,  /* well-formed request the library does not run   */
     LCE_EALIGN = 3,        /* pointer not aligned to its element type        */
     LCE_EHIP = 4           /* the HIP runtime reported an error at launch    */
 } lce_status;

@@ -16,7 +16,7 @@ from workloads import INT32_MAX, INT32_MIN, Layer, LayerInputs, config, make_lay
 
 POISON_I32 = -1431655766                      # 0xAAAAAAAA
 POISON_F32 = np.array([POISON_I32], np.int32).view(np.float32)[0]
-FLOAT_RTOL = 1e-6                             # spec tolerance for the float transform
+FLOAT_RTOL = 1e-6                             # relative tolerance of the float transform
 
 
 def clamp_of(layer: Layer):
