@@ -243,9 +243,9 @@ def test_mfma_fs_every_instance(schedule, ks, s, packed):
 
 
 # Layers whose filter-stationary shares are shorter than an output row, so
-# that each workgroup stages only its share's window of padded columns:
-# stride 1, 2, 3 and (1, 2), one and two filter blocks per workgroup, SAME
-# and VALID padding, several images.
+# that each workgroup stages only its share's window of padded columns (or
+# whole rows over fewer padded rows): stride 1, 2, 3 and (1, 2), one and two
+# filter blocks per workgroup, SAME and VALID padding, several images.
 WINDOW_LAYERS = [
     Layer("win_s1", 1, 20, 24, 64, 100, out="float", clamp=None),
     Layer("win_s2", 2, 17, 23, 96, 64, stride=2, out="bitpacked"),
@@ -253,6 +253,10 @@ WINDOW_LAYERS = [
     Layer("win_s3", 1, 11, 40, 64, 200, stride=3, out="bitpacked"),
     Layer("win_valid", 3, 9, 16, 256, 72, padding="valid", out="float", clamp=(-500, 700)),
     Layer("win_c1", 1, 30, 32, 32, 32, padding="valid", out="bitpacked"),
+    # a prime output width (no divisor short of the whole row: whole-row
+    # shares over fewer rows) and a one-column image (nothing to round)
+    Layer("win_prime", 2, 13, 13, 64, 72, out="bitpacked"),
+    Layer("win_ow1", 4, 9, 1, 64, 64, out="float", clamp=(-100, 200)),
 ]
 
 
